@@ -1,0 +1,428 @@
+/*
+ * CPU oracle for the plan-space estimator: TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the test suite, the smoke entry and the benchmark's CPU-baseline leg
+ * may load this library.  The product path never calls it; it shares no
+ * code, header or constant with the HIP library.
+ *
+ * It computes, plainly and slowly, in IEEE double precision from the f32
+ * input tables, what the estimator computes for one (job, GPU type, GPU
+ * count) cell:
+ *   - every adaptive-parallelism plan (dp, tp, pp, m) of the cell
+ *     (the joint space of Eq. 1 restricted to one scheduling plan; the grid
+ *      sharding of Sec. 3.2 fixes resources and pipeline degree);
+ *   - for each plan, the contiguous stage partition with the smallest
+ *     slowest-stage time (the balanced-stage criterion of Sec. 3.2: a
+ *     pipeline is bottlenecked by its slowest stage), found by the textbook
+ *     recursion over prefixes, and the canonical (lexicographically smallest)
+ *     optimal cut vector;
+ *   - the plan's iteration time: the 1F1B model of Sec. 3.4 (first
+ *     microbatch through every stage, plus B-1 further microbatches on the
+ *     slowest stage with point-to-point overlapped), stage latency as the sum
+ *     of its operators (Sec. 3.4), intra-stage communication in the stage
+ *     (Eq. 4's per-microbatch term), gradient all-reduce once per iteration
+ *     (Eq. 4's once-per-iteration term), latency proportional to volume
+ *     (Sec. 3.4), memory limits (Sec. 3.3);
+ *   - the best plan of the cell, its iteration time T and throughput
+ *     Bg / T: one entry of the throughput matrix of Eq. 5.
+ *
+ * Readings where the paper leaves the model open (units, memory model,
+ * link choice, tie-breaks) are listed in the repository's design notes;
+ * each function below states which one it follows.
+ *
+ * Parity pins: W* is pinned against brute force over every cut vector,
+ * the cuts against the brute-force lexicographic minimum, the plan price
+ * against hand-derived cells, closed forms and invariants (see tests/).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_MAX_L 128
+
+/* ------------------------------------------------------------------ */
+/* Stage partition                                                     */
+/* ------------------------------------------------------------------ */
+
+/* U[0] = 0, U[i] = U[i-1] + u[i-1]: left to right. */
+void oracle_prefix(const double* u, int L, double* U)
+{
+    U[0] = 0.0;
+    for (int i = 1; i <= L; ++i) U[i] = U[i - 1] + u[i - 1];
+}
+
+/* Segment [lo, hi) of the prefix U. */
+static double seg(const double* U, int lo, int hi) { return U[hi] - U[lo]; }
+
+/* Brute force over every cut vector 0 < c_1 < ... < c_{pp-1} < L, visited in
+ * lexicographic order; returns min over vectors of the largest segment and
+ * writes the first (lexicographically smallest) vector that attains it.
+ * This is the definition of the balanced partition (Sec. 3.2), written out.
+ * Cost C(L-1, pp-1): for small L only. */
+typedef struct {
+    const double* U;
+    int L, pp;
+    int cur[ORACLE_MAX_L + 1];
+    int best[ORACLE_MAX_L + 1];
+    double best_w;
+} bf_state;
+
+static void bf_rec(bf_state* s, int k, int start, double run_max)
+{
+    /* k = index of the cut being placed (1..pp-1); cur[k-1] is fixed. */
+    if (k == s->pp) {
+        double w = seg(s->U, s->cur[k - 1], s->L);
+        double m = run_max > w ? run_max : w;
+        if (m < s->best_w) {
+            s->best_w = m;
+            memcpy(s->best, s->cur, sizeof(int) * (size_t)(s->pp + 1));
+        }
+        return;
+    }
+    /* c_k ranges so that pp-k more non-empty segments still fit. */
+    for (int c = start; c <= s->L - (s->pp - k); ++c) {
+        double w = seg(s->U, s->cur[k - 1], c);
+        double m = run_max > w ? run_max : w;
+        s->cur[k] = c;
+        bf_rec(s, k + 1, c + 1, m);
+    }
+}
+
+double oracle_bottleneck_bruteforce(const double* U, int L, int pp, int* cuts)
+{
+    if (L < 1 || pp < 1 || pp > L || L > ORACLE_MAX_L) return NAN;
+    bf_state s;
+    s.U = U; s.L = L; s.pp = pp; s.best_w = INFINITY;
+    s.cur[0] = 0;
+    bf_rec(&s, 1, 1, -INFINITY);
+    if (cuts)
+        for (int k = 1; k < pp; ++k) cuts[k - 1] = s.best[k];
+    return s.best_w;
+}
+
+/* Textbook recursion: D_1(i) = U_i - U_0,
+ * D_k(i) = min over j in [k-1, i-1] of max(D_{k-1}(j), U_i - U_j);
+ * W*(pp) = D_pp(L).  O(pp L^2). */
+double oracle_bottleneck_dp(const double* U, int L, int pp)
+{
+    if (L < 1 || pp < 1 || pp > L || L > ORACLE_MAX_L) return NAN;
+    double prev[ORACLE_MAX_L + 1], cur[ORACLE_MAX_L + 1];
+    for (int i = 0; i <= L; ++i) prev[i] = INFINITY;
+    for (int i = 1; i <= L; ++i) prev[i] = seg(U, 0, i);
+    for (int k = 2; k <= pp; ++k) {
+        for (int i = 0; i <= L; ++i) cur[i] = INFINITY;
+        for (int i = k; i <= L; ++i) {
+            double best = INFINITY;
+            for (int j = k - 1; j <= i - 1; ++j) {
+                double a = prev[j], b = seg(U, j, i);
+                double m = a > b ? a : b;
+                if (m < best) best = m;
+            }
+            cur[i] = best;
+        }
+        memcpy(prev, cur, sizeof(cur));
+    }
+    return prev[L];
+}
+
+/* Canonical cuts: c_pp = L and, right to left,
+ * c_k = smallest c >= k with U_{c_{k+1}} - U_c <= W.
+ * This is the lexicographically smallest cut vector whose segments are all
+ * <= W (front stages as short as possible). */
+void oracle_canonical_cuts(const double* U, int L, int pp, double W, int* cuts)
+{
+    int next = L;
+    for (int k = pp - 1; k >= 1; --k) {
+        int c = k;
+        while (c < next - 1 && seg(U, c, next) > W) ++c;
+        cuts[k - 1] = c;
+        next = c;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Plan pricing                                                        */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    int L, Bg;
+    const float *t, *p, *a, *x, *a2a;
+} ojob;
+
+typedef struct {
+    double speed, mem, bw_intra, bw_inter;
+    int gpn; /* GPUs per node */
+} otype;
+
+/* Per-sample cost of each layer on one GPU of a plan (seconds/sample).
+ * Compute: the profiled fwd+bwd time of the whole global batch on a speed-1
+ * GPU, divided by the batch, the type's speed and the tensor degree (compute
+ * splits evenly over intra-stage GPUs, Sec. 3.3).  Tensor parallel: four ring
+ * all-reduces per layer and microbatch of the layer's output, on the intra-
+ * node link.  MoE all-to-all: tokens x hidden x 2 B on the inter-node link
+ * whenever the layer is spread over more than one GPU.  Comm terms scale
+ * with the grid's contention factor kappa.  Latency is volume / bandwidth
+ * (Sec. 3.4). */
+static void layer_costs(const ojob* jb, const otype* ty, double kappa, int dp, int tp, double* u)
+{
+    for (int l = 0; l < jb->L; ++l) {
+        double v = (double)jb->t[l] / ((double)jb->Bg * ty->speed * (double)tp);
+        if (tp > 1)
+            v += kappa * 8.0 * (double)(tp - 1) / (double)tp * (double)jb->x[l] / ty->bw_intra;
+        if (dp * tp > 1)
+            v += kappa * (double)jb->a2a[l] / ty->bw_inter;
+        u[l] = v;
+    }
+}
+
+typedef struct {
+    double T;        /* iteration time (s) */
+    double mem_max;  /* largest per-GPU footprint over stages (bytes) */
+    double s_max;    /* slowest stage, per sample (s) */
+    int feasible;
+} oplan;
+
+/* Price plan (dp, tp, pp, m) with stage cuts c_1..c_{pp-1} over prefix U.
+ *   b      = Bg / (dp m) samples per microbatch
+ *   W_k    = b (U_{c_{k+1}} - U_{c_k})               stage time per microbatch
+ *   p2p_k  = kappa 2 b x_{last layer of k} / B_pp    (k < pp-1) activation out +
+ *                                                     gradient back
+ *   AR_k   = kappa [dp>1] 2(dp-1)/dp (P_k/tp) / B_dp fp32 gradient ring all-reduce
+ *   Mem_k  = 4 P_k/tp + min(m, pp-k) b A_k/tp        weights, grads, two Adam
+ *                                                     moments + in-flight 1F1B
+ *                                                     activations
+ *   T      = sum_k (W_k + p2p_k) + (m-1) max_k W_k + max_k AR_k
+ * Pipeline neighbours sit dp*tp ranks apart (tp innermost, then dp, then pp):
+ * B_pp is the intra-node link only when the whole plan fits in one node; the
+ * dp group uses the intra-node link when it fits inside one node. */
+static oplan price_plan(const ojob* jb, const otype* ty, int n, double kappa,
+                        int dp, int tp, int pp, int m, const double* U, const int* cuts)
+{
+    oplan r;
+    int bound[ORACLE_MAX_L + 2];
+    bound[0] = 0;
+    for (int k = 1; k < pp; ++k) bound[k] = cuts[k - 1];
+    bound[pp] = jb->L;
+
+    double b = (double)jb->Bg / (double)(dp * m);
+    double B_pp = (n <= ty->gpn) ? ty->bw_intra : ty->bw_inter;
+    int grp = dp * tp;
+    double B_dp = (grp <= ty->gpn && ty->gpn % grp == 0) ? ty->bw_intra : ty->bw_inter;
+
+    double fill = 0.0, w_max = 0.0, ar_max = 0.0, mem_max = 0.0, s_max = 0.0;
+    for (int k = 0; k < pp; ++k) {
+        int lo = bound[k], hi = bound[k + 1];
+        double S = seg(U, lo, hi);
+        double W = b * S;
+        double Pk = 0.0, Ak = 0.0;
+        for (int l = lo; l < hi; ++l) { Pk += (double)jb->p[l]; Ak += (double)jb->a[l]; }
+        double p2p = 0.0;
+        if (k < pp - 1) p2p = kappa * 2.0 * b * (double)jb->x[hi - 1] / B_pp;
+        double AR = 0.0;
+        if (dp > 1) AR = kappa * 2.0 * (double)(dp - 1) / (double)dp * (Pk / (double)tp) / B_dp;
+        int inflight = m < pp - k ? m : pp - k;
+        double Mem = 4.0 * Pk / (double)tp + (double)inflight * b * Ak / (double)tp;
+        fill += W + p2p;
+        if (W > w_max) w_max = W;
+        if (S > s_max) s_max = S;
+        if (AR > ar_max) ar_max = AR;
+        if (Mem > mem_max) mem_max = Mem;
+    }
+    r.T = fill + (double)(m - 1) * w_max + ar_max;
+    r.mem_max = mem_max;
+    r.s_max = s_max;
+    r.feasible = (mem_max <= ty->mem) ? 1 : 0;
+    return r;
+}
+
+static int build_views(int j, int g, const int32_t* off, const float* t, const float* p,
+                       const float* a, const float* x, const float* a2a, const int32_t* batch,
+                       const float* speed, const float* mem, const float* bwi, const float* bwe,
+                       const int32_t* gpn, ojob* jb, otype* ty)
+{
+    int s = off[j];
+    jb->L = off[j + 1] - s;
+    jb->Bg = batch[j];
+    jb->t = t + s; jb->p = p + s; jb->a = a + s; jb->x = x + s; jb->a2a = a2a + s;
+    ty->speed = speed[g]; ty->mem = mem[g]; ty->bw_intra = bwi[g]; ty->bw_inter = bwe[g];
+    ty->gpn = gpn[g];
+    return (jb->L >= 1 && jb->L <= ORACLE_MAX_L) ? 0 : -1;
+}
+
+/* Price one plan of one cell.  If cuts_in is NULL the partition is the
+ * canonical optimal one; otherwise cuts_in (pp-1 first-layer indices of
+ * stages 1..pp-1) is priced as given.  out[0..3] = T, mem_max, s_max,
+ * feasible; cuts_out (nullable) receives the cuts used.  Returns 0 on
+ * success. */
+int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, int m,
+                     const int32_t* off, const float* t, const float* p, const float* a,
+                     const float* x, const float* a2a, const int32_t* batch,
+                     const float* speed, const float* mem, const float* bwi, const float* bwe,
+                     const int32_t* gpn, const int32_t* cuts_in, int32_t* cuts_out, double* out)
+{
+    ojob jb; otype ty;
+    if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
+    if (dp < 1 || tp < 1 || pp < 1 || m < 1 || dp * tp * pp != n || pp > jb.L) return -1;
+    double u[ORACLE_MAX_L], U[ORACLE_MAX_L + 1];
+    int cuts[ORACLE_MAX_L];
+    layer_costs(&jb, &ty, kappa, dp, tp, u);
+    oracle_prefix(u, jb.L, U);
+    if (cuts_in) {
+        for (int k = 0; k < pp - 1; ++k) {
+            cuts[k] = cuts_in[k];
+            int prevc = k == 0 ? 0 : cuts[k - 1];
+            if (cuts[k] <= prevc || cuts[k] >= jb.L) return -1;
+        }
+    } else {
+        double W = oracle_bottleneck_dp(U, jb.L, pp);
+        oracle_canonical_cuts(U, jb.L, pp, W, cuts);
+    }
+    oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
+    out[0] = r.T; out[1] = r.mem_max; out[2] = r.s_max; out[3] = (double)r.feasible;
+    if (cuts_out)
+        for (int k = 0; k < pp - 1; ++k) cuts_out[k] = cuts[k];
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Best plan of a cell                                                 */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    double T;
+    int dp, tp, pp, m, feasible;
+} ocand;
+
+/* Lexicographic plan key: fewer stages, then less tensor parallelism, then
+ * fewer microbatches. */
+static int key_less(const ocand* a, const ocand* b)
+{
+    if (a->pp != b->pp) return a->pp < b->pp;
+    if (a->tp != b->tp) return a->tp < b->tp;
+    return a->m < b->m;
+}
+
+/* Enumerate every plan of cell (j, g, n): tp divides n and the node size,
+ * pp divides n/tp and is at most the layer count, dp = n/(tp pp), and m is a
+ * listed microbatch count with dp*m dividing the global batch (the global
+ * batch is fixed under scaling, Sec. 3.5).  Each plan is priced with its
+ * balanced partition.  The cell's answer is the smallest (pp, tp, m) among
+ * feasible plans whose T is within a factor (1 + tie_eps) of the smallest
+ * feasible T.
+ * res[0] = T (inf if none), res[1] = throughput (samples/s, 0 if none);
+ * plan[0..3] = dp, tp, pp, m (0 if none); returns the number of plans
+ * enumerated, or -1 on a bad job. */
+int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const float* p,
+                const float* a, const float* x, const float* a2a, const int32_t* batch,
+                const float* speed, const float* mem, const float* bwi, const float* bwe,
+                const int32_t* gpn, const int32_t* counts, const float* kappa_grid, int n_counts,
+                const int32_t* m_values, int n_m, double tie_eps,
+                double* res, int32_t* plan, int32_t* cuts_out)
+{
+    ojob jb; otype ty;
+    if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
+    int n = counts[ci];
+    double kappa = (double)kappa_grid[g * n_counts + ci];
+    int L = jb.L;
+
+    int cap = 64, nc = 0;
+    ocand* cand = (ocand*)malloc(sizeof(ocand) * (size_t)cap);
+    double u[ORACLE_MAX_L], U[ORACLE_MAX_L + 1];
+    int cuts[ORACLE_MAX_L];
+
+    for (int tp = 1; tp <= n; ++tp) {
+        if (n % tp != 0 || tp > ty.gpn || ty.gpn % tp != 0) continue;
+        for (int pp = 1; pp <= n / tp; ++pp) {
+            if ((n / tp) % pp != 0 || pp > L) continue;
+            int dp = n / (tp * pp);
+            int any = 0;
+            for (int mi = 0; mi < n_m; ++mi)
+                if (jb.Bg % (dp * m_values[mi]) == 0) any = 1;
+            if (!any) continue;
+            layer_costs(&jb, &ty, kappa, dp, tp, u);
+            oracle_prefix(u, L, U);
+            double W = oracle_bottleneck_dp(U, L, pp);
+            oracle_canonical_cuts(U, L, pp, W, cuts);
+            for (int mi = 0; mi < n_m; ++mi) {
+                int m = m_values[mi];
+                if (jb.Bg % (dp * m) != 0) continue;
+                oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
+                if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
+                cand[nc].T = r.T; cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp;
+                cand[nc].m = m; cand[nc].feasible = r.feasible;
+                ++nc;
+            }
+        }
+    }
+
+    double tmin = INFINITY;
+    for (int i = 0; i < nc; ++i)
+        if (cand[i].feasible && cand[i].T < tmin) tmin = cand[i].T;
+    int win = -1;
+    if (tmin < INFINITY) {
+        double lim = tmin * (1.0 + tie_eps);
+        for (int i = 0; i < nc; ++i) {
+            if (!cand[i].feasible || !(cand[i].T <= lim)) continue;
+            if (win < 0 || key_less(&cand[i], &cand[win])) win = i;
+        }
+    }
+    if (win < 0) {
+        res[0] = INFINITY; res[1] = 0.0;
+        plan[0] = plan[1] = plan[2] = plan[3] = 0;
+    } else {
+        ocand* w = &cand[win];
+        res[0] = w->T;
+        res[1] = (double)jb.Bg / w->T;
+        plan[0] = w->dp; plan[1] = w->tp; plan[2] = w->pp; plan[3] = w->m;
+        if (cuts_out) {
+            layer_costs(&jb, &ty, kappa, w->dp, w->tp, u);
+            oracle_prefix(u, L, U);
+            double W = oracle_bottleneck_dp(U, L, w->pp);
+            oracle_canonical_cuts(U, L, w->pp, W, cuts);
+            for (int k = 0; k < w->pp - 1; ++k) cuts_out[k] = cuts[k];
+        }
+    }
+    free(cand);
+    return nc;
+}
+
+/* Batch driver: evaluates the listed cells (flat index (j*T + g)*NC + ci).
+ * res: 2 doubles per cell, plan: 4 ints per cell, cuts: cuts_stride ints
+ * per cell (-1 past the last cut), nplans: plans enumerated per cell. */
+int oracle_cells(int n_sel, const int64_t* cells, int n_types, int n_counts,
+                 const int32_t* off, const float* t, const float* p, const float* a,
+                 const float* x, const float* a2a, const int32_t* batch,
+                 const float* speed, const float* mem, const float* bwi, const float* bwe,
+                 const int32_t* gpn, const int32_t* counts, const float* kappa_grid,
+                 const int32_t* m_values, int n_m, double tie_eps,
+                 double* res, int32_t* plan, int32_t* cuts, int cuts_stride, int32_t* nplans)
+{
+    for (int s = 0; s < n_sel; ++s) {
+        int64_t c = cells[s];
+        int ci = (int)(c % n_counts);
+        int g = (int)((c / n_counts) % n_types);
+        int j = (int)(c / ((int64_t)n_counts * n_types));
+        int32_t* crow = cuts ? cuts + (int64_t)s * cuts_stride : NULL;
+        if (crow)
+            for (int k = 0; k < cuts_stride; ++k) crow[k] = -1;
+        int np = oracle_cell(j, g, ci, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn,
+                             counts, kappa_grid, n_counts, m_values, n_m, tie_eps,
+                             res + 2 * s, plan + 4 * s, crow);
+        if (np < 0) return -1;
+        nplans[s] = np;
+    }
+    return 0;
+}
+
+/* Per-layer costs exposed for tests (same function the pricing uses). */
+void oracle_layer_costs(int j, int g, double kappa, int dp, int tp,
+                        const int32_t* off, const float* t, const float* p, const float* a,
+                        const float* x, const float* a2a, const int32_t* batch,
+                        const float* speed, const float* mem, const float* bwi, const float* bwe,
+                        const int32_t* gpn, double* u)
+{
+    ojob jb; otype ty;
+    if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return;
+    layer_costs(&jb, &ty, kappa, dp, tp, u);
+}
