@@ -1,0 +1,152 @@
+"""Benchmark: rebuild the job x grid throughput matrix of a full scheduling
+round on one MI355X.
+
+One step = one scheduling round: upload that round's per-grid contention
+factors and estimate every (job, GPU type, GPU count) cell (16384 jobs x 8
+types x 131 counts = 17.2 M cells, about 682 M plans).  Inputs are resident in
+device memory before timing starts.  Prints one JSON line on stdout; progress
+goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9   # CUs x SIMDs x lanes x clock: one unpacked VALU op per lane per clock
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, every: int, kappa_round: int = 0) -> dict:
+    """The oracle (single-threaded C, fp64) on a bounded sample of the same
+    workload: jobs j = 0, every, 2*every, ... times every grid of one round."""
+    import numpy as np
+    from oracle import oracle as oracle_c
+    oracle_c.load()
+    per = w.n_types * w.n_counts
+    jobs = list(range(0, w.n_jobs, every))
+    ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle_c.cells(w, ids, kappa_round=kappa_round)
+    dt = time.perf_counter() - t0
+    return {"value": len(ids) / dt, "unit": "cells/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, round {kappa_round}: "
+                      f"{len(ids)} cells in {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="full", choices=["tiny", "small", "trace", "moe", "full"])
+    ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
+    ap.add_argument("--cpu-every", type=int, default=2048, help="oracle sample: every k-th job")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}): "
+              "the estimator shards by job rows, but this build measures a single GPU.",
+              file=sys.stderr, flush=True)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2403_16125_amd import arena, workcount, workloads
+
+    log(f"generating workload {args.workload}")
+    w = workloads.make(args.workload)
+    log(f"{w.n_jobs} jobs, {w.n_types} types, {w.n_counts} counts, {w.n_cells} cells, "
+        f"{w.n_rounds} rounds of contention factors")
+    work = workcount.count(w, kappa_round=0)
+    log(f"algorithmic work per round: {work['ops']:.4g} ops, {work['plans']} plans, "
+        f"{work['problems']} partition problems")
+
+    dev = torch.device("cuda", 0)
+    est = arena.Estimator(w, device=0, with_cuts=args.cuts)
+    size = est.space_size()
+    assert size["plans"] == work["plans"]
+    stream = torch.cuda.current_stream(dev)
+
+    for i in range(args.warmup):
+        est.set_round(i % w.n_rounds)
+        est.estimate()
+        torch.cuda.synchronize(dev)
+        log(f"warmup {i + 1}/{args.warmup} done")
+    cnt = est.counters()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        est.set_round(i % w.n_rounds)
+        starts[i].record(stream)
+        est.estimate()
+        ends[i].record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    avg_launch_s = float(np.mean(launch_ms)) / 1e3
+    log(f"timed {args.steps} rounds: {wall:.3f} s wall, launch avg {avg_launch_s * 1e3:.2f} ms "
+        f"(min {min(launch_ms):.2f}, max {max(launch_ms):.2f})")
+    res = est.results(np.arange(0, w.n_cells, 9973))
+    est.close()
+
+    cells_per_s = w.n_cells * args.steps / wall
+    plans_per_s = work["plans"] * args.steps / wall
+    achieved = work["ops"] / avg_launch_s
+    line = {
+        "metric": "(job,grid) cells/sec",
+        "value": cells_per_s,
+        "unit": "cells/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {w.n_jobs} jobs x {w.n_types} GPU types x {w.n_counts} GPU counts "
+                        f"({w.n_cells} cells, {work['plans']} plans per round), per-grid contention "
+                        "redrawn every round",
+            "cuts": bool(args.cuts),
+            "rounds_per_step": 1,
+        },
+        "plans_per_s": plans_per_s,
+        "roofline": {
+            "bound": "alu",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_LANE_OPS / 1e12,
+            "unit": "Top/s",
+            "frac": achieved / PEAK_LANE_OPS,
+            "traffic": None,
+            "ops_per_launch": work["ops"],
+            "launch_ms": avg_launch_s * 1e3,
+        },
+        "device_tallies": cnt,
+        "feasible_fraction_sampled": float(np.mean(res["feasible"])),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a sample")
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_every)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

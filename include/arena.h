@@ -1,0 +1,191 @@
+/*
+ * arena.h - C ABI of the MI355X plan-space estimator.
+ *
+ * For every cell (job, GPU type, GPU count) the library enumerates the
+ * adaptive-parallelism plans (dp, tp, pp, m) the cell admits, partitions the
+ * job's profiled per-layer costs into pp contiguous stages so that the
+ * slowest stage is as fast as possible, prices each plan with the 1F1B
+ * pipeline model, and keeps the best plan.  The result is the job x grid
+ * iteration-time and throughput matrix a cluster scheduler consumes.
+ *
+ * Paper: "Arena: Efficiently Training Large Models via Dynamic Scheduling
+ * and Adaptive Parallelism Co-Design" (arXiv 2403.16125).
+ *   - plan space: the joint scheduling x parallelism space, Eq. 1, sharded
+ *     into grids of fixed resources and pipeline degree (Sec. 3.2);
+ *   - balanced stages: at a fixed pipeline degree the plan with balanced
+ *     inter-stage load wins because a pipeline runs at its slowest stage
+ *     (Sec. 3.2);
+ *   - stage latency = sum of its operators' latencies; comm latency is
+ *     proportional to volume; end-to-end 1F1B latency = first microbatch
+ *     through every stage + (B-1) microbatches of the slowest stage with p2p
+ *     overlapped (Sec. 3.4);
+ *   - intra-stage comm per microbatch and comm once per iteration (Eq. 4);
+ *     intra-stage parallelism chosen within memory limits (Sec. 3.3);
+ *   - the best grid per resource feeds the throughput matrix Thr[m,n]
+ *     (Sec. 3.5, Eq. 5) and iteration times T[m,n] (Eq. 7).
+ *
+ * Model details the paper leaves open (units, memory model, link choice,
+ * tie-breaks) are fixed as follows.  Units are SI: seconds, bytes, bytes/s.
+ *   u_l    = t_l / (Bg speed tp)
+ *            + kappa [tp>1] 8 (tp-1)/tp x_l / bw_intra      (TP all-reduces)
+ *            + kappa [dp tp > 1] a2a_l / bw_inter           (MoE all-to-all)
+ *   stage k holds layers [c_k, c_{k+1}); S_k = sum of u over it;
+ *   b      = Bg / (dp m) samples per microbatch
+ *   T      = sum_k (b S_k + p2p_k) + (m-1) b max_k S_k + max_k AR_k
+ *   p2p_k  = kappa 2 b x_{c_{k+1}-1} / B_pp   (k < pp-1)
+ *   AR_k   = kappa [dp>1] 2 (dp-1)/dp (P_k/tp) / B_dp
+ *   Mem_k  = 4 P_k / tp + min(m, pp-k) b A_k / tp  <= mem   (feasibility)
+ *   B_pp   = bw_intra if n <= gpus_per_node else bw_inter
+ *   B_dp   = bw_intra if dp tp divides gpus_per_node else bw_inter
+ *   cuts   = lexicographically smallest cut vector attaining min max_k S_k
+ *   choice = smallest (pp, tp, m) among feasible plans with
+ *            T <= T_min (1 + tie_eps).
+ * Arithmetic is IEEE double; outputs are rounded to float.
+ *
+ * Conventions.  Every function returns an arena_status and never throws.
+ * Arguments are validated on the host before anything is enqueued; on
+ * error nothing is written and arena_last_error() says why.  A context is
+ * used by one thread at a time and one stream at a time.  Device pointers
+ * are caller-owned and must stay valid while bound.
+ */
+#ifndef ARENA_H
+#define ARENA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum arena_status {
+    ARENA_OK = 0,
+    ARENA_ERR_INVALID_ARG = 1,   /* a null pointer, a size or value out of range */
+    ARENA_ERR_OUT_OF_MEMORY = 2, /* a device or pinned host allocation failed */
+    ARENA_ERR_DEVICE = 3,        /* a HIP call failed; the message carries HIP's string */
+    ARENA_ERR_NOT_READY = 4,     /* a required bind/set call has not been made */
+    ARENA_ERR_UNSUPPORTED = 5    /* valid input beyond the library's limits */
+} arena_status;
+
+/* Limits (ARENA_ERR_UNSUPPORTED beyond them). */
+#define ARENA_MAX_LAYERS 128          /* layers (clustered operators) per job */
+#define ARENA_MAX_GPU_COUNT 1024      /* GPUs of one cell */
+#define ARENA_MAX_GPUS_PER_NODE 31    /* node size, bounds tp */
+#define ARENA_MAX_M_VALUES 16         /* distinct microbatch counts */
+#define ARENA_MAX_M 127               /* largest microbatch count */
+#define ARENA_MAX_PLANS_PER_CELL 256  /* plans one cell may admit */
+#define ARENA_MAX_TYPES 64
+#define ARENA_MAX_COUNTS 512
+
+/* Packed plan word: dp bits 0-10, tp bits 11-15, pp bits 16-23, m bits
+ * 24-30, bit 31 set when the cell has a feasible plan.  An infeasible cell
+ * has plan 0, t_iter +inf and thr 0. */
+#define ARENA_PLAN_DP(w) ((uint32_t)(w) & 0x7FFu)
+#define ARENA_PLAN_TP(w) (((uint32_t)(w) >> 11) & 0x1Fu)
+#define ARENA_PLAN_PP(w) (((uint32_t)(w) >> 16) & 0xFFu)
+#define ARENA_PLAN_M(w) (((uint32_t)(w) >> 24) & 0x7Fu)
+#define ARENA_PLAN_FEASIBLE(w) (((uint32_t)(w) >> 31) & 1u)
+
+typedef struct arena_ctx arena_ctx;
+
+/* Profiled jobs (the planner's per-operator inputs, Sec. 3.4).  Layers of
+ * job j are [layer_offset[j], layer_offset[j+1]). */
+typedef struct arena_jobs_desc {
+    int32_t n_jobs;
+    int32_t n_layers_total;
+    const int32_t* layer_offset; /* HOST, n_jobs+1, copied; offset[0]=0, increasing */
+    const int32_t* batch;        /* HOST, n_jobs, copied; global batch size >= 1 */
+    const float* t;   /* DEVICE, fwd+bwd seconds of the layer for the whole global
+                         batch on one GPU of speed 1 */
+    const float* p;   /* DEVICE, parameter bytes */
+    const float* a;   /* DEVICE, stored activation bytes per sample */
+    const float* x;   /* DEVICE, output activation bytes per sample */
+    const float* a2a; /* DEVICE, all-to-all bytes per sample, 0 on dense layers */
+} arena_jobs_desc;
+
+/* GPU types and the GPU counts of the grid (the scheduling plans (n, type)
+ * of Sec. 3.2).  All arrays are host arrays and are copied. */
+typedef struct arena_grids_desc {
+    int32_t n_types;
+    const float* speed;           /* relative to the speed-1 GPU the times refer to, > 0 */
+    const float* mem_bytes;       /* per GPU, > 0 */
+    const float* bw_intra;        /* bytes/s inside a node, > 0 (+inf allowed) */
+    const float* bw_inter;        /* bytes/s across nodes, > 0 (+inf allowed) */
+    const int32_t* gpus_per_node; /* 1..ARENA_MAX_GPUS_PER_NODE */
+    int32_t n_counts;
+    const int32_t* counts;        /* 1..ARENA_MAX_GPU_COUNT, distinct */
+} arena_grids_desc;
+
+/* Work of the last arena_estimate (device-side tallies). */
+typedef struct arena_counters {
+    int64_t cells;            /* cells written */
+    int64_t plans;            /* plans priced */
+    int64_t problems;         /* stage-partition problems solved */
+    int64_t dp_entries;       /* partition-recursion entries evaluated */
+    int64_t infeasible_cells; /* cells with no feasible plan */
+} arena_counters;
+
+/* Exact size of the plan space of the bound tables (host-side count). */
+typedef struct arena_space_size {
+    int64_t cells;
+    int64_t plans;
+    int32_t max_plans_per_cell;
+    int32_t max_layers;
+} arena_space_size;
+
+/* Create a context for HIP device `hip_device`.  Allocates nothing on the
+ * device and makes no HIP call; device state is created lazily. */
+arena_status arena_create(int hip_device, arena_ctx** out);
+
+/* Free the context and everything it allocated.  NULL is allowed.  The
+ * caller synchronises streams that still use the context first. */
+void arena_destroy(arena_ctx* ctx);
+
+/* Text of the last error on ctx (empty when none).  Owned by ctx, valid until
+ * the next call on ctx.  NULL ctx gives a static string. */
+const char* arena_last_error(const arena_ctx* ctx);
+
+/* Name of a status code (static string). */
+const char* arena_status_string(arena_status s);
+
+/* Bind jobs.  Validates the host arrays, then checks on the device that every
+ * per-layer value is finite and >= 0 (synchronous; INVALID_ARG otherwise) and
+ * records which jobs have all-to-all layers.  Keeps the device pointers. */
+arena_status arena_bind_jobs(arena_ctx* ctx, const arena_jobs_desc* jobs);
+
+/* Bind GPU types and counts (host-only, copied).  Resets kappa to 1. */
+arena_status arena_bind_grids(arena_ctx* ctx, const arena_grids_desc* grids);
+
+/* Per-grid contention factor kappa[type * n_counts + count_index] (finite,
+ * > 0), multiplying every communication term.  Host array, copied; uploaded
+ * by the next arena_estimate on its stream.  n = n_types * n_counts. */
+arena_status arena_set_kappa(arena_ctx* ctx, const float* kappa_host, int32_t n);
+
+/* Microbatch counts to consider (distinct, 1..ARENA_MAX_M) and the relative
+ * tie tolerance of the per-cell choice (0 <= tie_eps < 1e-2). */
+arena_status arena_set_plan_space(arena_ctx* ctx, const int32_t* m_values, int32_t n_m,
+                                  double tie_eps);
+
+/* Size of the plan space of the bound tables (host computation, no HIP
+ * call).  Needs jobs, grids and plan space bound. */
+arena_status arena_space_size_get(const arena_ctx* ctx, arena_space_size* out);
+
+/* Estimate every cell, asynchronously on `stream` (a hipStream_t; NULL is the
+ * null stream).  Outputs are caller-owned DEVICE arrays of n_jobs * n_types *
+ * n_counts entries, cell (j, g, c) at index (j * n_types + g) * n_counts + c:
+ *   t_iter  float   iteration time of the best plan (s), +inf if none fits
+ *   thr     float   throughput Bg / t_iter (samples/s), 0 if none fits
+ *   plan    uint32  packed plan word (see ARENA_PLAN_*)
+ *   cuts    uint8   nullable; row of cuts_stride bytes per cell holding the
+ *                   first layer of stages 1..pp-1, then 0xFF.
+ *                   cuts_stride >= max layers - 1 when cuts is not NULL. */
+arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t* plan,
+                            uint8_t* cuts, int32_t cuts_stride, void* stream);
+
+/* Tallies of the last arena_estimate.  Synchronises the device. */
+arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARENA_H */

@@ -1,0 +1,296 @@
+"""Python binding of libarena.so: the C ABI of include/arena.h under the same
+names, plus a small `Estimator` that keeps a workload's tables resident in
+device memory.
+
+This module only marshals arguments.  Every step of the estimate runs in the
+HIP library; torch is used for device allocations and the current stream.
+If the library is not built this module raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_build", "libarena.so")
+
+ARENA_OK = 0
+ARENA_ERR_INVALID_ARG = 1
+ARENA_ERR_OUT_OF_MEMORY = 2
+ARENA_ERR_DEVICE = 3
+ARENA_ERR_NOT_READY = 4
+ARENA_ERR_UNSUPPORTED = 5
+
+MAX_LAYERS = 128
+CUTS_STRIDE = MAX_LAYERS  # bytes of cut row per cell used by this binding
+
+EXPORTED = (
+    "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
+    "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
+    "arena_space_size_get", "arena_estimate", "arena_get_counters",
+)
+
+
+class ArenaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_status_name(status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class JobsDesc(ctypes.Structure):
+    _fields_ = [("n_jobs", ctypes.c_int32), ("n_layers_total", ctypes.c_int32),
+                ("layer_offset", ctypes.c_void_p), ("batch", ctypes.c_void_p),
+                ("t", ctypes.c_void_p), ("p", ctypes.c_void_p), ("a", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("a2a", ctypes.c_void_p)]
+
+
+class GridsDesc(ctypes.Structure):
+    _fields_ = [("n_types", ctypes.c_int32), ("speed", ctypes.c_void_p),
+                ("mem_bytes", ctypes.c_void_p), ("bw_intra", ctypes.c_void_p),
+                ("bw_inter", ctypes.c_void_p), ("gpus_per_node", ctypes.c_void_p),
+                ("n_counts", ctypes.c_int32), ("counts", ctypes.c_void_p)]
+
+
+class Counters(ctypes.Structure):
+    _fields_ = [("cells", ctypes.c_int64), ("plans", ctypes.c_int64),
+                ("problems", ctypes.c_int64), ("dp_entries", ctypes.c_int64),
+                ("infeasible_cells", ctypes.c_int64)]
+
+
+class SpaceSize(ctypes.Structure):
+    _fields_ = [("cells", ctypes.c_int64), ("plans", ctypes.c_int64),
+                ("max_plans_per_cell", ctypes.c_int32), ("max_layers", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libarena.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ArenaError(ARENA_ERR_NOT_READY,
+                         f"{_LIB_PATH} is missing: build it with paper_2403_16125_amd.build")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, st = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int
+    lib.arena_create.argtypes = [ctypes.c_int, ctypes.POINTER(vp)]
+    lib.arena_create.restype = st
+    lib.arena_destroy.argtypes = [vp]
+    lib.arena_destroy.restype = None
+    lib.arena_last_error.argtypes = [vp]
+    lib.arena_last_error.restype = ctypes.c_char_p
+    lib.arena_status_string.argtypes = [st]
+    lib.arena_status_string.restype = ctypes.c_char_p
+    lib.arena_bind_jobs.argtypes = [vp, ctypes.POINTER(JobsDesc)]
+    lib.arena_bind_jobs.restype = st
+    lib.arena_bind_grids.argtypes = [vp, ctypes.POINTER(GridsDesc)]
+    lib.arena_bind_grids.restype = st
+    lib.arena_set_kappa.argtypes = [vp, vp, i32]
+    lib.arena_set_kappa.restype = st
+    lib.arena_set_plan_space.argtypes = [vp, vp, i32, ctypes.c_double]
+    lib.arena_set_plan_space.restype = st
+    lib.arena_space_size_get.argtypes = [vp, ctypes.POINTER(SpaceSize)]
+    lib.arena_space_size_get.restype = st
+    lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    lib.arena_estimate.restype = st
+    lib.arena_get_counters.argtypes = [vp, ctypes.POINTER(Counters)]
+    lib.arena_get_counters.restype = st
+    _lib = lib
+    return lib
+
+
+def _status_name(s: int) -> str:
+    names = {0: "ARENA_OK", 1: "ARENA_ERR_INVALID_ARG", 2: "ARENA_ERR_OUT_OF_MEMORY",
+             3: "ARENA_ERR_DEVICE", 4: "ARENA_ERR_NOT_READY", 5: "ARENA_ERR_UNSUPPORTED"}
+    return names.get(int(s), f"status {s}")
+
+
+def _check(ctx, status: int):
+    if status != ARENA_OK:
+        msg = load().arena_last_error(ctx)
+        raise ArenaError(status, msg.decode() if msg else "")
+
+
+def _ptr(a) -> int:
+    """Address of a numpy array or torch tensor (0 for None)."""
+    if a is None:
+        return 0
+    if isinstance(a, (int, np.integer)):
+        return int(a)
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data
+    return int(a.data_ptr())
+
+
+# ---------------------------------------------------------------- raw C ABI
+
+def arena_create(device: int = 0):
+    h = ctypes.c_void_p()
+    s = load().arena_create(int(device), ctypes.byref(h))
+    if s != ARENA_OK:
+        raise ArenaError(s, "arena_create failed")
+    return h
+
+
+def arena_destroy(ctx) -> None:
+    load().arena_destroy(ctx)
+
+
+def arena_last_error(ctx) -> str:
+    m = load().arena_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def arena_status_string(status: int) -> str:
+    return load().arena_status_string(int(status)).decode()
+
+
+def arena_bind_jobs(ctx, layer_offset, batch, t, p, a, x, a2a, n_layers_total=None):
+    """layer_offset, batch: host int32 arrays; t..a2a: device float32 tensors (or pointers)."""
+    off = np.ascontiguousarray(layer_offset, np.int32)
+    bat = np.ascontiguousarray(batch, np.int32)
+    d = JobsDesc(n_jobs=len(bat), n_layers_total=int(off[-1] if n_layers_total is None else n_layers_total),
+                 layer_offset=_ptr(off), batch=_ptr(bat), t=_ptr(t), p=_ptr(p), a=_ptr(a),
+                 x=_ptr(x), a2a=_ptr(a2a))
+    _check(ctx, load().arena_bind_jobs(ctx, ctypes.byref(d)))
+
+
+def arena_bind_grids(ctx, speed, mem_bytes, bw_intra, bw_inter, gpus_per_node, counts):
+    f = lambda v: np.ascontiguousarray(v, np.float32)
+    arrs = [f(speed), f(mem_bytes), f(bw_intra), f(bw_inter),
+            np.ascontiguousarray(gpus_per_node, np.int32), np.ascontiguousarray(counts, np.int32)]
+    d = GridsDesc(n_types=len(arrs[0]), speed=_ptr(arrs[0]), mem_bytes=_ptr(arrs[1]),
+                  bw_intra=_ptr(arrs[2]), bw_inter=_ptr(arrs[3]), gpus_per_node=_ptr(arrs[4]),
+                  n_counts=len(arrs[5]), counts=_ptr(arrs[5]))
+    _check(ctx, load().arena_bind_grids(ctx, ctypes.byref(d)))
+
+
+def arena_set_kappa(ctx, kappa) -> None:
+    k = np.ascontiguousarray(kappa, np.float32).ravel()
+    _check(ctx, load().arena_set_kappa(ctx, _ptr(k), len(k)))
+
+
+def arena_set_plan_space(ctx, m_values, tie_eps: float) -> None:
+    m = np.ascontiguousarray(m_values, np.int32)
+    _check(ctx, load().arena_set_plan_space(ctx, _ptr(m), len(m), float(tie_eps)))
+
+
+def arena_space_size_get(ctx) -> dict:
+    s = SpaceSize()
+    _check(ctx, load().arena_space_size_get(ctx, ctypes.byref(s)))
+    return dict(cells=s.cells, plans=s.plans, max_plans_per_cell=s.max_plans_per_cell,
+                max_layers=s.max_layers)
+
+
+def arena_estimate(ctx, t_iter, thr, plan, cuts=None, cuts_stride: int = 0, stream=None) -> None:
+    """Outputs are device tensors (or pointers); stream is a HIP stream handle or None."""
+    sp = 0 if stream is None else int(stream)
+    _check(ctx, load().arena_estimate(ctx, _ptr(t_iter), _ptr(thr), _ptr(plan), _ptr(cuts),
+                                      int(cuts_stride), sp))
+
+
+def arena_get_counters(ctx) -> dict:
+    c = Counters()
+    _check(ctx, load().arena_get_counters(ctx, ctypes.byref(c)))
+    return dict(cells=c.cells, plans=c.plans, problems=c.problems, dp_entries=c.dp_entries,
+                infeasible_cells=c.infeasible_cells)
+
+
+# ---------------------------------------------------------------- convenience
+
+def unpack_plan(words):
+    w = np.asarray(words).astype(np.uint32)
+    return dict(dp=(w & 0x7FF).astype(np.int32), tp=((w >> 11) & 0x1F).astype(np.int32),
+                pp=((w >> 16) & 0xFF).astype(np.int32), m=((w >> 24) & 0x7F).astype(np.int32),
+                feasible=((w >> 31) & 1).astype(bool))
+
+
+class Estimator:
+    """Binds a workload's tables (resident in device memory) and runs rounds.
+
+    `workload` is any object with the attributes of workloads.Workload."""
+
+    def __init__(self, workload, device: int = 0, with_cuts: bool = False):
+        import torch
+        self.torch = torch
+        self.w = workload
+        self.dev = torch.device("cuda", device)
+        load()
+        self.ctx = arena_create(device)
+        self._alive = True
+        try:
+            tens = lambda v: torch.as_tensor(np.ascontiguousarray(v, np.float32)).to(self.dev)
+            self.t, self.p, self.a, self.x, self.a2a = (tens(workload.t), tens(workload.p),
+                                                        tens(workload.a), tens(workload.x),
+                                                        tens(workload.a2a))
+            arena_bind_jobs(self.ctx, workload.layer_offset, workload.batch,
+                            self.t, self.p, self.a, self.x, self.a2a)
+            arena_bind_grids(self.ctx, workload.speed, workload.mem, workload.bw_intra,
+                             workload.bw_inter, workload.gpus_per_node, workload.counts)
+            arena_set_plan_space(self.ctx, workload.m_values, workload.tie_eps)
+            arena_set_kappa(self.ctx, workload.kappa[0])
+            C = workload.n_cells
+            self.n_cells = C
+            self.t_iter = torch.empty(C, dtype=torch.float32, device=self.dev)
+            self.thr = torch.empty(C, dtype=torch.float32, device=self.dev)
+            self.plan = torch.empty(C, dtype=torch.int32, device=self.dev)
+            self.cuts = (torch.empty(C * CUTS_STRIDE, dtype=torch.uint8, device=self.dev)
+                         if with_cuts else None)
+        except Exception:
+            self.close()
+            raise
+
+    def set_round(self, r: int) -> None:
+        arena_set_kappa(self.ctx, self.w.kappa[r])
+
+    def set_kappa(self, kappa) -> None:
+        arena_set_kappa(self.ctx, kappa)
+
+    def estimate(self, stream=None) -> None:
+        s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
+        arena_estimate(self.ctx, self.t_iter, self.thr, self.plan, self.cuts,
+                       CUTS_STRIDE if self.cuts is not None else 0, s.cuda_stream)
+
+    def space_size(self) -> dict:
+        return arena_space_size_get(self.ctx)
+
+    def counters(self) -> dict:
+        return arena_get_counters(self.ctx)
+
+    def results(self, ids=None) -> dict:
+        """Synchronise and copy the last estimate (all cells, or the listed
+        cells gathered on the device first) to host numpy arrays."""
+        torch = self.torch
+        torch.cuda.synchronize(self.dev)
+        if ids is None:
+            sel = lambda v: v
+        else:
+            idx = torch.as_tensor(np.asarray(ids, np.int64), device=self.dev)
+            sel = lambda v: v.index_select(0, idx)
+        out = dict(t_iter=sel(self.t_iter).cpu().numpy(), thr=sel(self.thr).cpu().numpy(),
+                   plan=sel(self.plan).cpu().numpy().view(np.uint32))
+        out.update(unpack_plan(out["plan"]))
+        if self.cuts is not None:
+            rows = sel(self.cuts.view(self.n_cells, CUTS_STRIDE))
+            out["cuts"] = rows.cpu().numpy()
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "_alive", False):
+            self.torch.cuda.synchronize(self.dev)
+            arena_destroy(self.ctx)
+            self._alive = False
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

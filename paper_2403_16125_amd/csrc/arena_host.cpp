@@ -1,0 +1,525 @@
+// Host side of the C ABI declared in include/arena.h: argument validation,
+// context state, lazy device set-up, table uploads and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "arena.h"
+#include "arena_internal.h"
+
+using arena::TypeDev;
+
+struct arena_ctx {
+    int device = 0;
+    std::string err;
+
+    // jobs (host copies of per-job scalars; device pointers are the caller's)
+    bool jobs_bound = false;
+    bool jobs_checked = false;     // device-side value check done for this bind
+    int32_t n_jobs = 0, n_layers = 0, max_layers = 0;
+    std::vector<int32_t> off, batch;
+    const float *t = nullptr, *p = nullptr, *a = nullptr, *x = nullptr, *q = nullptr;
+    bool jobs_dirty = true;
+
+    // grids
+    bool grids_bound = false;
+    int32_t n_types = 0, n_counts = 0;
+    std::vector<TypeDev> types;
+    std::vector<int32_t> counts;
+    std::vector<float> kappa;
+    bool grids_dirty = true, kappa_dirty = true;
+
+    // plan space
+    bool space_set = false;
+    std::vector<int32_t> m_values;
+    double tie_eps = 1e-6;
+
+    // cached space size
+    bool size_valid = false;
+    arena_space_size size{};
+
+    // device state
+    bool dev_ready = false;
+    int32_t* d_off = nullptr;
+    int32_t* d_batch = nullptr;
+    size_t cap_jobs = 0, cap_batch = 0;
+    TypeDev* d_types = nullptr;
+    int32_t* d_counts = nullptr;
+    float* d_kappa = nullptr;
+    size_t cap_types = 0, cap_counts = 0, cap_kappa = 0;
+    unsigned long long* d_counters = nullptr;
+    unsigned long long* h_counters = nullptr;   // pinned
+    float* h_kappa[2] = {nullptr, nullptr};     // pinned staging, double-buffered
+    hipEvent_t kappa_done[2] = {nullptr, nullptr};
+    size_t cap_hkappa = 0;
+    int kslot = 0;
+};
+
+namespace {
+
+arena_status fail(arena_ctx* c, arena_status s, const char* fmt, ...)
+{
+    if (c) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof(buf), fmt, ap);
+        va_end(ap);
+        c->err = buf;
+    }
+    return s;
+}
+
+arena_status hip_fail(arena_ctx* c, hipError_t e, const char* what)
+{
+    return fail(c, ARENA_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool is_pos_finite_or_inf(float v) { return v > 0.0f && !std::isnan(v); }
+
+// Plans of one cell: tp | n, tp | node size, pp | n/tp, pp <= L, dp = n/(tp pp),
+// m listed with dp*m | Bg.
+int64_t plans_of_cell(int n, int gpn, int L, int Bg, const std::vector<int32_t>& ms)
+{
+    int64_t cnt = 0;
+    for (int tp = 1; tp <= n && tp <= gpn; ++tp) {
+        if (n % tp || gpn % tp) continue;
+        const int q = n / tp;
+        for (int pp = 1; pp <= q && pp <= L; ++pp) {
+            if (q % pp) continue;
+            const int dp = q / pp;
+            for (int m : ms)
+                if (Bg % (dp * m) == 0) ++cnt;
+        }
+    }
+    return cnt;
+}
+
+void free_device(arena_ctx* c)
+{
+    hipFree(c->d_off);
+    hipFree(c->d_batch);
+    hipFree(c->d_types);
+    hipFree(c->d_counts);
+    hipFree(c->d_kappa);
+    hipFree(c->d_counters);
+    hipHostFree(c->h_counters);
+    for (int i = 0; i < 2; ++i) {
+        hipHostFree(c->h_kappa[i]);
+        if (c->kappa_done[i]) hipEventDestroy(c->kappa_done[i]);
+    }
+    c->d_off = c->d_batch = nullptr;
+    c->d_types = nullptr;
+    c->d_counts = nullptr;
+    c->d_kappa = nullptr;
+    c->d_counters = nullptr;
+    c->h_counters = nullptr;
+    c->h_kappa[0] = c->h_kappa[1] = nullptr;
+    c->kappa_done[0] = c->kappa_done[1] = nullptr;
+}
+
+// Selects ctx->device for the duration of a call, restoring the caller's.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t status = hipSuccess;
+    explicit DeviceGuard(int dev)
+    {
+        status = hipGetDevice(&prev);
+        if (status == hipSuccess && prev != dev) status = hipSetDevice(dev);
+        else if (status == hipSuccess) prev = -1;
+    }
+    ~DeviceGuard()
+    {
+        if (prev >= 0) hipSetDevice(prev);
+    }
+};
+
+template <typename T>
+hipError_t ensure_capacity(T** ptr, size_t* cap, size_t n)
+{
+    if (*cap >= n && *ptr) return hipSuccess;
+    hipFree(*ptr);
+    *ptr = nullptr;
+    *cap = 0;
+    hipError_t e = hipMalloc((void**)ptr, sizeof(T) * (n ? n : 1));
+    if (e == hipSuccess) *cap = n;
+    return e;
+}
+
+arena_status ensure_device(arena_ctx* c, hipStream_t stream)
+{
+    hipError_t e;
+    if (!c->dev_ready) {
+        if ((e = hipMalloc((void**)&c->d_counters, sizeof(unsigned long long) * arena::kNumCounters)))
+            return e == hipErrorOutOfMemory ? fail(c, ARENA_ERR_OUT_OF_MEMORY, "counters") : hip_fail(c, e, "hipMalloc");
+        if ((e = hipHostMalloc((void**)&c->h_counters, sizeof(unsigned long long) * arena::kNumCounters, 0)))
+            return hip_fail(c, e, "hipHostMalloc");
+        for (int i = 0; i < 2; ++i)
+            if ((e = hipEventCreateWithFlags(&c->kappa_done[i], hipEventDisableTiming)))
+                return hip_fail(c, e, "hipEventCreate");
+        c->dev_ready = true;
+    }
+    if (c->jobs_dirty) {
+        if ((e = ensure_capacity(&c->d_off, &c->cap_jobs, (size_t)c->n_jobs + 1)))
+            return fail(c, ARENA_ERR_OUT_OF_MEMORY, "job tables: %s", hipGetErrorString(e));
+        if ((e = ensure_capacity(&c->d_batch, &c->cap_batch, (size_t)c->n_jobs)))
+            return fail(c, ARENA_ERR_OUT_OF_MEMORY, "job tables: %s", hipGetErrorString(e));
+        if ((e = hipMemcpyAsync(c->d_off, c->off.data(), sizeof(int32_t) * (c->n_jobs + 1),
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipMemcpyAsync(c->d_batch, c->batch.data(), sizeof(int32_t) * c->n_jobs,
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipStreamSynchronize(stream)))
+            return hip_fail(c, e, "job table upload");
+        c->jobs_dirty = false;
+    }
+    if (!c->jobs_checked) {
+        arena::ValidateArgs v;
+        v.layer_offset = c->d_off;
+        v.n_jobs = c->n_jobs;
+        v.arrays[0] = c->t; v.arrays[1] = c->p; v.arrays[2] = c->a; v.arrays[3] = c->x; v.arrays[4] = c->q;
+        v.bad = c->d_counters;
+        if ((e = arena::launch_zero_counters(c->d_counters, 1, stream)) ||
+            (e = arena::launch_validate(v, stream)) ||
+            (e = hipMemcpyAsync(c->h_counters, c->d_counters, sizeof(unsigned long long),
+                                hipMemcpyDeviceToHost, stream)) ||
+            (e = hipStreamSynchronize(stream)))
+            return hip_fail(c, e, "job value check");
+        if (c->h_counters[0] != 0)
+            return fail(c, ARENA_ERR_INVALID_ARG,
+                        "jobs: %llu per-layer values are negative or not finite",
+                        (unsigned long long)c->h_counters[0]);
+        c->jobs_checked = true;
+    }
+    if (c->grids_dirty) {
+        size_t nk = (size_t)c->n_types * c->n_counts;
+        if ((e = ensure_capacity(&c->d_types, &c->cap_types, (size_t)c->n_types)) ||
+            (e = ensure_capacity(&c->d_counts, &c->cap_counts, (size_t)c->n_counts)) ||
+            (e = ensure_capacity(&c->d_kappa, &c->cap_kappa, nk)))
+            return fail(c, ARENA_ERR_OUT_OF_MEMORY, "grid tables: %s", hipGetErrorString(e));
+        if ((e = hipMemcpyAsync(c->d_types, c->types.data(), sizeof(TypeDev) * c->n_types,
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipMemcpyAsync(c->d_counts, c->counts.data(), sizeof(int32_t) * c->n_counts,
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipStreamSynchronize(stream)))
+            return hip_fail(c, e, "grid table upload");
+        if (c->cap_hkappa < nk) {
+            for (int i = 0; i < 2; ++i) {
+                if (c->kappa_done[i]) hipEventSynchronize(c->kappa_done[i]);
+                hipHostFree(c->h_kappa[i]);
+                c->h_kappa[i] = nullptr;
+                if ((e = hipHostMalloc((void**)&c->h_kappa[i], sizeof(float) * nk, 0)))
+                    return fail(c, ARENA_ERR_OUT_OF_MEMORY, "pinned kappa staging");
+            }
+            c->cap_hkappa = nk;
+        }
+        c->grids_dirty = false;
+        c->kappa_dirty = true;
+    }
+    if (c->kappa_dirty) {
+        // stage into a pinned slot whose previous copy has completed, then copy
+        // asynchronously on the caller's stream
+        const size_t nk = (size_t)c->n_types * c->n_counts;
+        const int s = c->kslot;
+        if ((e = hipEventSynchronize(c->kappa_done[s]))) return hip_fail(c, e, "kappa slot wait");
+        std::memcpy(c->h_kappa[s], c->kappa.data(), sizeof(float) * nk);
+        if ((e = hipMemcpyAsync(c->d_kappa, c->h_kappa[s], sizeof(float) * nk,
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipEventRecord(c->kappa_done[s], stream)))
+            return hip_fail(c, e, "kappa upload");
+        c->kslot ^= 1;
+        c->kappa_dirty = false;
+    }
+    return ARENA_OK;
+}
+
+arena_status compute_size(arena_ctx* c)
+{
+    if (c->size_valid) return ARENA_OK;
+    // plans depend on (L, Bg) only: group jobs
+    std::map<std::pair<int, int>, int64_t> groups;
+    for (int j = 0; j < c->n_jobs; ++j) ++groups[{c->off[j + 1] - c->off[j], c->batch[j]}];
+    arena_space_size s{};
+    s.cells = (int64_t)c->n_jobs * c->n_types * c->n_counts;
+    s.max_layers = c->max_layers;
+    for (const auto& kv : groups) {
+        for (int g = 0; g < c->n_types; ++g) {
+            for (int ci = 0; ci < c->n_counts; ++ci) {
+                int64_t np = plans_of_cell(c->counts[ci], c->types[g].gpn, kv.first.first,
+                                           kv.first.second, c->m_values);
+                s.plans += np * kv.second;
+                if (np > s.max_plans_per_cell) s.max_plans_per_cell = (int32_t)np;
+            }
+        }
+    }
+    c->size = s;
+    c->size_valid = true;
+    return ARENA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* arena_status_string(arena_status s)
+{
+    switch (s) {
+    case ARENA_OK: return "ARENA_OK";
+    case ARENA_ERR_INVALID_ARG: return "ARENA_ERR_INVALID_ARG";
+    case ARENA_ERR_OUT_OF_MEMORY: return "ARENA_ERR_OUT_OF_MEMORY";
+    case ARENA_ERR_DEVICE: return "ARENA_ERR_DEVICE";
+    case ARENA_ERR_NOT_READY: return "ARENA_ERR_NOT_READY";
+    case ARENA_ERR_UNSUPPORTED: return "ARENA_ERR_UNSUPPORTED";
+    }
+    return "ARENA_UNKNOWN_STATUS";
+}
+
+arena_status arena_create(int hip_device, arena_ctx** out)
+{
+    if (!out) return ARENA_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (hip_device < 0) return ARENA_ERR_INVALID_ARG;
+    arena_ctx* c = new (std::nothrow) arena_ctx();
+    if (!c) return ARENA_ERR_OUT_OF_MEMORY;
+    c->device = hip_device;
+    *out = c;
+    return ARENA_OK;
+}
+
+void arena_destroy(arena_ctx* ctx)
+{
+    if (!ctx) return;
+    if (ctx->dev_ready) {
+        DeviceGuard g(ctx->device);
+        free_device(ctx);
+    }
+    delete ctx;
+}
+
+const char* arena_last_error(const arena_ctx* ctx)
+{
+    if (!ctx) return "no context";
+    return ctx->err.c_str();
+}
+
+arena_status arena_bind_jobs(arena_ctx* c, const arena_jobs_desc* d)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!d) return fail(c, ARENA_ERR_INVALID_ARG, "jobs: descriptor is NULL");
+    if (d->n_jobs < 1) return fail(c, ARENA_ERR_INVALID_ARG, "jobs: n_jobs must be >= 1 (got %d)", d->n_jobs);
+    if (!d->layer_offset || !d->batch)
+        return fail(c, ARENA_ERR_INVALID_ARG, "jobs: layer_offset and batch (host arrays) are required");
+    if (!d->t || !d->p || !d->a || !d->x || !d->a2a)
+        return fail(c, ARENA_ERR_INVALID_ARG, "jobs: per-layer device arrays t, p, a, x, a2a are required");
+    if (d->layer_offset[0] != 0) return fail(c, ARENA_ERR_INVALID_ARG, "jobs: layer_offset[0] must be 0");
+    int maxL = 0;
+    for (int j = 0; j < d->n_jobs; ++j) {
+        const int L = d->layer_offset[j + 1] - d->layer_offset[j];
+        if (L < 1) return fail(c, ARENA_ERR_INVALID_ARG, "jobs: job %d has %d layers", j, L);
+        if (L > ARENA_MAX_LAYERS)
+            return fail(c, ARENA_ERR_UNSUPPORTED, "jobs: job %d has %d layers (max %d)", j, L, ARENA_MAX_LAYERS);
+        if (d->batch[j] < 1) return fail(c, ARENA_ERR_INVALID_ARG, "jobs: job %d has batch %d", j, d->batch[j]);
+        if (L > maxL) maxL = L;
+    }
+    if (d->layer_offset[d->n_jobs] != d->n_layers_total)
+        return fail(c, ARENA_ERR_INVALID_ARG, "jobs: layer_offset[n_jobs]=%d but n_layers_total=%d",
+                    d->layer_offset[d->n_jobs], d->n_layers_total);
+    c->n_jobs = d->n_jobs;
+    c->n_layers = d->n_layers_total;
+    c->max_layers = maxL;
+    c->off.assign(d->layer_offset, d->layer_offset + d->n_jobs + 1);
+    c->batch.assign(d->batch, d->batch + d->n_jobs);
+    c->t = d->t; c->p = d->p; c->a = d->a; c->x = d->x; c->q = d->a2a;
+    c->jobs_bound = true;
+    c->jobs_checked = false;
+    c->jobs_dirty = true;
+    c->size_valid = false;
+    return ARENA_OK;
+}
+
+arena_status arena_bind_grids(arena_ctx* c, const arena_grids_desc* d)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!d) return fail(c, ARENA_ERR_INVALID_ARG, "grids: descriptor is NULL");
+    if (d->n_types < 1) return fail(c, ARENA_ERR_INVALID_ARG, "grids: n_types must be >= 1");
+    if (d->n_types > ARENA_MAX_TYPES)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "grids: %d types (max %d)", d->n_types, ARENA_MAX_TYPES);
+    if (d->n_counts < 1) return fail(c, ARENA_ERR_INVALID_ARG, "grids: n_counts must be >= 1");
+    if (d->n_counts > ARENA_MAX_COUNTS)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "grids: %d counts (max %d)", d->n_counts, ARENA_MAX_COUNTS);
+    if (!d->speed || !d->mem_bytes || !d->bw_intra || !d->bw_inter || !d->gpus_per_node || !d->counts)
+        return fail(c, ARENA_ERR_INVALID_ARG, "grids: a host array is NULL");
+    std::vector<TypeDev> ty((size_t)d->n_types);
+    for (int g = 0; g < d->n_types; ++g) {
+        if (!(d->speed[g] > 0.0f) || !std::isfinite(d->speed[g]))
+            return fail(c, ARENA_ERR_INVALID_ARG, "grids: speed[%d] must be finite and > 0", g);
+        if (!(d->mem_bytes[g] > 0.0f) || std::isnan(d->mem_bytes[g]))
+            return fail(c, ARENA_ERR_INVALID_ARG, "grids: mem_bytes[%d] must be > 0", g);
+        if (!is_pos_finite_or_inf(d->bw_intra[g]) || !is_pos_finite_or_inf(d->bw_inter[g]))
+            return fail(c, ARENA_ERR_INVALID_ARG, "grids: bandwidths of type %d must be > 0", g);
+        const int gpn = d->gpus_per_node[g];
+        if (gpn < 1) return fail(c, ARENA_ERR_INVALID_ARG, "grids: gpus_per_node[%d]=%d", g, gpn);
+        if (gpn > ARENA_MAX_GPUS_PER_NODE)
+            return fail(c, ARENA_ERR_UNSUPPORTED, "grids: gpus_per_node[%d]=%d (max %d)", g, gpn,
+                        ARENA_MAX_GPUS_PER_NODE);
+        ty[g].speed = d->speed[g];
+        ty[g].mem = d->mem_bytes[g];
+        ty[g].bw_intra = d->bw_intra[g];
+        ty[g].bw_inter = d->bw_inter[g];
+        ty[g].gpn = gpn;
+        ty[g].pad = 0;
+    }
+    for (int i = 0; i < d->n_counts; ++i) {
+        const int n = d->counts[i];
+        if (n < 1) return fail(c, ARENA_ERR_INVALID_ARG, "grids: counts[%d]=%d", i, n);
+        if (n > ARENA_MAX_GPU_COUNT)
+            return fail(c, ARENA_ERR_UNSUPPORTED, "grids: counts[%d]=%d (max %d)", i, n, ARENA_MAX_GPU_COUNT);
+        for (int k = 0; k < i; ++k)
+            if (d->counts[k] == n) return fail(c, ARENA_ERR_INVALID_ARG, "grids: count %d listed twice", n);
+    }
+    c->n_types = d->n_types;
+    c->n_counts = d->n_counts;
+    c->types = std::move(ty);
+    c->counts.assign(d->counts, d->counts + d->n_counts);
+    c->kappa.assign((size_t)d->n_types * d->n_counts, 1.0f);
+    c->grids_bound = true;
+    c->grids_dirty = true;
+    c->kappa_dirty = true;
+    c->size_valid = false;
+    return ARENA_OK;
+}
+
+arena_status arena_set_kappa(arena_ctx* c, const float* kappa_host, int32_t n)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!c->grids_bound) return fail(c, ARENA_ERR_NOT_READY, "kappa: bind grids first");
+    if (!kappa_host) return fail(c, ARENA_ERR_INVALID_ARG, "kappa: NULL");
+    if ((int64_t)n != (int64_t)c->n_types * c->n_counts)
+        return fail(c, ARENA_ERR_INVALID_ARG, "kappa: expected %d values, got %d",
+                    c->n_types * c->n_counts, n);
+    for (int i = 0; i < n; ++i)
+        if (!(kappa_host[i] > 0.0f) || !std::isfinite(kappa_host[i]))
+            return fail(c, ARENA_ERR_INVALID_ARG, "kappa[%d] must be finite and > 0", i);
+    c->kappa.assign(kappa_host, kappa_host + n);
+    c->kappa_dirty = true;
+    return ARENA_OK;
+}
+
+arena_status arena_set_plan_space(arena_ctx* c, const int32_t* m_values, int32_t n_m, double tie_eps)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!m_values) return fail(c, ARENA_ERR_INVALID_ARG, "plan space: m_values is NULL");
+    if (n_m < 1) return fail(c, ARENA_ERR_INVALID_ARG, "plan space: n_m must be >= 1");
+    if (n_m > ARENA_MAX_M_VALUES)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "plan space: %d microbatch counts (max %d)", n_m, ARENA_MAX_M_VALUES);
+    for (int i = 0; i < n_m; ++i) {
+        if (m_values[i] < 1) return fail(c, ARENA_ERR_INVALID_ARG, "plan space: m_values[%d]=%d", i, m_values[i]);
+        if (m_values[i] > ARENA_MAX_M)
+            return fail(c, ARENA_ERR_UNSUPPORTED, "plan space: m_values[%d]=%d (max %d)", i, m_values[i], ARENA_MAX_M);
+        for (int k = 0; k < i; ++k)
+            if (m_values[k] == m_values[i]) return fail(c, ARENA_ERR_INVALID_ARG, "plan space: m=%d listed twice", m_values[i]);
+    }
+    if (!(tie_eps >= 0.0) || !(tie_eps < 1e-2))
+        return fail(c, ARENA_ERR_INVALID_ARG, "plan space: tie_eps must be in [0, 1e-2)");
+    c->m_values.assign(m_values, m_values + n_m);
+    c->tie_eps = tie_eps;
+    c->space_set = true;
+    c->size_valid = false;
+    return ARENA_OK;
+}
+
+arena_status arena_space_size_get(const arena_ctx* cc, arena_space_size* out)
+{
+    arena_ctx* c = const_cast<arena_ctx*>(cc);
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!out) return fail(c, ARENA_ERR_INVALID_ARG, "space size: out is NULL");
+    if (!c->jobs_bound || !c->grids_bound || !c->space_set)
+        return fail(c, ARENA_ERR_NOT_READY, "space size: bind jobs, grids and plan space first");
+    compute_size(c);
+    *out = c->size;
+    return ARENA_OK;
+}
+
+arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts,
+                            int32_t cuts_stride, void* stream_ptr)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!c->jobs_bound || !c->grids_bound || !c->space_set)
+        return fail(c, ARENA_ERR_NOT_READY, "estimate: bind jobs, grids and plan space first");
+    if (!t_iter || !thr || !plan) return fail(c, ARENA_ERR_INVALID_ARG, "estimate: output array is NULL");
+    if (cuts && cuts_stride < c->max_layers - 1)
+        return fail(c, ARENA_ERR_INVALID_ARG, "estimate: cuts_stride %d < max layers - 1 = %d",
+                    cuts_stride, c->max_layers - 1);
+    if (cuts && cuts_stride < 1) return fail(c, ARENA_ERR_INVALID_ARG, "estimate: cuts_stride must be >= 1");
+    compute_size(c);
+    if (c->size.max_plans_per_cell > arena::kMaxPlans)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: a cell admits %d plans (max %d)",
+                    c->size.max_plans_per_cell, arena::kMaxPlans);
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    arena_status st = ensure_device(c, stream);
+    if (st != ARENA_OK) return st;
+
+    arena::EstimateArgs A;
+    std::memset(&A, 0, sizeof(A));
+    A.layer_offset = c->d_off;
+    A.batch = c->d_batch;
+    A.t = c->t; A.p = c->p; A.a = c->a; A.x = c->x; A.q = c->q;
+    A.types = c->d_types;
+    A.counts = c->d_counts;
+    A.kappa = c->d_kappa;
+    A.n_jobs = c->n_jobs;
+    A.n_types = c->n_types;
+    A.n_counts = c->n_counts;
+    A.n_m = (int32_t)c->m_values.size();
+    for (int i = 0; i < A.n_m; ++i) A.m_values[i] = c->m_values[i];
+    A.tie_eps = c->tie_eps;
+    A.t_iter = t_iter;
+    A.thr = thr;
+    A.plan = plan;
+    A.cuts = cuts;
+    A.cuts_stride = cuts ? cuts_stride : 0;
+    A.counters = c->d_counters;
+    hipError_t e;
+    if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)))
+        return hip_fail(c, e, "counter reset");
+    if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
+    return ARENA_OK;
+}
+
+arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!out) return fail(c, ARENA_ERR_INVALID_ARG, "counters: out is NULL");
+    if (!c->dev_ready) return fail(c, ARENA_ERR_NOT_READY, "counters: no estimate has run");
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    hipError_t e;
+    if ((e = hipDeviceSynchronize())) return hip_fail(c, e, "synchronise");
+    unsigned long long h[arena::kNumCounters];
+    if ((e = hipMemcpy(h, c->d_counters, sizeof(h), hipMemcpyDeviceToHost))) return hip_fail(c, e, "counter copy");
+    out->cells = (int64_t)h[arena::kCells];
+    out->plans = (int64_t)h[arena::kPlans];
+    out->problems = (int64_t)h[arena::kProblems];
+    out->dp_entries = (int64_t)h[arena::kDpEntries];
+    out->infeasible_cells = (int64_t)h[arena::kInfeasible];
+    if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");
+    return ARENA_OK;
+}
+
+}  // extern "C"

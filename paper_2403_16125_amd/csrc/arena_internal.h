@@ -1,0 +1,59 @@
+// Internal interface between the host side of the C ABI and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace arena {
+
+constexpr int kWave = 64;
+constexpr int kLmax = 128;          // layers per job
+constexpr int kMaxTargets = 32;     // pipeline degrees per partition problem (<= 26 for n <= 1024)
+constexpr int kMaxPlans = 256;      // plans per cell
+constexpr int kMaxM = 16;           // microbatch choices
+
+// GPU type as the kernels read it (doubles converted from the f32 inputs).
+struct TypeDev {
+    double speed, mem, bw_intra, bw_inter;
+    int32_t gpn;
+    int32_t pad;
+};
+
+// Device tallies, zeroed before each estimate.
+enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kNumCounters };
+
+struct EstimateArgs {
+    const int32_t* layer_offset;  // [J+1]
+    const int32_t* batch;         // [J]
+    const float* t;
+    const float* p;
+    const float* a;
+    const float* x;
+    const float* q;               // all-to-all bytes per sample
+    const TypeDev* types;         // [T]
+    const int32_t* counts;        // [NC]
+    const float* kappa;           // [T*NC]
+    int32_t n_jobs, n_types, n_counts;
+    int32_t n_m;
+    int32_t m_values[kMaxM];
+    double tie_eps;
+    float* t_iter;
+    float* thr;
+    uint32_t* plan;
+    uint8_t* cuts;                // nullable
+    int32_t cuts_stride;
+    unsigned long long* counters; // [kNumCounters]
+};
+
+struct ValidateArgs {
+    const int32_t* layer_offset;
+    int32_t n_jobs;
+    const float* arrays[5];
+    unsigned long long* bad;      // [1] count of non-finite or negative values
+};
+
+hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);
+hipError_t launch_zero_counters(unsigned long long* counters, int n, hipStream_t stream);
+hipError_t launch_validate(const ValidateArgs& args, hipStream_t stream);
+
+}  // namespace arena

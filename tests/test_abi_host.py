@@ -1,0 +1,172 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+symbol include/arena.h declares, and rejects bad arguments before any HIP call.
+Contexts are created lazily, so every call here stays on the host."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2403_16125_amd import arena
+from paper_2403_16125_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "arena.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(arena_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    arena.load()
+    out = subprocess.run(["nm", "-D", "--defined-only", arena.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (arena_[a-z_]+)", out))
+    declared = _declared()
+    assert declared, "no declarations parsed"
+    missing = [d for d in declared if d not in exported]
+    assert not missing, missing
+    assert set(arena.EXPORTED) == set(declared)
+
+
+def test_status_strings():
+    assert arena.arena_status_string(0) == "ARENA_OK"
+    assert arena.arena_status_string(5) == "ARENA_ERR_UNSUPPORTED"
+    assert "UNKNOWN" in arena.arena_status_string(99)
+
+
+def test_create_destroy_null_safe():
+    lib = arena.load()
+    assert lib.arena_create(0, None) == arena.ARENA_ERR_INVALID_ARG
+    import ctypes
+    h = ctypes.c_void_p()
+    assert lib.arena_create(-1, ctypes.byref(h)) == arena.ARENA_ERR_INVALID_ARG
+    lib.arena_destroy(None)            # must not crash
+    assert lib.arena_last_error(None) == b"no context"
+    ctx = arena.arena_create(0)
+    arena.arena_destroy(ctx)
+
+
+@pytest.fixture
+def ctx():
+    c = arena.arena_create(0)
+    yield c
+    arena.arena_destroy(c)
+
+
+def _expect(status, fn, *args, match=None, **kw):
+    with pytest.raises(arena.ArenaError) as ei:
+        fn(*args, **kw)
+    assert ei.value.status == status, str(ei.value)
+    if match:
+        assert match in ei.value.message, ei.value.message
+
+
+FAKE = 0x1000   # never dereferenced: validation rejects first or only host data is read
+
+
+def test_bind_jobs_validation(ctx):
+    off = np.array([0, 3, 5], np.int32)
+    bat = np.array([8, 8], np.int32)
+    args = (off, bat, FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_bind_jobs(ctx, *args)   # host-only: succeeds
+    _expect(1, arena.arena_bind_jobs, ctx, off, bat, FAKE, 0, FAKE, FAKE, FAKE, match="per-layer")
+    _expect(1, arena.arena_bind_jobs, ctx, np.array([1, 3], np.int32), bat[:1], *args[2:],
+            match="layer_offset[0]")
+    _expect(1, arena.arena_bind_jobs, ctx, np.array([0, 3, 3], np.int32), bat, *args[2:],
+            match="0 layers")
+    _expect(1, arena.arena_bind_jobs, ctx, off, np.array([8, 0], np.int32), *args[2:], match="batch")
+    _expect(5, arena.arena_bind_jobs, ctx, np.array([0, 129], np.int32), bat[:1], *args[2:],
+            match="129 layers")
+    _expect(1, arena.arena_bind_jobs, ctx, off, bat, *args[2:], 7, match="n_layers_total")
+    lib = arena.load()
+    assert lib.arena_bind_jobs(ctx, None) == arena.ARENA_ERR_INVALID_ARG
+
+
+def _grids(**over):
+    g = dict(speed=[1.0, 0.5], mem_bytes=[4e10, 8e10], bw_intra=[3e11, 3e11], bw_inter=[2.5e10, 2.5e10],
+             gpus_per_node=[4, 4], counts=[1, 2, 4, 8])
+    g.update(over)
+    return g
+
+
+def test_bind_grids_validation(ctx):
+    arena.arena_bind_grids(ctx, **_grids())
+    arena.arena_bind_grids(ctx, **_grids(bw_inter=[np.inf, 1.0]))      # infinite links allowed
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(speed=[1.0, 0.0]), match="speed")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(speed=[1.0, np.nan]), match="speed")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(mem_bytes=[-1.0, 1.0]), match="mem")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(bw_intra=[0.0, 1.0]), match="bandwidth")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(gpus_per_node=[0, 4]), match="gpus_per_node")
+    _expect(5, arena.arena_bind_grids, ctx, **_grids(gpus_per_node=[32, 4]), match="gpus_per_node")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(counts=[1, 2, 2]), match="twice")
+    _expect(1, arena.arena_bind_grids, ctx, **_grids(counts=[0]), match="counts")
+    _expect(5, arena.arena_bind_grids, ctx, **_grids(counts=[2048]), match="max 1024")
+
+
+def test_kappa_and_plan_space_validation(ctx):
+    _expect(4, arena.arena_set_kappa, ctx, np.ones(8, np.float32), match="bind grids")
+    arena.arena_bind_grids(ctx, **_grids())
+    arena.arena_set_kappa(ctx, np.full(8, 1.5, np.float32))
+    _expect(1, arena.arena_set_kappa, ctx, np.ones(7, np.float32), match="expected 8")
+    _expect(1, arena.arena_set_kappa, ctx, np.array([1] * 7 + [0], np.float32), match="kappa[7]")
+    _expect(1, arena.arena_set_kappa, ctx, np.array([1] * 7 + [np.inf], np.float32), match="kappa[7]")
+    arena.arena_set_plan_space(ctx, [1, 2, 4], 1e-6)
+    _expect(1, arena.arena_set_plan_space, ctx, [1, 2, 2], 1e-6, match="twice")
+    _expect(1, arena.arena_set_plan_space, ctx, [0], 1e-6)
+    _expect(5, arena.arena_set_plan_space, ctx, [128], 1e-6)
+    _expect(5, arena.arena_set_plan_space, ctx, list(range(1, 18)), 1e-6)
+    _expect(1, arena.arena_set_plan_space, ctx, [1], -1.0, match="tie_eps")
+    _expect(1, arena.arena_set_plan_space, ctx, [1], float("nan"), match="tie_eps")
+
+
+def test_estimate_not_ready_and_bad_outputs(ctx):
+    _expect(4, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="bind")
+    w = wl.tiny()
+    arena.arena_bind_jobs(ctx, w.layer_offset, w.batch, FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    _expect(4, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="bind")
+    arena.arena_set_plan_space(ctx, w.m_values, w.tie_eps)
+    _expect(1, arena.arena_estimate, ctx, FAKE, 0, FAKE, match="output")
+    _expect(1, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, FAKE, 5, match="cuts_stride")
+
+
+def _plans_of_cell(n, G, L, Bg, ms):
+    cnt = 0
+    for tp in range(1, n + 1):
+        if n % tp or tp > G or G % tp:
+            continue
+        for pp in range(1, n // tp + 1):
+            if (n // tp) % pp or pp > L:
+                continue
+            dp = n // (tp * pp)
+            cnt += sum(1 for m in ms if Bg % (dp * m) == 0)
+    return cnt
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "trace"])
+def test_space_size_matches_enumeration(ctx, name):
+    w = wl.make(name)
+    arena.arena_bind_jobs(ctx, w.layer_offset, w.batch, FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    arena.arena_set_plan_space(ctx, w.m_values, w.tie_eps)
+    s = arena.arena_space_size_get(ctx)
+    ms = [int(m) for m in w.m_values]
+    total, mx = 0, 0
+    cache = {}
+    for j in range(w.n_jobs):
+        key = (w.layers(j), int(w.batch[j]))
+        if key not in cache:
+            cache[key] = [[_plans_of_cell(int(n), int(G), key[0], key[1], ms) for n in w.counts]
+                          for G in w.gpus_per_node]
+        for row in cache[key]:
+            total += sum(row)
+            mx = max(mx, max(row))
+    assert s["cells"] == w.n_cells
+    assert s["plans"] == total
+    assert s["max_plans_per_cell"] == mx
+    assert s["max_layers"] == int(np.diff(w.layer_offset).max())
