@@ -5,8 +5,10 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <map>
+#include <numeric>
 #include <new>
 #include <string>
 #include <utility>
@@ -55,6 +57,10 @@ struct arena_ctx {
     int32_t* d_counts = nullptr;
     float* d_kappa = nullptr;
     size_t cap_types = 0, cap_counts = 0, cap_kappa = 0;
+    int32_t* d_item_order = nullptr;
+    int32_t* d_count_order = nullptr;
+    size_t cap_items = 0, cap_corder = 0;
+    bool order_dirty = true;
     unsigned long long* d_counters = nullptr;
     unsigned long long* h_counters = nullptr;   // pinned
     float* h_kappa[2] = {nullptr, nullptr};     // pinned staging, double-buffered
@@ -105,21 +111,25 @@ int64_t plans_of_cell(int n, int gpn, int L, int Bg, const std::vector<int32_t>&
 
 void free_device(arena_ctx* c)
 {
-    hipFree(c->d_off);
-    hipFree(c->d_batch);
-    hipFree(c->d_types);
-    hipFree(c->d_counts);
-    hipFree(c->d_kappa);
-    hipFree(c->d_counters);
-    hipHostFree(c->h_counters);
+    (void)hipFree(c->d_off);
+    (void)hipFree(c->d_batch);
+    (void)hipFree(c->d_types);
+    (void)hipFree(c->d_counts);
+    (void)hipFree(c->d_kappa);
+    (void)hipFree(c->d_item_order);
+    (void)hipFree(c->d_count_order);
+    (void)hipFree(c->d_counters);
+    (void)hipHostFree(c->h_counters);
     for (int i = 0; i < 2; ++i) {
-        hipHostFree(c->h_kappa[i]);
-        if (c->kappa_done[i]) hipEventDestroy(c->kappa_done[i]);
+        (void)hipHostFree(c->h_kappa[i]);
+        if (c->kappa_done[i]) (void)hipEventDestroy(c->kappa_done[i]);
     }
     c->d_off = c->d_batch = nullptr;
     c->d_types = nullptr;
     c->d_counts = nullptr;
     c->d_kappa = nullptr;
+    c->d_item_order = nullptr;
+    c->d_count_order = nullptr;
     c->d_counters = nullptr;
     c->h_counters = nullptr;
     c->h_kappa[0] = c->h_kappa[1] = nullptr;
@@ -138,7 +148,7 @@ struct DeviceGuard {
     }
     ~DeviceGuard()
     {
-        if (prev >= 0) hipSetDevice(prev);
+        if (prev >= 0) (void)hipSetDevice(prev);
     }
 };
 
@@ -146,7 +156,7 @@ template <typename T>
 hipError_t ensure_capacity(T** ptr, size_t* cap, size_t n)
 {
     if (*cap >= n && *ptr) return hipSuccess;
-    hipFree(*ptr);
+    (void)hipFree(*ptr);
     *ptr = nullptr;
     *cap = 0;
     hipError_t e = hipMalloc((void**)ptr, sizeof(T) * (n ? n : 1));
@@ -212,8 +222,8 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
             return hip_fail(c, e, "grid table upload");
         if (c->cap_hkappa < nk) {
             for (int i = 0; i < 2; ++i) {
-                if (c->kappa_done[i]) hipEventSynchronize(c->kappa_done[i]);
-                hipHostFree(c->h_kappa[i]);
+                if (c->kappa_done[i]) (void)hipEventSynchronize(c->kappa_done[i]);
+                (void)hipHostFree(c->h_kappa[i]);
                 c->h_kappa[i] = nullptr;
                 if ((e = hipHostMalloc((void**)&c->h_kappa[i], sizeof(float) * nk, 0)))
                     return fail(c, ARENA_ERR_OUT_OF_MEMORY, "pinned kappa staging");
@@ -238,6 +248,63 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
         c->kappa_dirty = false;
     }
     return ARENA_OK;
+}
+
+// Work order: (job, type) blocks with the most estimated work first (so the
+// longest blocks do not form the tail), and within a block the largest GPU
+// counts first.  The estimate is plans x layers per cell.
+arena_status upload_orders(arena_ctx* c, hipStream_t stream)
+{
+    std::vector<int32_t> corder((size_t)c->n_counts);
+    std::iota(corder.begin(), corder.end(), 0);
+    std::stable_sort(corder.begin(), corder.end(),
+                     [&](int a, int b) { return c->counts[a] > c->counts[b]; });
+    std::map<std::pair<int, int>, std::vector<double>> cost;
+    const size_t items = (size_t)c->n_jobs * c->n_types;
+    std::vector<double> icost(items);
+    for (int j = 0; j < c->n_jobs; ++j) {
+        const int L = c->off[j + 1] - c->off[j];
+        auto key = std::make_pair(L, (int)c->batch[j]);
+        auto it = cost.find(key);
+        if (it == cost.end()) {
+            std::vector<double> per((size_t)c->n_types, 0.0);
+            for (int g = 0; g < c->n_types; ++g)
+                for (int ci = 0; ci < c->n_counts; ++ci)
+                    per[g] += (double)plans_of_cell(c->counts[ci], c->types[g].gpn, L, key.second,
+                                                    c->m_values) * (double)(L + 16);
+            it = cost.emplace(key, std::move(per)).first;
+        }
+        for (int g = 0; g < c->n_types; ++g) icost[(size_t)j * c->n_types + g] = it->second[g];
+    }
+    std::vector<int32_t> iorder(items);
+    std::iota(iorder.begin(), iorder.end(), 0);
+    std::stable_sort(iorder.begin(), iorder.end(), [&](int a, int b) { return icost[a] > icost[b]; });
+    hipError_t e;
+    if ((e = ensure_capacity(&c->d_item_order, &c->cap_items, items)) ||
+        (e = ensure_capacity(&c->d_count_order, &c->cap_corder, (size_t)c->n_counts)))
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "work order: %s", hipGetErrorString(e));
+    if ((e = hipMemcpyAsync(c->d_item_order, iorder.data(), sizeof(int32_t) * items,
+                            hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(c->d_count_order, corder.data(), sizeof(int32_t) * c->n_counts,
+                            hipMemcpyHostToDevice, stream)) ||
+        (e = hipStreamSynchronize(stream)))
+        return hip_fail(c, e, "work order upload");
+    c->order_dirty = false;
+    return ARENA_OK;
+}
+
+// Some type has one contention factor for all its counts: the kernel then
+// shares every tensor-degree problem of a (job, type) across counts.
+bool kappa_shared(const arena_ctx* c)
+{
+    if (c->n_counts < 2) return false;
+    for (int g = 0; g < c->n_types; ++g) {
+        bool same = true;
+        for (int ci = 1; ci < c->n_counts && same; ++ci)
+            same = c->kappa[(size_t)g * c->n_counts + ci] == c->kappa[(size_t)g * c->n_counts];
+        if (same) return true;
+    }
+    return false;
 }
 
 arena_status compute_size(arena_ctx* c)
@@ -341,6 +408,7 @@ arena_status arena_bind_jobs(arena_ctx* c, const arena_jobs_desc* d)
     c->jobs_bound = true;
     c->jobs_checked = false;
     c->jobs_dirty = true;
+    c->order_dirty = true;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -394,6 +462,7 @@ arena_status arena_bind_grids(arena_ctx* c, const arena_grids_desc* d)
     c->grids_bound = true;
     c->grids_dirty = true;
     c->kappa_dirty = true;
+    c->order_dirty = true;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -435,6 +504,7 @@ arena_status arena_set_plan_space(arena_ctx* c, const int32_t* m_values, int32_t
     c->m_values.assign(m_values, m_values + n_m);
     c->tie_eps = tie_eps;
     c->space_set = true;
+    c->order_dirty = true;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -473,6 +543,7 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
     arena_status st = ensure_device(c, stream);
     if (st != ARENA_OK) return st;
+    if (c->order_dirty && (st = upload_orders(c, stream)) != ARENA_OK) return st;
 
     arena::EstimateArgs A;
     std::memset(&A, 0, sizeof(A));
@@ -485,6 +556,9 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.n_jobs = c->n_jobs;
     A.n_types = c->n_types;
     A.n_counts = c->n_counts;
+    A.item_order = c->d_item_order;
+    A.count_order = c->d_count_order;
+    A.share_tp = kappa_shared(c) ? 1 : 0;
     A.n_m = (int32_t)c->m_values.size();
     for (int i = 0; i < A.n_m; ++i) A.m_values[i] = c->m_values[i];
     A.tie_eps = c->tie_eps;

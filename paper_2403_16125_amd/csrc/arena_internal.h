@@ -11,6 +11,8 @@ constexpr int kLmax = 128;          // layers per job
 constexpr int kMaxTargets = 32;     // pipeline degrees per partition problem (<= 26 for n <= 1024)
 constexpr int kMaxPlans = 256;      // plans per cell
 constexpr int kMaxM = 16;           // microbatch choices
+constexpr int kWavesPerBlock = 4;   // waves of one (job, type) block, each on its own cells
+constexpr int kMaxDp = 1024;        // largest data-parallel degree (counts are <= 1024)
 
 // GPU type as the kernels read it (doubles converted from the f32 inputs).
 struct TypeDev {
@@ -33,7 +35,10 @@ struct EstimateArgs {
     const TypeDev* types;         // [T]
     const int32_t* counts;        // [NC]
     const float* kappa;           // [T*NC]
+    const int32_t* item_order;    // [J*T] (job, type) items, most work first
+    const int32_t* count_order;   // [NC] count indices, largest count first
     int32_t n_jobs, n_types, n_counts;
+    int32_t share_tp;             // some type has one kappa for all its counts: share tp problems
     int32_t n_m;
     int32_t m_values[kMaxM];
     double tie_eps;

@@ -1,18 +1,23 @@
 // HIP kernels of the plan-space estimator (gfx950 / CDNA4).
 //
-// One 64-lane wavefront owns one (job, GPU type) pair and walks the GPU counts
-// of the grid.  For each count it solves the stage-partition problems of the
-// cell (one per tensor degree, plus the no-all-to-all variant of MoE jobs),
-// prices every plan, and reduces to the cell's best plan.  Nothing here is a
-// dense contraction, so no MFMA: the work is compares, min/max and adds on
-// the vector ALU, with the job's tables, the prefix sums and the recursion
-// rows staged in LDS.
+// A block of four 64-lane wavefronts owns one (job, GPU type) pair.
+//   set-up   the job's layer tables, parameter/activation prefix sums and the
+//            pure-compute cost prefix are staged in LDS once;
+//   shared   stage-partition problems that do not depend on the GPU count
+//            (the pure-compute problem, and every tensor degree when the
+//            type has one contention factor for all counts) are solved once
+//            per block for the union of the degrees any count requests;
+//   cells    the waves then take GPU counts from an LDS work counter, solve
+//            the count-specific problems, price every plan and reduce to the
+//            cell's best plan.
+// Nothing here is a dense contraction, so no MFMA: the work is compares,
+// min/max and adds on the vector ALU; reductions use DPP row operations.
 //
 // Arithmetic is IEEE double.  The per-layer cost, its prefix sums, the
 // balanced-partition value and the canonical cuts are evaluated in the same
 // operation order as a plain left-to-right evaluation of the formulas in
-// arena.h, so they are bit-reproducible; only the sum of stage times is
-// reduced in tree order.
+// arena.h, so they are bit-reproducible; sums over stages are reduced in
+// tree order.
 #include <math.h>
 
 #include "arena_internal.h"
@@ -21,72 +26,111 @@ namespace arena {
 namespace {
 
 constexpr double kInf = __builtin_huge_val();
+constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree problems
 
-struct Lds {
-    double U[kLmax + 1];        // prefix of the per-sample layer cost of the current problem
-    double Pp[kLmax + 1];       // prefix of parameter bytes of the job
-    double Ap[kLmax + 1];       // prefix of activation bytes of the job
-    double D[2][kLmax + 1];     // two rows of the partition recursion
-    double planT[kMaxPlans];    // iteration time of each plan of the cell (+inf: does not fit)
-    double planW[kMaxPlans];    // its slowest stage per sample
-    uint32_t planKey[kMaxPlans];
+struct WaveLds {
+    double U[kLmax + 1];          // cost prefix of the wave's current problem
+    double D[kLmax + 1];          // partition recursion row, updated in place
+    double Wt[kMaxTargets];       // bottleneck per requested degree (by rank)
+    double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
+    uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
+};
+
+template <int SLOTS>
+struct BlockLds {
     float t[kLmax];
     float x[kLmax];
     float q[kLmax];
-    int32_t tg[kMaxTargets];    // pipeline degrees requested of the current problem, ascending
+    double Pp[kLmax + 1];         // prefix of parameter bytes
+    double Ap[kLmax + 1];         // prefix of activation bytes
+    double Upure[kLmax + 1];      // prefix of the pure-compute per-sample cost
+    double Wtab[SLOTS][kLmax + 1];// bottleneck of each shared problem, by degree
+    uint32_t adm[kMaxDp / 32];    // bit dp-1: some listed m has dp*m dividing the batch
+    int32_t slot_tp[SLOTS];
+    int32_t slot_var[SLOTS];
+    int32_t n_slots;
+    int32_t next_cell;
+    int32_t uniform;              // one kappa for every count of this type
+    int32_t moe;
+    WaveLds w[kWavesPerBlock];
 };
 
-__device__ __forceinline__ void sync() { __syncthreads(); }
+// ------------------------------------------------------------ wave helpers
+
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
 
 __device__ __forceinline__ double bcast(double v, int src)
 {
-    unsigned long long b = (unsigned long long)__double_as_longlong(v);
-    int lo = __builtin_amdgcn_readlane((int)(unsigned)(b & 0xffffffffull), src);
-    int hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), src);
+    const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)(unsigned)(b & 0xffffffffull), src);
+    const int hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), src);
     return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) |
                                             (unsigned long long)(unsigned)lo));
 }
 
-__device__ __forceinline__ double wave_max(double v)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp(double v, double ident)
 {
-    for (int m = 32; m >= 1; m >>= 1) v = fmax(v, __shfl_xor(v, m));
-    return v;
+    const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+    const unsigned long long e = (unsigned long long)__double_as_longlong(ident);
+    const int lo = __builtin_amdgcn_update_dpp((int)(unsigned)e, (int)(unsigned)b, CTRL, ROWS, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(unsigned)(e >> 32), (int)(unsigned)(b >> 32), CTRL,
+                                               ROWS, 0xf, false);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) |
+                                            (unsigned long long)(unsigned)lo));
 }
 
-__device__ __forceinline__ double wave_min(double v)
+// Whole-wave reductions: quad swaps, row rotations, then row broadcasts leave
+// the total in lane 63, which is broadcast (so every lane sees one value).
+struct OpSum {
+    static __device__ __forceinline__ double ident() { return 0.0; }
+    static __device__ __forceinline__ double op(double a, double b) { return a + b; }
+};
+struct OpMax {
+    static __device__ __forceinline__ double ident() { return -kInf; }
+    static __device__ __forceinline__ double op(double a, double b) { return fmax(a, b); }
+};
+struct OpMin {
+    static __device__ __forceinline__ double ident() { return kInf; }
+    static __device__ __forceinline__ double op(double a, double b) { return fmin(a, b); }
+};
+
+template <class Op, int N>
+__device__ __forceinline__ void wave_reduce(double (&v)[N])
 {
-    for (int m = 32; m >= 1; m >>= 1) v = fmin(v, __shfl_xor(v, m));
-    return v;
+    const double id = Op::ident();
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0xB1, 0xf>(v[i], id));   // quad_perm 1,0,3,2
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0x4E, 0xf>(v[i], id));   // quad_perm 2,3,0,1
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0x124, 0xf>(v[i], id));  // row_ror 4
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0x128, 0xf>(v[i], id));  // row_ror 8
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0x142, 0xa>(v[i], id));  // row_bcast 15
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = Op::op(v[i], dpp<0x143, 0xc>(v[i], id));  // row_bcast 31
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = bcast(v[i], 63);
 }
 
-// Tree sum; every lane returns lane 0's value so the result is uniform.
-__device__ __forceinline__ double wave_sum(double v)
+template <class Op>
+__device__ __forceinline__ double wave_reduce1(double x)
 {
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return bcast(v, 0);
+    double v[1] = {x};
+    wave_reduce<Op, 1>(v);
+    return v[0];
 }
 
-__device__ __forceinline__ unsigned wave_min_u(unsigned v)
-{
-    for (int m = 32; m >= 1; m >>= 1) {
-        unsigned o = (unsigned)__shfl_xor((int)v, m);
-        v = o < v ? o : v;
-    }
-    return v;
-}
-
-__device__ __forceinline__ int wave_max_i(int v)
-{
-    for (int m = 32; m >= 1; m >>= 1) {
-        int o = __shfl_xor(v, m);
-        v = o > v ? o : v;
-    }
-    return v;
-}
-
-// Left-to-right prefix sum of a per-lane pair (element lane, element lane+64)
-// of L values: out[0] = 0, out[i] = out[i-1] + v[i-1].  Sequential on purpose
-// (the rounding of a prefix must not depend on the reduction tree).
+// Left-to-right prefix of L values held as (element lane, element lane+64):
+// out[0] = 0, out[i] = out[i-1] + v[i-1].  Sequential on purpose: the rounding
+// of a prefix must not depend on a reduction tree.
 __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out)
 {
     double acc = 0.0, r0 = 0.0, r1 = 0.0;
@@ -104,20 +148,22 @@ __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane
     if (lane + 64 < L) out[lane + 65] = r1;
 }
 
-struct Cell {
-    int n;          // GPUs of the cell
-    double kappa;   // contention factor of the grid
-    double B_pp;    // link between pipeline neighbours
-};
+// ------------------------------------------------------------ model pieces
 
 struct JobCtx {
     int L, Bg;
     bool moe;       // has all-to-all layers
 };
 
-// Per-sample cost of each layer (formula in arena.h), prefix-summed into S.U.
-__device__ void build_prefix_u(Lds& S, int lane, const JobCtx& jb, const TypeDev& ty,
-                               double kappa, int tp, bool a2a_on)
+struct Cell {
+    int n;          // GPUs of the cell
+    double kappa;   // contention factor of the grid
+    double B_pp;    // link between pipeline neighbours
+};
+
+// Per-sample cost of each layer (formula in arena.h), prefix-summed into U.
+__device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, int lane,
+                               const JobCtx& jb, const TypeDev& ty, double kappa, int tp, bool a2a_on)
 {
     const double denom = (double)jb.Bg * ty.speed * (double)tp;
     const double ctp = kappa * 8.0 * (double)(tp - 1) / (double)tp;
@@ -126,75 +172,185 @@ __device__ void build_prefix_u(Lds& S, int lane, const JobCtx& jb, const TypeDev
     for (int s = 0; s < 2; ++s) {
         const int l = lane + 64 * s;
         if (l < jb.L) {
-            double v = (double)S.t[l] / denom;
-            if (tp > 1) v += ctp * (double)S.x[l] / ty.bw_intra;
-            if (a2a_on) v += kappa * (double)S.q[l] / ty.bw_inter;
+            double v = (double)t[l] / denom;
+            if (tp > 1) v += ctp * (double)x[l] / ty.bw_intra;
+            if (a2a_on) v += kappa * (double)q[l] / ty.bw_inter;
             u[s] = v;
         }
     }
-    seq_prefix(u[0], u[1], jb.L, lane, S.U);
-    sync();
+    seq_prefix(u[0], u[1], jb.L, lane, U);
+    wave_sync();
 }
 
-// Pipeline degrees the problem must answer: divisors pp of n/tp with
-// pp <= L, at least one admissible microbatch count, and the all-to-all
-// condition of the variant.  Writes S.tg ascending, returns how many.
-__device__ int build_targets(Lds& S, int lane, const JobCtx& jb, int n, int tp, int variant,
-                             const EstimateArgs& A)
+__device__ __forceinline__ bool adm_ok(const uint32_t* adm, int dp)
 {
-    const int q = n / tp;
-    int nt = 0;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int pp = 1 + lane + 64 * s;
-        bool ok = pp <= jb.L && (q % pp) == 0;
-        if (ok) ok = (variant == 0) ? (!jb.moe || pp < n) : (pp == n);
-        if (ok) {
-            const int dp = q / pp;
-            bool anym = false;
-            for (int i = 0; i < A.n_m; ++i) anym |= (jb.Bg % (dp * A.m_values[i])) == 0;
-            ok = anym;
-        }
-        const unsigned long long mask = __ballot(ok);
-        if (ok) S.tg[nt + __popcll(mask & ((1ull << lane) - 1ull))] = pp;
-        nt += __popcll(mask);
-    }
-    sync();
-    return nt;
+    return (adm[(dp - 1) >> 5] >> ((dp - 1) & 31)) & 1u;
 }
 
-// Canonical cuts for degree pp and bottleneck W: c_pp = L and, right to
-// left, c_k = max(k, next(c_{k+1})) with next(e) the smallest c such that
-// U_e - U_c <= W.  Returns stage bounds in registers: stage s = lane + 64*h
-// holds layers [st_h, en_h).
+// Is pp a requested degree of problem (n, tp, variant)?  pp divides n/tp, is
+// at most the layer count, leaves an admissible data-parallel degree, and
+// meets the all-to-all condition of the variant (variant 1: the MoE job's
+// single-GPU-per-stage plan dp = tp = 1, which has no all-to-all).
+__device__ __forceinline__ bool target_ok(const uint32_t* adm, const JobCtx& jb, int n, int tp,
+                                          int variant, int pp)
+{
+    const int qn = n / tp;
+    if (pp > jb.L || pp > qn || qn % pp != 0) return false;
+    if (variant == 0) {
+        if (jb.moe && pp >= n) return false;
+    } else if (pp != n) {
+        return false;
+    }
+    return adm_ok(adm, qn / pp);
+}
+
+// Degrees as a 128-bit mask (bit pp-1), uniform across the wave.
+struct Mask {
+    unsigned long long lo, hi;
+    __device__ __forceinline__ bool test(int pp) const
+    {
+        return pp <= 64 ? ((lo >> (pp - 1)) & 1ull) : ((hi >> (pp - 65)) & 1ull);
+    }
+    __device__ __forceinline__ int count() const { return __popcll(lo) + __popcll(hi); }
+    __device__ __forceinline__ int last() const
+    {
+        return hi ? 128 - __clzll(hi) : (lo ? 64 - __clzll(lo) : 0);
+    }
+    // smallest set degree >= from (0 if none)
+    __device__ __forceinline__ int next(int from) const
+    {
+        if (from <= 64) {
+            const unsigned long long m = from <= 1 ? lo : (lo & ~((1ull << (from - 1)) - 1ull));
+            if (m) return __ffsll((long long)m);
+            return hi ? 64 + __ffsll((long long)hi) : 0;
+        }
+        if (from > 128) return 0;
+        const unsigned long long m = hi & ~((1ull << (from - 65)) - 1ull);
+        return m ? 64 + __ffsll((long long)m) : 0;
+    }
+};
+
+__device__ __forceinline__ Mask ballot_mask(bool ok0, bool ok1)
+{
+    Mask m;
+    m.lo = __ballot(ok0);
+    m.hi = __ballot(ok1);
+    return m;
+}
+
+// ------------------------------------------------------------ partition
+
+// One lane of row k of the recursion D_k(i) = min_j max(D_{k-1}(j), U_i - U_j)
+// (D holds row k-1 and receives row k in place).  The crossing j -- the first
+// j with D_{k-1}(j) >= U_i - U_j -- never moves left as i or k grows, so the
+// lane starts from its previous crossing, gallops and then bisects.
+__device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int& jp)
+{
+    const bool act = i >= k && i <= hi;
+    double v = 0.0;
+    if (act) {
+        const double Ui = U[i];
+        int a = jp > k - 1 ? jp : k - 1;   // every j < a fails
+        int b = i;                         // crossing <= b (b = i: none)
+        int step = 1;
+        while (a < b) {
+            int p = a + step - 1;
+            p = p < b - 1 ? p : b - 1;
+            if (D[p] >= Ui - U[p]) { b = p; break; }
+            a = p + 1;
+            step <<= 1;
+        }
+        while (a < b) {
+            const int mid = (a + b) >> 1;
+            if (D[mid] >= Ui - U[mid]) b = mid; else a = mid + 1;
+        }
+        jp = a;
+        v = (a < i) ? D[a] : kInf;
+        if (a - 1 >= k - 1) v = fmin(v, Ui - U[a - 1]);
+    }
+    // every lane has read row k-1 before any lane overwrites it
+    __asm__ volatile("" ::: "memory");
+    if (act) D[i] = v;
+}
+
+// Bottleneck W*(pp) for every degree in `tm`, written to Wout[pp] (by_pp) or
+// Wout[rank of pp].  Row k is evaluated for i in [k, L - tau(k) + k] only,
+// tau(k) the smallest requested degree >= k: larger i cannot reach a
+// requested cell.
+__device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, double* Wout, bool by_pp,
+                         int lane, unsigned long long& entries)
+{
+    const int P = tm.last();
+    int tau = tm.next(1);
+    int rank = 0;
+    {
+        const int hi = L - tau + 1;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const int i = 1 + lane + 64 * s;
+            if (i <= hi) D[i] = U[i];
+        }
+        entries += (unsigned long long)hi;
+        wave_sync();
+        if (tau == 1) {
+            if (lane == 0) Wout[by_pp ? 1 : 0] = D[L];
+            ++rank;
+            tau = tm.next(2);
+        }
+    }
+    int jp0 = 0, jp1 = 0;
+    for (int k = 2; k <= P; ++k) {
+        const int hi = L - tau + k;
+        if (hi >= 65) dp_entry(U, D, k, hi, 65 + lane, jp1);   // high half first: in-place update
+        if (k <= 64) dp_entry(U, D, k, hi, 1 + lane, jp0);
+        entries += (unsigned long long)(hi - k + 1);
+        wave_sync();
+        if (k == tau) {
+            if (lane == 0) Wout[by_pp ? k : rank] = D[L];
+            ++rank;
+            tau = tm.next(k + 1);
+        }
+    }
+    wave_sync();
+}
+
+// Canonical cuts for degree pp and bottleneck W: c_pp = L and, right to left,
+// c_k = max(k, next(c_{k+1})) with next(e) the smallest c such that
+// U_e - U_c <= W.  Stage s = lane + 64*h holds layers [st_h, en_h).
 struct Stages {
     int st0, st1, en0, en1;
 };
 
+// Record value v for stage `stage` in the lane that owns it (pure selects:
+// no indexed register arrays).
 __device__ __forceinline__ void put_stage_start(Stages& r, int lane, int stage, int v)
 {
-    if (stage < 64) { if (lane == stage) r.st0 = v; }
-    else if (lane == stage - 64) r.st1 = v;
+    const bool mine = lane == (stage & 63);
+    const bool high = stage >= 64;
+    r.st0 = (mine && !high) ? v : r.st0;
+    r.st1 = (mine && high) ? v : r.st1;
 }
 
 __device__ __forceinline__ void put_stage_end(Stages& r, int lane, int stage, int v)
 {
-    if (stage < 64) { if (lane == stage) r.en0 = v; }
-    else if (lane == stage - 64) r.en1 = v;
+    const bool mine = lane == (stage & 63);
+    const bool high = stage >= 64;
+    r.en0 = (mine && !high) ? v : r.en0;
+    r.en1 = (mine && high) ? v : r.en1;
 }
 
-__device__ Stages canonical_stages(const Lds& S, int lane, int L, int pp, double W)
+__device__ Stages canonical_stages(const double* U, int lane, int L, int pp, double W)
 {
     int nx0 = 0, nx1 = 0;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const int e = 1 + lane + 64 * s;
         if (e <= L) {
-            const double Ue = S.U[e];
+            const double Ue = U[e];
             int lo = 0, hi = e - 1;
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
-                if (Ue - S.U[mid] <= W) hi = mid; else lo = mid + 1;
+                if (Ue - U[mid] <= W) hi = mid; else lo = mid + 1;
             }
             if (s == 0) nx0 = lo; else nx1 = lo;
         }
@@ -220,178 +376,199 @@ __device__ Stages canonical_stages(const Lds& S, int lane, int L, int pp, double
     return r;
 }
 
-// Price every admissible microbatch count of plan (dp, tp, pp) given the
-// canonical stages; appends to the cell's plan buffer.
-__device__ void price_target(Lds& S, int lane, const JobCtx& jb, const TypeDev& ty,
-                             const Cell& cell, int tp, int pp, double W, int& np,
-                             const EstimateArgs& A, unsigned long long& overflow)
+// Price every admissible microbatch count of plan (dp, tp, pp) with the
+// canonical stages of bottleneck W; appends to the wave's plan buffer.
+template <int SLOTS>
+__device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane,
+                             const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
+                             double W, int& np, const EstimateArgs& A, unsigned long long& overflow)
 {
-    const Stages sg = canonical_stages(S, lane, jb.L, pp, W);
-
+    const Stages sg = canonical_stages(U, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
     const double B_dp = (grp <= ty.gpn && ty.gpn % grp == 0) ? ty.bw_intra : ty.bw_inter;
 
-    double Sk[2], Pk[2], Ak[2], xk[2];
-    bool act[2];
-    double pmax = 0.0;
+    double Pk[2], Ak[2];
+    double red[2] = {0.0, 0.0};   // sum of boundary activations, largest stage parameters
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const int stage = lane + 64 * s;
-        act[s] = stage < pp;
-        Sk[s] = Pk[s] = Ak[s] = xk[s] = 0.0;
-        if (act[s]) {
+        Pk[s] = Ak[s] = 0.0;
+        if (stage < pp) {
             const int lo = s == 0 ? sg.st0 : sg.st1;
             const int hi = s == 0 ? sg.en0 : sg.en1;
-            Sk[s] = S.U[hi] - S.U[lo];
-            Pk[s] = S.Pp[hi] - S.Pp[lo];
-            Ak[s] = S.Ap[hi] - S.Ap[lo];
-            xk[s] = (stage < pp - 1) ? (double)S.x[hi - 1] : 0.0;
-            pmax = fmax(pmax, Pk[s]);
+            Pk[s] = B.Pp[hi] - B.Pp[lo];
+            Ak[s] = B.Ap[hi] - B.Ap[lo];
+            if (stage < pp - 1) red[0] += (double)B.x[hi - 1];
+            red[1] = fmax(red[1], Pk[s]);
         }
     }
-    pmax = wave_max(pmax);
+    {
+        double sx[1] = {red[0]}, pm[1] = {red[1]};
+        wave_reduce<OpSum, 1>(sx);
+        wave_reduce<OpMax, 1>(pm);
+        red[0] = sx[0];
+        red[1] = pm[0];
+    }
+    const double sumX = red[0];
+    const double sumS = U[jb.L];   // the stages tile the layers: sum of stage costs
     const double ar = (dp > 1)
-        ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp * (pmax / (double)tp) / B_dp
+        ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp * (red[1] / (double)tp) / B_dp
         : 0.0;
 
-    for (int mi = 0; mi < A.n_m; ++mi) {
-        const int m = A.m_values[mi];
-        if (jb.Bg % (dp * m) != 0) continue;
-        const double b = (double)jb.Bg / (double)(dp * m);
-        double fill = 0.0, mem = 0.0;
+    constexpr int kChunk = 4;
+    for (int m0 = 0; m0 < A.n_m; m0 += kChunk) {
+        double mem[kChunk];
+        bool ok[kChunk];
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            if (!act[s]) continue;
-            const int stage = lane + 64 * s;
-            const double Wk = b * Sk[s];
-            const double p2p = (stage < pp - 1) ? cell.kappa * 2.0 * b * xk[s] / cell.B_pp : 0.0;
-            fill += Wk + p2p;
-            const int inflight = m < pp - stage ? m : pp - stage;
-            const double Mk = 4.0 * Pk[s] / (double)tp + (double)inflight * b * Ak[s] / (double)tp;
-            mem = fmax(mem, Mk);
-        }
-        fill = wave_sum(fill);
-        mem = wave_max(mem);
-        const double wmax = b * W;
-        const double T = fill + (double)(m - 1) * wmax + ar;
-        if (np < kMaxPlans) {
-            if (lane == 0) {
-                S.planT[np] = (mem <= ty.mem) ? T : kInf;
-                S.planW[np] = W;
-                S.planKey[np] = ((unsigned)pp << 16) | ((unsigned)tp << 8) | (unsigned)m;
-            }
-            ++np;
-        } else {
-            overflow = 1;
-        }
-    }
-}
-
-// Solve one partition problem: the recursion D_k(i) = min over j of
-// max(D_{k-1}(j), U_i - U_j), row by row, lanes over i.  The crossing j where
-// D_{k-1}(j) >= U_i - U_j first holds never moves left as i or k grows, so
-// each lane keeps its crossing from row to row and only walks it forward.
-// Row k is evaluated for i in [k, L - tau(k) + k] only, tau(k) being the
-// smallest requested degree >= k (larger i cannot reach a requested cell).
-__device__ void solve_problem(Lds& S, int lane, const JobCtx& jb, const TypeDev& ty,
-                              const Cell& cell, int tp, int nt, int& np,
-                              const EstimateArgs& A, unsigned long long& dp_entries,
-                              unsigned long long& overflow)
-{
-    const int L = jb.L;
-    double* Dp = S.D[0];
-    double* Dc = S.D[1];
-    int ti = 0;
-    int tau = S.tg[0];
-    const int P = S.tg[nt - 1];
-    int jp[2] = {0, 0};
-
-    // row 1
-    {
-        const int hi = L - tau + 1;
+        for (int c = 0; c < kChunk; ++c) {
+            mem[c] = 0.0;
+            const int mi = m0 + c;
+            ok[c] = mi < A.n_m && (jb.Bg % (dp * A.m_values[mi < A.n_m ? mi : 0]) == 0);
+            if (!ok[c]) continue;
+            const int m = A.m_values[mi];
+            const double b = (double)jb.Bg / (double)(dp * m);
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int i = 1 + lane + 64 * s;
-            if (i <= hi) Dc[i] = S.U[i];
-        }
-        dp_entries += (unsigned long long)hi;
-        sync();
-        double* tmp = Dp; Dp = Dc; Dc = tmp;
-        if (tau == 1) {
-            price_target(S, lane, jb, ty, cell, tp, 1, Dp[L], np, A, overflow);
-            ++ti;
-            tau = ti < nt ? S.tg[ti] : 0;
-        }
-    }
-    for (int k = 2; k <= P; ++k) {
-        const int hi = L - tau + k;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int i = 1 + lane + 64 * s;
-            if (i >= k && i <= hi) {
-                const double Ui = S.U[i];
-                int j = jp[s] > k - 1 ? jp[s] : k - 1;
-                while (j < i) {
-                    if (Dp[j] >= Ui - S.U[j]) break;
-                    ++j;
+            for (int s = 0; s < 2; ++s) {
+                const int stage = lane + 64 * s;
+                if (stage < pp) {
+                    const int inflight = m < pp - stage ? m : pp - stage;
+                    const double Mk = 4.0 * Pk[s] / (double)tp + (double)inflight * b * Ak[s] / (double)tp;
+                    mem[c] = fmax(mem[c], Mk);
                 }
-                jp[s] = j;
-                double v = (j < i) ? Dp[j] : kInf;
-                if (j - 1 >= k - 1) v = fmin(v, Ui - S.U[j - 1]);
-                Dc[i] = v;
             }
         }
-        dp_entries += (unsigned long long)(hi - k + 1);
-        sync();
-        double* tmp = Dp; Dp = Dc; Dc = tmp;
-        if (k == tau) {
-            price_target(S, lane, jb, ty, cell, tp, k, Dp[L], np, A, overflow);
-            ++ti;
-            tau = ti < nt ? S.tg[ti] : 0;
+        wave_reduce<OpMax, kChunk>(mem);
+#pragma unroll
+        for (int c = 0; c < kChunk; ++c) {
+            if (!ok[c]) continue;
+            const int m = A.m_values[m0 + c];
+            const double b = (double)jb.Bg / (double)(dp * m);
+            const double fill = b * sumS + cell.kappa * 2.0 * b * sumX / cell.B_pp;
+            const double T = fill + (double)(m - 1) * (b * W) + ar;
+            if (np < kMaxPlans) {
+                if (lane == 0) {
+                    Wv.planT[np] = (mem[c] <= ty.mem) ? T : kInf;
+                    Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
+                }
+                ++np;
+            } else {
+                overflow = 1;
+            }
         }
     }
-    sync();
 }
 
-__global__ __launch_bounds__(64) void estimate_kernel(EstimateArgs A)
+// ------------------------------------------------------------ the kernel
+
+template <int SLOTS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
 {
-    __shared__ Lds S;
-    const int lane = threadIdx.x;
-    const int item = blockIdx.x;
+    __shared__ BlockLds<SLOTS> B;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    WaveLds& Wv = B.w[wid];
+
+    const int item = A.item_order[blockIdx.x];
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
-
     const int off = A.layer_offset[j];
     JobCtx jb;
     jb.L = A.layer_offset[j + 1] - off;
     jb.Bg = A.batch[j];
     const TypeDev ty = A.types[g];
 
-    // stage the job
+    // ---- stage the job
     bool has_q = false;
-    double pv[2] = {0.0, 0.0}, av[2] = {0.0, 0.0};
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int l = lane + 64 * s;
-        if (l < jb.L) {
-            S.t[l] = A.t[off + l];
-            S.x[l] = A.x[off + l];
-            const float qv = A.q[off + l];
-            S.q[l] = qv;
-            has_q |= qv > 0.0f;
-            pv[s] = (double)A.p[off + l];
-            av[s] = (double)A.a[off + l];
+    if (tid < jb.L) {
+        B.t[tid] = A.t[off + tid];
+        B.x[tid] = A.x[off + tid];
+        const float qv = A.q[off + tid];
+        B.q[tid] = qv;
+        has_q = qv > 0.0f;
+    }
+    jb.moe = __syncthreads_or(has_q) != 0;
+    if (wid == 0 || wid == 1) {
+        const float* src = (wid == 0 ? A.p : A.a) + off;
+        const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
+        const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
+        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap);
+    } else if (wid == 2) {
+        build_prefix_u(B.t, B.x, B.q, B.Upure, lane, jb, ty, 1.0, 1, false);
+    } else {
+        bool same = true;
+        for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
+        const bool uni = __ballot(!same) == 0ull;
+        if (lane == 0) {
+            B.uniform = uni ? 1 : 0;
+            B.next_cell = 0;
+            B.moe = jb.moe ? 1 : 0;
         }
     }
-    jb.moe = __ballot(has_q) != 0ull;
-    seq_prefix(pv[0], pv[1], jb.L, lane, S.Pp);
-    seq_prefix(av[0], av[1], jb.L, lane, S.Ap);
-    sync();
+    // admissible data-parallel degrees: dp*m divides the batch for a listed m
+    for (int base = 0; base < kMaxDp; base += 256) {
+        const int dp = base + tid + 1;
+        bool ok = false;
+        for (int i = 0; i < A.n_m; ++i) ok |= (jb.Bg % (dp * A.m_values[i])) == 0;
+        const unsigned long long bits = __ballot(ok);
+        if (lane == 0) {
+            B.adm[(base + 64 * wid) >> 5] = (uint32_t)(bits & 0xffffffffull);
+            B.adm[((base + 64 * wid) >> 5) + 1] = (uint32_t)(bits >> 32);
+        }
+    }
+    __syncthreads();
+
+    // ---- shared problems: the pure-compute one, and every tensor degree when
+    // the type's contention factor is the same for all counts
+    if (tid == 0) {
+        int ns = 0;
+        B.slot_tp[ns] = 1;
+        B.slot_var[ns] = jb.moe ? 1 : 0;
+        ++ns;
+        if (SLOTS > 1 && A.share_tp && B.uniform) {
+            for (int tp = 1; tp <= ty.gpn && ns < SLOTS; ++tp) {
+                if (ty.gpn % tp != 0 || (tp == 1 && !jb.moe)) continue;
+                B.slot_tp[ns] = tp;
+                B.slot_var[ns] = 0;
+                ++ns;
+            }
+        }
+        B.n_slots = ns;
+    }
+    __syncthreads();
+    const int n_slots = B.n_slots;
 
     unsigned long long n_plans = 0, n_problems = 0, dp_entries = 0, n_infeasible = 0, overflow = 0;
 
-    for (int ci = 0; ci < A.n_counts; ++ci) {
+    for (int s = wid; s < n_slots; s += kWavesPerBlock) {
+        const int tp = B.slot_tp[s], var = B.slot_var[s];
+        bool ok0 = false, ok1 = false;
+        for (int c = 0; c < A.n_counts; ++c) {
+            const int n = A.counts[c];
+            if (n % tp != 0) continue;
+            ok0 |= target_ok(B.adm, jb, n, tp, var, 1 + lane);
+            ok1 |= target_ok(B.adm, jb, n, tp, var, 65 + lane);
+        }
+        const Mask tm = ballot_mask(ok0, ok1);
+        if (tm.count() == 0) continue;
+        const double* U = B.Upure;
+        if (s > 0) {
+            build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp, true);
+            U = Wv.U;
+        }
+        solve_dp(U, Wv.D, jb.L, tm, B.Wtab[s], true, lane, dp_entries);
+        ++n_problems;
+    }
+    __syncthreads();
+
+    // ---- cells: take counts, largest first, from the block's work counter
+    for (;;) {
+        int cix = 0;
+        if (lane == 0) cix = atomicAdd(&B.next_cell, 1);
+        cix = __builtin_amdgcn_readfirstlane(cix);
+        if (cix >= A.n_counts) break;
+        const int ci = A.count_order[cix];
         Cell cell;
         cell.n = A.counts[ci];
         cell.kappa = (double)A.kappa[g * A.n_counts + ci];
@@ -401,21 +578,41 @@ __global__ __launch_bounds__(64) void estimate_kernel(EstimateArgs A)
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
         for (int tp = 1; tp <= tpmax; ++tp) {
             if (cell.n % tp != 0 || ty.gpn % tp != 0) continue;
-            for (int variant = 0; variant < 2; ++variant) {
-                if (variant == 1 && !(jb.moe && tp == 1)) break;
-                const int nt = build_targets(S, lane, jb, cell.n, tp, variant, A);
-                if (nt == 0) continue;
-                build_prefix_u(S, lane, jb, ty, cell.kappa, tp, variant == 0);
-                solve_problem(S, lane, jb, ty, cell, tp, nt, np, A, dp_entries, overflow);
-                ++n_problems;
+            for (int var = 0; var < 2; ++var) {
+                if (var == 1 && !(jb.moe && tp == 1)) break;
+                const Mask tm = ballot_mask(target_ok(B.adm, jb, cell.n, tp, var, 1 + lane),
+                                            target_ok(B.adm, jb, cell.n, tp, var, 65 + lane));
+                if (tm.count() == 0) continue;
+                // shared problem?
+                int slot = -1;
+                if (tp == 1 && (var == 1 || !jb.moe)) slot = 0;
+                else
+                    for (int s = 1; s < n_slots; ++s)
+                        if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
+                const double* U;
+                if (slot == 0) {
+                    U = B.Upure;
+                } else {
+                    build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, cell.kappa, tp, var == 0);
+                    U = Wv.U;
+                }
+                if (slot < 0) {
+                    solve_dp(U, Wv.D, jb.L, tm, Wv.Wt, false, lane, dp_entries);
+                    ++n_problems;
+                }
+                int rank = 0;
+                for (int pp = tm.next(1); pp; pp = tm.next(pp + 1), ++rank) {
+                    const double W = slot >= 0 ? B.Wtab[slot][pp] : Wv.Wt[rank];
+                    price_target(B, Wv, U, lane, jb, ty, cell, tp, pp, W, np, A, overflow);
+                }
             }
         }
-        sync();
+        wave_sync();
 
         // best plan of the cell: smallest key among plans within the tie window
         double tl = kInf;
-        for (int e = lane; e < np; e += 64) tl = fmin(tl, S.planT[e]);
-        const double tmin = wave_min(tl);
+        for (int e = lane; e < np; e += 64) tl = fmin(tl, Wv.planT[e]);
+        const double tmin = wave_reduce1<OpMin>(tl);
         const long long cidx = ((long long)j * A.n_types + g) * A.n_counts + ci;
         n_plans += (unsigned long long)np;
         if (!(tmin < kInf)) {
@@ -429,23 +626,23 @@ __global__ __launch_bounds__(64) void estimate_kernel(EstimateArgs A)
                 uint8_t* row = A.cuts + cidx * A.cuts_stride;
                 for (int e = lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
             }
-            sync();
+            wave_sync();
             continue;
         }
         const double lim = tmin * (1.0 + A.tie_eps);
-        unsigned kl = 0xFFFFFFFFu;
+        double kl = kInf;
         for (int e = lane; e < np; e += 64)
-            if (S.planT[e] <= lim) kl = S.planKey[e] < kl ? S.planKey[e] : kl;
-        const unsigned kbest = wave_min_u(kl);
-        int il = -1;
+            if (Wv.planT[e] <= lim) kl = fmin(kl, (double)Wv.planKey[e]);
+        const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
+        double il = -1.0;
         for (int e = lane; e < np; e += 64)
-            if (S.planKey[e] == kbest) il = e;
-        const int ib = wave_max_i(il);
-        const double Tb = S.planT[ib];
-        const double Wb = S.planW[ib];
-        const int pp = (int)(kbest >> 16);
-        const int tp = (int)((kbest >> 8) & 0xFFu);
-        const int m = (int)(kbest & 0xFFu);
+            if (Wv.planKey[e] == kbest) il = (double)e;
+        int ib = (int)wave_reduce1<OpMax>(il);
+        ib = ib < 0 ? 0 : (ib >= np ? np - 1 : ib);
+        const double Tb = Wv.planT[ib];
+        const int pp = (int)(kbest >> 12);
+        const int tp = (int)((kbest >> 7) & 0x1Fu);
+        const int m = (int)(kbest & 0x7Fu);
         const int dp = cell.n / (tp * pp);
         if (lane == 0) {
             A.t_iter[cidx] = (float)Tb;
@@ -454,9 +651,32 @@ __global__ __launch_bounds__(64) void estimate_kernel(EstimateArgs A)
                            ((unsigned)m << 24) | (1u << 31);
         }
         if (A.cuts) {
-            const bool a2a_on = !jb.moe || dp * tp > 1;
-            build_prefix_u(S, lane, jb, ty, cell.kappa, tp, a2a_on);
-            const Stages sg = canonical_stages(S, lane, jb.L, pp, Wb);
+            // re-derive the winner's bottleneck and cuts
+            const int var = (jb.moe && dp * tp == 1) ? 1 : 0;
+            int slot = -1;
+            if (tp == 1 && (var == 1 || !jb.moe)) slot = 0;
+            else
+                for (int s = 1; s < n_slots; ++s)
+                    if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
+            const double* U;
+            if (slot == 0) {
+                U = B.Upure;
+            } else {
+                build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, cell.kappa, tp, var == 0);
+                U = Wv.U;
+            }
+            double W;
+            if (slot >= 0) {
+                W = B.Wtab[slot][pp];
+            } else {
+                Mask one;
+                one.lo = pp <= 64 ? (1ull << (pp - 1)) : 0ull;
+                one.hi = pp > 64 ? (1ull << (pp - 65)) : 0ull;
+                unsigned long long scratch_entries = 0;
+                solve_dp(U, Wv.D, jb.L, one, Wv.Wt, false, lane, scratch_entries);
+                W = Wv.Wt[0];
+            }
+            const Stages sg = canonical_stages(U, lane, jb.L, pp, W);
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
@@ -466,11 +686,11 @@ __global__ __launch_bounds__(64) void estimate_kernel(EstimateArgs A)
             }
             for (int e = 128 + lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
         }
-        sync();
+        wave_sync();
     }
 
     if (lane == 0) {
-        atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
+        if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
         atomicAdd(&A.counters[kPlans], n_plans);
         atomicAdd(&A.counters[kProblems], n_problems);
         atomicAdd(&A.counters[kDpEntries], dp_entries);
@@ -508,7 +728,10 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
 {
     const long long blocks = (long long)args.n_jobs * args.n_types;
     if (blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(estimate_kernel, dim3((unsigned)blocks), dim3(64), 0, stream, args);
+    if (args.share_tp)
+        hipLaunchKernelGGL(estimate_kernel<kSlotsShared>, dim3((unsigned)blocks), dim3(256), 0, stream, args);
+    else
+        hipLaunchKernelGGL(estimate_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, stream, args);
     return hipGetLastError();
 }
 
