@@ -159,6 +159,7 @@ struct Cell {
     int n;          // GPUs of the cell
     double kappa;   // contention factor of the grid
     double B_pp;    // link between pipeline neighbours
+    double c_p2p;   // kappa 2 / B_pp: p2p seconds per byte and sample, both directions
 };
 
 // Per-sample cost of each layer (formula in arena.h), prefix-summed into U.
@@ -243,30 +244,39 @@ __device__ __forceinline__ Mask ballot_mask(bool ok0, bool ok1)
 // One lane of row k of the recursion D_k(i) = min_j max(D_{k-1}(j), U_i - U_j)
 // (D holds row k-1 and receives row k in place).  The crossing j -- the first
 // j with D_{k-1}(j) >= U_i - U_j -- never moves left as i or k grows, so the
-// lane starts from its previous crossing, gallops and then bisects.
+// lane starts from its previous crossing: usually the crossing is right there
+// (one probe); otherwise it gallops and then bisects.
 __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int& jp)
 {
-    const bool act = i >= k && i <= hi;
+    const bool act = i <= hi;
     double v = 0.0;
     if (act) {
         const double Ui = U[i];
-        int a = jp > k - 1 ? jp : k - 1;   // every j < a fails
-        int b = i;                         // crossing <= b (b = i: none)
-        int step = 1;
-        while (a < b) {
-            int p = a + step - 1;
-            p = p < b - 1 ? p : b - 1;
-            if (D[p] >= Ui - U[p]) { b = p; break; }
-            a = p + 1;
-            step <<= 1;
-        }
-        while (a < b) {
-            const int mid = (a + b) >> 1;
-            if (D[mid] >= Ui - U[mid]) b = mid; else a = mid + 1;
+        int a = jp > k - 1 ? jp : k - 1;   // every j < a fails; a <= i - 1
+        double da = D[a];
+        double ua = U[a];
+        double um = U[a - 1];              // a >= 1
+        if (!(da >= Ui - ua)) {
+            // slow path: crossing in (a, i]
+            int lo = a + 1, b = i, step = 1;
+            while (lo < b) {
+                int p = lo + step - 1;
+                p = p < b - 1 ? p : b - 1;
+                if (D[p] >= Ui - U[p]) { b = p; break; }
+                lo = p + 1;
+                step <<= 1;
+            }
+            while (lo < b) {
+                const int mid = (lo + b) >> 1;
+                if (D[mid] >= Ui - U[mid]) b = mid; else lo = mid + 1;
+            }
+            a = lo;
+            da = (a < i) ? D[a] : kInf;
+            um = U[a - 1];
         }
         jp = a;
-        v = (a < i) ? D[a] : kInf;
-        if (a - 1 >= k - 1) v = fmin(v, Ui - U[a - 1]);
+        v = da;
+        if (a - 1 >= k - 1) v = fmin(v, Ui - um);
     }
     // every lane has read row k-1 before any lane overwrites it
     __asm__ volatile("" ::: "memory");
@@ -276,7 +286,9 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
 // Bottleneck W*(pp) for every degree in `tm`, written to Wout[pp] (by_pp) or
 // Wout[rank of pp].  Row k is evaluated for i in [k, L - tau(k) + k] only,
 // tau(k) the smallest requested degree >= k: larger i cannot reach a
-// requested cell.
+// requested cell.  Lane l of row k takes i = k + l (+64): the window width
+// never grows with k, so after the first rows one pass covers a row, and a
+// lane's crossing from row k-1 (for i-1) is a lower bound for row k.
 __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, double* Wout, bool by_pp,
                          int lane, unsigned long long& entries)
 {
@@ -301,8 +313,8 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
     int jp0 = 0, jp1 = 0;
     for (int k = 2; k <= P; ++k) {
         const int hi = L - tau + k;
-        if (hi >= 65) dp_entry(U, D, k, hi, 65 + lane, jp1);   // high half first: in-place update
-        if (k <= 64) dp_entry(U, D, k, hi, 1 + lane, jp0);
+        if (hi - k >= 64) dp_entry(U, D, k, hi, k + 64 + lane, jp1);   // high part first: in place
+        dp_entry(U, D, k, hi, k + lane, jp0);
         entries += (unsigned long long)(hi - k + 1);
         wave_sync();
         if (k == tau) {
@@ -316,28 +328,11 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
 
 // Canonical cuts for degree pp and bottleneck W: c_pp = L and, right to left,
 // c_k = max(k, next(c_{k+1})) with next(e) the smallest c such that
-// U_e - U_c <= W.  Stage s = lane + 64*h holds layers [st_h, en_h).
+// U_e - U_c <= W.  Returns the bounds of stage s = lane + 64h as
+// [lo_h, hi_h) = [c_s, c_{s+1}).
 struct Stages {
-    int st0, st1, en0, en1;
+    int lo0, lo1, hi0, hi1;
 };
-
-// Record value v for stage `stage` in the lane that owns it (pure selects:
-// no indexed register arrays).
-__device__ __forceinline__ void put_stage_start(Stages& r, int lane, int stage, int v)
-{
-    const bool mine = lane == (stage & 63);
-    const bool high = stage >= 64;
-    r.st0 = (mine && !high) ? v : r.st0;
-    r.st1 = (mine && high) ? v : r.st1;
-}
-
-__device__ __forceinline__ void put_stage_end(Stages& r, int lane, int stage, int v)
-{
-    const bool mine = lane == (stage & 63);
-    const bool high = stage >= 64;
-    r.en0 = (mine && !high) ? v : r.en0;
-    r.en1 = (mine && high) ? v : r.en1;
-}
 
 __device__ Stages canonical_stages(const double* U, int lane, int L, int pp, double W)
 {
@@ -345,7 +340,7 @@ __device__ Stages canonical_stages(const double* U, int lane, int L, int pp, dou
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const int e = 1 + lane + 64 * s;
-        if (e <= L) {
+        if (e <= L && pp > 1) {
             const double Ue = U[e];
             int lo = 0, hi = e - 1;
             while (lo < hi) {
@@ -355,24 +350,37 @@ __device__ Stages canonical_stages(const double* U, int lane, int L, int pp, dou
             if (s == 0) nx0 = lo; else nx1 = lo;
         }
     }
-    Stages r = {0, 0, 0, 0};
-    put_stage_end(r, lane, pp - 1, L);      // stage 0 starts at 0 (already 0)
+    // c_k lives in lane k & 63 of cA (k < 64) or cB (k >= 64); c_0 = 0, c_pp = L
+    int cA = 0, cB = 0;
+    cA = (pp < 64 && lane == pp) ? L : cA;
+    cB = (pp >= 64 && lane == pp - 64) ? L : cB;
     int cur = L;
     for (int k = pp - 1; k >= 1; --k) {
         const int e = cur - 1;
-        const int nxt = (e < 64) ? __builtin_amdgcn_readlane(nx0, e)
-                                 : __builtin_amdgcn_readlane(nx1, e - 64);
+        const int na = __builtin_amdgcn_readlane(nx0, e & 63);
+        const int nb = __builtin_amdgcn_readlane(nx1, e & 63);
+        const int nxt = e < 64 ? na : nb;
         const int c = nxt > k ? nxt : k;
-        put_stage_start(r, lane, k, c);
-        put_stage_end(r, lane, k - 1, c);
+        cA = (k < 64 && lane == k) ? c : cA;
+        cB = (k >= 64 && lane == k - 64) ? c : cB;
         cur = c;
         if (c == k) {
             // every earlier stage holds exactly one layer
-            if (lane < k) { r.st0 = lane; r.en0 = lane + 1; }
-            if (lane + 64 < k) { r.st1 = lane + 64; r.en1 = lane + 65; }
+            cA = lane < k ? lane : cA;
+            cB = lane + 64 < k ? lane + 64 : cB;
             break;
         }
     }
+    // stage s ends where stage s+1 starts: the next lane's cut
+    const int nA = __shfl_down(cA, 1, 64);
+    const int nB = __shfl_down(cB, 1, 64);
+    const int b0 = __builtin_amdgcn_readlane(cB, 0);
+    const int b1 = pp == 128 ? L : 0;
+    Stages r;
+    r.lo0 = cA;
+    r.hi0 = lane == 63 ? b0 : nA;
+    r.lo1 = cB;
+    r.hi1 = lane == 63 ? b1 : nB;
     return r;
 }
 
@@ -388,73 +396,52 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
     const int grp = dp * tp;
     const double B_dp = (grp <= ty.gpn && ty.gpn % grp == 0) ? ty.bw_intra : ty.bw_inter;
 
-    double Pk[2], Ak[2];
-    double red[2] = {0.0, 0.0};   // sum of boundary activations, largest stage parameters
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int stage = lane + 64 * s;
-        Pk[s] = Ak[s] = 0.0;
-        if (stage < pp) {
-            const int lo = s == 0 ? sg.st0 : sg.st1;
-            const int hi = s == 0 ? sg.en0 : sg.en1;
-            Pk[s] = B.Pp[hi] - B.Pp[lo];
-            Ak[s] = B.Ap[hi] - B.Ap[lo];
-            if (stage < pp - 1) red[0] += (double)B.x[hi - 1];
-            red[1] = fmax(red[1], Pk[s]);
-        }
+    // per-stage parameter and activation bytes of the lane's stages
+    const bool act0 = lane < pp, act1 = lane + 64 < pp;
+    double P0 = 0.0, A0 = 0.0, P1 = 0.0, A1 = 0.0, sx = 0.0;
+    if (act0) {
+        P0 = B.Pp[sg.hi0] - B.Pp[sg.lo0];
+        A0 = B.Ap[sg.hi0] - B.Ap[sg.lo0];
+        if (lane < pp - 1) sx = (double)B.x[sg.hi0 - 1];
     }
-    {
-        double sx[1] = {red[0]}, pm[1] = {red[1]};
-        wave_reduce<OpSum, 1>(sx);
-        wave_reduce<OpMax, 1>(pm);
-        red[0] = sx[0];
-        red[1] = pm[0];
+    if (act1) {
+        P1 = B.Pp[sg.hi1] - B.Pp[sg.lo1];
+        A1 = B.Ap[sg.hi1] - B.Ap[sg.lo1];
+        if (lane + 64 < pp - 1) sx += (double)B.x[sg.hi1 - 1];
     }
-    const double sumX = red[0];
+    double rs[1] = {sx}, rm[1] = {fmax(P0, P1)};
+    wave_reduce<OpSum, 1>(rs);
+    wave_reduce<OpMax, 1>(rm);
+    const double sumX = rs[0];
+    const double pmax = rm[0];
     const double sumS = U[jb.L];   // the stages tile the layers: sum of stage costs
     const double ar = (dp > 1)
-        ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp * (red[1] / (double)tp) / B_dp
+        ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp * (pmax / (double)tp) / B_dp
         : 0.0;
+    const double per_sample = sumS + cell.c_p2p * sumX;   // fill time per sample
+    const double cap = ty.mem * (double)tp;                // memory test scaled by tp
+    const double fP0 = 4.0 * P0, fP1 = 4.0 * P1;
+    const int r0 = pp - lane, r1 = pp - lane - 64;         // stages from the lane's to the last
 
-    constexpr int kChunk = 4;
-    for (int m0 = 0; m0 < A.n_m; m0 += kChunk) {
-        double mem[kChunk];
-        bool ok[kChunk];
-#pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
-            mem[c] = 0.0;
-            const int mi = m0 + c;
-            ok[c] = mi < A.n_m && (jb.Bg % (dp * A.m_values[mi < A.n_m ? mi : 0]) == 0);
-            if (!ok[c]) continue;
-            const int m = A.m_values[mi];
-            const double b = (double)jb.Bg / (double)(dp * m);
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                const int stage = lane + 64 * s;
-                if (stage < pp) {
-                    const int inflight = m < pp - stage ? m : pp - stage;
-                    const double Mk = 4.0 * Pk[s] / (double)tp + (double)inflight * b * Ak[s] / (double)tp;
-                    mem[c] = fmax(mem[c], Mk);
-                }
+    for (int mi = 0; mi < A.n_m; ++mi) {
+        const int m = A.m_values[mi];
+        const int dm = dp * m;
+        if (jb.Bg % dm != 0) continue;
+        const double b = (double)(jb.Bg / dm);             // exact: dm divides the batch
+        // memory: 4 P_k + min(m, pp-k) b A_k <= mem tp on every stage
+        const double i0 = (double)(m < r0 ? m : r0) * b;
+        const double i1 = (double)(m < r1 ? m : r1) * b;
+        const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
+        const bool fits = __ballot(over) == 0ull;
+        const double T = b * per_sample + (double)(m - 1) * (b * W) + ar;
+        if (np < kMaxPlans) {
+            if (lane == 0) {
+                Wv.planT[np] = fits ? T : kInf;
+                Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
             }
-        }
-        wave_reduce<OpMax, kChunk>(mem);
-#pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
-            if (!ok[c]) continue;
-            const int m = A.m_values[m0 + c];
-            const double b = (double)jb.Bg / (double)(dp * m);
-            const double fill = b * sumS + cell.kappa * 2.0 * b * sumX / cell.B_pp;
-            const double T = fill + (double)(m - 1) * (b * W) + ar;
-            if (np < kMaxPlans) {
-                if (lane == 0) {
-                    Wv.planT[np] = (mem[c] <= ty.mem) ? T : kInf;
-                    Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
-                }
-                ++np;
-            } else {
-                overflow = 1;
-            }
+            ++np;
+        } else {
+            overflow = 1;
         }
     }
 }
@@ -573,6 +560,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         cell.n = A.counts[ci];
         cell.kappa = (double)A.kappa[g * A.n_counts + ci];
         cell.B_pp = (cell.n <= ty.gpn) ? ty.bw_intra : ty.bw_inter;
+        cell.c_p2p = cell.kappa * 2.0 / cell.B_pp;
         int np = 0;
 
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
@@ -681,7 +669,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
                 const int idx = lane + 64 * s;
-                const int en = s == 0 ? sg.en0 : sg.en1;
+                const int en = s == 0 ? sg.hi0 : sg.hi1;
                 if (idx < A.cuts_stride) row[idx] = (idx < pp - 1) ? (uint8_t)en : (uint8_t)0xFF;
             }
             for (int e = 128 + lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
