@@ -29,8 +29,8 @@ constexpr double kInf = __builtin_huge_val();
 constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree problems
 
 struct WaveLds {
-    double U[kLmax + 1];          // cost prefix of the wave's current problem
-    double D[kLmax + 1];          // partition recursion row, updated in place
+    double U[kLmax + 8];          // cost prefix of the wave's current problem (padded for probes)
+    double D[kLmax + 8];          // partition recursion row, updated in place (padded for probes)
     double Wt[kMaxTargets];       // bottleneck per requested degree (by rank)
     double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
     uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
@@ -43,7 +43,7 @@ struct BlockLds {
     float q[kLmax];
     double Pp[kLmax + 1];         // prefix of parameter bytes
     double Ap[kLmax + 1];         // prefix of activation bytes
-    double Upure[kLmax + 1];      // prefix of the pure-compute per-sample cost
+    double Upure[kLmax + 8];      // prefix of the pure-compute per-sample cost (padded for probes)
     double Wtab[SLOTS][kLmax + 1];// bottleneck of each shared problem, by degree
     uint32_t adm[kMaxDp / 32];    // bit dp-1: some listed m has dp*m dividing the batch
     int32_t slot_tp[SLOTS];
@@ -241,24 +241,41 @@ __device__ __forceinline__ Mask ballot_mask(bool ok0, bool ok1)
 
 // ------------------------------------------------------------ partition
 
+// DPP lane shift: lane l receives lane l+1's value (lane 63 keeps `last`).
+__device__ __forceinline__ int from_next_lane(int v, int last)
+{
+    return __builtin_amdgcn_update_dpp(last, v, 0x130, 0xf, 0xf, false);   // wave_shl:1
+}
+
 // One lane of row k of the recursion D_k(i) = min_j max(D_{k-1}(j), U_i - U_j)
-// (D holds row k-1 and receives row k in place).  The crossing j -- the first
-// j with D_{k-1}(j) >= U_i - U_j -- never moves left as i or k grows, so the
-// lane starts from its previous crossing: usually the crossing is right there
-// (one probe); otherwise it gallops and then bisects.
-__device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int& jp)
+// (D holds row k-1 and receives row k in place).  The crossing c -- the first
+// j with D_{k-1}(j) >= U_i - U_j, or i if none -- never moves left as i or k
+// grows, so it is at least the crossing this lane found for i-1 and the one
+// the next lane found for i in row k-1 (`lb`).  Four candidates from there are
+// tested in one round of loads; farther crossings gallop and then bisect.
+__device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int lb, int& jp)
 {
     const bool act = i <= hi;
     double v = 0.0;
     if (act) {
         const double Ui = U[i];
-        int a = jp > k - 1 ? jp : k - 1;   // every j < a fails; a <= i - 1
-        double da = D[a];
-        double ua = U[a];
-        double um = U[a - 1];              // a >= 1
-        if (!(da >= Ui - ua)) {
-            // slow path: crossing in (a, i]
-            int lo = a + 1, b = i, step = 1;
+        const int a = lb > k - 1 ? lb : k - 1;   // every j < a fails
+        int c;
+        double dc, uc;                           // D[c] and U[c-1] (dc = inf when c = i)
+        {
+            const double d0 = D[a], d1 = D[a + 1], d2 = D[a + 2], d3 = D[a + 3];
+            const double um = U[a - 1], u0 = U[a], u1 = U[a + 1], u2 = U[a + 2], u3 = U[a + 3];
+            const bool f0 = a >= i || d0 >= Ui - u0;
+            const bool f1 = a + 1 >= i || d1 >= Ui - u1;
+            const bool f2 = a + 2 >= i || d2 >= Ui - u2;
+            const bool f3 = a + 3 >= i || d3 >= Ui - u3;
+            c = f0 ? a : f1 ? a + 1 : f2 ? a + 2 : f3 ? a + 3 : -1;
+            dc = f0 ? d0 : f1 ? d1 : f2 ? d2 : d3;
+            uc = f0 ? um : f1 ? u0 : f2 ? u1 : u2;
+        }
+        if (c < 0) {
+            // rare: crossing in (a+3, i]
+            int lo = a + 4, b = i, step = 1;
             while (lo < b) {
                 int p = lo + step - 1;
                 p = p < b - 1 ? p : b - 1;
@@ -270,13 +287,14 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
                 const int mid = (lo + b) >> 1;
                 if (D[mid] >= Ui - U[mid]) b = mid; else lo = mid + 1;
             }
-            a = lo;
-            da = (a < i) ? D[a] : kInf;
-            um = U[a - 1];
+            c = lo;
+            dc = D[c];
+            uc = U[c - 1];
         }
-        jp = a;
-        v = da;
-        if (a - 1 >= k - 1) v = fmin(v, Ui - um);
+        if (c >= i) { c = i; dc = kInf; }
+        jp = c;
+        v = dc;
+        if (c - 1 >= k - 1) v = fmin(v, Ui - uc);
     }
     // every lane has read row k-1 before any lane overwrites it
     __asm__ volatile("" ::: "memory");
@@ -313,8 +331,14 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
     int jp0 = 0, jp1 = 0;
     for (int k = 2; k <= P; ++k) {
         const int hi = L - tau + k;
-        if (hi - k >= 64) dp_entry(U, D, k, hi, k + 64 + lane, jp1);   // high part first: in place
-        dp_entry(U, D, k, hi, k + lane, jp0);
+        // lower bounds: own crossing (i-1, row k-1) and the next lane's (i, row k-1)
+        const int top1 = __builtin_amdgcn_readlane(jp1, 0);
+        const int nb0 = from_next_lane(jp0, top1);
+        const int nb1 = from_next_lane(jp1, jp1);
+        const int lb0 = jp0 > nb0 ? jp0 : nb0;
+        const int lb1 = jp1 > nb1 ? jp1 : nb1;
+        if (hi - k >= 64) dp_entry(U, D, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
+        dp_entry(U, D, k, hi, k + lane, lb0, jp0);
         entries += (unsigned long long)(hi - k + 1);
         wave_sync();
         if (k == tau) {
