@@ -130,22 +130,23 @@ __device__ __forceinline__ double wave_reduce1(double x)
 
 // Left-to-right prefix of L values held as (element lane, element lane+64):
 // out[0] = 0, out[i] = out[i-1] + v[i-1].  Sequential on purpose: the rounding
-// of a prefix must not depend on a reduction tree.
-__device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out)
+// of a prefix must not depend on a reduction tree.  The values are staged in
+// `tmp` (LDS) and one lane accumulates them in order: one add per layer.
+__device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out, double* tmp)
 {
-    double acc = 0.0, r0 = 0.0, r1 = 0.0;
-    const int n0 = L < 64 ? L : 64;
-    for (int i = 0; i < n0; ++i) {
-        acc = acc + bcast(v0, i);
-        if (lane == i) r0 = acc;
+    if (lane < L) tmp[lane] = v0;
+    if (lane + 64 < L) tmp[lane + 64] = v1;
+    wave_sync();
+    if (lane == 0) {
+        double acc = 0.0;
+        out[0] = 0.0;
+#pragma unroll 8
+        for (int i = 0; i < L; ++i) {
+            acc = acc + tmp[i];
+            out[i + 1] = acc;
+        }
     }
-    for (int i = 64; i < L; ++i) {
-        acc = acc + bcast(v1, i - 64);
-        if (lane == i - 64) r1 = acc;
-    }
-    if (lane == 0) out[0] = 0.0;
-    if (lane < L) out[lane + 1] = r0;
-    if (lane + 64 < L) out[lane + 65] = r1;
+    wave_sync();
 }
 
 // ------------------------------------------------------------ model pieces
@@ -163,8 +164,9 @@ struct Cell {
 };
 
 // Per-sample cost of each layer (formula in arena.h), prefix-summed into U.
-__device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, int lane,
-                               const JobCtx& jb, const TypeDev& ty, double kappa, int tp, bool a2a_on)
+__device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, double* tmp,
+                               int lane, const JobCtx& jb, const TypeDev& ty, double kappa, int tp,
+                               bool a2a_on)
 {
     const double denom = (double)jb.Bg * ty.speed * (double)tp;
     const double ctp = kappa * 8.0 * (double)(tp - 1) / (double)tp;
@@ -179,8 +181,7 @@ __device__ void build_prefix_u(const float* t, const float* x, const float* q, d
             u[s] = v;
         }
     }
-    seq_prefix(u[0], u[1], jb.L, lane, U);
-    wave_sync();
+    seq_prefix(u[0], u[1], jb.L, lane, U, tmp);
 }
 
 __device__ __forceinline__ bool adm_ok(const uint32_t* adm, int dp)
@@ -395,16 +396,13 @@ __device__ Stages canonical_stages(const double* U, int lane, int L, int pp, dou
             break;
         }
     }
-    // stage s ends where stage s+1 starts: the next lane's cut
-    const int nA = __shfl_down(cA, 1, 64);
-    const int nB = __shfl_down(cB, 1, 64);
-    const int b0 = __builtin_amdgcn_readlane(cB, 0);
-    const int b1 = pp == 128 ? L : 0;
+    // stage s ends where stage s+1 starts: the next lane's cut (lane 63 of the
+    // low half takes c_64, lane 63 of the high half c_128)
     Stages r;
     r.lo0 = cA;
-    r.hi0 = lane == 63 ? b0 : nA;
+    r.hi0 = from_next_lane(cA, __builtin_amdgcn_readlane(cB, 0));
     r.lo1 = cB;
-    r.hi1 = lane == 63 ? b1 : nB;
+    r.hi1 = from_next_lane(cB, pp == 128 ? L : 0);
     return r;
 }
 
@@ -440,7 +438,7 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
     const double pmax = rm[0];
     const double sumS = U[jb.L];   // the stages tile the layers: sum of stage costs
     const double ar = (dp > 1)
-        ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp * (pmax / (double)tp) / B_dp
+        ? pmax * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
         : 0.0;
     const double per_sample = sumS + cell.c_p2p * sumX;   // fill time per sample
     const double cap = ty.mem * (double)tp;                // memory test scaled by tp
@@ -504,9 +502,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const float* src = (wid == 0 ? A.p : A.a) + off;
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
-        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap);
+        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.D);
     } else if (wid == 2) {
-        build_prefix_u(B.t, B.x, B.q, B.Upure, lane, jb, ty, 1.0, 1, false);
+        build_prefix_u(B.t, B.x, B.q, B.Upure, Wv.D, lane, jb, ty, 1.0, 1, false);
     } else {
         bool same = true;
         for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
@@ -565,7 +563,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (tm.count() == 0) continue;
         const double* U = B.Upure;
         if (s > 0) {
-            build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp, true);
+            build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp,
+                           true);
             U = Wv.U;
         }
         solve_dp(U, Wv.D, jb.L, tm, B.Wtab[s], true, lane, dp_entries);
@@ -605,7 +604,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 if (slot == 0) {
                     U = B.Upure;
                 } else {
-                    build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, cell.kappa, tp, var == 0);
+                    build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
                     U = Wv.U;
                 }
                 if (slot < 0) {
@@ -674,7 +673,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             if (slot == 0) {
                 U = B.Upure;
             } else {
-                build_prefix_u(B.t, B.x, B.q, Wv.U, lane, jb, ty, cell.kappa, tp, var == 0);
+                build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
                 U = Wv.U;
             }
             double W;
