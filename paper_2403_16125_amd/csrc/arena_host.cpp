@@ -559,8 +559,11 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.item_order = c->d_item_order;
     A.count_order = c->d_count_order;
     A.share_tp = kappa_shared(c) ? 1 : 0;
-    A.n_m = (int32_t)c->m_values.size();
-    for (int i = 0; i < A.n_m; ++i) A.m_values[i] = c->m_values[i];
+    // ascending: the kernel bisects the microbatch counts for the memory limit
+    std::vector<int32_t> ms(c->m_values);
+    std::sort(ms.begin(), ms.end());
+    A.n_m = (int32_t)ms.size();
+    for (int i = 0; i < A.n_m; ++i) A.m_values[i] = ms[i];
     A.tie_eps = c->tie_eps;
     A.t_iter = t_iter;
     A.thr = thr;

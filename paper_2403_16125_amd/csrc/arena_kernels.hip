@@ -27,14 +27,21 @@ namespace {
 
 constexpr double kInf = __builtin_huge_val();
 constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree problems
+constexpr int kPad = 8;            // prefix arrays hold +inf past the last layer
+constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
+constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 
 struct WaveLds {
-    double U[kLmax + 8];          // cost prefix of the wave's current problem (padded for probes)
-    double D[kLmax + 8];          // partition recursion row, updated in place (padded for probes)
+    double U[kLmax + kPad];       // cost prefix of the wave's current problem (+inf padded)
+    double D[kLmax + kPad];       // partition recursion row, updated in place; while a plan is
+                                  // priced, its bytes hold the successor tables of the cuts
     double Wt[kMaxTargets];       // bottleneck per requested degree (by rank)
     double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
     uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
+    double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
+    int32_t mq[kMaxM];            // those microbatch counts
 };
+static_assert(kLevels * kLevelStride <= (int)sizeof(double) * (kLmax + kPad), "successor tables fit in D");
 
 template <int SLOTS>
 struct BlockLds {
@@ -43,7 +50,7 @@ struct BlockLds {
     float q[kLmax];
     double Pp[kLmax + 1];         // prefix of parameter bytes
     double Ap[kLmax + 1];         // prefix of activation bytes
-    double Upure[kLmax + 8];      // prefix of the pure-compute per-sample cost (padded for probes)
+    double Upure[kLmax + kPad];   // prefix of the pure-compute per-sample cost (+inf padded)
     double Wtab[SLOTS][kLmax + 1];// bottleneck of each shared problem, by degree
     uint32_t adm[kMaxDp / 32];    // bit dp-1: some listed m has dp*m dividing the batch
     int32_t slot_tp[SLOTS];
@@ -132,10 +139,14 @@ __device__ __forceinline__ double wave_reduce1(double x)
 // out[0] = 0, out[i] = out[i-1] + v[i-1].  Sequential on purpose: the rounding
 // of a prefix must not depend on a reduction tree.  The values are staged in
 // `tmp` (LDS) and one lane accumulates them in order: one add per layer.
-__device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out, double* tmp)
+// With `pad`, out[L+1 .. kLmax+kPad-1] = +inf (out has kLmax + kPad entries).
+__device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out, double* tmp,
+                                           bool pad)
 {
     if (lane < L) tmp[lane] = v0;
     if (lane + 64 < L) tmp[lane + 64] = v1;
+    if (pad)
+        for (int e = L + 1 + lane; e < kLmax + kPad; e += 64) out[e] = kInf;
     wave_sync();
     if (lane == 0) {
         double acc = 0.0;
@@ -181,7 +192,7 @@ __device__ void build_prefix_u(const float* t, const float* x, const float* q, d
             u[s] = v;
         }
     }
-    seq_prefix(u[0], u[1], jb.L, lane, U, tmp);
+    seq_prefix(u[0], u[1], jb.L, lane, U, tmp, true);
 }
 
 __device__ __forceinline__ bool adm_ok(const uint32_t* adm, int dp)
@@ -250,10 +261,17 @@ __device__ __forceinline__ int from_next_lane(int v, int last)
 
 // One lane of row k of the recursion D_k(i) = min_j max(D_{k-1}(j), U_i - U_j)
 // (D holds row k-1 and receives row k in place).  The crossing c -- the first
-// j with D_{k-1}(j) >= U_i - U_j, or i if none -- never moves left as i or k
-// grows, so it is at least the crossing this lane found for i-1 and the one
-// the next lane found for i in row k-1 (`lb`).  Four candidates from there are
-// tested in one round of loads; farther crossings gallop and then bisect.
+// j >= k-1 with D_{k-1}(j) >= U_i - U_j -- never moves left as i or k grows,
+// so it is at least the crossing this lane found for i-1 and the one the next
+// lane found for i in row k-1 (`lb`).  Position i always passes the test: D[i]
+// holds D_{k-1}(i) >= 0 = U_i - U_i, or +inf where row k-1 stopped short of i,
+// so the first passing position of a probe is c whenever the probe reaches i
+// and nothing to the right of i is ever looked at.  Four candidates are tested
+// in one round of loads; farther crossings gallop and then bisect.
+//   D_k(i) = min(D_{k-1}(c), U_i - U_{c-1})   (second term only for c-1 >= k-1)
+// At c = i the first term is D_{k-1}(i) >= U_i - U_{i-1} (every partition of
+// the first i layers has a stage holding layer i-1 whole) or +inf, so the
+// minimum is U_i - U_{i-1}, the value of the only split left.
 __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int lb, int& jp)
 {
     const bool act = i <= hi;
@@ -261,21 +279,13 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
     if (act) {
         const double Ui = U[i];
         const int a = lb > k - 1 ? lb : k - 1;   // every j < a fails
-        int c;
-        double dc, uc;                           // D[c] and U[c-1] (dc = inf when c = i)
-        {
-            const double d0 = D[a], d1 = D[a + 1], d2 = D[a + 2], d3 = D[a + 3];
-            const double um = U[a - 1], u0 = U[a], u1 = U[a + 1], u2 = U[a + 2], u3 = U[a + 3];
-            const bool f0 = a >= i || d0 >= Ui - u0;
-            const bool f1 = a + 1 >= i || d1 >= Ui - u1;
-            const bool f2 = a + 2 >= i || d2 >= Ui - u2;
-            const bool f3 = a + 3 >= i || d3 >= Ui - u3;
-            c = f0 ? a : f1 ? a + 1 : f2 ? a + 2 : f3 ? a + 3 : -1;
-            dc = f0 ? d0 : f1 ? d1 : f2 ? d2 : d3;
-            uc = f0 ? um : f1 ? u0 : f2 ? u1 : u2;
-        }
-        if (c < 0) {
-            // rare: crossing in (a+3, i]
+        const bool f0 = D[a] >= Ui - U[a];
+        const bool f1 = D[a + 1] >= Ui - U[a + 1];
+        const bool f2 = D[a + 2] >= Ui - U[a + 2];
+        const bool f3 = D[a + 3] >= Ui - U[a + 3];
+        int c = f0 ? a : f1 ? a + 1 : f2 ? a + 2 : a + 3;
+        if (!(f0 | f1 | f2 | f3)) {
+            // rare: crossing in (a+3, i]; i passes without a look
             int lo = a + 4, b = i, step = 1;
             while (lo < b) {
                 int p = lo + step - 1;
@@ -289,13 +299,11 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
                 if (D[mid] >= Ui - U[mid]) b = mid; else lo = mid + 1;
             }
             c = lo;
-            dc = D[c];
-            uc = U[c - 1];
         }
-        if (c >= i) { c = i; dc = kInf; }
         jp = c;
-        v = dc;
-        if (c - 1 >= k - 1) v = fmin(v, Ui - uc);
+        const double dc = D[c];
+        const double t = Ui - U[c - 1];
+        v = (c >= k && t < dc) ? t : dc;
     }
     // every lane has read row k-1 before any lane overwrites it
     __asm__ volatile("" ::: "memory");
@@ -307,13 +315,15 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
 // tau(k) the smallest requested degree >= k: larger i cannot reach a
 // requested cell.  Lane l of row k takes i = k + l (+64): the window width
 // never grows with k, so after the first rows one pass covers a row, and a
-// lane's crossing from row k-1 (for i-1) is a lower bound for row k.
+// lane's crossing from row k-1 (for i-1) is a lower bound for row k.  After
+// each row, D[hi+1] = +inf marks the first position the row did not reach.
 __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, double* Wout, bool by_pp,
                          int lane, unsigned long long& entries)
 {
     const int P = tm.last();
     int tau = tm.next(1);
     int rank = 0;
+    unsigned n_ent = 0;
     {
         const int hi = L - tau + 1;
 #pragma unroll
@@ -321,7 +331,8 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
             const int i = 1 + lane + 64 * s;
             if (i <= hi) D[i] = U[i];
         }
-        entries += (unsigned long long)hi;
+        if (lane == 0) D[hi + 1] = kInf;
+        n_ent += (unsigned)hi;
         wave_sync();
         if (tau == 1) {
             if (lane == 0) Wout[by_pp ? 1 : 0] = D[L];
@@ -340,7 +351,8 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
         const int lb1 = jp1 > nb1 ? jp1 : nb1;
         if (hi - k >= 64) dp_entry(U, D, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
         dp_entry(U, D, k, hi, k + lane, lb0, jp0);
-        entries += (unsigned long long)(hi - k + 1);
+        if (lane == 0) D[hi + 1] = kInf;
+        n_ent += (unsigned)(hi - k + 1);
         wave_sync();
         if (k == tau) {
             if (lane == 0) Wout[by_pp ? k : rank] = D[L];
@@ -348,57 +360,95 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
             tau = tm.next(k + 1);
         }
     }
+    entries += n_ent;
     wave_sync();
 }
 
 // Canonical cuts for degree pp and bottleneck W: c_pp = L and, right to left,
 // c_k = max(k, next(c_{k+1})) with next(e) the smallest c such that
-// U_e - U_c <= W.  Returns the bounds of stage s = lane + 64h as
-// [lo_h, hi_h) = [c_s, c_{s+1}).
+// U_e - U_c <= W.  Unrolled: next(e) < e, so a_k = next^(pp-k)(L) falls by at
+// least one per step and a_k - k never decreases as k falls; once the clamp
+// bites it bites for every smaller k, hence c_k = max(k, a_k).  Every lane
+// finds next(e) for its layers by binary lifting over U, the wave builds the
+// successor tables next^(2^s) in LDS bytes `J` (level s at J + s kLevelStride,
+// node 0 maps to itself) and lane k walks pp-k steps from L in log2 jumps.
+// Returns the bounds of stage s = lane + 64h as [lo_h, hi_h) = [c_s, c_{s+1}).
 struct Stages {
     int lo0, lo1, hi0, hi1;
 };
 
-__device__ Stages canonical_stages(const double* U, int lane, int L, int pp, double W)
+__device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L, int pp, double W)
 {
-    int nx0 = 0, nx1 = 0;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int e = 1 + lane + 64 * s;
-        if (e <= L && pp > 1) {
-            const double Ue = U[e];
-            int lo = 0, hi = e - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (Ue - U[mid] <= W) hi = mid; else lo = mid + 1;
-            }
-            if (s == 0) nx0 = lo; else nx1 = lo;
-        }
+    Stages r;
+    if (pp == 1) {
+        r.lo0 = 0; r.hi0 = L; r.lo1 = 0; r.hi1 = 0;
+        return r;
     }
-    // c_k lives in lane k & 63 of cA (k < 64) or cB (k >= 64); c_0 = 0, c_pp = L
+    const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
+    // next(e): the failing c (U_e - U_c > W) form a prefix of [0, e); c = e-1
+    // passes (W is at least every single-layer cost) and so does every c > e-1
+    // (U is non-decreasing and +inf past L)
+    int cur0 = 0, cur1 = 0;
+    const int e0 = 1 + lane, e1 = 65 + lane;
+    if (e0 <= L) {
+        const double Ue = U[e0];
+        int pos = 0;
+#pragma unroll
+        for (int step = 32; step >= 1; step >>= 1)
+            if (Ue - U[pos + step - 1] > W) pos += step;
+        cur0 = pos;
+        J[e0] = (uint8_t)pos;
+    }
+    if (L > 64 && e1 <= L) {
+        const double Ue = U[e1];
+        int pos = 0;
+#pragma unroll
+        for (int step = 64; step >= 1; step >>= 1)
+            if (Ue - U[pos + step - 1] > W) pos += step;
+        cur1 = pos;
+        J[e1] = (uint8_t)pos;
+    }
+    if (lane < levels) J[lane * kLevelStride] = 0;
+    wave_sync();
+    for (int s = 1; s < levels; ++s) {
+        const uint8_t* prev = J + (s - 1) * kLevelStride;
+        uint8_t* lev = J + s * kLevelStride;
+        if (e0 <= L) cur0 = prev[cur0];
+        if (L > 64 && e1 <= L) cur1 = prev[cur1];
+        if (e0 <= L) lev[e0] = (uint8_t)cur0;
+        if (L > 64 && e1 <= L) lev[e1] = (uint8_t)cur1;
+        wave_sync();
+    }
+    // c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0, c_pp = L
     int cA = 0, cB = 0;
-    cA = (pp < 64 && lane == pp) ? L : cA;
-    cB = (pp >= 64 && lane == pp - 64) ? L : cB;
-    int cur = L;
-    for (int k = pp - 1; k >= 1; --k) {
-        const int e = cur - 1;
-        const int na = __builtin_amdgcn_readlane(nx0, e & 63);
-        const int nb = __builtin_amdgcn_readlane(nx1, e & 63);
-        const int nxt = e < 64 ? na : nb;
-        const int c = nxt > k ? nxt : k;
-        cA = (k < 64 && lane == k) ? c : cA;
-        cB = (k >= 64 && lane == k - 64) ? c : cB;
-        cur = c;
-        if (c == k) {
-            // every earlier stage holds exactly one layer
-            cA = lane < k ? lane : cA;
-            cB = lane + 64 < k ? lane + 64 : cB;
-            break;
+    {
+        const int k = lane;
+        if (k >= 1 && k < pp) {
+            const int d = pp - k;
+            int node = L;
+            for (int s = 0; s < levels; ++s) {
+                const int nd = J[s * kLevelStride + node];
+                node = ((d >> s) & 1) ? nd : node;
+            }
+            cA = node > k ? node : k;
         }
+        cA = k == pp ? L : cA;
+    }
+    if (pp >= 64) {
+        const int k = lane + 64;
+        if (k < pp) {
+            const int d = pp - k;
+            int node = L;
+            for (int s = 0; s < levels; ++s) {
+                const int nd = J[s * kLevelStride + node];
+                node = ((d >> s) & 1) ? nd : node;
+            }
+            cB = node > k ? node : k;
+        }
+        cB = k == pp ? L : cB;
     }
     // stage s ends where stage s+1 starts: the next lane's cut (lane 63 of the
     // low half takes c_64, lane 63 of the high half c_128)
-    Stages r;
     r.lo0 = cA;
     r.hi0 = from_next_lane(cA, __builtin_amdgcn_readlane(cB, 0));
     r.lo1 = cB;
@@ -407,13 +457,17 @@ __device__ Stages canonical_stages(const double* U, int lane, int L, int pp, dou
 }
 
 // Price every admissible microbatch count of plan (dp, tp, pp) with the
-// canonical stages of bottleneck W; appends to the wave's plan buffer.
+// canonical stages of bottleneck W; appends to the wave's plan buffer.  Lane
+// mi < n_m holds m_values[mi] (ascending) in `mv`: the lanes price one count
+// each.  A stage's memory is non-increasing in m (min(m, pp-k) b is the batch
+// share Bg/dp while m <= pp-k and falls after), so the counts that fit are the
+// top of the admissible list; the first one is found by bisection.
 template <int SLOTS>
-__device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane,
+__device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                              const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
-                             double W, int& np, const EstimateArgs& A, unsigned long long& overflow)
+                             double W, int& np, unsigned long long& overflow)
 {
-    const Stages sg = canonical_stages(U, lane, jb.L, pp, W);
+    const Stages sg = canonical_stages(U, reinterpret_cast<uint8_t*>(Wv.D), lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
     const double B_dp = (grp <= ty.gpn && ty.gpn % grp == 0) ? ty.bw_intra : ty.bw_inter;
@@ -441,30 +495,55 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
         ? pmax * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
         : 0.0;
     const double per_sample = sumS + cell.c_p2p * sumX;   // fill time per sample
-    const double cap = ty.mem * (double)tp;                // memory test scaled by tp
+
+    // lanes over the microbatch counts: admissible when dp m divides the batch
+    // (the quotient of a correctly rounded division is exact then)
+    bool adm = false;
+    double b = 0.0;
+    if (mv > 0) {
+        const double dm = (double)(dp * mv);
+        const double q = rint((double)jb.Bg / dm);
+        adm = q * dm == (double)jb.Bg;
+        b = q;
+    }
+    const unsigned long long amask = __ballot(adm);
+    const int nadm = __popcll(amask);
+    if (nadm == 0) return;
+    const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32),
+                                               __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
+    if (adm) {
+        Wv.bq[rank] = b;
+        Wv.mq[rank] = mv;
+    }
+    wave_sync();
+
+    // memory: 4 P_k + min(m, pp-k) b A_k <= mem tp on every stage
+    const double cap = ty.mem * (double)tp;
     const double fP0 = 4.0 * P0, fP1 = 4.0 * P1;
     const int r0 = pp - lane, r1 = pp - lane - 64;         // stages from the lane's to the last
-
-    for (int mi = 0; mi < A.n_m; ++mi) {
-        const int m = A.m_values[mi];
-        const int dm = dp * m;
-        if (jb.Bg % dm != 0) continue;
-        const double b = (double)(jb.Bg / dm);             // exact: dm divides the batch
-        // memory: 4 P_k + min(m, pp-k) b A_k <= mem tp on every stage
-        const double i0 = (double)(m < r0 ? m : r0) * b;
-        const double i1 = (double)(m < r1 ? m : r1) * b;
+    int lo = 0, hi = nadm;                                  // first fitting rank in [lo, hi]
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        const double bm = Wv.bq[mid];
+        const int m = Wv.mq[mid];
+        const double i0 = (double)(m < r0 ? m : r0) * bm;
+        const double i1 = (double)(m < r1 ? m : r1) * bm;
         const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
-        const bool fits = __ballot(over) == 0ull;
-        const double T = b * per_sample + (double)(m - 1) * (b * W) + ar;
-        if (np < kMaxPlans) {
-            if (lane == 0) {
-                Wv.planT[np] = fits ? T : kInf;
-                Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
-            }
-            ++np;
-        } else {
-            overflow = 1;
+        if (__ballot(over) == 0ull) hi = mid; else lo = mid + 1;
+    }
+
+    if (adm) {
+        const double T = b * per_sample + (double)(mv - 1) * (b * W) + ar;
+        const int slot = np + rank;
+        if (slot < kMaxPlans) {
+            Wv.planT[slot] = rank >= lo ? T : kInf;
+            Wv.planKey[slot] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)mv;
         }
+    }
+    np += nadm;
+    if (np > kMaxPlans) {
+        overflow = 1;
+        np = kMaxPlans;
     }
 }
 
@@ -487,6 +566,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     jb.L = A.layer_offset[j + 1] - off;
     jb.Bg = A.batch[j];
     const TypeDev ty = A.types[g];
+    int mv = 0;                      // lane mi: the mi-th microbatch count (ascending), 0 past the list
+#pragma unroll
+    for (int i = 0; i < kMaxM; ++i)
+        if (lane == i && i < A.n_m) mv = A.m_values[i];
 
     // ---- stage the job
     bool has_q = false;
@@ -502,7 +585,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const float* src = (wid == 0 ? A.p : A.a) + off;
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
-        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.D);
+        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.D, false);
     } else if (wid == 2) {
         build_prefix_u(B.t, B.x, B.q, B.Upure, Wv.D, lane, jb, ty, 1.0, 1, false);
     } else {
@@ -614,7 +697,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 int rank = 0;
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1), ++rank) {
                     const double W = slot >= 0 ? B.Wtab[slot][pp] : Wv.Wt[rank];
-                    price_target(B, Wv, U, lane, jb, ty, cell, tp, pp, W, np, A, overflow);
+                    price_target(B, Wv, U, lane, mv, jb, ty, cell, tp, pp, W, np, overflow);
                 }
             }
         }
@@ -687,7 +770,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 solve_dp(U, Wv.D, jb.L, one, Wv.Wt, false, lane, scratch_entries);
                 W = Wv.Wt[0];
             }
-            const Stages sg = canonical_stages(U, lane, jb.L, pp, W);
+            const Stages sg = canonical_stages(U, reinterpret_cast<uint8_t*>(Wv.D), lane, jb.L, pp, W);
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
