@@ -122,6 +122,14 @@ typedef struct arena_counters {
     int64_t problems;         /* stage-partition problems solved */
     int64_t dp_entries;       /* partition-recursion entries evaluated */
     int64_t infeasible_cells; /* cells with no feasible plan */
+    int64_t plans_skipped;    /* plans never priced: a lower bound of their iteration time
+                                 lies above the tie window of a plan already priced, or no
+                                 stage split of their degree fits memory.
+                                 plans + plans_skipped = the plan space */
+    int64_t alg_ops;          /* algorithmic operations of the work done: 8 per layer of each
+                                 solved problem (layer costs and prefix), 8 per recursion entry,
+                                 4 L per priced pipeline degree (cuts), 12 pp + 40 per priced
+                                 plan */
 } arena_counters;
 
 /* Exact size of the plan space of the bound tables (host-side count). */

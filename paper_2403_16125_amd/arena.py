@@ -56,7 +56,8 @@ class GridsDesc(ctypes.Structure):
 class Counters(ctypes.Structure):
     _fields_ = [("cells", ctypes.c_int64), ("plans", ctypes.c_int64),
                 ("problems", ctypes.c_int64), ("dp_entries", ctypes.c_int64),
-                ("infeasible_cells", ctypes.c_int64)]
+                ("infeasible_cells", ctypes.c_int64), ("plans_skipped", ctypes.c_int64),
+                ("alg_ops", ctypes.c_int64)]
 
 
 class SpaceSize(ctypes.Structure):
@@ -201,7 +202,7 @@ def arena_get_counters(ctx) -> dict:
     c = Counters()
     _check(ctx, load().arena_get_counters(ctx, ctypes.byref(c)))
     return dict(cells=c.cells, plans=c.plans, problems=c.problems, dp_entries=c.dp_entries,
-                infeasible_cells=c.infeasible_cells)
+                infeasible_cells=c.infeasible_cells, plans_skipped=c.plans_skipped, alg_ops=c.alg_ops)
 
 
 # ---------------------------------------------------------------- convenience

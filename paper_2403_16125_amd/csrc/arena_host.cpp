@@ -595,6 +595,8 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     out->problems = (int64_t)h[arena::kProblems];
     out->dp_entries = (int64_t)h[arena::kDpEntries];
     out->infeasible_cells = (int64_t)h[arena::kInfeasible];
+    out->plans_skipped = (int64_t)h[arena::kSkipped];
+    out->alg_ops = (int64_t)h[arena::kAlgOps];
     if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");
     return ARENA_OK;
 }

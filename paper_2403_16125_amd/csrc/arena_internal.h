@@ -22,7 +22,7 @@ struct TypeDev {
 };
 
 // Device tallies, zeroed before each estimate.
-enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kNumCounters };
+enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kSkipped, kAlgOps, kNumCounters };
 
 struct EstimateArgs {
     const int32_t* layer_offset;  // [J+1]

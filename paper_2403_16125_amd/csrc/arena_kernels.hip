@@ -33,15 +33,14 @@ constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 
 struct WaveLds {
     double U[kLmax + kPad];       // cost prefix of the wave's current problem (+inf padded)
-    double D[kLmax + kPad];       // partition recursion row, updated in place; while a plan is
-                                  // priced, its bytes hold the successor tables of the cuts
-    double Wt[kMaxTargets];       // bottleneck per requested degree (by rank)
+    double D[kLmax + kPad];       // partition recursion row, updated in place
     double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
     uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
     double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
     int32_t mq[kMaxM];            // those microbatch counts
+    double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
+    uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
-static_assert(kLevels * kLevelStride <= (int)sizeof(double) * (kLmax + kPad), "successor tables fit in D");
 
 template <int SLOTS>
 struct BlockLds {
@@ -51,8 +50,12 @@ struct BlockLds {
     double Pp[kLmax + 1];         // prefix of parameter bytes
     double Ap[kLmax + 1];         // prefix of activation bytes
     double Upure[kLmax + kPad];   // prefix of the pure-compute per-sample cost (+inf padded)
-    double Wtab[SLOTS][kLmax + 1];// bottleneck of each shared problem, by degree
-    uint32_t adm[kMaxDp / 32];    // bit dp-1: some listed m has dp*m dividing the batch
+    double Wtab[SLOTS][kLmax + 1];// bottleneck of each shared problem, by degree (slot 0, the
+                                  // pure-compute problem: every degree up to the layer count)
+    uint8_t mmax[kMaxDp];         // [dp-1]: largest listed m with dp*m dividing the batch, 0: none
+    uint8_t mcnt[kMaxDp];         // [dp-1]: how many listed m have dp*m dividing the batch
+    double p_layer_max;           // largest parameter bytes of one layer
+    double x_layer_min;           // smallest boundary activation bytes of one layer
     int32_t slot_tp[SLOTS];
     int32_t slot_var[SLOTS];
     int32_t n_slots;
@@ -162,6 +165,15 @@ __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane
 
 // ------------------------------------------------------------ model pieces
 
+// Link bandwidth by value (a conditional over two fields of one struct would
+// select an address and keep the struct in private memory).
+__device__ __forceinline__ double link_bw(bool intra, const TypeDev& ty)
+{
+    const double a = ty.bw_intra;
+    const double b = ty.bw_inter;
+    return intra ? a : b;
+}
+
 struct JobCtx {
     int L, Bg;
     bool moe;       // has all-to-all layers
@@ -174,17 +186,17 @@ struct Cell {
     double c_p2p;   // kappa 2 / B_pp: p2p seconds per byte and sample, both directions
 };
 
-// Per-sample cost of each layer (formula in arena.h), prefix-summed into U.
-__device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, double* tmp,
-                               int lane, const JobCtx& jb, const TypeDev& ty, double kappa, int tp,
-                               bool a2a_on)
+// Per-sample cost of layers lane and lane+64 (formula in arena.h; 0 past L).
+__device__ __forceinline__ void layer_costs(const float* t, const float* x, const float* q, int lane,
+                                            const JobCtx& jb, const TypeDev& ty, double kappa, int tp,
+                                            bool a2a_on, double (&u)[2])
 {
     const double denom = (double)jb.Bg * ty.speed * (double)tp;
     const double ctp = kappa * 8.0 * (double)(tp - 1) / (double)tp;
-    double u[2] = {0.0, 0.0};
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const int l = lane + 64 * s;
+        u[s] = 0.0;
         if (l < jb.L) {
             double v = (double)t[l] / denom;
             if (tp > 1) v += ctp * (double)x[l] / ty.bw_intra;
@@ -192,19 +204,28 @@ __device__ void build_prefix_u(const float* t, const float* x, const float* q, d
             u[s] = v;
         }
     }
+}
+
+// Per-sample cost of each layer, prefix-summed into U (+inf past L).
+__device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, double* tmp,
+                               int lane, const JobCtx& jb, const TypeDev& ty, double kappa, int tp,
+                               bool a2a_on)
+{
+    double u[2];
+    layer_costs(t, x, q, lane, jb, ty, kappa, tp, a2a_on, u);
     seq_prefix(u[0], u[1], jb.L, lane, U, tmp, true);
 }
 
-__device__ __forceinline__ bool adm_ok(const uint32_t* adm, int dp)
+__device__ __forceinline__ bool adm_ok(const uint8_t* mmax, int dp)
 {
-    return (adm[(dp - 1) >> 5] >> ((dp - 1) & 31)) & 1u;
+    return mmax[dp - 1] != 0;
 }
 
 // Is pp a requested degree of problem (n, tp, variant)?  pp divides n/tp, is
 // at most the layer count, leaves an admissible data-parallel degree, and
 // meets the all-to-all condition of the variant (variant 1: the MoE job's
 // single-GPU-per-stage plan dp = tp = 1, which has no all-to-all).
-__device__ __forceinline__ bool target_ok(const uint32_t* adm, const JobCtx& jb, int n, int tp,
+__device__ __forceinline__ bool target_ok(const uint8_t* adm, const JobCtx& jb, int n, int tp,
                                           int variant, int pp)
 {
     const int qn = n / tp;
@@ -225,6 +246,8 @@ struct Mask {
         return pp <= 64 ? ((lo >> (pp - 1)) & 1ull) : ((hi >> (pp - 65)) & 1ull);
     }
     __device__ __forceinline__ int count() const { return __popcll(lo) + __popcll(hi); }
+    __device__ __forceinline__ bool any() const { return (lo | hi) != 0ull; }
+    __device__ __forceinline__ Mask operator&(const Mask& o) const { return Mask{lo & o.lo, hi & o.hi}; }
     __device__ __forceinline__ int last() const
     {
         return hi ? 128 - __clzll(hi) : (lo ? 64 - __clzll(lo) : 0);
@@ -310,19 +333,21 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
     if (act) D[i] = v;
 }
 
-// Bottleneck W*(pp) for every degree in `tm`, written to Wout[pp] (by_pp) or
-// Wout[rank of pp].  Row k is evaluated for i in [k, L - tau(k) + k] only,
-// tau(k) the smallest requested degree >= k: larger i cannot reach a
-// requested cell.  Lane l of row k takes i = k + l (+64): the window width
-// never grows with k, so after the first rows one pass covers a row, and a
-// lane's crossing from row k-1 (for i-1) is a lower bound for row k.  After
-// each row, D[hi+1] = +inf marks the first position the row did not reach.
-__device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, double* Wout, bool by_pp,
-                         int lane, unsigned long long& entries)
+// Bottleneck W*(pp) = D_pp(L) for the degrees in `tm`, handed to
+// on_target(pp, W, tm) as soon as row pp is done; it returns the degrees
+// still wanted (it may drop larger ones), and rows stop after the last.  Row
+// k is evaluated for i in [k, L - tau(k) + k] only, tau(k) the smallest wanted
+// degree >= k: larger i cannot reach a wanted cell.  Lane l of row k takes
+// i = k + l (+64): the window width never grows with k, so after the first
+// rows one pass covers a row, and a lane's crossing from row k-1 (for i-1) is
+// a lower bound for row k.  After each row, D[hi+1] = +inf marks the first
+// position the row did not reach.
+template <class OnTarget>
+__device__ void solve_dp(const double* U, double* D, int L, Mask tm, int lane, unsigned long long& entries,
+                         OnTarget&& on_target)
 {
-    const int P = tm.last();
     int tau = tm.next(1);
-    int rank = 0;
+    if (tau == 0) return;
     unsigned n_ent = 0;
     {
         const int hi = L - tau + 1;
@@ -335,13 +360,12 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
         n_ent += (unsigned)hi;
         wave_sync();
         if (tau == 1) {
-            if (lane == 0) Wout[by_pp ? 1 : 0] = D[L];
-            ++rank;
+            tm = on_target(1, U[L], tm);
             tau = tm.next(2);
         }
     }
     int jp0 = 0, jp1 = 0;
-    for (int k = 2; k <= P; ++k) {
+    for (int k = 2; tau != 0; ++k) {
         const int hi = L - tau + k;
         // lower bounds: own crossing (i-1, row k-1) and the next lane's (i, row k-1)
         const int top1 = __builtin_amdgcn_readlane(jp1, 0);
@@ -355,8 +379,7 @@ __device__ void solve_dp(const double* U, double* D, int L, const Mask& tm, doub
         n_ent += (unsigned)(hi - k + 1);
         wave_sync();
         if (k == tau) {
-            if (lane == 0) Wout[by_pp ? k : rank] = D[L];
-            ++rank;
+            tm = on_target(k, D[L], tm);
             tau = tm.next(k + 1);
         }
     }
@@ -461,16 +484,18 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
 // mi < n_m holds m_values[mi] (ascending) in `mv`: the lanes price one count
 // each.  A stage's memory is non-increasing in m (min(m, pp-k) b is the batch
 // share Bg/dp while m <= pp-k and falls after), so the counts that fit are the
-// top of the admissible list; the first one is found by bisection.
+// top of the admissible list; the first one is found by bisection.  Returns
+// the iteration time of the largest admissible count if it fits (+inf if
+// not): a plan of the cell, so an upper bound of the cell's best time.
 template <int SLOTS>
-__device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
-                             const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
-                             double W, int& np, unsigned long long& overflow)
+__device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
+                               const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
+                               double W, int& np, unsigned long long& overflow, unsigned long long& ops)
 {
-    const Stages sg = canonical_stages(U, reinterpret_cast<uint8_t*>(Wv.D), lane, jb.L, pp, W);
+    const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
-    const double B_dp = (grp <= ty.gpn && ty.gpn % grp == 0) ? ty.bw_intra : ty.bw_inter;
+    const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
 
     // per-stage parameter and activation bytes of the lane's stages
     const bool act0 = lane < pp, act1 = lane + 64 < pp;
@@ -508,7 +533,8 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
     }
     const unsigned long long amask = __ballot(adm);
     const int nadm = __popcll(amask);
-    if (nadm == 0) return;
+    ops += 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull);
+    if (nadm == 0) return kInf;
     const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32),
                                                __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
     if (adm) {
@@ -532,8 +558,9 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
         if (__ballot(over) == 0ull) hi = mid; else lo = mid + 1;
     }
 
+    double T = kInf;
     if (adm) {
-        const double T = b * per_sample + (double)(mv - 1) * (b * W) + ar;
+        T = b * per_sample + (double)(mv - 1) * (b * W) + ar;
         const int slot = np + rank;
         if (slot < kMaxPlans) {
             Wv.planT[slot] = rank >= lo ? T : kInf;
@@ -545,6 +572,63 @@ __device__ void price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double
         overflow = 1;
         np = kMaxPlans;
     }
+    if (lo >= nadm) return kInf;
+    return bcast(T, 63 - __clzll(amask));   // the largest admissible count fits
+}
+
+// Lower bound of the iteration time of every plan of degree pp (any listed m)
+// of a problem whose per-sample layer costs sum to UL, or +inf when no split
+// of the layers into pp stages fits memory.  Bounded below without the cuts:
+//   W*(pp) >= UL / pp (the stages tile the layers) and >= Wpure(pp) / tp (the
+//   problem's layer costs are at least the pure-compute ones over tp);
+//   the p2p bytes over the pp-1 stage boundaries >= (pp-1) min_l x_l;
+//   the largest stage's parameters >= max(P / pp, max_l p_l).
+// For fixed dp, T = Bg/dp W + Bg/(dp m) (fill - W) + AR falls as m grows
+// (fill >= W), so the largest admissible m gives the bound.  A relative
+// margin of 1e-9 covers rounding.
+template <int SLOTS>
+__device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const TypeDev& ty, const Cell& cell,
+                               unsigned gpn_divs, int tp, int pp, double UL)
+{
+    const int qn = cell.n / tp;
+    const int dp = (int)rintf((float)qn * __builtin_amdgcn_rcpf((float)pp));   // exact: pp divides qn
+    const int m = B.mmax[dp - 1];
+    const double P = B.Pp[jb.L];
+    const double plb = fmax(P / (double)pp, B.p_layer_max);
+    if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
+    const double b = (double)jb.Bg / (double)(dp * m);
+    const double Wlb = fmax(UL / (double)pp, B.Wtab[0][pp] / (double)tp);
+    const double fill = UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
+    const int grp = dp * tp;
+    const double B_dp = link_bw(grp < 32 && ((gpn_divs >> grp) & 1u), ty);
+    const double ar = dp > 1
+        ? plb * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
+        : 0.0;
+    return (b * fill + (double)(m - 1) * (b * Wlb) + ar) * (1.0 - 1e-9);
+}
+
+// Plans of the degrees in `before` but not in `after` (qn = n / tp).
+template <int SLOTS>
+__device__ __forceinline__ unsigned long long dropped_plans(const BlockLds<SLOTS>& B, const Mask& before,
+                                                            const Mask& after, int lane, int qn)
+{
+    const bool d0 = ((before.lo & ~after.lo) >> lane) & 1ull;
+    const bool d1 = ((before.hi & ~after.hi) >> lane) & 1ull;
+    double c = 0.0;
+    if (d0) c += (double)B.mcnt[(int)rintf((float)qn * __builtin_amdgcn_rcpf((float)(1 + lane))) - 1];
+    if (d1) c += (double)B.mcnt[(int)rintf((float)qn * __builtin_amdgcn_rcpf((float)(65 + lane))) - 1];
+    return (unsigned long long)wave_reduce1<OpSum>(c);
+}
+
+// Slot of the shared problem (tp, variant), -1 if the cell solves its own.
+template <int SLOTS>
+__device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, bool moe, int tp, int var)
+{
+    if (tp == 1 && (var == 1 || !moe)) return 0;
+    int slot = -1;
+    for (int s = 1; s < n_slots; ++s)
+        if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
+    return slot;
 }
 
 // ------------------------------------------------------------ the kernel
@@ -570,6 +654,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 #pragma unroll
     for (int i = 0; i < kMaxM; ++i)
         if (lane == i && i < A.n_m) mv = A.m_values[i];
+    unsigned gpn_divs = 0;           // bit d: d divides the node size
+    for (int d = 1; d <= ty.gpn; ++d)
+        if (ty.gpn % d == 0) gpn_divs |= 1u << d;
 
     // ---- stage the job
     bool has_q = false;
@@ -586,33 +673,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
         seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.D, false);
+        if (wid == 0) {
+            const double pm = wave_reduce1<OpMax>(fmax(v0, v1));
+            if (lane == 0) B.p_layer_max = pm;
+        }
     } else if (wid == 2) {
         build_prefix_u(B.t, B.x, B.q, B.Upure, Wv.D, lane, jb, ty, 1.0, 1, false);
     } else {
         bool same = true;
         for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
         const bool uni = __ballot(!same) == 0ull;
+        const double x0 = lane < jb.L ? (double)A.x[off + lane] : kInf;
+        const double x1 = lane + 64 < jb.L ? (double)A.x[off + lane + 64] : kInf;
+        const double xm = wave_reduce1<OpMin>(fmin(x0, x1));
         if (lane == 0) {
             B.uniform = uni ? 1 : 0;
             B.next_cell = 0;
             B.moe = jb.moe ? 1 : 0;
+            B.x_layer_min = xm;
         }
     }
-    // admissible data-parallel degrees: dp*m divides the batch for a listed m
-    for (int base = 0; base < kMaxDp; base += 256) {
-        const int dp = base + tid + 1;
-        bool ok = false;
-        for (int i = 0; i < A.n_m; ++i) ok |= (jb.Bg % (dp * A.m_values[i])) == 0;
-        const unsigned long long bits = __ballot(ok);
-        if (lane == 0) {
-            B.adm[(base + 64 * wid) >> 5] = (uint32_t)(bits & 0xffffffffull);
-            B.adm[((base + 64 * wid) >> 5) + 1] = (uint32_t)(bits >> 32);
-        }
+    // largest admissible microbatch count of each data-parallel degree
+    for (int dp = tid + 1; dp <= kMaxDp; dp += 256) {
+        int mm = 0, mc = 0;
+        for (int i = 0; i < A.n_m; ++i)
+            if (jb.Bg % (dp * A.m_values[i]) == 0) {
+                mm = A.m_values[i] > mm ? A.m_values[i] : mm;
+                ++mc;
+            }
+        B.mmax[dp - 1] = (uint8_t)mm;
+        B.mcnt[dp - 1] = (uint8_t)mc;
     }
     __syncthreads();
 
-    // ---- shared problems: the pure-compute one, and every tensor degree when
-    // the type's contention factor is the same for all counts
+    // ---- shared problems: the pure-compute one (every degree up to L: its
+    // bottlenecks also bound the other problems'), and every tensor degree
+    // when the type's contention factor is the same for all counts
     if (tid == 0) {
         int ns = 0;
         B.slot_tp[ns] = 1;
@@ -631,27 +727,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     __syncthreads();
     const int n_slots = B.n_slots;
 
-    unsigned long long n_plans = 0, n_problems = 0, dp_entries = 0, n_infeasible = 0, overflow = 0;
+    unsigned long long n_plans = 0, n_problems = 0, dp_entries = 0, n_infeasible = 0, overflow = 0, n_skipped = 0;
+    unsigned long long ops = 0;      // algorithmic operations besides the recursion entries
 
     for (int s = wid; s < n_slots; s += kWavesPerBlock) {
         const int tp = B.slot_tp[s], var = B.slot_var[s];
-        bool ok0 = false, ok1 = false;
-        for (int c = 0; c < A.n_counts; ++c) {
-            const int n = A.counts[c];
-            if (n % tp != 0) continue;
-            ok0 |= target_ok(B.adm, jb, n, tp, var, 1 + lane);
-            ok1 |= target_ok(B.adm, jb, n, tp, var, 65 + lane);
+        Mask tm;
+        if (s == 0) {
+            tm = ballot_mask(1 + lane <= jb.L, 65 + lane <= jb.L);
+        } else {
+            bool ok0 = false, ok1 = false;
+            for (int c = 0; c < A.n_counts; ++c) {
+                const int n = A.counts[c];
+                if (n % tp != 0) continue;
+                ok0 |= target_ok(B.mmax, jb, n, tp, var, 1 + lane);
+                ok1 |= target_ok(B.mmax, jb, n, tp, var, 65 + lane);
+            }
+            tm = ballot_mask(ok0, ok1);
         }
-        const Mask tm = ballot_mask(ok0, ok1);
-        if (tm.count() == 0) continue;
+        if (!tm.any()) continue;
         const double* U = B.Upure;
         if (s > 0) {
             build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp,
                            true);
             U = Wv.U;
         }
-        solve_dp(U, Wv.D, jb.L, tm, B.Wtab[s], true, lane, dp_entries);
+        double* Wrow = B.Wtab[s];
+        solve_dp(U, Wv.D, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
+            if (lane == 0) Wrow[pp] = W;
+            return m;
+        });
         ++n_problems;
+        ops += 8ull * (unsigned)jb.L;
     }
     __syncthreads();
 
@@ -665,40 +772,73 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         Cell cell;
         cell.n = A.counts[ci];
         cell.kappa = (double)A.kappa[g * A.n_counts + ci];
-        cell.B_pp = (cell.n <= ty.gpn) ? ty.bw_intra : ty.bw_inter;
+        cell.B_pp = link_bw(cell.n <= ty.gpn, ty);
         cell.c_p2p = cell.kappa * 2.0 / cell.B_pp;
         int np = 0;
+        double best = kInf;          // time of a fitting plan priced so far: bounds the cell's best
 
+        // plans of the pure-compute problem first: their bottlenecks are shared
+        {
+            const int var = jb.moe ? 1 : 0;
+            const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, 1, var, 1 + lane),
+                                        target_ok(B.mmax, jb, cell.n, 1, var, 65 + lane));
+            for (int pp = tm.next(1); pp; pp = tm.next(pp + 1))
+                best = fmin(best, price_target(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp, B.Wtab[0][pp],
+                                               np, overflow, ops));
+        }
+        // the other problems, largest tensor degree first; a degree whose
+        // lower bound exceeds the tie window of `best` cannot hold the cell's
+        // plan and is skipped, and the recursion stops after the last degree
+        // still wanted
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
-        for (int tp = 1; tp <= tpmax; ++tp) {
-            if (cell.n % tp != 0 || ty.gpn % tp != 0) continue;
-            for (int var = 0; var < 2; ++var) {
-                if (var == 1 && !(jb.moe && tp == 1)) break;
-                const Mask tm = ballot_mask(target_ok(B.adm, jb, cell.n, tp, var, 1 + lane),
-                                            target_ok(B.adm, jb, cell.n, tp, var, 65 + lane));
-                if (tm.count() == 0) continue;
-                // shared problem?
-                int slot = -1;
-                if (tp == 1 && (var == 1 || !jb.moe)) slot = 0;
-                else
-                    for (int s = 1; s < n_slots; ++s)
-                        if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
-                const double* U;
-                if (slot == 0) {
-                    U = B.Upure;
-                } else {
-                    build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
-                    U = Wv.U;
+        for (int tp = tpmax; tp >= 1; --tp) {
+            if (cell.n % tp != 0 || ((gpn_divs >> tp) & 1u) == 0) continue;
+            if (tp == 1 && !jb.moe) continue;          // the pure-compute problem
+            Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
+                                  target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
+            if (!tm.any()) continue;
+            double u[2];
+            layer_costs(B.t, B.x, B.q, lane, jb, ty, cell.kappa, tp, true, u);
+            const double UL = wave_reduce1<OpSum>(u[0] + u[1]);
+            const double lb0 = tm.test(1 + lane) ? target_bound(B, jb, ty, cell, gpn_divs, tp, 1 + lane, UL) : kInf;
+            const double lb1 = (jb.L > 64 && tm.test(65 + lane))
+                ? target_bound(B, jb, ty, cell, gpn_divs, tp, 65 + lane, UL) : kInf;
+            Wv.lbnd[lane] = lb0;
+            Wv.lbnd[lane + 64] = lb1;
+            // kept: no bound yet (+inf: memory rules the degree out), or within the window
+            double lim = best * (1.0 + A.tie_eps);
+            {
+                const Mask keep = tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim);
+                if (keep.lo != tm.lo || keep.hi != tm.hi) n_skipped += dropped_plans(B, tm, keep, lane, cell.n / tp);
+                tm = keep;
+            }
+            if (!tm.any()) continue;
+            seq_prefix(u[0], u[1], jb.L, lane, Wv.U, Wv.D, true);
+            ops += 8ull * (unsigned)jb.L;
+            const int slot = find_slot(B, n_slots, jb.moe, tp, 0);
+            if (slot > 0) {
+                for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
+                    const double lbp = Wv.lbnd[pp - 1];
+                    if (!(lbp <= lim)) {
+                        n_skipped += B.mcnt[cell.n / (tp * pp) - 1];
+                        continue;
+                    }
+                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
+                                                   np, overflow, ops));
+                    lim = best * (1.0 + A.tie_eps);
                 }
-                if (slot < 0) {
-                    solve_dp(U, Wv.D, jb.L, tm, Wv.Wt, false, lane, dp_entries);
-                    ++n_problems;
-                }
-                int rank = 0;
-                for (int pp = tm.next(1); pp; pp = tm.next(pp + 1), ++rank) {
-                    const double W = slot >= 0 ? B.Wtab[slot][pp] : Wv.Wt[rank];
-                    price_target(B, Wv, U, lane, mv, jb, ty, cell, tp, pp, W, np, overflow);
-                }
+            } else {
+                solve_dp(Wv.U, Wv.D, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
+                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, W, np, overflow, ops));
+                    lim = best * (1.0 + A.tie_eps);
+                    Mask rest = m;                       // degrees still to come
+                    if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
+                    const Mask keep = rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim);
+                    if (keep.lo != rest.lo || keep.hi != rest.hi)
+                        n_skipped += dropped_plans(B, rest, keep, lane, cell.n / tp);
+                    return keep;
+                });
+                ++n_problems;
             }
         }
         wave_sync();
@@ -723,10 +863,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             wave_sync();
             continue;
         }
-        const double lim = tmin * (1.0 + A.tie_eps);
+        const double tlim = tmin * (1.0 + A.tie_eps);
         double kl = kInf;
         for (int e = lane; e < np; e += 64)
-            if (Wv.planT[e] <= lim) kl = fmin(kl, (double)Wv.planKey[e]);
+            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)Wv.planKey[e]);
         const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
         double il = -1.0;
         for (int e = lane; e < np; e += 64)
@@ -747,11 +887,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (A.cuts) {
             // re-derive the winner's bottleneck and cuts
             const int var = (jb.moe && dp * tp == 1) ? 1 : 0;
-            int slot = -1;
-            if (tp == 1 && (var == 1 || !jb.moe)) slot = 0;
-            else
-                for (int s = 1; s < n_slots; ++s)
-                    if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
+            const int slot = find_slot(B, n_slots, jb.moe, tp, var);
             const double* U;
             if (slot == 0) {
                 U = B.Upure;
@@ -759,7 +895,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
                 U = Wv.U;
             }
-            double W;
+            double W = 0.0;
             if (slot >= 0) {
                 W = B.Wtab[slot][pp];
             } else {
@@ -767,15 +903,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 one.lo = pp <= 64 ? (1ull << (pp - 1)) : 0ull;
                 one.hi = pp > 64 ? (1ull << (pp - 65)) : 0ull;
                 unsigned long long scratch_entries = 0;
-                solve_dp(U, Wv.D, jb.L, one, Wv.Wt, false, lane, scratch_entries);
-                W = Wv.Wt[0];
+                solve_dp(U, Wv.D, jb.L, one, lane, scratch_entries, [&](int, double Wk, Mask mk) {
+                    W = Wk;
+                    return mk;
+                });
             }
-            const Stages sg = canonical_stages(U, reinterpret_cast<uint8_t*>(Wv.D), lane, jb.L, pp, W);
+            const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
                 const int idx = lane + 64 * s;
-                const int en = s == 0 ? sg.hi0 : sg.hi1;
+                const int en = s == 0 ? +sg.hi0 : +sg.hi1;
                 if (idx < A.cuts_stride) row[idx] = (idx < pp - 1) ? (uint8_t)en : (uint8_t)0xFF;
             }
             for (int e = 128 + lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
@@ -790,6 +928,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         atomicAdd(&A.counters[kDpEntries], dp_entries);
         atomicAdd(&A.counters[kInfeasible], n_infeasible);
         if (overflow) atomicAdd(&A.counters[kOverflow], 1ull);
+        atomicAdd(&A.counters[kSkipped], n_skipped);
+        atomicAdd(&A.counters[kAlgOps], ops + 8ull * dp_entries);
     }
 }
 
