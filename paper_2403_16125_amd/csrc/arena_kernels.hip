@@ -30,10 +30,11 @@ constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree pro
 constexpr int kPad = 8;            // prefix arrays hold +inf past the last layer
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
+constexpr int kUD = kLmax + kPad;  // the recursion row D sits right after the prefix U
 
 struct WaveLds {
     double U[kLmax + kPad];       // cost prefix of the wave's current problem (+inf padded)
-    double D[kLmax + kPad];       // partition recursion row, updated in place
+    double D[kLmax + kPad];       // partition recursion row, updated in place (D = U + kUD)
     double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
     uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
     double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
@@ -295,8 +296,10 @@ __device__ __forceinline__ int from_next_lane(int v, int last)
 // At c = i the first term is D_{k-1}(i) >= U_i - U_{i-1} (every partition of
 // the first i layers has a stage holding layer i-1 whole) or +inf, so the
 // minimum is U_i - U_{i-1}, the value of the only split left.
-__device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int hi, int i, int lb, int& jp)
+__device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int lb, int& jp)
 {
+    const double* U = UD;
+    double* D = UD + kUD;
     const bool act = i <= hi;
     double v = 0.0;
     if (act) {
@@ -306,10 +309,14 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
         const bool f1 = D[a + 1] >= Ui - U[a + 1];
         const bool f2 = D[a + 2] >= Ui - U[a + 2];
         const bool f3 = D[a + 3] >= Ui - U[a + 3];
-        int c = f0 ? a : f1 ? a + 1 : f2 ? a + 2 : a + 3;
-        if (!(f0 | f1 | f2 | f3)) {
+        int off = f3 ? 3 : 4;                      // first passing candidate, 4 if none
+        off = f2 ? 2 : off;
+        off = f1 ? 1 : off;
+        off = f0 ? 0 : off;
+        int c = a + off;
+        if (off == 4) {
             // rare: crossing in (a+3, i]; i passes without a look
-            int lo = a + 4, b = i, step = 1;
+            int lo = c, b = i, step = 1;
             while (lo < b) {
                 int p = lo + step - 1;
                 p = p < b - 1 ? p : b - 1;
@@ -343,9 +350,10 @@ __device__ __forceinline__ void dp_entry(const double* U, double* D, int k, int 
 // a lower bound for row k.  After each row, D[hi+1] = +inf marks the first
 // position the row did not reach.
 template <class OnTarget>
-__device__ void solve_dp(const double* U, double* D, int L, Mask tm, int lane, unsigned long long& entries,
-                         OnTarget&& on_target)
+__device__ void solve_dp(double* UD, int L, Mask tm, int lane, unsigned long long& entries, OnTarget&& on_target)
 {
+    const double* U = UD;
+    double* D = UD + kUD;
     int tau = tm.next(1);
     if (tau == 0) return;
     unsigned n_ent = 0;
@@ -373,8 +381,8 @@ __device__ void solve_dp(const double* U, double* D, int L, Mask tm, int lane, u
         const int nb1 = from_next_lane(jp1, jp1);
         const int lb0 = jp0 > nb0 ? jp0 : nb0;
         const int lb1 = jp1 > nb1 ? jp1 : nb1;
-        if (hi - k >= 64) dp_entry(U, D, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
-        dp_entry(U, D, k, hi, k + lane, lb0, jp0);
+        if (hi - k >= 64) dp_entry(UD, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
+        dp_entry(UD, k, hi, k + lane, lb0, jp0);
         if (lane == 0) D[hi + 1] = kInf;
         n_ent += (unsigned)(hi - k + 1);
         wave_sync();
@@ -746,14 +754,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             tm = ballot_mask(ok0, ok1);
         }
         if (!tm.any()) continue;
-        const double* U = B.Upure;
         if (s > 0) {
             build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp,
                            true);
-            U = Wv.U;
+        } else {
+            for (int e = lane; e < kLmax + kPad; e += 64) Wv.U[e] = B.Upure[e];
+            wave_sync();
         }
         double* Wrow = B.Wtab[s];
-        solve_dp(U, Wv.D, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
+        solve_dp(Wv.U, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
             if (lane == 0) Wrow[pp] = W;
             return m;
         });
@@ -828,7 +837,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                     lim = best * (1.0 + A.tie_eps);
                 }
             } else {
-                solve_dp(Wv.U, Wv.D, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
+                solve_dp(Wv.U, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
                     best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, W, np, overflow, ops));
                     lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
@@ -888,12 +897,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             // re-derive the winner's bottleneck and cuts
             const int var = (jb.moe && dp * tp == 1) ? 1 : 0;
             const int slot = find_slot(B, n_slots, jb.moe, tp, var);
-            const double* U;
+            const double* U = Wv.U;
             if (slot == 0) {
-                U = B.Upure;
+                for (int e = lane; e < kLmax + kPad; e += 64) Wv.U[e] = B.Upure[e];
+                wave_sync();
             } else {
                 build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
-                U = Wv.U;
             }
             double W = 0.0;
             if (slot >= 0) {
@@ -903,7 +912,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 one.lo = pp <= 64 ? (1ull << (pp - 1)) : 0ull;
                 one.hi = pp > 64 ? (1ull << (pp - 65)) : 0ull;
                 unsigned long long scratch_entries = 0;
-                solve_dp(U, Wv.D, jb.L, one, lane, scratch_entries, [&](int, double Wk, Mask mk) {
+                solve_dp(Wv.U, jb.L, one, lane, scratch_entries, [&](int, double Wk, Mask mk) {
                     W = Wk;
                     return mk;
                 });
