@@ -68,11 +68,14 @@ struct BlockLds {
 
 // ------------------------------------------------------------ wave helpers
 
+// Orders the LDS accesses of the lanes of one wave: its memory operations
+// execute in order, so wavefront-scope fences only stop the compiler from
+// moving accesses across (no wait for completion).
 __device__ __forceinline__ void wave_sync()
 {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ double bcast(double v, int src)
