@@ -40,6 +40,7 @@ struct WaveLds {
     double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
     int32_t mq[kMaxM];            // those microbatch counts
     double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
+    unsigned long long tally[kNumCounters];   // the wave's work tallies (lane 0 updates)
     uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
 
@@ -165,6 +166,12 @@ __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane
         }
     }
     wave_sync();
+}
+
+// Adds a wave-uniform amount to one of the wave's tallies.
+__device__ __forceinline__ void tally(WaveLds& Wv, int lane, int which, unsigned long long v)
+{
+    if (lane == 0) Wv.tally[which] += v;
 }
 
 // ------------------------------------------------------------ model pieces
@@ -353,8 +360,9 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
 // a lower bound for row k.  After each row, D[hi+1] = +inf marks the first
 // position the row did not reach.
 template <class OnTarget>
-__device__ void solve_dp(double* UD, int L, Mask tm, int lane, unsigned long long& entries, OnTarget&& on_target)
+__device__ void solve_dp(WaveLds& Wv, int L, Mask tm, int lane, OnTarget&& on_target)
 {
+    double* UD = Wv.U;
     const double* U = UD;
     double* D = UD + kUD;
     int tau = tm.next(1);
@@ -394,7 +402,7 @@ __device__ void solve_dp(double* UD, int L, Mask tm, int lane, unsigned long lon
             tau = tm.next(k + 1);
         }
     }
-    entries += n_ent;
+    tally(Wv, lane, kDpEntries, n_ent);
     wave_sync();
 }
 
@@ -501,7 +509,7 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
 template <int SLOTS>
 __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
-                               double W, int& np, unsigned long long& overflow, unsigned long long& ops)
+                               double W, int& np)
 {
     const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
@@ -544,7 +552,7 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     }
     const unsigned long long amask = __ballot(adm);
     const int nadm = __popcll(amask);
-    ops += 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull);
+    tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull));
     if (nadm == 0) return kInf;
     const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32),
                                                __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
@@ -580,7 +588,7 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     }
     np += nadm;
     if (np > kMaxPlans) {
-        overflow = 1;
+        tally(Wv, lane, kOverflow, 1);
         np = kMaxPlans;
     }
     if (lo >= nadm) return kInf;
@@ -738,8 +746,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     __syncthreads();
     const int n_slots = B.n_slots;
 
-    unsigned long long n_plans = 0, n_problems = 0, dp_entries = 0, n_infeasible = 0, overflow = 0, n_skipped = 0;
-    unsigned long long ops = 0;      // algorithmic operations besides the recursion entries
+    if (lane < kNumCounters) Wv.tally[lane] = 0ull;
+    wave_sync();
 
     for (int s = wid; s < n_slots; s += kWavesPerBlock) {
         const int tp = B.slot_tp[s], var = B.slot_var[s];
@@ -765,12 +773,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             wave_sync();
         }
         double* Wrow = B.Wtab[s];
-        solve_dp(Wv.U, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
+        solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
             if (lane == 0) Wrow[pp] = W;
             return m;
         });
-        ++n_problems;
-        ops += 8ull * (unsigned)jb.L;
+        tally(Wv, lane, kProblems, 1);
+        tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
     }
     __syncthreads();
 
@@ -796,7 +804,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                         target_ok(B.mmax, jb, cell.n, 1, var, 65 + lane));
             for (int pp = tm.next(1); pp; pp = tm.next(pp + 1))
                 best = fmin(best, price_target(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp, B.Wtab[0][pp],
-                                               np, overflow, ops));
+                                               np));
         }
         // the other problems, largest tensor degree first; a degree whose
         // lower bound exceeds the tie window of `best` cannot hold the cell's
@@ -818,39 +826,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             Wv.lbnd[lane] = lb0;
             Wv.lbnd[lane + 64] = lb1;
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
-            double lim = best * (1.0 + A.tie_eps);
             {
+                const double lim = best * (1.0 + A.tie_eps);
                 const Mask keep = tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim);
-                if (keep.lo != tm.lo || keep.hi != tm.hi) n_skipped += dropped_plans(B, tm, keep, lane, cell.n / tp);
+                if (keep.lo != tm.lo || keep.hi != tm.hi)
+                    tally(Wv, lane, kSkipped, dropped_plans(B, tm, keep, lane, cell.n / tp));
                 tm = keep;
             }
             if (!tm.any()) continue;
             seq_prefix(u[0], u[1], jb.L, lane, Wv.U, Wv.D, true);
-            ops += 8ull * (unsigned)jb.L;
+            tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
             const int slot = find_slot(B, n_slots, jb.moe, tp, 0);
             if (slot > 0) {
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
-                    if (!(lbp <= lim)) {
-                        n_skipped += B.mcnt[cell.n / (tp * pp) - 1];
+                    if (!(lbp <= best * (1.0 + A.tie_eps))) {
+                        tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
                         continue;
                     }
                     best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
-                                                   np, overflow, ops));
-                    lim = best * (1.0 + A.tie_eps);
+                                                   np));
                 }
             } else {
-                solve_dp(Wv.U, jb.L, tm, lane, dp_entries, [&](int pp, double W, Mask m) {
-                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, W, np, overflow, ops));
-                    lim = best * (1.0 + A.tie_eps);
+                solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
+                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, W, np));
+                    const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
                     const Mask keep = rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim);
                     if (keep.lo != rest.lo || keep.hi != rest.hi)
-                        n_skipped += dropped_plans(B, rest, keep, lane, cell.n / tp);
+                        tally(Wv, lane, kSkipped, dropped_plans(B, rest, keep, lane, cell.n / tp));
                     return keep;
                 });
-                ++n_problems;
+                tally(Wv, lane, kProblems, 1);
             }
         }
         wave_sync();
@@ -860,9 +868,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         for (int e = lane; e < np; e += 64) tl = fmin(tl, Wv.planT[e]);
         const double tmin = wave_reduce1<OpMin>(tl);
         const long long cidx = ((long long)j * A.n_types + g) * A.n_counts + ci;
-        n_plans += (unsigned long long)np;
+        tally(Wv, lane, kPlans, (unsigned long long)np);
         if (!(tmin < kInf)) {
-            ++n_infeasible;
+            tally(Wv, lane, kInfeasible, 1);
             if (lane == 0) {
                 A.t_iter[cidx] = __builtin_huge_valf();
                 A.thr[cidx] = 0.0f;
@@ -914,11 +922,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 Mask one;
                 one.lo = pp <= 64 ? (1ull << (pp - 1)) : 0ull;
                 one.hi = pp > 64 ? (1ull << (pp - 65)) : 0ull;
-                unsigned long long scratch_entries = 0;
-                solve_dp(Wv.U, jb.L, one, lane, scratch_entries, [&](int, double Wk, Mask mk) {
+                const unsigned long long e0 = Wv.tally[kDpEntries];   // the cuts' rerun is not tallied
+                solve_dp(Wv, jb.L, one, lane, [&](int, double Wk, Mask mk) {
                     W = Wk;
                     return mk;
                 });
+                if (lane == 0) Wv.tally[kDpEntries] = e0;
             }
             const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
@@ -935,13 +944,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
     if (lane == 0) {
         if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
-        atomicAdd(&A.counters[kPlans], n_plans);
-        atomicAdd(&A.counters[kProblems], n_problems);
-        atomicAdd(&A.counters[kDpEntries], dp_entries);
-        atomicAdd(&A.counters[kInfeasible], n_infeasible);
-        if (overflow) atomicAdd(&A.counters[kOverflow], 1ull);
-        atomicAdd(&A.counters[kSkipped], n_skipped);
-        atomicAdd(&A.counters[kAlgOps], ops + 8ull * dp_entries);
+        const unsigned long long* t = Wv.tally;
+        atomicAdd(&A.counters[kPlans], t[kPlans]);
+        atomicAdd(&A.counters[kProblems], t[kProblems]);
+        atomicAdd(&A.counters[kDpEntries], t[kDpEntries]);
+        atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
+        if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
+        atomicAdd(&A.counters[kSkipped], t[kSkipped]);
+        atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
     }
 }
 
