@@ -30,11 +30,11 @@ constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree pro
 constexpr int kPad = 8;            // prefix arrays hold +inf past the last layer
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
-constexpr int kUD = kLmax + kPad;  // the recursion row D sits right after the prefix U
 
 struct WaveLds {
-    double U[kLmax + kPad];       // cost prefix of the wave's current problem (+inf padded)
-    double D[kLmax + kPad];       // partition recursion row, updated in place (D = U + kUD)
+    // the wave's current problem, pairs (U_j, D_j): U the cost prefix (+inf
+    // padded), D the partition recursion row, updated in place
+    alignas(16) double UD[2 * (kLmax + kPad)];
     double planT[kMaxPlans];      // iteration time of each plan of the cell (+inf: does not fit)
     uint32_t planKey[kMaxPlans];  // pp << 12 | tp << 7 | m
     double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
@@ -148,21 +148,23 @@ __device__ __forceinline__ double wave_reduce1(double x)
 // of a prefix must not depend on a reduction tree.  The values are staged in
 // `tmp` (LDS) and one lane accumulates them in order: one add per layer.
 // With `pad`, out[L+1 .. kLmax+kPad-1] = +inf (out has kLmax + kPad entries).
+// Element e of out (tmp) sits at out[e * OS] (tmp[e * TS]).
+template <int OS, int TS>
 __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane, double* out, double* tmp,
                                            bool pad)
 {
-    if (lane < L) tmp[lane] = v0;
-    if (lane + 64 < L) tmp[lane + 64] = v1;
+    if (lane < L) tmp[lane * TS] = v0;
+    if (lane + 64 < L) tmp[(lane + 64) * TS] = v1;
     if (pad)
-        for (int e = L + 1 + lane; e < kLmax + kPad; e += 64) out[e] = kInf;
+        for (int e = L + 1 + lane; e < kLmax + kPad; e += 64) out[e * OS] = kInf;
     wave_sync();
     if (lane == 0) {
         double acc = 0.0;
         out[0] = 0.0;
 #pragma unroll 8
         for (int i = 0; i < L; ++i) {
-            acc = acc + tmp[i];
-            out[i + 1] = acc;
+            acc = acc + tmp[i * TS];
+            out[(i + 1) * OS] = acc;
         }
     }
     wave_sync();
@@ -217,14 +219,16 @@ __device__ __forceinline__ void layer_costs(const float* t, const float* x, cons
     }
 }
 
-// Per-sample cost of each layer, prefix-summed into U (+inf past L).
+// Per-sample cost of each layer, prefix-summed into U (+inf past L; element
+// e at U[e * OS]), staged in tmp (element e at tmp[2 e]).
+template <int OS>
 __device__ void build_prefix_u(const float* t, const float* x, const float* q, double* U, double* tmp,
                                int lane, const JobCtx& jb, const TypeDev& ty, double kappa, int tp,
                                bool a2a_on)
 {
     double u[2];
     layer_costs(t, x, q, lane, jb, ty, kappa, tp, a2a_on, u);
-    seq_prefix(u[0], u[1], jb.L, lane, U, tmp, true);
+    seq_prefix<OS, 2>(u[0], u[1], jb.L, lane, U, tmp, true);
 }
 
 __device__ __forceinline__ bool adm_ok(const uint8_t* mmax, int dp)
@@ -308,17 +312,17 @@ __device__ __forceinline__ int from_next_lane(int v, int last)
 // minimum is U_i - U_{i-1}, the value of the only split left.
 __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int lb, int& jp)
 {
-    const double* U = UD;
-    double* D = UD + kUD;
+    // U_j = UD[2j], D_j = UD[2j+1]
     const bool act = i <= hi;
     double v = 0.0;
     if (act) {
-        const double Ui = U[i];
+        const double Ui = UD[2 * i];
         const int a = lb > k - 1 ? lb : k - 1;   // every j < a fails
-        const bool f0 = D[a] >= Ui - U[a];
-        const bool f1 = D[a + 1] >= Ui - U[a + 1];
-        const bool f2 = D[a + 2] >= Ui - U[a + 2];
-        const bool f3 = D[a + 3] >= Ui - U[a + 3];
+        const double* P = UD + 2 * a;
+        const bool f0 = P[1] >= Ui - P[0];
+        const bool f1 = P[3] >= Ui - P[2];
+        const bool f2 = P[5] >= Ui - P[4];
+        const bool f3 = P[7] >= Ui - P[6];
         int off = f3 ? 3 : 4;                      // first passing candidate, 4 if none
         off = f2 ? 2 : off;
         off = f1 ? 1 : off;
@@ -330,24 +334,24 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
             while (lo < b) {
                 int p = lo + step - 1;
                 p = p < b - 1 ? p : b - 1;
-                if (D[p] >= Ui - U[p]) { b = p; break; }
+                if (UD[2 * p + 1] >= Ui - UD[2 * p]) { b = p; break; }
                 lo = p + 1;
                 step <<= 1;
             }
             while (lo < b) {
                 const int mid = (lo + b) >> 1;
-                if (D[mid] >= Ui - U[mid]) b = mid; else lo = mid + 1;
+                if (UD[2 * mid + 1] >= Ui - UD[2 * mid]) b = mid; else lo = mid + 1;
             }
             c = lo;
         }
         jp = c;
-        const double dc = D[c];
-        const double t = Ui - U[c - 1];
+        const double dc = UD[2 * c + 1];
+        const double t = Ui - UD[2 * c - 2];
         v = (c >= k && t < dc) ? t : dc;
     }
     // every lane has read row k-1 before any lane overwrites it
     __asm__ volatile("" ::: "memory");
-    if (act) D[i] = v;
+    if (act) UD[2 * i + 1] = v;
 }
 
 // Bottleneck W*(pp) = D_pp(L) for the degrees in `tm`, handed to
@@ -362,9 +366,7 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
 template <class OnTarget>
 __device__ void solve_dp(WaveLds& Wv, int L, Mask tm, int lane, OnTarget&& on_target)
 {
-    double* UD = Wv.U;
-    const double* U = UD;
-    double* D = UD + kUD;
+    double* UD = Wv.UD;
     int tau = tm.next(1);
     if (tau == 0) return;
     unsigned n_ent = 0;
@@ -373,13 +375,13 @@ __device__ void solve_dp(WaveLds& Wv, int L, Mask tm, int lane, OnTarget&& on_ta
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
             const int i = 1 + lane + 64 * s;
-            if (i <= hi) D[i] = U[i];
+            if (i <= hi) UD[2 * i + 1] = UD[2 * i];
         }
-        if (lane == 0) D[hi + 1] = kInf;
+        if (lane == 0) UD[2 * hi + 3] = kInf;
         n_ent += (unsigned)hi;
         wave_sync();
         if (tau == 1) {
-            tm = on_target(1, U[L], tm);
+            tm = on_target(1, UD[2 * L], tm);
             tau = tm.next(2);
         }
     }
@@ -394,11 +396,11 @@ __device__ void solve_dp(WaveLds& Wv, int L, Mask tm, int lane, OnTarget&& on_ta
         const int lb1 = jp1 > nb1 ? jp1 : nb1;
         if (hi - k >= 64) dp_entry(UD, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
         dp_entry(UD, k, hi, k + lane, lb0, jp0);
-        if (lane == 0) D[hi + 1] = kInf;
+        if (lane == 0) UD[2 * hi + 3] = kInf;
         n_ent += (unsigned)(hi - k + 1);
         wave_sync();
         if (k == tau) {
-            tm = on_target(k, D[L], tm);
+            tm = on_target(k, UD[2 * L + 1], tm);
             tau = tm.next(k + 1);
         }
     }
@@ -419,6 +421,7 @@ struct Stages {
     int lo0, lo1, hi0, hi1;
 };
 
+template <int S>
 __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L, int pp, double W)
 {
     Stages r;
@@ -433,20 +436,20 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     int cur0 = 0, cur1 = 0;
     const int e0 = 1 + lane, e1 = 65 + lane;
     if (e0 <= L) {
-        const double Ue = U[e0];
+        const double Ue = U[e0 * S];
         int pos = 0;
 #pragma unroll
         for (int step = 32; step >= 1; step >>= 1)
-            if (Ue - U[pos + step - 1] > W) pos += step;
+            if (Ue - U[(pos + step - 1) * S] > W) pos += step;
         cur0 = pos;
         J[e0] = (uint8_t)pos;
     }
     if (L > 64 && e1 <= L) {
-        const double Ue = U[e1];
+        const double Ue = U[e1 * S];
         int pos = 0;
 #pragma unroll
         for (int step = 64; step >= 1; step >>= 1)
-            if (Ue - U[pos + step - 1] > W) pos += step;
+            if (Ue - U[(pos + step - 1) * S] > W) pos += step;
         cur1 = pos;
         J[e1] = (uint8_t)pos;
     }
@@ -506,12 +509,12 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
 // top of the admissible list; the first one is found by bisection.  Returns
 // the iteration time of the largest admissible count if it fits (+inf if
 // not): a plan of the cell, so an upper bound of the cell's best time.
-template <int SLOTS>
+template <int SLOTS, int S>
 __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
                                double W, int& np)
 {
-    const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
+    const Stages sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
     const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
@@ -534,7 +537,7 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     wave_reduce<OpMax, 1>(rm);
     const double sumX = rs[0];
     const double pmax = rm[0];
-    const double sumS = U[jb.L];   // the stages tile the layers: sum of stage costs
+    const double sumS = U[jb.L * S];   // the stages tile the layers: sum of stage costs
     const double ar = (dp > 1)
         ? pmax * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
         : 0.0;
@@ -691,13 +694,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const float* src = (wid == 0 ? A.p : A.a) + off;
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
-        seq_prefix(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.D, false);
+        seq_prefix<1, 2>(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.UD + 1, false);
         if (wid == 0) {
             const double pm = wave_reduce1<OpMax>(fmax(v0, v1));
             if (lane == 0) B.p_layer_max = pm;
         }
     } else if (wid == 2) {
-        build_prefix_u(B.t, B.x, B.q, B.Upure, Wv.D, lane, jb, ty, 1.0, 1, false);
+        build_prefix_u<1>(B.t, B.x, B.q, B.Upure, Wv.UD + 1, lane, jb, ty, 1.0, 1, false);
     } else {
         bool same = true;
         for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
@@ -766,10 +769,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         }
         if (!tm.any()) continue;
         if (s > 0) {
-            build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, (double)A.kappa[g * A.n_counts], tp,
-                           true);
+            build_prefix_u<2>(B.t, B.x, B.q, Wv.UD, Wv.UD + 1, lane, jb, ty, (double)A.kappa[g * A.n_counts],
+                              tp, true);
         } else {
-            for (int e = lane; e < kLmax + kPad; e += 64) Wv.U[e] = B.Upure[e];
+            for (int e = lane; e < kLmax + kPad; e += 64) Wv.UD[2 * e] = B.Upure[e];
             wave_sync();
         }
         double* Wrow = B.Wtab[s];
@@ -803,7 +806,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, 1, var, 1 + lane),
                                         target_ok(B.mmax, jb, cell.n, 1, var, 65 + lane));
             for (int pp = tm.next(1); pp; pp = tm.next(pp + 1))
-                best = fmin(best, price_target(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp, B.Wtab[0][pp],
+                best = fmin(best, price_target<SLOTS, 1>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp, B.Wtab[0][pp],
                                                np));
         }
         // the other problems, largest tensor degree first; a degree whose
@@ -834,7 +837,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 tm = keep;
             }
             if (!tm.any()) continue;
-            seq_prefix(u[0], u[1], jb.L, lane, Wv.U, Wv.D, true);
+            seq_prefix<2, 2>(u[0], u[1], jb.L, lane, Wv.UD, Wv.UD + 1, true);
             tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
             const int slot = find_slot(B, n_slots, jb.moe, tp, 0);
             if (slot > 0) {
@@ -844,12 +847,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
                         continue;
                     }
-                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
+                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
                                                    np));
                 }
             } else {
                 solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
-                    best = fmin(best, price_target(B, Wv, Wv.U, lane, mv, jb, ty, cell, tp, pp, W, np));
+                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W, np));
                     const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
@@ -908,12 +911,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             // re-derive the winner's bottleneck and cuts
             const int var = (jb.moe && dp * tp == 1) ? 1 : 0;
             const int slot = find_slot(B, n_slots, jb.moe, tp, var);
-            const double* U = Wv.U;
+            const double* U = Wv.UD;
             if (slot == 0) {
-                for (int e = lane; e < kLmax + kPad; e += 64) Wv.U[e] = B.Upure[e];
+                for (int e = lane; e < kLmax + kPad; e += 64) Wv.UD[2 * e] = B.Upure[e];
                 wave_sync();
             } else {
-                build_prefix_u(B.t, B.x, B.q, Wv.U, Wv.D, lane, jb, ty, cell.kappa, tp, var == 0);
+                build_prefix_u<2>(B.t, B.x, B.q, Wv.UD, Wv.UD + 1, lane, jb, ty, cell.kappa, tp, var == 0);
             }
             double W = 0.0;
             if (slot >= 0) {
@@ -929,7 +932,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 });
                 if (lane == 0) Wv.tally[kDpEntries] = e0;
             }
-            const Stages sg = canonical_stages(U, Wv.J, lane, jb.L, pp, W);
+            const Stages sg = canonical_stages<2>(U, Wv.J, lane, jb.L, pp, W);
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
