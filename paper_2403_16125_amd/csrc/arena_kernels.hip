@@ -433,64 +433,66 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     // next(e): the failing c (U_e - U_c > W) form a prefix of [0, e); c = e-1
     // passes (W is at least every single-layer cost) and so does every c > e-1
     // (U is non-decreasing and +inf past L)
-    int cur0 = 0, cur1 = 0;
+    // binary lifting of both halves in step (lanes past L read the +inf
+    // padding and store nothing)
+    const bool two = L > 64;
     const int e0 = 1 + lane, e1 = 65 + lane;
-    if (e0 <= L) {
-        const double Ue = U[e0 * S];
-        int pos = 0;
+    int cur0 = 0, cur1 = 0;
+    {
+        const double Ue0 = U[e0 * S];
+        if (two) {
+            const double Ue1 = U[e1 * S];
+            cur1 = Ue1 - U[63 * S] > W ? 64 : 0;
 #pragma unroll
-        for (int step = 32; step >= 1; step >>= 1)
-            if (Ue - U[(pos + step - 1) * S] > W) pos += step;
-        cur0 = pos;
-        J[e0] = (uint8_t)pos;
-    }
-    if (L > 64 && e1 <= L) {
-        const double Ue = U[e1 * S];
-        int pos = 0;
+            for (int step = 32; step >= 1; step >>= 1) {
+                const bool g0 = Ue0 - U[(cur0 + step - 1) * S] > W;
+                const bool g1 = Ue1 - U[(cur1 + step - 1) * S] > W;
+                cur0 += g0 ? step : 0;
+                cur1 += g1 ? step : 0;
+            }
+        } else {
 #pragma unroll
-        for (int step = 64; step >= 1; step >>= 1)
-            if (Ue - U[(pos + step - 1) * S] > W) pos += step;
-        cur1 = pos;
-        J[e1] = (uint8_t)pos;
+            for (int step = 32; step >= 1; step >>= 1)
+                cur0 += Ue0 - U[(cur0 + step - 1) * S] > W ? step : 0;
+        }
     }
+    // lanes past L follow node 0 (a fixed point) so every read stays in range
+    cur0 = e0 <= L ? cur0 : 0;
+    cur1 = (two && e1 <= L) ? cur1 : 0;
+    if (e0 <= L) J[e0] = (uint8_t)cur0;
+    if (two && e1 <= L) J[e1] = (uint8_t)cur1;
     if (lane < levels) J[lane * kLevelStride] = 0;
     wave_sync();
     for (int s = 1; s < levels; ++s) {
         const uint8_t* prev = J + (s - 1) * kLevelStride;
         uint8_t* lev = J + s * kLevelStride;
-        if (e0 <= L) cur0 = prev[cur0];
-        if (L > 64 && e1 <= L) cur1 = prev[cur1];
+        cur0 = prev[cur0];
+        if (two) cur1 = prev[cur1];
         if (e0 <= L) lev[e0] = (uint8_t)cur0;
-        if (L > 64 && e1 <= L) lev[e1] = (uint8_t)cur1;
+        if (two && e1 <= L) lev[e1] = (uint8_t)cur1;
         wave_sync();
     }
-    // c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0, c_pp = L
-    int cA = 0, cB = 0;
-    {
-        const int k = lane;
-        if (k >= 1 && k < pp) {
-            const int d = pp - k;
-            int node = L;
-            for (int s = 0; s < levels; ++s) {
-                const int nd = J[s * kLevelStride + node];
-                node = ((d >> s) & 1) ? nd : node;
-            }
-            cA = node > k ? node : k;
+    // c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0, c_pp = L.  Every
+    // lane walks (nodes stay in [0, L]); only lanes 1 <= k < pp keep the result.
+    const bool hi_half = pp >= 64;
+    const int k0 = lane, k1 = lane + 64;
+    const int d0 = pp - k0, d1 = pp - k1;
+    int n0 = L, n1 = L;
+    for (int s = 0; s < levels; ++s) {
+        const uint8_t* lev = J + s * kLevelStride;
+        const int nd0 = lev[n0];
+        n0 = ((d0 >> s) & 1) ? nd0 : n0;
+        if (hi_half) {
+            const int nd1 = lev[n1];
+            n1 = ((d1 >> s) & 1) ? nd1 : n1;
         }
-        cA = k == pp ? L : cA;
     }
-    if (pp >= 64) {
-        const int k = lane + 64;
-        if (k < pp) {
-            const int d = pp - k;
-            int node = L;
-            for (int s = 0; s < levels; ++s) {
-                const int nd = J[s * kLevelStride + node];
-                node = ((d >> s) & 1) ? nd : node;
-            }
-            cB = node > k ? node : k;
-        }
-        cB = k == pp ? L : cB;
+    int cA = (k0 >= 1 && k0 < pp) ? (n0 > k0 ? n0 : k0) : 0;
+    cA = k0 == pp ? L : cA;
+    int cB = 0;
+    if (hi_half) {
+        cB = k1 < pp ? (n1 > k1 ? n1 : k1) : 0;
+        cB = k1 == pp ? L : cB;
     }
     // stage s ends where stage s+1 starts: the next lane's cut (lane 63 of the
     // low half takes c_64, lane 63 of the high half c_128)
@@ -805,9 +807,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const int var = jb.moe ? 1 : 0;
             const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, 1, var, 1 + lane),
                                         target_ok(B.mmax, jb, cell.n, 1, var, 65 + lane));
-            for (int pp = tm.next(1); pp; pp = tm.next(pp + 1))
-                best = fmin(best, price_target<SLOTS, 1>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp, B.Wtab[0][pp],
-                                               np));
+            if (tm.any()) {
+                // bounds with the exact bottleneck; a degree is priced unless its
+                // bound is past the tie window of the best plan so far
+                const double ULp = B.Upure[jb.L];
+                const double lb0 = tm.test(1 + lane) ? target_bound(B, jb, ty, cell, gpn_divs, 1, 1 + lane, ULp) : kInf;
+                const double lb1 = (jb.L > 64 && tm.test(65 + lane))
+                    ? target_bound(B, jb, ty, cell, gpn_divs, 1, 65 + lane, ULp) : kInf;
+                Wv.lbnd[lane] = lb0;
+                Wv.lbnd[lane + 64] = lb1;
+                wave_sync();
+                for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
+                    const double lbp = Wv.lbnd[pp - 1];
+                    if (!(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
+                        tally(Wv, lane, kSkipped, B.mcnt[cell.n / pp - 1]);
+                        continue;
+                    }
+                    best = fmin(best, price_target<SLOTS, 1>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
+                                                             B.Wtab[0][pp], np));
+                }
+            }
         }
         // the other problems, largest tensor degree first; a degree whose
         // lower bound exceeds the tie window of `best` cannot hold the cell's
