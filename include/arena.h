@@ -173,6 +173,14 @@ arena_status arena_set_kappa(arena_ctx* ctx, const float* kappa_host, int32_t n)
 arena_status arena_set_plan_space(arena_ctx* ctx, const int32_t* m_values, int32_t n_m,
                                   double tie_eps);
 
+/* Bound pruning of the plan search (default: on).  With it, a pipeline
+ * degree whose lower bound of the iteration time lies above the tie window of
+ * a plan already priced, or none of whose stage splits fits memory, is not
+ * priced, and the partition recursion stops after the last degree still
+ * wanted.  The results are identical either way; only the work differs (see
+ * plans_skipped).  0 turns it off, any other value on. */
+arena_status arena_set_bound_pruning(arena_ctx* ctx, int32_t enabled);
+
 /* Size of the plan space of the bound tables (host computation, no HIP
  * call).  Needs jobs, grids and plan space bound. */
 arena_status arena_space_size_get(const arena_ctx* ctx, arena_space_size* out);

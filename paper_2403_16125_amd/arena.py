@@ -28,7 +28,7 @@ CUTS_STRIDE = MAX_LAYERS  # bytes of cut row per cell used by this binding
 EXPORTED = (
     "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
-    "arena_space_size_get", "arena_estimate", "arena_get_counters",
+    "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
 )
 
 
@@ -98,6 +98,8 @@ def load():
     lib.arena_set_kappa.restype = st
     lib.arena_set_plan_space.argtypes = [vp, vp, i32, ctypes.c_double]
     lib.arena_set_plan_space.restype = st
+    lib.arena_set_bound_pruning.argtypes = [vp, i32]
+    lib.arena_set_bound_pruning.restype = st
     lib.arena_space_size_get.argtypes = [vp, ctypes.POINTER(SpaceSize)]
     lib.arena_space_size_get.restype = st
     lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
@@ -184,6 +186,10 @@ def arena_set_plan_space(ctx, m_values, tie_eps: float) -> None:
     _check(ctx, load().arena_set_plan_space(ctx, _ptr(m), len(m), float(tie_eps)))
 
 
+def arena_set_bound_pruning(ctx, enabled: bool) -> None:
+    _check(ctx, load().arena_set_bound_pruning(ctx, 1 if enabled else 0))
+
+
 def arena_space_size_get(ctx) -> dict:
     s = SpaceSize()
     _check(ctx, load().arena_space_size_get(ctx, ctypes.byref(s)))
@@ -219,7 +225,7 @@ class Estimator:
 
     `workload` is any object with the attributes of workloads.Workload."""
 
-    def __init__(self, workload, device: int = 0, with_cuts: bool = False):
+    def __init__(self, workload, device: int = 0, with_cuts: bool = False, prune: bool = True):
         import torch
         self.torch = torch
         self.w = workload
@@ -238,6 +244,7 @@ class Estimator:
                              workload.bw_inter, workload.gpus_per_node, workload.counts)
             arena_set_plan_space(self.ctx, workload.m_values, workload.tie_eps)
             arena_set_kappa(self.ctx, workload.kappa[0])
+            arena_set_bound_pruning(self.ctx, prune)
             C = workload.n_cells
             self.n_cells = C
             self.t_iter = torch.empty(C, dtype=torch.float32, device=self.dev)

@@ -43,6 +43,7 @@ struct arena_ctx {
     bool space_set = false;
     std::vector<int32_t> m_values;
     double tie_eps = 1e-6;
+    bool prune = true;
 
     // cached space size
     bool size_valid = false;
@@ -509,6 +510,14 @@ arena_status arena_set_plan_space(arena_ctx* c, const int32_t* m_values, int32_t
     return ARENA_OK;
 }
 
+arena_status arena_set_bound_pruning(arena_ctx* c, int32_t enabled)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    c->prune = enabled != 0;
+    return ARENA_OK;
+}
+
 arena_status arena_space_size_get(const arena_ctx* cc, arena_space_size* out)
 {
     arena_ctx* c = const_cast<arena_ctx*>(cc);
@@ -565,6 +574,7 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.n_m = (int32_t)ms.size();
     for (int i = 0; i < A.n_m; ++i) A.m_values[i] = ms[i];
     A.tie_eps = c->tie_eps;
+    A.prune = c->prune ? 1 : 0;
     A.t_iter = t_iter;
     A.thr = thr;
     A.plan = plan;

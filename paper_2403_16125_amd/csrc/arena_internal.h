@@ -42,6 +42,7 @@ struct EstimateArgs {
     int32_t n_m;
     int32_t m_values[kMaxM];
     double tie_eps;
+    int32_t prune;                // bound pruning on
     float* t_iter;
     float* thr;
     uint32_t* plan;

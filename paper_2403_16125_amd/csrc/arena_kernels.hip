@@ -819,7 +819,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 wave_sync();
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
-                    if (!(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
+                    if (A.prune && !(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / pp - 1]);
                         continue;
                     }
@@ -850,7 +850,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
             {
                 const double lim = best * (1.0 + A.tie_eps);
-                const Mask keep = tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim);
+                const Mask keep = A.prune ? tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim)
+                                          : tm;
                 if (keep.lo != tm.lo || keep.hi != tm.hi)
                     tally(Wv, lane, kSkipped, dropped_plans(B, tm, keep, lane, cell.n / tp));
                 tm = keep;
@@ -862,7 +863,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             if (slot > 0) {
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
-                    if (!(lbp <= best * (1.0 + A.tie_eps))) {
+                    if (A.prune && !(lbp <= best * (1.0 + A.tie_eps))) {
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
                         continue;
                     }
@@ -875,7 +876,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                     const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
-                    const Mask keep = rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim);
+                    const Mask keep = A.prune ? rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim)
+                                              : rest;
                     if (keep.lo != rest.lo || keep.hi != rest.hi)
                         tally(Wv, lane, kSkipped, dropped_plans(B, rest, keep, lane, cell.n / tp));
                     return keep;

@@ -197,3 +197,38 @@ def test_invalid_device_values_are_rejected():
         assert (est.t_iter.cpu() == 7.0).all()      # nothing written
     finally:
         est.close()
+
+
+def _both_modes(w, rnd, with_cuts):
+    out = {}
+    for prune in (True, False):
+        est = arena.Estimator(w, with_cuts=with_cuts, prune=prune)
+        try:
+            if rnd:
+                est.set_round(rnd)
+            est.estimate()
+            out[prune] = (est.results(), est.counters(), est.space_size())
+        finally:
+            est.close()
+    return out
+
+
+@pytest.mark.parametrize("name,rnd,with_cuts", [("full", 3, False), ("trace", 0, True), ("moe", 0, True)])
+def test_bound_pruning_is_exact(name, rnd, with_cuts):
+    """Bound pruning changes only the work: every cell (and every cut row) is
+    bitwise identical with it on and off, and every plan is either priced or
+    skipped."""
+    w = wl.make(name)
+    _say(f"{name} round {rnd}: {w.n_cells} cells with and without bound pruning")
+    out = _both_modes(w, rnd, with_cuts)
+    (a, ca, size), (b, cb, _) = out[True], out[False]
+    keys = ("t_iter", "thr", "plan") + (("cuts",) if with_cuts else ())
+    for k in keys:
+        assert np.array_equal(a[k], b[k]), k
+    _say(f"  pruned: {ca['plans']} plans priced, {ca['plans_skipped']} skipped, {ca['dp_entries']} entries; "
+         f"exhaustive: {cb['plans']} plans, {cb['dp_entries']} entries")
+    assert cb["plans_skipped"] == 0 and cb["plans"] == size["plans"]
+    assert ca["plans"] + ca["plans_skipped"] == size["plans"]
+    # shared problems (one contention factor per type) are solved whole either way
+    assert ca["plans_skipped"] > 0 and ca["dp_entries"] <= cb["dp_entries"]
+    assert ca["infeasible_cells"] == cb["infeasible_cells"]
