@@ -40,6 +40,7 @@ struct WaveLds {
     double bq[kMaxM];             // samples per microbatch of the admissible counts, ascending m
     int32_t mq[kMaxM];            // those microbatch counts
     double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
+    uint8_t tq[64];               // a problem's requested degrees, compacted
     unsigned long long tally[kNumCounters];   // the wave's work tallies (lane 0 updates)
     uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
@@ -58,6 +59,7 @@ struct BlockLds {
     uint8_t mcnt[kMaxDp];         // [dp-1]: how many listed m have dp*m dividing the batch
     double p_layer_max;           // largest parameter bytes of one layer
     double x_layer_min;           // smallest boundary activation bytes of one layer
+    double x_sum, q_sum;          // sums over the layers of x and of the all-to-all bytes
     int32_t slot_tp[SLOTS];
     int32_t slot_var[SLOTS];
     int32_t n_slots;
@@ -244,13 +246,16 @@ __device__ __forceinline__ bool target_ok(const uint8_t* adm, const JobCtx& jb, 
                                           int variant, int pp)
 {
     const int qn = n / tp;
-    if (pp > jb.L || pp > qn || qn % pp != 0) return false;
+    if (pp > jb.L || pp > qn) return false;
+    // qn / pp when pp divides qn (qn <= 1024: the float quotient is within 1e-3)
+    const int d = (int)rintf((float)qn * __builtin_amdgcn_rcpf((float)pp));
+    if (__umul24(d, pp) != qn) return false;
     if (variant == 0) {
         if (jb.moe && pp >= n) return false;
     } else if (pp != n) {
         return false;
     }
-    return adm_ok(adm, qn / pp);
+    return adm_ok(adm, d);
 }
 
 // Degrees as a 128-bit mask (bit pp-1), uniform across the wave.
@@ -644,6 +649,29 @@ __device__ __forceinline__ unsigned long long dropped_plans(const BlockLds<SLOTS
     return (unsigned long long)wave_reduce1<OpSum>(c);
 }
 
+// Lower bounds of the degrees in `tm` into Wv.lbnd[pp - 1], one lane per
+// degree (a problem requests at most 32 degrees: the divisors of n / tp).
+template <int SLOTS>
+__device__ __forceinline__ void degree_bounds(const BlockLds<SLOTS>& B, WaveLds& Wv, const Mask& tm, int lane,
+                                              const JobCtx& jb, const TypeDev& ty, const Cell& cell,
+                                              unsigned gpn_divs, int tp, double UL)
+{
+    const bool b0 = (tm.lo >> lane) & 1ull, b1 = (tm.hi >> lane) & 1ull;
+    const unsigned r0 = __builtin_amdgcn_mbcnt_hi((unsigned)(tm.lo >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo((unsigned)tm.lo, 0u));
+    const unsigned r1 = (unsigned)__popcll(tm.lo) +
+                        __builtin_amdgcn_mbcnt_hi((unsigned)(tm.hi >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo((unsigned)tm.hi, 0u));
+    if (b0 && r0 < 64u) Wv.tq[r0] = (uint8_t)(1 + lane);
+    if (b1 && r1 < 64u) Wv.tq[r1] = (uint8_t)(65 + lane);
+    wave_sync();
+    if (lane < tm.count()) {
+        const int pp = Wv.tq[lane];
+        Wv.lbnd[pp - 1] = target_bound(B, jb, ty, cell, gpn_divs, tp, pp, UL);
+    }
+    wave_sync();
+}
+
 // Slot of the shared problem (tp, variant), -1 if the cell solves its own.
 template <int SLOTS>
 __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, bool moe, int tp, int var)
@@ -710,7 +738,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const double x0 = lane < jb.L ? (double)A.x[off + lane] : kInf;
         const double x1 = lane + 64 < jb.L ? (double)A.x[off + lane + 64] : kInf;
         const double xm = wave_reduce1<OpMin>(fmin(x0, x1));
+        const double xs = wave_reduce1<OpSum>((lane < jb.L ? (double)A.x[off + lane] : 0.0) +
+                                              (lane + 64 < jb.L ? (double)A.x[off + lane + 64] : 0.0));
+        const double qs = wave_reduce1<OpSum>((lane < jb.L ? (double)A.q[off + lane] : 0.0) +
+                                              (lane + 64 < jb.L ? (double)A.q[off + lane + 64] : 0.0));
         if (lane == 0) {
+            B.x_sum = xs;
+            B.q_sum = qs;
             B.uniform = uni ? 1 : 0;
             B.next_cell = 0;
             B.moe = jb.moe ? 1 : 0;
@@ -810,13 +844,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             if (tm.any()) {
                 // bounds with the exact bottleneck; a degree is priced unless its
                 // bound is past the tie window of the best plan so far
-                const double ULp = B.Upure[jb.L];
-                const double lb0 = tm.test(1 + lane) ? target_bound(B, jb, ty, cell, gpn_divs, 1, 1 + lane, ULp) : kInf;
-                const double lb1 = (jb.L > 64 && tm.test(65 + lane))
-                    ? target_bound(B, jb, ty, cell, gpn_divs, 1, 65 + lane, ULp) : kInf;
-                Wv.lbnd[lane] = lb0;
-                Wv.lbnd[lane + 64] = lb1;
-                wave_sync();
+                degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, 1, B.Upure[jb.L]);
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
                     if (A.prune && !(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
@@ -839,16 +867,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
                                   target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
             if (!tm.any()) continue;
-            double u[2];
-            layer_costs(B.t, B.x, B.q, lane, jb, ty, cell.kappa, tp, true, u);
-            const double UL = wave_reduce1<OpSum>(u[0] + u[1]);
-            const double lb0 = tm.test(1 + lane) ? target_bound(B, jb, ty, cell, gpn_divs, tp, 1 + lane, UL) : kInf;
-            const double lb1 = (jb.L > 64 && tm.test(65 + lane))
-                ? target_bound(B, jb, ty, cell, gpn_divs, tp, 65 + lane, UL) : kInf;
-            Wv.lbnd[lane] = lb0;
-            Wv.lbnd[lane + 64] = lb1;
+            // the layer costs sum to at least this (the job's sums of x and of the
+            // all-to-all bytes in the cost formula; margin for the rounding)
+            double ULb = B.Upure[jb.L] / (double)tp +
+                         cell.kappa * 8.0 * (double)(tp - 1) / (double)tp * B.x_sum / ty.bw_intra;
+            if (jb.moe) ULb += cell.kappa * B.q_sum / ty.bw_inter;
+            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, tp, ULb * (1.0 - 1e-12));
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
             {
+                const double lb0 = Wv.lbnd[lane], lb1 = Wv.lbnd[lane + 64];
                 const double lim = best * (1.0 + A.tie_eps);
                 const Mask keep = A.prune ? tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim)
                                           : tm;
@@ -857,6 +884,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 tm = keep;
             }
             if (!tm.any()) continue;
+            double u[2];
+            layer_costs(B.t, B.x, B.q, lane, jb, ty, cell.kappa, tp, true, u);
             seq_prefix<2, 2>(u[0], u[1], jb.L, lane, Wv.UD, Wv.UD + 1, true);
             tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
             const int slot = find_slot(B, n_slots, jb.moe, tp, 0);
