@@ -170,3 +170,24 @@ def test_space_size_matches_enumeration(ctx, name):
     assert s["plans"] == total
     assert s["max_plans_per_cell"] == mx
     assert s["max_layers"] == int(np.diff(w.layer_offset).max())
+
+
+def test_bound_pruning_switch(ctx):
+    lib = arena.load()
+    assert lib.arena_set_bound_pruning(None, 1) == arena.ARENA_ERR_INVALID_ARG
+    arena.arena_set_bound_pruning(ctx, False)     # any state; host only
+    arena.arena_set_bound_pruning(ctx, True)
+
+
+def test_unsorted_microbatch_counts_accepted(ctx):
+    # the library sorts them for the kernel; the caller's order is free
+    arena.arena_set_plan_space(ctx, [8, 1, 4, 2], 1e-6)
+
+
+def test_counter_struct_layout():
+    # the binding's view of arena_counters matches the header's field order
+    src = open(HEADER).read()
+    body = re.search(r"typedef struct arena_counters \{(.*?)\} arena_counters;", src, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"int64_t\s+(\w+);", body)
+    assert fields == [f for f, _ in arena.Counters._fields_]

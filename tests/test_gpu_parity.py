@@ -232,3 +232,15 @@ def test_bound_pruning_is_exact(name, rnd, with_cuts):
     # shared problems (one contention factor per type) are solved whole either way
     assert ca["plans_skipped"] > 0 and ca["dp_entries"] <= cb["dp_entries"]
     assert ca["infeasible_cells"] == cb["infeasible_cells"]
+
+
+def test_microbatch_order_irrelevant():
+    """The plan space is a set: the order of the listed microbatch counts
+    (sorted by the library for the kernel) does not change any result."""
+    import dataclasses
+    w = wl.make("small")
+    w2 = dataclasses.replace(w, m_values=np.ascontiguousarray(w.m_values[::-1]))
+    a, _, _ = _run(w)
+    b, _, _ = _run(w2)
+    for k in ("t_iter", "thr", "plan", "cuts"):
+        assert np.array_equal(a[k], b[k]), k
