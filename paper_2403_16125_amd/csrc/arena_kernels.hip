@@ -41,6 +41,9 @@ struct WaveLds {
     int32_t mq[kMaxM];            // those microbatch counts
     double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
     uint8_t tq[64];               // a problem's requested degrees, compacted
+    uint8_t cutrow[kLmax];        // with cuts on: the cut row of the degree holding the best time
+    double cut_T;                 //   that time (+inf: none yet)
+    int32_t cut_tp, cut_pp;       //   and its degrees
     unsigned long long tally[kNumCounters];   // the wave's work tallies (lane 0 updates)
     uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
@@ -519,7 +522,7 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
 template <int SLOTS, int S>
 __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
-                               double W, int& np)
+                               double W, int& np, bool keep_cuts)
 {
     const Stages sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
@@ -602,7 +605,18 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
         np = kMaxPlans;
     }
     if (lo >= nadm) return kInf;
-    return bcast(T, 63 - __clzll(amask));   // the largest admissible count fits
+    const double best_t = bcast(T, 63 - __clzll(amask));   // the largest admissible count fits
+    if (keep_cuts && best_t < Wv.cut_T) {
+        // the cell's best time so far: keep this degree's cut row for the output
+        if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sg.hi0;
+        if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sg.hi1;
+        if (lane == 0) {
+            Wv.cut_T = best_t;
+            Wv.cut_tp = tp;
+            Wv.cut_pp = pp;
+        }
+    }
+    return best_t;
 }
 
 // Lower bound of the iteration time of every plan of degree pp (any listed m)
@@ -835,6 +849,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         cell.c_p2p = cell.kappa * 2.0 / cell.B_pp;
         int np = 0;
         double best = kInf;          // time of a fitting plan priced so far: bounds the cell's best
+        if (lane == 0) Wv.cut_T = kInf;
 
         // plans of the pure-compute problem first: their bottlenecks are shared
         {
@@ -852,7 +867,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                         continue;
                     }
                     best = fmin(best, price_target<SLOTS, 1>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
-                                                             B.Wtab[0][pp], np));
+                                                             B.Wtab[0][pp], np, A.cuts != nullptr));
                 }
             }
         }
@@ -897,11 +912,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                         continue;
                     }
                     best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
-                                                   np));
+                                                   np, A.cuts != nullptr));
                 }
             } else {
                 solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
-                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W, np));
+                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W, np,
+                                                             A.cuts != nullptr));
                     const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
@@ -957,7 +973,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             A.plan[cidx] = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) |
                            ((unsigned)m << 24) | (1u << 31);
         }
-        if (A.cuts) {
+        if (A.cuts && Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf) {
+            // the winner is the degree kept while pricing (cuts depend on tp and pp only)
+            uint8_t* row = A.cuts + cidx * A.cuts_stride;
+            for (int e = lane; e < A.cuts_stride; e += 64)
+                row[e] = (e < pp - 1) ? Wv.cutrow[e] : (uint8_t)0xFF;
+        } else if (A.cuts) {
             // re-derive the winner's bottleneck and cuts
             const int var = (jb.moe && dp * tp == 1) ? 1 : 0;
             const int slot = find_slot(B, n_slots, jb.moe, tp, var);
