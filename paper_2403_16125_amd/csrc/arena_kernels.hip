@@ -327,14 +327,18 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
         const double Ui = UD[2 * i];
         const int a = lb > k - 1 ? lb : k - 1;   // every j < a fails
         const double* P = UD + 2 * a;
+        // two candidates for every lane, two more only where neither passed
+        // (an inactive lane moves no LDS data)
         const bool f0 = P[1] >= Ui - P[0];
         const bool f1 = P[3] >= Ui - P[2];
-        const bool f2 = P[5] >= Ui - P[4];
-        const bool f3 = P[7] >= Ui - P[6];
-        int off = f3 ? 3 : 4;                      // first passing candidate, 4 if none
-        off = f2 ? 2 : off;
-        off = f1 ? 1 : off;
+        int off = f1 ? 1 : 2;
         off = f0 ? 0 : off;
+        if (off == 2) {
+            const bool f2 = P[5] >= Ui - P[4];
+            const bool f3 = P[7] >= Ui - P[6];
+            off = f3 ? 3 : 4;
+            off = f2 ? 2 : off;
+        }
         int c = a + off;
         if (off == 4) {
             // rare: crossing in (a+3, i]; i passes without a look
