@@ -1,0 +1,163 @@
+"""CPU oracle of one scheduling step over the throughput matrix.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/ and nothing on the product path.
+
+Follows the event-driven scheduling of Sec. 3.5 (Algorithm 1) with the
+throughput-maximisation objective of Eq. 5, written out with plain loops.
+The paper leaves the inner steps open; the readings used here are:
+
+S1  Queued jobs are visited in the given queue order (the caller sorts by
+    priority class, smaller first).
+S2  A job launches on the grid (type g, count n) with the highest throughput
+    among grids with throughput > 0 and n <= the free GPUs of type g; ties go
+    to the smaller count, then the lower type.  Jobs stay on one type
+    (intra-job homogeneity, Sec. 3.5).
+S3  If it cannot launch, the in-flight job whose scale-down loses the least
+    throughput per GPU freed is scaled down (GetOptimalScaleDown): a job on a
+    type where the queued job has some grid with throughput > 0 moves to the
+    largest smaller count with throughput > 0; cost = (thr(n) - thr(n')) /
+    (n - n') in float64 from the float32 matrix; ties go to the lower job id.
+S4  Scale-downs repeat until the job launches or D of them were made; if it
+    still cannot launch they are undone and the job stays queued.
+S5  Priority rule of Algorithm 1: lam' starts above every class; a job that
+    cannot launch sets lam' to its class if that is <= lam', and stops the
+    visit if its class is > lam'.
+S6  Then in-flight jobs are scaled up (GetOptimalScaleUp): each job's best
+    move is to the larger count n' on its type with n' - n <= the free GPUs
+    of the type and thr(n') > thr(n) that maximises (thr(n') - thr(n)) /
+    (n' - n) (ties: the smaller n'); the job with the largest such gain moves
+    (ties: the lower job id); at most D moves.
+
+Returns the new allocation, which queued jobs launched, and the move counts
+(scale-downs kept, launches, scale-ups).
+"""
+from __future__ import annotations
+
+
+def _free(thr, counts, capacity, alloc_type, alloc_count):
+    free = [int(c) for c in capacity]
+    for j in range(len(alloc_type)):
+        g = int(alloc_type[j])
+        if g >= 0:
+            free[g] -= int(counts[int(alloc_count[j])])
+    return free
+
+
+def launch_grid(thr_j, counts, free):
+    """S2: best grid of one job under the free GPUs, or None."""
+    best = None
+    for g in range(len(free)):
+        for c in range(len(counts)):
+            v = float(thr_j[g][c])
+            if v > 0.0 and int(counts[c]) <= free[g]:
+                key = (-v, int(counts[c]), g)
+                if best is None or key < best[0]:
+                    best = (key, g, c)
+    return None if best is None else (best[1], best[2])
+
+
+def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types):
+    """S3: (cost, job, new count index) of the cheapest scale-down, or None."""
+    best = None
+    for i in range(len(alloc_type)):
+        g = int(alloc_type[i])
+        if g < 0 or g not in usable_types:
+            continue
+        c = int(alloc_count[i])
+        c2 = c - 1
+        while c2 >= 0 and not float(thr[i][g][c2]) > 0.0:
+            c2 -= 1
+        if c2 < 0:
+            continue
+        cost = (float(thr[i][g][c]) - float(thr[i][g][c2])) / float(int(counts[c]) - int(counts[c2]))
+        if best is None or cost < best[0]:
+            best = (cost, i, c2)
+    return best
+
+
+def scale_up_move(thr, counts, alloc_type, alloc_count, free):
+    """S6: (gain, job, new count index) of the best scale-up, or None."""
+    best = None
+    for i in range(len(alloc_type)):
+        g = int(alloc_type[i])
+        if g < 0:
+            continue
+        c = int(alloc_count[i])
+        n, t = int(counts[c]), float(thr[i][g][c])
+        mine = None
+        for c2 in range(c + 1, len(counts)):
+            dn = int(counts[c2]) - n
+            if dn > free[g]:
+                break
+            t2 = float(thr[i][g][c2])
+            if t2 > t:
+                gain = (t2 - t) / float(dn)
+                if mine is None or gain > mine[0]:
+                    mine = (gain, c2)
+        if mine is not None and (best is None or mine[0] > best[0]):
+            best = (mine[0], i, mine[1])
+    return best
+
+
+def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, depth):
+    """One scheduling step (Algorithm 1, readings S1-S6)."""
+    alloc_type = [int(v) for v in alloc_type]
+    alloc_count = [int(v) for v in alloc_count]
+    for k in range(1, len(counts)):
+        if not int(counts[k]) > int(counts[k - 1]):
+            raise ValueError("counts must be strictly ascending")
+    free = _free(thr, counts, capacity, alloc_type, alloc_count)
+    if any(f < 0 for f in free):
+        raise ValueError("the running jobs exceed the capacity")
+    n_types = len(free)
+    launched = [0] * len(queue)
+    kept_down = launches = 0
+    lam = max((int(p) for p in priority), default=0) + 1
+    for q in range(len(queue)):
+        j = int(queue[q])
+        usable = {g for g in range(n_types) if any(float(v) > 0.0 for v in thr[j][g])}
+        log = []
+        while True:
+            grid = launch_grid(thr[j], counts, free)
+            if grid is not None:
+                g, c = grid
+                alloc_type[j], alloc_count[j] = g, c
+                free[g] -= int(counts[c])
+                launched[q] = 1
+                launches += 1
+                kept_down += len(log)
+                break
+            if len(log) >= depth:
+                grid = None
+            else:
+                mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable)
+                if mv is not None:
+                    _, i, c2 = mv
+                    g = alloc_type[i]
+                    log.append((i, alloc_count[i]))
+                    free[g] += int(counts[alloc_count[i]]) - int(counts[c2])
+                    alloc_count[i] = c2
+                    continue
+            # no launch: undo the scale-downs, newest first
+            for i, c_old in reversed(log):
+                g = alloc_type[i]
+                free[g] -= int(counts[c_old]) - int(counts[alloc_count[i]])
+                alloc_count[i] = c_old
+            break
+        if not launched[q]:
+            if int(priority[q]) <= lam:
+                lam = int(priority[q])
+            else:
+                break
+    ups = 0
+    while ups < depth:
+        mv = scale_up_move(thr, counts, alloc_type, alloc_count, free)
+        if mv is None:
+            break
+        _, i, c2 = mv
+        g = alloc_type[i]
+        free[g] -= int(counts[c2]) - int(counts[alloc_count[i]])
+        alloc_count[i] = c2
+        ups += 1
+    return dict(alloc_type=alloc_type, alloc_count=alloc_count, launched=launched,
+                moves=[kept_down, launches, ups], free=free)

@@ -1,0 +1,130 @@
+"""Pins of the scheduler oracle (CPU): hand-derived steps of Algorithm 1 under
+the throughput objective (Eq. 5), and invariants on random cluster states."""
+import numpy as np
+import pytest
+
+from oracle import scheduler_oracle as so
+from paper_2403_16125_amd import sched_states as ss
+
+
+def _thr(rows):
+    """rows: {job: [[thr per count] per type]} -> f32 [J, T, NC]"""
+    J = max(rows) + 1
+    T = len(next(iter(rows.values())))
+    NC = len(next(iter(rows.values()))[0])
+    a = np.zeros((J, T, NC), np.float32)
+    for j, r in rows.items():
+        a[j] = np.asarray(r, np.float32)
+    return a
+
+
+def test_launch_takes_the_fastest_grid_that_fits():
+    thr = _thr({0: [[10, 18, 30], [12, 20, 25]]})
+    r = so.schedule(thr, [1, 2, 4], [4, 4], [-1], [0], [0], [0], 4)
+    assert r["launched"] == [1] and (r["alloc_type"][0], r["alloc_count"][0]) == (0, 2)
+    # only 2 GPUs of type 0 free: type 1 with 4 GPUs (25) beats type 0 with 2 (18)
+    r = so.schedule(thr, [1, 2, 4], [2, 4], [-1], [0], [0], [0], 4)
+    assert (r["alloc_type"][0], r["alloc_count"][0]) == (1, 2)
+
+
+def test_launch_ties_go_to_fewer_gpus_then_lower_type():
+    thr = _thr({0: [[10, 20, 20], [5, 20, 20]]})
+    r = so.schedule(thr, [1, 2, 4], [4, 4], [-1], [0], [0], [0], 4)
+    assert (r["alloc_type"][0], r["alloc_count"][0]) == (0, 1)
+
+
+def _scale_down_case():
+    # job 0 queued (needs 2 GPUs); jobs 1 and 2 each run on 2 of the 4 GPUs.
+    # Scaling job 1 from 2 to 1 GPU costs 19 - 10 = 9 per GPU, job 2 costs 20 - 3 = 17.
+    thr = _thr({0: [[0, 50, 80]], 1: [[10, 19, 0]], 2: [[3, 20, 0]]})
+    return thr, [1, 2, 4], [4], [-1, 0, 0], [0, 1, 1], [0], [0]
+
+
+def test_scale_down_cheapest_first_until_the_job_fits():
+    thr, counts, cap, at, ac, q, p = _scale_down_case()
+    r = so.schedule(thr, counts, cap, at, ac, q, p, 4)
+    # job 1 goes to 1 GPU (cost 9), one GPU is not enough, job 1 has no smaller
+    # count left, so job 2 goes to 1 GPU (cost 17); job 0 then runs on 2 GPUs
+    assert r["launched"] == [1]
+    assert r["alloc_count"] == [1, 0, 0] and r["alloc_type"] == [0, 0, 0]
+    assert r["moves"] == [2, 1, 0]
+
+
+def test_scale_downs_are_undone_when_the_depth_runs_out():
+    thr, counts, cap, at, ac, q, p = _scale_down_case()
+    r = so.schedule(thr, counts, cap, at, ac, q, p, 1)
+    assert r["launched"] == [0]
+    assert r["alloc_count"] == [0, 1, 1] and r["alloc_type"] == [-1, 0, 0]
+    assert r["moves"] == [0, 0, 0]
+
+
+def test_scale_down_only_on_types_the_queued_job_can_use():
+    # job 0 only runs on type 1; the cheap scale-down sits on type 0
+    thr = _thr({0: [[0, 0], [0, 40]], 1: [[10, 11], [0, 0]], 2: [[0, 0], [5, 30]]})
+    r = so.schedule(thr, [1, 2], [2, 2], [-1, 0, 1], [0, 1, 1], [0], [0], 4)
+    # stepping job 2 down frees one GPU of type 1, not enough for job 0: undone;
+    # job 1 (type 0, useless to job 0) is never touched
+    assert r["launched"] == [0]
+    assert r["alloc_count"] == [0, 1, 1]
+    # with 3 GPUs of type 1 the one freed GPU is enough
+    r = so.schedule(thr, [1, 2], [2, 3], [-1, 0, 1], [0, 1, 1], [0], [0], 4)
+    assert r["launched"] == [1] and r["alloc_count"][2] == 0 and r["alloc_count"][1] == 1
+
+
+def test_priority_rule_stops_after_a_failed_class():
+    # one type, 2 GPUs; a (class 0) takes both; b (class 0) fails and sets
+    # lam' = 0; c (class 1) fails -> stop; d (class 1, would fit on 1 GPU of a
+    # free cluster) is never visited
+    thr = _thr({0: [[0, 9]], 1: [[5, 8]], 2: [[0, 7]], 3: [[4, 0]]})
+    r = so.schedule(thr, [1, 2], [2], [-1] * 4, [0] * 4, [0, 1, 2, 3], [0, 0, 1, 1], 4)
+    assert r["launched"] == [1, 0, 0, 0]
+    # same class: a failed job does not stop the visit
+    thr2 = _thr({0: [[0, 9]], 1: [[0, 8]], 2: [[0, 0]], 3: [[4, 0]]})
+    r = so.schedule(thr2, [1, 2], [3], [-1] * 4, [0] * 4, [0, 1, 2, 3], [0, 0, 0, 0], 4)
+    assert r["launched"] == [1, 0, 0, 1]
+
+
+def test_scale_up_best_gain_per_gpu_first():
+    thr = _thr({0: [[5, 9, 16, 20]], 1: [[4, 10, 19, 30]]})
+    r = so.schedule(thr, [1, 2, 4, 8], [8], [0, 0], [1, 1], [], [], 8)
+    # free 4: job 1 to 4 GPUs (gain 4.5/GPU) beats job 0 (3.5/GPU); then job 0 to 4
+    assert r["alloc_count"] == [2, 2] and r["moves"] == [0, 0, 2] and r["free"] == [0]
+    r = so.schedule(thr, [1, 2, 4, 8], [8], [0, 0], [1, 1], [], [], 1)
+    assert r["alloc_count"] == [1, 2] and r["moves"] == [0, 0, 1]
+
+
+def test_scale_up_takes_the_best_step_not_the_next():
+    # from 1 GPU: to 2 gains 1/GPU, to 4 gains (40 - 10) / 3 = 10/GPU
+    thr = _thr({0: [[10, 11, 40]]})
+    r = so.schedule(thr, [1, 2, 4], [4], [0], [0], [], [], 4)
+    assert r["alloc_count"] == [2]
+
+
+def test_rejects_bad_states():
+    thr = _thr({0: [[1, 2]], 1: [[1, 2]]})
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [2], [0, 0], [1, 1], [], [], 1)     # 4 GPUs busy of 2
+    with pytest.raises(ValueError):
+        so.schedule(thr, [2, 1], [4], [-1, -1], [0, 0], [], [], 1)   # counts not ascending
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_invariants_on_random_states(seed):
+    counts = [1, 2, 4, 8, 16, 32]
+    thr = ss.synthetic_thr(seed, 60, 3, counts)
+    st = ss.random_state(seed, thr, counts, [40, 24, 16], running_frac=0.5, queued_frac=0.3, depth=4)
+    r = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
+                    st.priority, st.depth)
+    used = np.zeros(3, np.int64)
+    for j in range(st.n_jobs):
+        g = r["alloc_type"][j]
+        if g >= 0:
+            used[g] += counts[r["alloc_count"][j]]
+            assert st.thr[j, g, r["alloc_count"][j]] > 0 or st.alloc_type[j] == g
+            if st.alloc_type[j] >= 0:
+                assert g == st.alloc_type[j]        # running jobs keep their type
+    assert (used <= st.capacity).all()
+    assert list(used + np.asarray(r["free"])) == list(st.capacity)
+    assert r["moves"][2] <= st.depth
+    for q, j in enumerate(st.queue):
+        assert (r["alloc_type"][j] >= 0) == bool(r["launched"][q])
