@@ -109,6 +109,10 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
     free = _free(thr, counts, capacity, alloc_type, alloc_count)
     if any(f < 0 for f in free):
         raise ValueError("the running jobs exceed the capacity")
+    if len(set(int(j) for j in queue)) != len(queue) or any(alloc_type[int(j)] >= 0 for j in queue):
+        raise ValueError("queued jobs must be distinct and not running")
+    if any(int(p) < 0 for p in priority):
+        raise ValueError("priority classes must be >= 0")
     n_types = len(free)
     launched = [0] * len(queue)
     kept_down = launches = 0

@@ -55,10 +55,12 @@ def synthetic_thr(seed: int, n_jobs: int, n_types: int, counts) -> np.ndarray:
 
 
 def random_state(seed: int, thr: np.ndarray, counts, capacity, running_frac: float = 0.5,
-                 queued_frac: float = 0.1, n_classes: int = 3, depth: int = 8) -> SchedState:
+                 queued_frac: float = 0.1, n_classes: int = 3, depth: int = 8,
+                 max_count: int | None = None) -> SchedState:
     """A cluster state over the throughput matrix `thr`: a random share of jobs
     running on random feasible grids that fit the capacity (drawn in job
-    order), a random share queued with random priority classes."""
+    order, with at most `max_count` GPUs if given), a random share queued with
+    random priority classes."""
     J, T, NC = thr.shape
     counts = np.asarray(counts, np.int32)
     cap = np.asarray(capacity, np.int32)
@@ -71,7 +73,8 @@ def random_state(seed: int, thr: np.ndarray, counts, capacity, running_frac: flo
     for j in range(J):
         if u[3 * j] < running_frac:
             feas = [(g, c) for g in range(T) for c in range(NC)
-                    if thr[j, g, c] > 0 and used[g] + counts[c] <= cap[g]]
+                    if thr[j, g, c] > 0 and used[g] + counts[c] <= cap[g]
+                    and (max_count is None or counts[c] <= max_count)]
             if feas:
                 g, c = feas[int(u[3 * j + 1] * len(feas)) % len(feas)]
                 alloc_type[j], alloc_count[j] = g, c

@@ -106,6 +106,12 @@ def test_rejects_bad_states():
         so.schedule(thr, [1, 2], [2], [0, 0], [1, 1], [], [], 1)     # 4 GPUs busy of 2
     with pytest.raises(ValueError):
         so.schedule(thr, [2, 1], [4], [-1, -1], [0, 0], [], [], 1)   # counts not ascending
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [0, -1], [0, 0], [0], [0], 1)   # queued job already running
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [1, 1], [0, 0], 1)   # listed twice
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [1], [-1], 1)        # negative class
 
 
 @pytest.mark.parametrize("seed", [1, 2, 3])
