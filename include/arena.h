@@ -200,6 +200,56 @@ arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t*
 /* Tallies of the last arena_estimate.  Synchronises the device. */
 arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
 
+/* ------------------------------------------------------------------ */
+/* Scheduler consumer of the throughput matrix                          */
+/* ------------------------------------------------------------------ */
+
+#define ARENA_MAX_SCHED_JOBS 65536
+#define ARENA_MAX_SCHED_DEPTH 256
+#define ARENA_MAX_SCHED_CAPACITY (1 << 24)   /* GPUs of one type */
+
+/* One scheduling step over a throughput matrix (for instance the thr output
+ * of arena_estimate): event-driven scheduling with the throughput objective
+ * (Sec. 3.5, Algorithm 1, Eq. 5).  Queued jobs are visited in queue order;
+ * each launches on its fastest grid that fits the free GPUs (ties: fewer
+ * GPUs, then the lower type), or, while it does not fit and fewer than
+ * `depth` moves were made, the running job whose scale-down to its next
+ * smaller count with throughput > 0 loses the least throughput per freed GPU
+ * (on a type the queued job can use; ties: lower job id) is scaled down;
+ * moves of a job that still does not fit are undone.  A job that does not
+ * launch stops the visit if its priority class is above the smallest class
+ * that failed before it.  Finally up to `depth` scale-ups are made, each the
+ * running job's move to a larger count on its type, within the free GPUs,
+ * with the largest throughput gained per added GPU (ties: smaller count,
+ * lower job id).  Costs and gains are float64 from the float32 matrix.
+ * Running jobs keep their GPU type.  Asynchronous on `stream`; everything runs
+ * in one workgroup of the device. */
+typedef struct arena_sched_desc {
+    int32_t n_jobs, n_types, n_counts;
+    const float* thr;            /* DEVICE [n_jobs * n_types * n_counts], (j, g, c) at (j*T + g)*NC + c;
+                                    samples/s, finite and >= 0, 0 where the grid does not fit (other
+                                    values are not checked: the decisions are then unspecified) */
+    const int32_t* counts;       /* HOST [n_counts], strictly ascending, 1..ARENA_MAX_GPU_COUNT; copied */
+    const int32_t* capacity;     /* HOST [n_types], GPUs of each type, 0..ARENA_MAX_SCHED_CAPACITY; copied */
+    int32_t* alloc_type;         /* DEVICE [n_jobs] in/out: a running job's type, -1 if not running */
+    int32_t* alloc_count;        /* DEVICE [n_jobs] in/out: a running job's count index */
+    const int32_t* queue;        /* DEVICE [n_queue]: queued job ids (distinct, not running), visiting order */
+    const int32_t* priority;     /* DEVICE [n_queue]: priority class of each queued job, >= 0 */
+    int32_t n_queue;             /* 0..n_jobs */
+    int32_t depth;               /* search depth D, 1..ARENA_MAX_SCHED_DEPTH */
+    int32_t* launched;           /* DEVICE [n_queue] out: 1 if the job launched */
+    int32_t* result;             /* DEVICE [4] out: status (0 ok; 1 the running jobs exceed the
+                                    capacity; 2 an index out of range, a queued job running or listed
+                                    twice, or a negative class -- nothing is changed then), scale-downs
+                                    kept, launches, scale-ups */
+} arena_sched_desc;
+
+/* Host checks (sizes, pointers, counts, capacity, depth) return an error
+ * before anything is enqueued; device-side state errors are reported in
+ * result[0].  n_jobs <= ARENA_MAX_SCHED_JOBS, n_types <= ARENA_MAX_TYPES,
+ * n_counts <= ARENA_MAX_COUNTS. */
+arena_status arena_schedule(arena_ctx* ctx, const arena_sched_desc* d, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

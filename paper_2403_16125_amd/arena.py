@@ -1,6 +1,7 @@
 """Python binding of libarena.so: the C ABI of include/arena.h under the same
 names, plus a small `Estimator` that keeps a workload's tables resident in
-device memory.
+device memory and a `Scheduler` that runs scheduling steps over a throughput
+matrix.
 
 This module only marshals arguments.  Every step of the estimate runs in the
 HIP library; torch is used for device allocations and the current stream.
@@ -29,7 +30,11 @@ EXPORTED = (
     "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
+    "arena_schedule",
 )
+
+MAX_SCHED_JOBS = 65536
+MAX_SCHED_DEPTH = 256
 
 
 class ArenaError(RuntimeError):
@@ -58,6 +63,15 @@ class Counters(ctypes.Structure):
                 ("problems", ctypes.c_int64), ("dp_entries", ctypes.c_int64),
                 ("infeasible_cells", ctypes.c_int64), ("plans_skipped", ctypes.c_int64),
                 ("alg_ops", ctypes.c_int64)]
+
+
+class SchedDesc(ctypes.Structure):
+    _fields_ = [("n_jobs", ctypes.c_int32), ("n_types", ctypes.c_int32), ("n_counts", ctypes.c_int32),
+                ("thr", ctypes.c_void_p), ("counts", ctypes.c_void_p), ("capacity", ctypes.c_void_p),
+                ("alloc_type", ctypes.c_void_p), ("alloc_count", ctypes.c_void_p),
+                ("queue", ctypes.c_void_p), ("priority", ctypes.c_void_p),
+                ("n_queue", ctypes.c_int32), ("depth", ctypes.c_int32),
+                ("launched", ctypes.c_void_p), ("result", ctypes.c_void_p)]
 
 
 class SpaceSize(ctypes.Structure):
@@ -106,6 +120,8 @@ def load():
     lib.arena_estimate.restype = st
     lib.arena_get_counters.argtypes = [vp, ctypes.POINTER(Counters)]
     lib.arena_get_counters.restype = st
+    lib.arena_schedule.argtypes = [vp, ctypes.POINTER(SchedDesc), vp]
+    lib.arena_schedule.restype = st
     _lib = lib
     return lib
 
@@ -211,6 +227,19 @@ def arena_get_counters(ctx) -> dict:
                 infeasible_cells=c.infeasible_cells, plans_skipped=c.plans_skipped, alg_ops=c.alg_ops)
 
 
+def arena_schedule(ctx, n_jobs, n_types, n_counts, thr, counts, capacity, alloc_type, alloc_count,
+                   queue, priority, n_queue, depth, launched, result, stream=None) -> None:
+    """thr, alloc_type, alloc_count, queue, priority, launched and result are
+    device tensors (or pointers); counts and capacity are host int32 arrays."""
+    counts = np.ascontiguousarray(counts, np.int32)
+    capacity = np.ascontiguousarray(capacity, np.int32)
+    d = SchedDesc(int(n_jobs), int(n_types), int(n_counts), _ptr(thr), _ptr(counts), _ptr(capacity),
+                  _ptr(alloc_type), _ptr(alloc_count), _ptr(queue), _ptr(priority), int(n_queue),
+                  int(depth), _ptr(launched), _ptr(result))
+    sp = 0 if stream is None else int(stream)
+    _check(ctx, load().arena_schedule(ctx, ctypes.byref(d), sp))
+
+
 # ---------------------------------------------------------------- convenience
 
 def unpack_plan(words):
@@ -290,6 +319,90 @@ class Estimator:
             rows = sel(self.cuts.view(self.n_cells, CUTS_STRIDE))
             out["cuts"] = rows.cpu().numpy()
         return out
+
+    def close(self) -> None:
+        if getattr(self, "_alive", False):
+            self.torch.cuda.synchronize(self.dev)
+            arena_destroy(self.ctx)
+            self._alive = False
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Scheduler:
+    """Runs scheduling steps (arena_schedule) over a throughput matrix held in
+    device memory: `thr` is a float32 [J, T, NC] array or device tensor (the
+    thr output of an estimate, viewed as [J, T, NC], serves directly)."""
+
+    def __init__(self, thr, counts, capacity, device: int = 0):
+        import torch
+        self.torch = torch
+        self.dev = torch.device("cuda", device)
+        load()
+        self.ctx = arena_create(device)
+        self._alive = True
+        try:
+            if isinstance(thr, torch.Tensor):
+                self.thr = thr.to(self.dev, torch.float32).contiguous()
+            else:
+                self.thr = torch.as_tensor(np.ascontiguousarray(thr, np.float32)).to(self.dev)
+            if self.thr.dim() != 3:
+                raise ValueError("thr must be [jobs, types, counts]")
+            self.n_jobs, self.n_types, self.n_counts = (int(v) for v in self.thr.shape)
+            self.counts = np.ascontiguousarray(counts, np.int32)
+            self.capacity = np.ascontiguousarray(capacity, np.int32)
+            if self.counts.shape != (self.n_counts,) or self.capacity.shape != (self.n_types,):
+                raise ValueError("counts / capacity do not match thr")
+            i32 = dict(dtype=torch.int32, device=self.dev)
+            self.alloc_type = torch.empty(self.n_jobs, **i32)
+            self.alloc_count = torch.empty(self.n_jobs, **i32)
+            self.queue = torch.empty(max(1, self.n_jobs), **i32)
+            self.priority = torch.empty(max(1, self.n_jobs), **i32)
+            self.launched = torch.empty(max(1, self.n_jobs), **i32)
+            self.result = torch.empty(4, **i32)
+            self.n_queue = 0
+        except Exception:
+            self.close()
+            raise
+
+    def load_state(self, alloc_type, alloc_count, queue, priority) -> None:
+        """Copy a cluster state (allocation and queue) to the device (synchronously)."""
+        torch = self.torch
+        self.alloc_type.copy_(torch.as_tensor(np.ascontiguousarray(alloc_type, np.int32)))
+        self.alloc_count.copy_(torch.as_tensor(np.ascontiguousarray(alloc_count, np.int32)))
+        self.load_queue(queue, priority)
+
+    def load_queue(self, queue, priority) -> None:
+        """Replace the queue, keeping the allocation on the device (synchronously)."""
+        torch = self.torch
+        q = np.ascontiguousarray(queue, np.int32)
+        p = np.ascontiguousarray(priority, np.int32)
+        if q.shape != p.shape or q.ndim != 1 or len(q) > self.n_jobs:
+            raise ValueError("queue / priority must be 1-D of equal length <= n_jobs")
+        self.n_queue = len(q)
+        if len(q):
+            self.queue[: len(q)].copy_(torch.as_tensor(q))
+            self.priority[: len(q)].copy_(torch.as_tensor(p))
+        torch.cuda.synchronize(self.dev)
+
+    def step(self, depth: int, stream=None) -> None:
+        """One scheduling step on the loaded state (asynchronous)."""
+        s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
+        arena_schedule(self.ctx, self.n_jobs, self.n_types, self.n_counts, self.thr, self.counts,
+                       self.capacity, self.alloc_type, self.alloc_count, self.queue, self.priority,
+                       self.n_queue, depth, self.launched, self.result, s.cuda_stream)
+
+    def results(self) -> dict:
+        """Synchronise and copy the state after the last step to the host."""
+        self.torch.cuda.synchronize(self.dev)
+        res = self.result.cpu().numpy()
+        return dict(status=int(res[0]), moves=[int(v) for v in res[1:4]],
+                    alloc_type=self.alloc_type.cpu().numpy(), alloc_count=self.alloc_count.cpu().numpy(),
+                    launched=self.launched[: self.n_queue].cpu().numpy())
 
     def close(self) -> None:
         if getattr(self, "_alive", False):

@@ -68,6 +68,12 @@ struct arena_ctx {
     hipEvent_t kappa_done[2] = {nullptr, nullptr};
     size_t cap_hkappa = 0;
     int kslot = 0;
+
+    // scheduler: device copy of counts and capacity, staged through pinned memory
+    int32_t* d_sched = nullptr;
+    int32_t* h_sched = nullptr;
+    size_t cap_sched = 0, cap_hsched = 0;
+    hipEvent_t sched_done = nullptr;
 };
 
 namespace {
@@ -121,6 +127,12 @@ void free_device(arena_ctx* c)
     (void)hipFree(c->d_count_order);
     (void)hipFree(c->d_counters);
     (void)hipHostFree(c->h_counters);
+    (void)hipFree(c->d_sched);
+    (void)hipHostFree(c->h_sched);
+    if (c->sched_done) (void)hipEventDestroy(c->sched_done);
+    c->d_sched = c->h_sched = nullptr;
+    c->cap_sched = c->cap_hsched = 0;
+    c->sched_done = nullptr;
     for (int i = 0; i < 2; ++i) {
         (void)hipHostFree(c->h_kappa[i]);
         if (c->kappa_done[i]) (void)hipEventDestroy(c->kappa_done[i]);
@@ -608,6 +620,80 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     out->plans_skipped = (int64_t)h[arena::kSkipped];
     out->alg_ops = (int64_t)h[arena::kAlgOps];
     if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");
+    return ARENA_OK;
+}
+
+arena_status arena_schedule(arena_ctx* c, const arena_sched_desc* d, void* stream_ptr)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!d) return fail(c, ARENA_ERR_INVALID_ARG, "schedule: descriptor is NULL");
+    if (d->n_jobs < 0) return fail(c, ARENA_ERR_INVALID_ARG, "schedule: n_jobs=%d", d->n_jobs);
+    if (d->n_jobs > ARENA_MAX_SCHED_JOBS)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "schedule: %d jobs (max %d)", d->n_jobs, ARENA_MAX_SCHED_JOBS);
+    if (d->n_types < 1) return fail(c, ARENA_ERR_INVALID_ARG, "schedule: n_types must be >= 1");
+    if (d->n_types > ARENA_MAX_TYPES)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "schedule: %d types (max %d)", d->n_types, ARENA_MAX_TYPES);
+    if (d->n_counts < 1) return fail(c, ARENA_ERR_INVALID_ARG, "schedule: n_counts must be >= 1");
+    if (d->n_counts > ARENA_MAX_COUNTS)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "schedule: %d counts (max %d)", d->n_counts, ARENA_MAX_COUNTS);
+    if (d->n_queue < 0 || d->n_queue > d->n_jobs)
+        return fail(c, ARENA_ERR_INVALID_ARG, "schedule: n_queue=%d not in 0..n_jobs", d->n_queue);
+    if (d->depth < 1 || d->depth > ARENA_MAX_SCHED_DEPTH)
+        return fail(c, ARENA_ERR_INVALID_ARG, "schedule: depth=%d not in 1..%d", d->depth, ARENA_MAX_SCHED_DEPTH);
+    if (!d->counts || !d->capacity) return fail(c, ARENA_ERR_INVALID_ARG, "schedule: a host array is NULL");
+    if (!d->result || (d->n_jobs > 0 && (!d->thr || !d->alloc_type || !d->alloc_count)) ||
+        (d->n_queue > 0 && (!d->queue || !d->priority || !d->launched)))
+        return fail(c, ARENA_ERR_INVALID_ARG, "schedule: a device array is NULL");
+    for (int i = 0; i < d->n_counts; ++i) {
+        const int n = d->counts[i];
+        if (n < 1 || n > ARENA_MAX_GPU_COUNT)
+            return fail(c, ARENA_ERR_INVALID_ARG, "schedule: counts[%d]=%d not in 1..%d", i, n, ARENA_MAX_GPU_COUNT);
+        if (i > 0 && n <= d->counts[i - 1])
+            return fail(c, ARENA_ERR_INVALID_ARG, "schedule: counts must be strictly ascending");
+    }
+    for (int g = 0; g < d->n_types; ++g)
+        if (d->capacity[g] < 0 || d->capacity[g] > ARENA_MAX_SCHED_CAPACITY)
+            return fail(c, ARENA_ERR_INVALID_ARG, "schedule: capacity[%d]=%d not in 0..%d", g, d->capacity[g],
+                        ARENA_MAX_SCHED_CAPACITY);
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    hipError_t e;
+    const size_t n = (size_t)arena::kMaxSchedCounts + arena::kMaxSchedTypes;
+    if (!c->sched_done && (e = hipEventCreateWithFlags(&c->sched_done, hipEventDisableTiming)))
+        return hip_fail(c, e, "hipEventCreate");
+    if ((e = ensure_capacity(&c->d_sched, &c->cap_sched, n)))
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "schedule tables: %s", hipGetErrorString(e));
+    if (!c->h_sched) {
+        if ((e = hipHostMalloc((void**)&c->h_sched, sizeof(int32_t) * n, 0)))
+            return fail(c, ARENA_ERR_OUT_OF_MEMORY, "pinned schedule staging");
+        c->cap_hsched = n;
+    }
+    // the previous call's upload must have left the staging buffer
+    if ((e = hipEventSynchronize(c->sched_done))) return hip_fail(c, e, "schedule staging wait");
+    std::memcpy(c->h_sched, d->counts, sizeof(int32_t) * d->n_counts);
+    std::memcpy(c->h_sched + arena::kMaxSchedCounts, d->capacity, sizeof(int32_t) * d->n_types);
+    if ((e = hipMemcpyAsync(c->d_sched, c->h_sched, sizeof(int32_t) * n, hipMemcpyHostToDevice, stream)) ||
+        (e = hipEventRecord(c->sched_done, stream)))
+        return hip_fail(c, e, "schedule table upload");
+    arena::SchedArgs A;
+    std::memset(&A, 0, sizeof(A));
+    A.thr = d->thr;
+    A.counts = c->d_sched;
+    A.capacity = c->d_sched + arena::kMaxSchedCounts;
+    A.alloc_type = d->alloc_type;
+    A.alloc_count = d->alloc_count;
+    A.queue = d->queue;
+    A.priority = d->priority;
+    A.launched = d->launched;
+    A.result = d->result;
+    A.n_jobs = d->n_jobs;
+    A.n_types = d->n_types;
+    A.n_counts = d->n_counts;
+    A.n_queue = d->n_queue;
+    A.depth = d->depth;
+    if ((e = arena::launch_schedule(A, stream))) return hip_fail(c, e, "schedule launch");
     return ARENA_OK;
 }
 

@@ -58,7 +58,27 @@ struct ValidateArgs {
     unsigned long long* bad;      // [1] count of non-finite or negative values
 };
 
+// One scheduling step over the throughput matrix (arena_schedule).
+constexpr int kMaxSchedTypes = 64;
+constexpr int kMaxSchedCounts = 512;
+constexpr int kMaxSchedDepth = 256;
+constexpr int kMaxSchedJobs = 65536;
+
+struct SchedArgs {
+    const float* thr;             // [J * T * NC]
+    const int32_t* counts;        // [NC] device copy, strictly ascending
+    const int32_t* capacity;      // [T] device copy
+    int32_t* alloc_type;          // [J] in/out
+    int32_t* alloc_count;         // [J] in/out
+    const int32_t* queue;         // [Q]
+    const int32_t* priority;      // [Q]
+    int32_t* launched;            // [Q] out
+    int32_t* result;              // [4] out: status, scale-downs kept, launches, scale-ups
+    int32_t n_jobs, n_types, n_counts, n_queue, depth;
+};
+
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);
+hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream);
 hipError_t launch_zero_counters(unsigned long long* counters, int n, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& args, hipStream_t stream);
 

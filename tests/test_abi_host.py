@@ -191,3 +191,59 @@ def test_counter_struct_layout():
     body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
     fields = re.findall(r"int64_t\s+(\w+);", body)
     assert fields == [f for f, _ in arena.Counters._fields_]
+
+
+def test_sched_desc_layout(tmp_path):
+    # the binding's arena_sched_desc has the C field offsets (compiled with gcc)
+    import ctypes
+    names = [f for f, _ in arena.SchedDesc._fields_]
+    prog = tmp_path / "off.c"
+    prog.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"arena.h\"\nint main(void){\n"
+                    + "".join(f'printf("%zu\\n", offsetof(arena_sched_desc, {n}));\n' for n in names)
+                    + 'printf("%zu\\n", sizeof(arena_sched_desc));\nreturn 0;}\n')
+    exe = tmp_path / "off"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(prog)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [getattr(arena.SchedDesc, n).offset for n in names] + [ctypes.sizeof(arena.SchedDesc)]
+    assert got == want
+
+
+def test_schedule_validation(ctx):
+    # every case is rejected on the host before any HIP call (the pointers are
+    # never dereferenced)
+    lib = arena.load()
+    fake = 0x1000
+    base = dict(n_jobs=4, n_types=2, n_counts=3, thr=fake, counts=[1, 2, 4], capacity=[4, 4],
+                alloc_type=fake, alloc_count=fake, queue=fake, priority=fake, n_queue=2, depth=4,
+                launched=fake, result=fake)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        with pytest.raises(arena.ArenaError) as e:
+            arena.arena_schedule(ctx, **a)
+        return e.value.status
+
+    assert lib.arena_schedule(None, None, None) == arena.ARENA_ERR_INVALID_ARG
+    assert lib.arena_schedule(ctx, None, None) == arena.ARENA_ERR_INVALID_ARG
+    assert call(n_jobs=-1) == arena.ARENA_ERR_INVALID_ARG
+    assert call(n_jobs=arena.MAX_SCHED_JOBS + 1) == arena.ARENA_ERR_UNSUPPORTED
+    assert call(n_types=0, capacity=[]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(n_types=65, capacity=[1] * 65) == arena.ARENA_ERR_UNSUPPORTED
+    assert call(n_counts=0, counts=[]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(n_counts=513, counts=list(range(1, 514))) == arena.ARENA_ERR_UNSUPPORTED
+    assert call(n_queue=5) == arena.ARENA_ERR_INVALID_ARG
+    assert call(n_queue=-1) == arena.ARENA_ERR_INVALID_ARG
+    assert call(depth=0) == arena.ARENA_ERR_INVALID_ARG
+    assert call(depth=arena.MAX_SCHED_DEPTH + 1) == arena.ARENA_ERR_INVALID_ARG
+    assert call(counts=[1, 4, 2]) == arena.ARENA_ERR_INVALID_ARG
+    assert "ascending" in arena.arena_last_error(ctx)
+    assert call(counts=[1, 2, 2]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(counts=[0, 2, 4]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(counts=[1, 2, 2048]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(capacity=[4, -1]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(capacity=[4, (1 << 24) + 1]) == arena.ARENA_ERR_INVALID_ARG
+    assert call(thr=None) == arena.ARENA_ERR_INVALID_ARG
+    assert call(result=None) == arena.ARENA_ERR_INVALID_ARG
+    assert call(queue=None) == arena.ARENA_ERR_INVALID_ARG
+    assert call(launched=None) == arena.ARENA_ERR_INVALID_ARG

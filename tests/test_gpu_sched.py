@@ -1,0 +1,228 @@
+"""Parity of the HIP scheduling step (arena_schedule) with the CPU oracle of
+Algorithm 1 under the throughput objective (Sec. 3.5, Eq. 5), through the C ABI.
+
+Both sides take every decision in float64 from the same float32 throughput
+matrix, so the agreement is exact: the new allocation of every job, which
+queued jobs launched, and the move counts.  Inputs are seeded synthetic
+throughput curves and cluster states (sched_states)."""
+import numpy as np
+import pytest
+
+from oracle import scheduler_oracle as so
+from paper_2403_16125_amd import sched_states as ss
+
+FULL_COUNTS = sorted(set([1, 2, 4] + [2 ** k for k in range(3, 11)] + list(range(8, 1025, 8))))
+
+
+def _gpu(st):
+    from paper_2403_16125_amd import arena
+    s = arena.Scheduler(st.thr, st.counts, st.capacity)
+    try:
+        s.load_state(st.alloc_type, st.alloc_count, st.queue, st.priority)
+        s.step(st.depth)
+        return s.results()
+    finally:
+        s.close()
+
+
+def _check(st):
+    print(f"schedule: J={st.n_jobs} T={st.thr.shape[1]} NC={st.thr.shape[2]} Q={len(st.queue)} "
+          f"D={st.depth}", flush=True)
+    want = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
+                       st.priority, st.depth)
+    got = _gpu(st)
+    assert got["status"] == 0
+    assert got["moves"] == want["moves"]
+    assert list(got["launched"]) == want["launched"]
+    bad = np.nonzero((got["alloc_type"] != np.asarray(want["alloc_type"])) |
+                     (got["alloc_count"] != np.asarray(want["alloc_count"])))[0]
+    assert len(bad) == 0, f"{len(bad)} jobs differ, first {bad[:8]}"
+    return want
+
+
+def _state(thr_rows, counts, capacity, alloc_type, alloc_count, queue, priority, depth):
+    J = max(thr_rows) + 1
+    T = len(next(iter(thr_rows.values())))
+    thr = np.zeros((J, T, len(counts)), np.float32)
+    for j, r in thr_rows.items():
+        thr[j] = np.asarray(r, np.float32)
+    return ss.SchedState(thr=thr, counts=np.asarray(counts, np.int32),
+                         capacity=np.asarray(capacity, np.int32),
+                         alloc_type=np.asarray(alloc_type, np.int32),
+                         alloc_count=np.asarray(alloc_count, np.int32),
+                         queue=np.asarray(queue, np.int32), priority=np.asarray(priority, np.int32),
+                         depth=int(depth))
+
+
+HAND = {
+    "launch": ({0: [[10, 18, 30], [12, 20, 25]]}, [1, 2, 4], [2, 4], [-1], [0], [0], [0], 4),
+    "launch_tie": ({0: [[10, 20, 20], [5, 20, 20]]}, [1, 2, 4], [4, 4], [-1], [0], [0], [0], 4),
+    "scale_down": ({0: [[0, 50, 80]], 1: [[10, 19, 0]], 2: [[3, 20, 0]]}, [1, 2, 4], [4],
+                   [-1, 0, 0], [0, 1, 1], [0], [0], 4),
+    "rollback": ({0: [[0, 50, 80]], 1: [[10, 19, 0]], 2: [[3, 20, 0]]}, [1, 2, 4], [4],
+                 [-1, 0, 0], [0, 1, 1], [0], [0], 1),
+    "usable_types": ({0: [[0, 0], [0, 40]], 1: [[10, 11], [0, 0]], 2: [[0, 0], [5, 30]]}, [1, 2],
+                     [2, 3], [-1, 0, 1], [0, 1, 1], [0], [0], 4),
+    "priority": ({0: [[0, 9]], 1: [[5, 8]], 2: [[0, 7]], 3: [[4, 0]]}, [1, 2], [2], [-1] * 4,
+                 [0] * 4, [0, 1, 2, 3], [0, 0, 1, 1], 4),
+    "scale_up": ({0: [[5, 9, 16, 20]], 1: [[4, 10, 19, 30]]}, [1, 2, 4, 8], [8], [0, 0], [1, 1],
+                 [], [], 8),
+    "scale_up_best_step": ({0: [[10, 11, 40]]}, [1, 2, 4], [4], [0], [0], [], [], 4),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", sorted(HAND))
+def test_hand_cases(name):
+    _check(_state(*HAND[name]))
+
+
+@pytest.mark.gpu
+def test_hand_case_values():
+    # the GPU reproduces the hand-derived outcomes the oracle is pinned to
+    got = _gpu(_state(*HAND["scale_down"]))
+    assert list(got["alloc_count"]) == [1, 0, 0] and got["moves"] == [2, 1, 0]
+    got = _gpu(_state(*HAND["rollback"]))
+    assert list(got["alloc_count"]) == [0, 1, 1] and list(got["alloc_type"]) == [-1, 0, 0]
+    got = _gpu(_state(*HAND["scale_up"]))
+    assert list(got["alloc_count"]) == [2, 2] and got["moves"] == [0, 0, 2]
+
+
+# (seed, jobs, types, counts, capacity, running share, queued share, classes, depth, max count)
+RANDOM = [
+    (1, 60, 3, [1, 2, 4, 8, 16, 32], [40, 24, 16], 0.5, 0.3, 3, 4, None),
+    (2, 60, 3, [1, 2, 4, 8, 16, 32], [40, 24, 16], 0.9, 0.1, 2, 1, None),
+    (3, 300, 4, [1, 2, 3, 4, 6, 8, 12, 16], [64, 32, 32, 16], 0.7, 0.2, 3, 8, 8),
+    (4, 1100, 5, [1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128], [256, 128, 128, 64, 64], 0.6, 0.1, 4,
+     16, 16),
+    (5, 1500, 8, [1, 2, 4, 8, 16, 32, 64], [96] * 8, 0.3, 0.3, 1, 3, 4),
+    (6, 777, 6, [1, 2, 4, 8, 16, 32, 64, 128], [200, 0, 150, 90, 60, 30], 0.8, 0.15, 3, 256, 32),
+    (7, 64, 2, [1, 2, 4, 8], [0, 0], 0.0, 0.5, 2, 3, None),            # no GPUs at all
+    (8, 200, 3, [2, 4, 8], [512, 512, 512], 0.2, 0.6, 3, 2, None),     # roomy cluster: scale-ups
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", RANDOM, ids=[f"seed{c[0]}_J{c[1]}" for c in RANDOM])
+def test_random_states(case):
+    seed, J, T, counts, cap, rf, qf, ncls, depth, mc = case
+    thr = ss.synthetic_thr(seed, J, T, counts)
+    st = ss.random_state(seed, thr, counts, cap, running_frac=rf, queued_frac=qf, n_classes=ncls,
+                         depth=depth, max_count=mc)
+    _check(st)
+
+
+def test_random_states_cover_every_move():
+    # the random cases above exercise kept scale-downs, launches, scale-ups and
+    # jobs left queued (CPU only: checked on the oracle's outcome)
+    seen = np.zeros(4, np.int64)
+    for seed, J, T, counts, cap, rf, qf, ncls, depth, mc in RANDOM:
+        thr = ss.synthetic_thr(seed, J, T, counts)
+        st = ss.random_state(seed, thr, counts, cap, running_frac=rf, queued_frac=qf,
+                             n_classes=ncls, depth=depth, max_count=mc)
+        r = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
+                        st.priority, st.depth)
+        seen[:3] += r["moves"]
+        seen[3] += len(st.queue) - sum(r["launched"])
+    assert (seen > 0).all(), seen
+
+
+@pytest.mark.gpu
+def test_full_round_matrix():
+    # the full scheduling-round size: 16384 jobs x 8 types x 131 counts, a
+    # 1280-GPU cluster, search depth 3
+    thr = ss.synthetic_thr(11, 16384, 8, FULL_COUNTS)
+    st = ss.random_state(11, thr, FULL_COUNTS, [160] * 8, running_frac=0.5, queued_frac=0.02,
+                         n_classes=3, depth=3, max_count=32)
+    want = _check(st)
+    assert want["moves"][1] > 0
+
+
+@pytest.mark.gpu
+def test_empty_queue_and_no_jobs():
+    st = _state({0: [[1, 2]], 1: [[3, 4]]}, [1, 2], [4], [0, -1], [0, 0], [], [], 2)
+    _check(st)
+    from paper_2403_16125_amd import arena
+    s = arena.Scheduler(np.zeros((0, 2, 3), np.float32), [1, 2, 4], [4, 4])
+    try:
+        s.load_state(np.zeros(0, np.int32), np.zeros(0, np.int32), [], [])
+        s.step(1)
+        r = s.results()
+        assert r["status"] == 0 and r["moves"] == [0, 0, 0]
+    finally:
+        s.close()
+
+
+@pytest.mark.gpu
+def test_largest_shapes():
+    # 64 types x 512 counts (the limits), depth 256
+    counts = list(range(1, 513))
+    thr = ss.synthetic_thr(21, 40, 64, counts)
+    st = ss.random_state(21, thr, counts, [300] * 64, running_frac=0.6, queued_frac=0.4,
+                         n_classes=2, depth=256, max_count=64)
+    _check(st)
+
+
+@pytest.mark.parametrize("kind", ["over_capacity", "queued_running", "listed_twice", "bad_type",
+                                  "bad_count", "negative_class", "queue_out_of_range"])
+@pytest.mark.gpu
+def test_bad_states_leave_everything_unchanged(kind):
+    from paper_2403_16125_amd import arena
+    base = dict(at=[0, -1, -1], ac=[1, 0, 0], q=[1, 2], p=[0, 1], cap=[4])
+    if kind == "over_capacity":
+        base.update(ac=[2, 0, 0], cap=[3])
+    elif kind == "queued_running":
+        base.update(q=[0, 2])
+    elif kind == "listed_twice":
+        base.update(q=[1, 1])
+    elif kind == "bad_type":
+        base.update(at=[1, -1, -1])
+    elif kind == "bad_count":
+        base.update(ac=[3, 0, 0])
+    elif kind == "negative_class":
+        base.update(p=[0, -1])
+    elif kind == "queue_out_of_range":
+        base.update(q=[1, 3])
+    thr = np.full((3, 1, 3), 5.0, np.float32)
+    s = arena.Scheduler(thr, [1, 2, 4], base["cap"])
+    try:
+        s.load_state(base["at"], base["ac"], base["q"], base["p"])
+        s.launched.fill_(-7)
+        s.step(2)
+        r = s.results()
+        assert r["status"] == (1 if kind == "over_capacity" else 2)
+        assert list(r["alloc_type"]) == base["at"] and list(r["alloc_count"]) == base["ac"]
+        assert (r["launched"] == -7).all()
+    finally:
+        s.close()
+
+
+@pytest.mark.gpu
+def test_repeated_steps_on_device_state():
+    # steps chain on the device-resident allocation: each step equals the
+    # oracle's step from the state the previous oracle step left; only the
+    # queue (the jobs still waiting) is uploaded between steps
+    counts = [1, 2, 4, 8, 16]
+    thr = ss.synthetic_thr(31, 400, 4, counts)
+    st = ss.random_state(31, thr, counts, [64, 48, 32, 16], running_frac=0.7, queued_frac=0.25,
+                         n_classes=3, depth=3, max_count=8)
+    from paper_2403_16125_amd import arena
+    s = arena.Scheduler(st.thr, st.counts, st.capacity)
+    try:
+        at, ac = st.alloc_type.copy(), st.alloc_count.copy()
+        queue, prio = list(st.queue), list(st.priority)
+        s.load_state(at, ac, queue, prio)
+        for step in range(4):
+            want = so.schedule(st.thr, counts, st.capacity, at, ac, queue, prio, st.depth)
+            s.step(st.depth)
+            got = s.results()
+            assert got["status"] == 0 and got["moves"] == want["moves"], step
+            assert list(got["alloc_type"]) == want["alloc_type"], step
+            assert list(got["alloc_count"]) == want["alloc_count"], step
+            at = np.asarray(want["alloc_type"], np.int32)
+            ac = np.asarray(want["alloc_count"], np.int32)
+            keep = [k for k in range(len(queue)) if not want["launched"][k]]
+            queue, prio = [queue[k] for k in keep], [prio[k] for k in keep]
+            s.load_queue(queue, prio)
+    finally:
+        s.close()
