@@ -139,6 +139,33 @@ def test_full_round_matrix():
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("n_run", [4096, 5000])
+def test_many_running_jobs(n_run):
+    # running jobs beyond what the kernel keeps in its LDS list (5000), and a
+    # list that is full at the start (4096) so that the first launch of the
+    # step overflows it: the rest of the step scans every job
+    counts = [1, 2, 4, 8]
+    J = n_run + 150
+    thr = ss.synthetic_thr(41, J, 2, counts)
+    at = np.full(J, -1, np.int32)
+    ac = np.zeros(J, np.int32)
+    used = np.zeros(2, np.int64)
+    for j in range(n_run):
+        g = j % 2
+        c = int(np.argmax(thr[j, g] > 0))     # smallest count with throughput > 0
+        assert thr[j, g, c] > 0
+        at[j], ac[j] = g, c
+        used[g] += counts[c]
+    cap = (used + 64).astype(np.int32)
+    queue = np.arange(n_run, J, dtype=np.int32)
+    st = ss.SchedState(thr=thr, counts=np.asarray(counts, np.int32), capacity=cap, alloc_type=at,
+                       alloc_count=ac, queue=queue, priority=np.zeros(len(queue), np.int32),
+                       depth=4)
+    want = _check(st)
+    assert want["moves"][0] > 0 and want["moves"][1] > 0
+
+
+@pytest.mark.gpu
 def test_empty_queue_and_no_jobs():
     st = _state({0: [[1, 2]], 1: [[3, 4]]}, [1, 2], [4], [0, -1], [0, 0], [], [], 2)
     _check(st)
