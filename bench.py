@@ -6,6 +6,10 @@ factors and estimate every (job, GPU type, GPU count) cell (16384 jobs x 8
 types x 131 counts = 17.2 M cells, about 682 M plans).  Inputs are resident in
 device memory before timing starts.  Prints one JSON line on stdout; progress
 goes to stderr.
+
+With --schedule it times instead the scheduling step that consumes such a
+matrix (Algorithm 1 with the throughput objective) on a 1280-GPU cluster
+state over the same 16384 x 8 x 131 shape, and prints that line.
 """
 from __future__ import annotations
 
@@ -58,6 +62,110 @@ def cpu_baseline(w, every: int, kappa_round: int = 0) -> dict:
                       f"{len(ids)} cells in {dt:.1f} s"}
 
 
+def schedule_cpu_baseline(st, min_seconds: float = 10.0) -> dict:
+    """The scheduler oracle (single-threaded Python) on the same state,
+    repeated until about min_seconds of CPU work."""
+    from oracle import scheduler_oracle as so
+    n, t0 = 0, time.perf_counter()
+    while True:
+        so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
+                    st.priority, st.depth)
+        n += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds and n >= 2:
+            break
+    return {"value": n / dt, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"the same state, {n} steps in {dt:.1f} s"}
+
+
+def bench_schedule(args) -> int:
+    """One step = one scheduling step (Algorithm 1, throughput objective) on
+    the full-round state, from the same starting allocation every time."""
+    import numpy as np
+    import torch
+
+    from paper_2403_16125_amd import arena, sched_states
+
+    log("generating the full-round scheduler state")
+    st = sched_states.full_round()
+    J, T, NC = st.thr.shape
+    log(f"{J} jobs x {T} types x {NC} counts, {int((st.alloc_type >= 0).sum())} running, "
+        f"{len(st.queue)} queued, depth {st.depth}")
+    dev = torch.device("cuda", 0)
+    sch = arena.Scheduler(st.thr, st.counts, st.capacity, device=0)
+    sch.load_state(st.alloc_type, st.alloc_count, st.queue, st.priority)
+    at0, ac0 = sch.alloc_type.clone(), sch.alloc_count.clone()
+    stream = torch.cuda.current_stream(dev)
+
+    def reset():
+        sch.alloc_type.copy_(at0)
+        sch.alloc_count.copy_(ac0)
+
+    for i in range(args.warmup):
+        reset()
+        sch.step(st.depth)
+        torch.cuda.synchronize(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        reset()
+        starts[i].record(stream)
+        sch.step(st.depth)
+        ends[i].record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    launch_ms = [a.elapsed_time(b) for a, b in zip(starts, ends)]
+    res = sch.results()
+    sch.close()
+    if res["status"] != 0:
+        log(f"schedule status {res['status']}")
+        return 1
+    step_s = float(np.mean(launch_ms)) / 1e3
+    log(f"timed {args.steps} steps: {wall:.3f} s wall, kernel avg {step_s * 1e3:.3f} ms, "
+        f"{res['decisions']} decisions, moves {res['moves']}")
+    achieved = res["scanned"] / step_s
+    line = {
+        "metric": "scheduling steps/sec",
+        "value": 1.0 / step_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"scheduling step over the full-round throughput matrix: {J} jobs x {T} GPU types "
+                        f"x {NC} GPU counts, 1280-GPU cluster, {int((st.alloc_type >= 0).sum())} running, "
+                        f"{len(st.queue)} queued in 3 classes, search depth {st.depth}",
+        },
+        "decisions": res["decisions"],
+        "ns_per_decision": step_s / max(1, res["decisions"]) * 1e9,
+        "moves": {"scale_downs_kept": res["moves"][0], "launches": res["moves"][1],
+                  "scale_ups": res["moves"][2]},
+        "roofline": {
+            "bound": "alu",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_LANE_OPS / 1e12,
+            "unit": "Top/s",
+            "frac": achieved / PEAK_LANE_OPS,
+            "traffic": None,
+            "ops_per_launch": res["scanned"],
+            "launch_ms": step_s * 1e3,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the scheduler oracle on the same state")
+        line["cpu_baseline"] = schedule_cpu_baseline(st)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,6 +175,8 @@ def main() -> int:
     ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
     ap.add_argument("--cpu-every", type=int, default=256, help="oracle sample: every k-th job")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--schedule", action="store_true",
+                    help="time the scheduling step that consumes the throughput matrix instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain elementwise copy of known size (HBM counter calibration)")
     args = ap.parse_args()
@@ -77,6 +187,9 @@ def main() -> int:
               "the estimator shards by job rows, but this build measures a single GPU.",
               file=sys.stderr, flush=True)
         return 2
+
+    if args.schedule:
+        return bench_schedule(args)
 
     import numpy as np
     import torch

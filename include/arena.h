@@ -238,10 +238,12 @@ typedef struct arena_sched_desc {
     int32_t n_queue;             /* 0..n_jobs */
     int32_t depth;               /* search depth D, 1..ARENA_MAX_SCHED_DEPTH */
     int32_t* launched;           /* DEVICE [n_queue] out: 1 if the job launched */
-    int32_t* result;             /* DEVICE [4] out: status (0 ok; 1 the running jobs exceed the
+    int32_t* result;             /* DEVICE [8] out: status (0 ok; 1 the running jobs exceed the
                                     capacity; 2 an index out of range, a queued job running or listed
                                     twice, or a negative class -- nothing is changed then), scale-downs
-                                    kept, launches, scale-ups */
+                                    kept, launches, scale-ups, decisions taken (launch, scale-down and
+                                    scale-up searches), candidates they examined (64-bit: low word,
+                                    high word), 0 */
 } arena_sched_desc;
 
 /* Host checks (sizes, pointers, counts, capacity, depth) return an error

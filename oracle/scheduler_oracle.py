@@ -28,8 +28,9 @@ S6  Then in-flight jobs are scaled up (GetOptimalScaleUp): each job's best
     (n' - n) (ties: the smaller n'); the job with the largest such gain moves
     (ties: the lower job id); at most D moves.
 
-Returns the new allocation, which queued jobs launched, and the move counts
-(scale-downs kept, launches, scale-ups).
+Returns the new allocation, which queued jobs launched, the move counts
+(scale-downs kept, launches, scale-ups) and the number of searches made
+(launch, scale-down and scale-up: the decisions of the step).
 """
 from __future__ import annotations
 
@@ -116,6 +117,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
     n_types = len(free)
     launched = [0] * len(queue)
     kept_down = launches = 0
+    decisions = 0
     lam = max((int(p) for p in priority), default=0) + 1
     for q in range(len(queue)):
         j = int(queue[q])
@@ -123,6 +125,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
         log = []
         while True:
             grid = launch_grid(thr[j], counts, free)
+            decisions += 1
             if grid is not None:
                 g, c = grid
                 alloc_type[j], alloc_count[j] = g, c
@@ -135,6 +138,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
                 grid = None
             else:
                 mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable)
+                decisions += 1
                 if mv is not None:
                     _, i, c2 = mv
                     g = alloc_type[i]
@@ -156,6 +160,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
     ups = 0
     while ups < depth:
         mv = scale_up_move(thr, counts, alloc_type, alloc_count, free)
+        decisions += 1
         if mv is None:
             break
         _, i, c2 = mv
@@ -164,4 +169,4 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
         alloc_count[i] = c2
         ups += 1
     return dict(alloc_type=alloc_type, alloc_count=alloc_count, launched=launched,
-                moves=[kept_down, launches, ups], free=free)
+                moves=[kept_down, launches, ups], free=free, decisions=decisions)

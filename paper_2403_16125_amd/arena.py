@@ -363,7 +363,7 @@ class Scheduler:
             self.queue = torch.empty(max(1, self.n_jobs), **i32)
             self.priority = torch.empty(max(1, self.n_jobs), **i32)
             self.launched = torch.empty(max(1, self.n_jobs), **i32)
-            self.result = torch.empty(4, **i32)
+            self.result = torch.empty(8, **i32)
             self.n_queue = 0
         except Exception:
             self.close()
@@ -400,7 +400,9 @@ class Scheduler:
         """Synchronise and copy the state after the last step to the host."""
         self.torch.cuda.synchronize(self.dev)
         res = self.result.cpu().numpy()
-        return dict(status=int(res[0]), moves=[int(v) for v in res[1:4]],
+        scanned = int(np.uint32(res[5])) | (int(np.uint32(res[6])) << 32)
+        return dict(status=int(res[0]), moves=[int(v) for v in res[1:4]], decisions=int(res[4]),
+                    scanned=scanned,
                     alloc_type=self.alloc_type.cpu().numpy(), alloc_count=self.alloc_count.cpu().numpy(),
                     launched=self.launched[: self.n_queue].cpu().numpy())
 

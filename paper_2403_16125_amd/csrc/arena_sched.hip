@@ -452,6 +452,8 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
 
     int phase = 0;
     int kept_down = 0, launches = 0, ups = 0;
+    int passes = 0;                  // decisions taken (launch, scale-down and scale-up searches)
+    unsigned long long scanned = 0;  // candidates those searches examined
     // S5: lam' starts above every class
     {
         int pm = 0;
@@ -502,6 +504,8 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
         for (;;) {
             unsigned long long usable = 0ull;
             const Best lg = launch_grid(A, S, j, buf, nlog == 0, phase, usable, eg);
+            ++passes;
+            scanned += (unsigned long long)ng;
             if (lg.aux >= 0) {
                 const int g = lg.aux / A.n_counts, c = lg.aux - g * A.n_counts;
                 if (tid == 0) {
@@ -525,6 +529,8 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             if (nlog >= A.depth) break;
             if (nlog == 0 && tid == 0) S.usable = usable;
             __syncthreads();
+            ++passes;
+            scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
             const Best sd = scale_down(A, S, phase);
             if (sd.aux < 0) break;
             if (tid == 0) {
@@ -592,6 +598,8 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
         }
     }
     while (ups < A.depth) {              // S6
+        ++passes;
+        scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
         const Best su = scale_up(A, S, phase);
         if (su.aux < 0) break;
         if (tid == 0) {
@@ -620,6 +628,10 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
         A.result[1] = kept_down;
         A.result[2] = launches;
         A.result[3] = ups;
+        A.result[4] = passes;
+        A.result[5] = (int32_t)(uint32_t)scanned;
+        A.result[6] = (int32_t)(uint32_t)(scanned >> 32);
+        A.result[7] = 0;
     }
 }
 

@@ -19,12 +19,21 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 
 
-def kernel_source_sha() -> str:
-    """Hash of every source file the HIP library is built from."""
-    files = [os.path.join(ROOT, "include", "arena.h")]
-    csrc = os.path.join(PKG, "csrc")
-    files += sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
-                    if f.endswith((".hip", ".cpp", ".h")))
+# the sources that decide what each kernel does (device code, shared
+# definitions, and the host code that prepares its launch)
+KERNEL_SOURCES = {
+    "estimate_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
+                        "paper_2403_16125_amd/csrc/arena_host.cpp",
+                        "paper_2403_16125_amd/csrc/arena_kernels.hip"),
+    "schedule_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
+                        "paper_2403_16125_amd/csrc/arena_host.cpp",
+                        "paper_2403_16125_amd/csrc/arena_sched.hip"),
+}
+
+
+def kernel_source_sha(kernel: str = "estimate_kernel") -> str:
+    """Hash of the source files one kernel is built from."""
+    files = [os.path.join(ROOT, f) for f in KERNEL_SOURCES[kernel]]
     h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
@@ -86,7 +95,7 @@ def traffic(fetch_db, write_db, copy_fetch_db, copy_write_db, kernel, copy_bytes
     w_scale = copy_bytes / (cw_kib * 1024.0)
     fetch_b = f_kib * 1024.0 * f_scale
     write_b = w_kib * 1024.0 * w_scale
-    return dict(workload=workload, kernel=kernel, kernel_source_sha=kernel_source_sha(),
+    return dict(workload=workload, kernel=kernel, kernel_source_sha=kernel_source_sha(kernel),
                 fetch_kib_per_dispatch=f_kib, write_kib_per_dispatch=w_kib,
                 copy_fetch_kib=cf_kib, copy_write_kib=cw_kib, copy_bytes=copy_bytes,
                 fetch_scale=f_scale, write_scale=w_scale,
@@ -115,7 +124,8 @@ def main() -> int:
     ds = dispatch_stats(a.db, a.kernel)
     cs = counter_stats(a.db, a.kernel)
     if a.json:
-        print(json.dumps(dict(dispatches=ds, counters=cs, kernel_source_sha=kernel_source_sha())))
+        print(json.dumps(dict(dispatches=ds, counters=cs,
+                              kernel_source_sha=kernel_source_sha(a.kernel or "estimate_kernel"))))
         return 0
     if ds:
         print(f"{'calls':>6} {'total_us':>14} {'avg_us':>14} {'min_us':>14} {'max_us':>14}  kernel")

@@ -17,7 +17,7 @@ import dataclasses
 
 import numpy as np
 
-from .workloads import SplitMix64, _stream
+from .workloads import SplitMix64, _stream, _trace_counts
 
 
 @dataclasses.dataclass
@@ -86,3 +86,16 @@ def random_state(seed: int, thr: np.ndarray, counts, capacity, running_frac: flo
                       alloc_type=alloc_type, alloc_count=alloc_count,
                       queue=np.asarray([j for _, j in queued], np.int32),
                       priority=np.asarray([p for p, _ in queued], np.int32), depth=int(depth))
+
+
+def full_round(seed: int = 11) -> SchedState:
+    """The scheduling step at the full-round size: the throughput matrix of
+    16384 jobs x 8 GPU types x 131 GPU counts (powers of two and multiples of
+    8 up to 1024), a 1280-GPU cluster (160 of each type, the size of the
+    paper's simulated cluster), about half the jobs drawn as running on up to
+    32 GPUs until the cluster is full, 2 % queued in 3 priority classes, and
+    search depth 3 (the depth used in the paper's simulations)."""
+    counts = np.asarray(_trace_counts(1024), np.int32)
+    thr = synthetic_thr(seed, 16384, 8, counts)
+    return random_state(seed, thr, counts, [160] * 8, running_frac=0.5, queued_frac=0.02,
+                        n_classes=3, depth=3, max_count=32)

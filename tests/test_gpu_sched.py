@@ -11,9 +11,6 @@ import pytest
 from oracle import scheduler_oracle as so
 from paper_2403_16125_amd import sched_states as ss
 
-FULL_COUNTS = sorted(set([1, 2, 4] + [2 ** k for k in range(3, 11)] + list(range(8, 1025, 8))))
-
-
 def _gpu(st):
     from paper_2403_16125_amd import arena
     s = arena.Scheduler(st.thr, st.counts, st.capacity)
@@ -33,6 +30,7 @@ def _check(st):
     got = _gpu(st)
     assert got["status"] == 0
     assert got["moves"] == want["moves"]
+    assert got["decisions"] == want["decisions"]
     assert list(got["launched"]) == want["launched"]
     bad = np.nonzero((got["alloc_type"] != np.asarray(want["alloc_type"])) |
                      (got["alloc_count"] != np.asarray(want["alloc_count"])))[0]
@@ -129,12 +127,9 @@ def test_random_states_cover_every_move():
 
 @pytest.mark.gpu
 def test_full_round_matrix():
-    # the full scheduling-round size: 16384 jobs x 8 types x 131 counts, a
+    # the state the benchmark times: 16384 jobs x 8 types x 131 counts, a
     # 1280-GPU cluster, search depth 3
-    thr = ss.synthetic_thr(11, 16384, 8, FULL_COUNTS)
-    st = ss.random_state(11, thr, FULL_COUNTS, [160] * 8, running_frac=0.5, queued_frac=0.02,
-                         n_classes=3, depth=3, max_count=32)
-    want = _check(st)
+    want = _check(ss.full_round())
     assert want["moves"][1] > 0
 
 

@@ -48,6 +48,9 @@ def test_scale_down_cheapest_first_until_the_job_fits():
     assert r["launched"] == [1]
     assert r["alloc_count"] == [1, 0, 0] and r["alloc_type"] == [0, 0, 0]
     assert r["moves"] == [2, 1, 0]
+    # searches: launch (fails), scale-down, launch (fails), scale-down, launch,
+    # then one scale-up search that finds no free GPU
+    assert r["decisions"] == 6
 
 
 def test_scale_downs_are_undone_when_the_depth_runs_out():
@@ -56,6 +59,7 @@ def test_scale_downs_are_undone_when_the_depth_runs_out():
     assert r["launched"] == [0]
     assert r["alloc_count"] == [0, 1, 1] and r["alloc_type"] == [-1, 0, 0]
     assert r["moves"] == [0, 0, 0]
+    assert r["decisions"] == 4      # launch, scale-down, launch, (undo), scale-up search
 
 
 def test_scale_down_only_on_types_the_queued_job_can_use():
