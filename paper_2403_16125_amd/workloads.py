@@ -32,6 +32,7 @@ _GAMMA = 0x9E3779B97F4A7C15
 
 SEQ_LEN = 1024          # tokens per sample (Sec. 5.1)
 F_REF = 1.0e14          # FLOP/s of a speed-1.0 GPU, converts FLOPs to seconds
+HBM_REF = 2.0e12        # memory bandwidth of a speed-1.0 GPU, bytes/s (scaled by speed per type)
 BASE_SEED = 240316125   # workloads use BASE_SEED + index
 
 
@@ -109,6 +110,12 @@ class Workload:
     m_values: np.ndarray       # int32 [NM]
     kappa: np.ndarray          # f32 [R, T*NC] per-grid contention factor per round
     tie_eps: float = 1e-6
+    hbm: np.ndarray | None = None   # f32 [T] memory bandwidth bytes/s (roofline loads); None: HBM_REF * speed
+
+    def hbm_bw(self) -> np.ndarray:
+        if self.hbm is not None:
+            return np.asarray(self.hbm, np.float32)
+        return (HBM_REF * self.speed.astype(np.float64)).astype(np.float32)
 
     @property
     def n_jobs(self) -> int:
