@@ -201,6 +201,59 @@ arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t*
 arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
 
 /* ------------------------------------------------------------------ */
+/* Proxy-plan planner                                                   */
+/* ------------------------------------------------------------------ */
+
+#define ARENA_MAX_PROXY_OPS 16
+
+/* The load-aware planner of Sec. 3.3, which picks one plan per grid without
+ * execution, for every cell of the bound jobs and grids (same bindings,
+ * plan space, contention factors and cell order as arena_estimate):
+ *   - the job's L layers form O = min(L, n_ops) clustered operators,
+ *     operator i holding layers floor(iL/O) .. floor((i+1)L/O) - 1;
+ *   - an operator's load is its roofline time (Eq. 2): FLOPs = f_ref * sum t
+ *     over its layers, memory traffic = sum (p + batch a); load =
+ *     max(FLOPs / (speed f_ref), traffic / hbm_bw) -- FLOPs over the rate
+ *     the roofline allows at the operator's arithmetic intensity;
+ *   - its GPU share is proportional: d_i = (load_i / sum load) n;
+ *   - for every pipeline degree s (one grid per s, Sec. 3.2) every
+ *     contiguous grouping of the operators into s stages gets power-of-two
+ *     stage GPU counts summing to n that minimise the computation bias of
+ *     Eq. 3 (the sorted pairing of each multiset; the bias summed over
+ *     stages in stage order; ties: the lexicographically larger sorted
+ *     multiset, equal shares give the larger count to the earlier stage);
+ *   - for each microbatch count B of the plan space, among groupings whose
+ *     every stage fits memory, the proxy plan has the least bias, then the
+ *     least communication load of Eq. 4, (B-1) max_j C_j + sum_j C_j +
+ *     sum_j AR_j, with each stage's (dp, tp) chosen for the least
+ *     communication per iteration within memory (ties: smaller tp), then the
+ *     lexicographically smallest cut vector;
+ *   - each grid's proxy is priced by the 1F1B model of arena_estimate with
+ *     per-stage GPU counts (samples per replica Bg / (dp_j B); point-to-point
+ *     traffic Bg / (B min(dp_j, dp_j+1)) samples per boundary); the cell
+ *     keeps the fastest grid, T within (1 + tie_eps) of the least counting as
+ *     a tie, broken by fewer stages, then fewer microbatches.
+ * Outputs (caller-owned device buffers, C cells in arena_estimate's order):
+ *   t_iter  f32 [C]  iteration time of the chosen proxy plan (+inf: no grid fits)
+ *   thr     f32 [C]  batch / t_iter (0 when infeasible)
+ *   plan    u64 [3C] word 0: bits 0-14 stage starts (bit i-1 set: a stage
+ *                    starts at operator i), bits 16-20 s, bits 24-30 B, bit
+ *                    31 feasible; word 1: log2 of each stage's GPU count,
+ *                    4 bits per stage (stage j at bits 4j); word 2: log2 of
+ *                    each stage's tensor degree, same layout.  All zero when
+ *                    infeasible.
+ * Asynchronous on `stream`.  A job whose operators all have zero load has no
+ * proxy plan. */
+typedef struct arena_proxy_desc {
+    const float* hbm_bw;   /* HOST [n_types] memory bandwidth of each type, bytes/s, finite > 0; copied */
+    double f_ref;          /* FLOP/s of a speed-1.0 GPU, finite > 0 */
+    int32_t n_ops;         /* operators per job (clusters of consecutive layers), 1..ARENA_MAX_PROXY_OPS */
+} arena_proxy_desc;
+
+arena_status arena_proxy_estimate(arena_ctx* ctx, const arena_proxy_desc* d, float* t_iter, float* thr,
+                                  uint64_t* plan, void* stream);
+
+/* ------------------------------------------------------------------ */
 /* Scheduler consumer of the throughput matrix                          */
 /* ------------------------------------------------------------------ */
 

@@ -68,6 +68,7 @@ typedef struct {
     double xlast[PO_MAX_OPS];        /* x of the operator's last layer (pipeline boundary) */
     double load[PO_MAX_OPS];         /* Eq. 2 */
     double d[PO_MAX_OPS];            /* proportional GPU share */
+    double lsum;                     /* total load; a job without any has no proxy plan */
 } pops;
 
 static void build_ops(const pjob* jb, const ptype* ty, double f_ref, int n_ops, int n, pops* o)
@@ -95,6 +96,7 @@ static void build_ops(const pjob* jb, const ptype* ty, double f_ref, int n_ops, 
         o->load[i] = compute > memory ? compute : memory;
         lsum += o->load[i];
     }
+    o->lsum = lsum;
     for (int i = 0; i < O; ++i) o->d[i] = (o->load[i] / lsum) * (double)n;
 }
 
@@ -173,6 +175,7 @@ double proxy_oracle_normalize(const double* D, int s, int n, int32_t* m_out)
         st.ord[q] = j;
     }
     for (int q = 0; q < s; ++q) st.pos[st.ord[q]] = q;
+
     int maxe = 0;
     while ((1 << (maxe + 1)) <= n) ++maxe;
     norm_rec(&st, 0, n, maxe);
@@ -398,7 +401,7 @@ static void grid_proxies(const pjob* jb, const ptype* ty, const pops* o, double 
     memset(&e, 0, sizeof(e));
     e.jb = jb; e.ty = ty; e.o = o; e.kappa = kappa; e.n = n; e.s = s;
     e.m_values = m_values; e.n_m = n_m;
-    enum_rec(&e, 0, 0);
+    if (o->lsum > 0.0) enum_rec(&e, 0, 0);      /* zero total load: no shares, no proxy */
     for (int q = 0; q < n_m; ++q) {
         out[q] = e.best[q];
         if (out[q].ok) {

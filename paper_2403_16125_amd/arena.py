@@ -30,8 +30,10 @@ EXPORTED = (
     "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
-    "arena_schedule",
+    "arena_schedule", "arena_proxy_estimate",
 )
+
+MAX_PROXY_OPS = 16
 
 MAX_SCHED_JOBS = 65536
 MAX_SCHED_DEPTH = 256
@@ -63,6 +65,10 @@ class Counters(ctypes.Structure):
                 ("problems", ctypes.c_int64), ("dp_entries", ctypes.c_int64),
                 ("infeasible_cells", ctypes.c_int64), ("plans_skipped", ctypes.c_int64),
                 ("alg_ops", ctypes.c_int64)]
+
+
+class ProxyDesc(ctypes.Structure):
+    _fields_ = [("hbm_bw", ctypes.c_void_p), ("f_ref", ctypes.c_double), ("n_ops", ctypes.c_int32)]
 
 
 class SchedDesc(ctypes.Structure):
@@ -120,6 +126,8 @@ def load():
     lib.arena_estimate.restype = st
     lib.arena_get_counters.argtypes = [vp, ctypes.POINTER(Counters)]
     lib.arena_get_counters.restype = st
+    lib.arena_proxy_estimate.argtypes = [vp, ctypes.POINTER(ProxyDesc), vp, vp, vp, vp]
+    lib.arena_proxy_estimate.restype = st
     lib.arena_schedule.argtypes = [vp, ctypes.POINTER(SchedDesc), vp]
     lib.arena_schedule.restype = st
     _lib = lib
@@ -227,6 +235,32 @@ def arena_get_counters(ctx) -> dict:
                 infeasible_cells=c.infeasible_cells, plans_skipped=c.plans_skipped, alg_ops=c.alg_ops)
 
 
+def arena_proxy_estimate(ctx, hbm_bw, f_ref: float, n_ops: int, t_iter, thr, plan, stream=None) -> None:
+    """hbm_bw: host f32 [n_types]; outputs are device tensors (or pointers)."""
+    hbm = np.ascontiguousarray(hbm_bw, np.float32)
+    d = ProxyDesc(_ptr(hbm), float(f_ref), int(n_ops))
+    sp = 0 if stream is None else int(stream)
+    _check(ctx, load().arena_proxy_estimate(ctx, ctypes.byref(d), _ptr(t_iter), _ptr(thr), _ptr(plan), sp))
+
+
+def unpack_proxy_plan(words):
+    """[C, 3] uint64 plan words -> dict of s, B, feasible, stage-start mask,
+    GPUs and tensor degree per stage ([C, 16], 0 past the last stage)."""
+    w = np.asarray(words, np.uint64).reshape(-1, 3)
+    w0 = w[:, 0]
+    s = ((w0 >> np.uint64(16)) & np.uint64(31)).astype(np.int32)
+    out = dict(s=s, B=((w0 >> np.uint64(24)) & np.uint64(127)).astype(np.int32),
+               feasible=((w0 >> np.uint64(31)) & np.uint64(1)).astype(bool),
+               starts=(w0 & np.uint64(0x7FFF)).astype(np.int64))
+    k = np.arange(16, dtype=np.uint64)
+    dexp = ((w[:, 1:2] >> (np.uint64(4) * k)) & np.uint64(15)).astype(np.int64)
+    texp = ((w[:, 2:3] >> (np.uint64(4) * k)) & np.uint64(15)).astype(np.int64)
+    live = np.arange(16)[None, :] < s[:, None]
+    out["Dn"] = np.where(live, 1 << dexp, 0).astype(np.int32)
+    out["tp"] = np.where(live, 1 << texp, 0).astype(np.int32)
+    return out
+
+
 def arena_schedule(ctx, n_jobs, n_types, n_counts, thr, counts, capacity, alloc_type, alloc_count,
                    queue, priority, n_queue, depth, launched, result, stream=None) -> None:
     """thr, alloc_type, alloc_count, queue, priority, launched and result are
@@ -295,6 +329,34 @@ class Estimator:
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
         arena_estimate(self.ctx, self.t_iter, self.thr, self.plan, self.cuts,
                        CUTS_STRIDE if self.cuts is not None else 0, s.cuda_stream)
+
+    def proxy_estimate(self, f_ref: float = 1e14, n_ops: int = 16, hbm_bw=None, stream=None) -> None:
+        """The proxy-plan planner over the same cells (outputs kept beside the
+        estimate's)."""
+        torch = self.torch
+        if getattr(self, "p_t_iter", None) is None:
+            C = self.n_cells
+            self.p_t_iter = torch.empty(C, dtype=torch.float32, device=self.dev)
+            self.p_thr = torch.empty(C, dtype=torch.float32, device=self.dev)
+            self.p_plan = torch.empty(C * 3, dtype=torch.int64, device=self.dev)
+        hbm = self.w.hbm_bw() if hbm_bw is None else hbm_bw
+        s = torch.cuda.current_stream(self.dev) if stream is None else stream
+        arena_proxy_estimate(self.ctx, hbm, f_ref, n_ops, self.p_t_iter, self.p_thr, self.p_plan,
+                             s.cuda_stream)
+
+    def proxy_results(self, ids=None) -> dict:
+        torch = self.torch
+        torch.cuda.synchronize(self.dev)
+        if ids is None:
+            sel = lambda v: v
+        else:
+            idx = torch.as_tensor(np.asarray(ids, np.int64), device=self.dev)
+            sel = lambda v: v.index_select(0, idx)
+        words = sel(self.p_plan.view(self.n_cells, 3)).cpu().numpy().view(np.uint64)
+        out = dict(t_iter=sel(self.p_t_iter).cpu().numpy(), thr=sel(self.p_thr).cpu().numpy(),
+                   words=words)
+        out.update(unpack_proxy_plan(words))
+        return out
 
     def space_size(self) -> dict:
         return arena_space_size_get(self.ctx)

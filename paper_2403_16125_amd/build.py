@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "_build", "libarena.so")
 SOURCES = [os.path.join(CSRC, "arena_host.cpp"), os.path.join(CSRC, "arena_kernels.hip"),
-           os.path.join(CSRC, "arena_sched.hip")]
+           os.path.join(CSRC, "arena_sched.hip"), os.path.join(CSRC, "arena_proxy.hip")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -69,6 +69,15 @@ struct arena_ctx {
     size_t cap_hkappa = 0;
     int kslot = 0;
 
+    // proxy planner: power-of-two multisets per (count, stage count), memory bandwidths
+    bool msets_dirty = true;
+    std::vector<unsigned long long> msets;
+    std::vector<int32_t> mset_off;
+    unsigned long long* d_msets = nullptr;
+    int32_t* d_mset_off = nullptr;
+    double* d_hbm = nullptr;
+    size_t cap_msets = 0, cap_mset_off = 0, cap_hbm = 0;
+
     // scheduler: device copy of counts and capacity, staged through pinned memory
     int32_t* d_sched = nullptr;
     int32_t* h_sched = nullptr;
@@ -127,6 +136,14 @@ void free_device(arena_ctx* c)
     (void)hipFree(c->d_count_order);
     (void)hipFree(c->d_counters);
     (void)hipHostFree(c->h_counters);
+    (void)hipFree(c->d_msets);
+    (void)hipFree(c->d_mset_off);
+    (void)hipFree(c->d_hbm);
+    c->d_msets = nullptr;
+    c->d_mset_off = nullptr;
+    c->d_hbm = nullptr;
+    c->cap_msets = c->cap_mset_off = c->cap_hbm = 0;
+    c->msets_dirty = true;
     (void)hipFree(c->d_sched);
     (void)hipHostFree(c->h_sched);
     if (c->sched_done) (void)hipEventDestroy(c->sched_done);
@@ -474,6 +491,7 @@ arena_status arena_bind_grids(arena_ctx* c, const arena_grids_desc* d)
     c->kappa.assign((size_t)d->n_types * d->n_counts, 1.0f);
     c->grids_bound = true;
     c->grids_dirty = true;
+    c->msets_dirty = true;
     c->kappa_dirty = true;
     c->order_dirty = true;
     c->size_valid = false;
@@ -620,6 +638,127 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     out->plans_skipped = (int64_t)h[arena::kSkipped];
     out->alg_ops = (int64_t)h[arena::kAlgOps];
     if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");
+    return ARENA_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Multisets of s powers of two summing to n (exponents non-increasing,
+// packed 4 bits per position, largest first), in lexicographically
+// descending order.
+void pow2_multisets(int n, int s, int k, int maxe, unsigned long long cur, std::vector<unsigned long long>& out)
+{
+    if (k == s) {
+        if (n == 0) out.push_back(cur);
+        return;
+    }
+    const int left = s - k - 1;
+    for (int e = maxe; e >= 0; --e) {
+        const int v = 1 << e;
+        if (v > n - left) continue;
+        if ((long long)(left + 1) * v < n) break;     // the rest take at most v each
+        pow2_multisets(n - v, s, k + 1, e, cur | ((unsigned long long)e << (4 * k)), out);
+    }
+}
+
+arena_status build_msets(arena_ctx* c)
+{
+    c->msets.clear();
+    c->mset_off.assign((size_t)c->n_counts * 17 + 1, 0);
+    for (int ci = 0; ci < c->n_counts; ++ci) {
+        const int n = c->counts[ci];
+        int maxe = 0;
+        while ((1 << (maxe + 1)) <= n) ++maxe;
+        for (int s = 0; s < 17; ++s) {
+            c->mset_off[(size_t)ci * 17 + s] = (int32_t)c->msets.size();
+            if (s == 0) continue;
+            const size_t before = c->msets.size();
+            pow2_multisets(n, s, 0, maxe, 0ull, c->msets);
+            if (c->msets.size() - before > (size_t)arena::kProxyMaxMultisets)
+                return fail(c, ARENA_ERR_UNSUPPORTED, "proxy: %zu power-of-two splits of %d GPUs into %d stages (max %d)",
+                            c->msets.size() - before, n, s, arena::kProxyMaxMultisets);
+        }
+    }
+    c->mset_off[(size_t)c->n_counts * 17] = (int32_t)c->msets.size();
+    return ARENA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+arena_status arena_proxy_estimate(arena_ctx* c, const arena_proxy_desc* d, float* t_iter, float* thr,
+                                  uint64_t* plan, void* stream_ptr)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (!c->jobs_bound || !c->grids_bound || !c->space_set)
+        return fail(c, ARENA_ERR_NOT_READY, "proxy: bind jobs, grids and plan space first");
+    if (!d) return fail(c, ARENA_ERR_INVALID_ARG, "proxy: descriptor is NULL");
+    if (!t_iter || !thr || !plan) return fail(c, ARENA_ERR_INVALID_ARG, "proxy: output array is NULL");
+    if (!d->hbm_bw) return fail(c, ARENA_ERR_INVALID_ARG, "proxy: hbm_bw is NULL");
+    if (!(d->f_ref > 0.0) || !std::isfinite(d->f_ref))
+        return fail(c, ARENA_ERR_INVALID_ARG, "proxy: f_ref must be finite and > 0");
+    if (d->n_ops < 1 || d->n_ops > ARENA_MAX_PROXY_OPS)
+        return fail(c, ARENA_ERR_INVALID_ARG, "proxy: n_ops=%d not in 1..%d", d->n_ops, ARENA_MAX_PROXY_OPS);
+    if ((long long)c->n_jobs * c->n_types * c->n_counts > 0x7fffffffLL)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "proxy: more than 2^31-1 cells");
+    std::vector<double> hbm((size_t)c->n_types);
+    for (int g = 0; g < c->n_types; ++g) {
+        if (!(d->hbm_bw[g] > 0.0f) || !std::isfinite(d->hbm_bw[g]))
+            return fail(c, ARENA_ERR_INVALID_ARG, "proxy: hbm_bw[%d] must be finite and > 0", g);
+        hbm[g] = (double)d->hbm_bw[g];
+    }
+    arena_status st;
+    if (c->msets_dirty && (st = build_msets(c)) != ARENA_OK) return st;
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    if ((st = ensure_device(c, stream)) != ARENA_OK) return st;
+    hipError_t e;
+    if (c->msets_dirty) {
+        if ((e = ensure_capacity(&c->d_msets, &c->cap_msets, c->msets.size())) ||
+            (e = ensure_capacity(&c->d_mset_off, &c->cap_mset_off, c->mset_off.size())))
+            return fail(c, ARENA_ERR_OUT_OF_MEMORY, "proxy tables: %s", hipGetErrorString(e));
+        if ((e = hipMemcpyAsync(c->d_msets, c->msets.data(), sizeof(unsigned long long) * c->msets.size(),
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipMemcpyAsync(c->d_mset_off, c->mset_off.data(), sizeof(int32_t) * c->mset_off.size(),
+                                hipMemcpyHostToDevice, stream)) ||
+            (e = hipStreamSynchronize(stream)))
+            return hip_fail(c, e, "proxy table upload");
+        c->msets_dirty = false;
+    }
+    if ((e = ensure_capacity(&c->d_hbm, &c->cap_hbm, hbm.size())))
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "proxy bandwidths: %s", hipGetErrorString(e));
+    if ((e = hipMemcpyAsync(c->d_hbm, hbm.data(), sizeof(double) * hbm.size(), hipMemcpyHostToDevice, stream)) ||
+        (e = hipStreamSynchronize(stream)))
+        return hip_fail(c, e, "proxy bandwidth upload");
+
+    arena::ProxyArgs A;
+    std::memset(&A, 0, sizeof(A));
+    A.layer_offset = c->d_off;
+    A.batch = c->d_batch;
+    A.t = c->t; A.p = c->p; A.a = c->a; A.x = c->x; A.q = c->q;
+    A.types = c->d_types;
+    A.hbm = c->d_hbm;
+    A.counts = c->d_counts;
+    A.kappa = c->d_kappa;
+    A.msets = c->d_msets;
+    A.mset_off = c->d_mset_off;
+    A.n_jobs = c->n_jobs;
+    A.n_types = c->n_types;
+    A.n_counts = c->n_counts;
+    A.n_ops = d->n_ops;
+    A.n_m = (int32_t)c->m_values.size();
+    for (int i = 0; i < A.n_m; ++i) A.m_values[i] = c->m_values[i];
+    A.tie_eps = c->tie_eps;
+    A.f_ref = d->f_ref;
+    A.t_iter = t_iter;
+    A.thr = thr;
+    A.plan = (unsigned long long*)plan;
+    if ((e = arena::launch_proxy(A, stream))) return hip_fail(c, e, "proxy launch");
     return ARENA_OK;
 }
 

@@ -58,6 +58,39 @@ struct ValidateArgs {
     unsigned long long* bad;      // [1] count of non-finite or negative values
 };
 
+// Proxy-plan planner (arena_proxy_estimate).
+constexpr int kProxyMaxOps = 16;            // clustered operators per job
+constexpr int kProxyMaxMultisets = 1280;    // power-of-two multisets of one (count, stage count)
+constexpr int kProxyPlanWords = 3;          // u64 words of plan per cell
+
+struct ProxyArgs {
+    const int32_t* layer_offset;  // [J+1]
+    const int32_t* batch;         // [J]
+    const float* t;
+    const float* p;
+    const float* a;
+    const float* x;
+    const float* q;               // all-to-all bytes per sample
+    const TypeDev* types;         // [T]
+    const double* hbm;            // [T] memory bandwidth, bytes/s
+    const int32_t* counts;        // [NC]
+    const float* kappa;           // [T*NC]
+    // multisets of s powers of two summing to counts[c], exponents at bits
+    // 4k (k-th largest), lexicographically descending; (c, s) spans
+    // msets[mset_off[c*17 + s] .. mset_off[c*17 + s + 1])
+    const unsigned long long* msets;
+    const int32_t* mset_off;      // [NC*17 + 1]
+    int32_t n_jobs, n_types, n_counts, n_ops;
+    int32_t n_m;
+    int32_t m_values[kMaxM];
+    double tie_eps, f_ref;
+    float* t_iter;
+    float* thr;
+    unsigned long long* plan;     // [C * kProxyPlanWords]
+};
+
+hipError_t launch_proxy(const ProxyArgs& args, hipStream_t stream);
+
 // One scheduling step over the throughput matrix (arena_schedule).
 constexpr int kMaxSchedTypes = 64;
 constexpr int kMaxSchedCounts = 512;

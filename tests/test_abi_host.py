@@ -247,3 +247,52 @@ def test_schedule_validation(ctx):
     assert call(result=None) == arena.ARENA_ERR_INVALID_ARG
     assert call(queue=None) == arena.ARENA_ERR_INVALID_ARG
     assert call(launched=None) == arena.ARENA_ERR_INVALID_ARG
+
+
+def test_proxy_desc_layout(tmp_path):
+    import ctypes
+    names = [f for f, _ in arena.ProxyDesc._fields_]
+    prog = tmp_path / "off.c"
+    prog.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"arena.h\"\nint main(void){\n"
+                    + "".join(f'printf("%zu\\n", offsetof(arena_proxy_desc, {n}));\n' for n in names)
+                    + 'printf("%zu\\n", sizeof(arena_proxy_desc));\nreturn 0;}\n')
+    exe = tmp_path / "off"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(prog)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [getattr(arena.ProxyDesc, n).offset for n in names] + [ctypes.sizeof(arena.ProxyDesc)]
+    assert got == want
+
+
+def test_proxy_validation(ctx):
+    # rejected on the host before any HIP call (output pointers never touched)
+    lib = arena.load()
+    fake = 0x1000
+    assert lib.arena_proxy_estimate(None, None, None, None, None, None) == arena.ARENA_ERR_INVALID_ARG
+    with pytest.raises(arena.ArenaError) as e:
+        arena.arena_proxy_estimate(ctx, [2e12], 1e14, 16, fake, fake, fake)
+    assert e.value.status == arena.ARENA_ERR_NOT_READY
+    w = wl.make("tiny")
+    arena.arena_bind_jobs(ctx, w.layer_offset, w.batch, fake, fake, fake, fake, fake,
+                          n_layers_total=int(w.layer_offset[-1]))
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    arena.arena_set_plan_space(ctx, w.m_values, 1e-6)
+    hbm = w.hbm_bw()
+
+    def status(**kw):
+        a = dict(hbm_bw=hbm, f_ref=1e14, n_ops=16, t_iter=fake, thr=fake, plan=fake)
+        a.update(kw)
+        with pytest.raises(arena.ArenaError) as ex:
+            arena.arena_proxy_estimate(ctx, a["hbm_bw"], a["f_ref"], a["n_ops"], a["t_iter"], a["thr"],
+                                       a["plan"])
+        return ex.value.status
+
+    assert status(n_ops=0) == arena.ARENA_ERR_INVALID_ARG
+    assert status(n_ops=17) == arena.ARENA_ERR_INVALID_ARG
+    assert status(f_ref=0.0) == arena.ARENA_ERR_INVALID_ARG
+    assert status(f_ref=float("inf")) == arena.ARENA_ERR_INVALID_ARG
+    assert status(hbm_bw=[2e12, 0.0]) == arena.ARENA_ERR_INVALID_ARG
+    assert status(hbm_bw=[2e12, float("nan")]) == arena.ARENA_ERR_INVALID_ARG
+    assert status(t_iter=None) == arena.ARENA_ERR_INVALID_ARG
+    assert status(plan=None) == arena.ARENA_ERR_INVALID_ARG
+    assert lib.arena_proxy_estimate(ctx, None, fake, fake, fake, None) == arena.ARENA_ERR_INVALID_ARG
