@@ -9,7 +9,9 @@ goes to stderr.
 
 With --schedule it times instead the scheduling step that consumes such a
 matrix (Algorithm 1 with the throughput objective) on a 1280-GPU cluster
-state over the same 16384 x 8 x 131 shape, and prints that line.
+state over the same 16384 x 8 x 131 shape, and prints that line.  With
+--proxy it times the proxy-plan planner (Sec. 3.3) over every cell of the
+trace-like workload and scores its plans against the exhaustive estimate.
 """
 from __future__ import annotations
 
@@ -76,6 +78,105 @@ def schedule_cpu_baseline(st, min_seconds: float = 10.0) -> dict:
             break
     return {"value": n / dt, "unit": "steps/s", "cores": 1, "kind": "oracle",
             "sample": f"the same state, {n} steps in {dt:.1f} s"}
+
+
+def proxy_cpu_baseline(w, every: int, kappa_round: int = 0) -> dict:
+    """The proxy-planner oracle (single-threaded C, fp64) on a bounded sample
+    of the same workload: every `every`-th cell."""
+    import numpy as np
+    from oracle import proxy as proxy_c
+    proxy_c.load()
+    ids = np.arange(0, w.n_cells, every, dtype=np.int64)
+    t0 = time.perf_counter()
+    proxy_c.cells(w, ids, kappa_round=kappa_round)
+    dt = time.perf_counter() - t0
+    return {"value": len(ids) / dt, "unit": "cells/s", "cores": 1, "kind": "oracle",
+            "sample": f"every {every}th cell of {args_workload_name(w)}: {len(ids)} cells in {dt:.1f} s"}
+
+
+def args_workload_name(w) -> str:
+    return f"{w.name} ({w.n_jobs} jobs x {w.n_types} types x {w.n_counts} counts)"
+
+
+def bench_proxy(args) -> int:
+    """One step = the proxy-plan planner (Sec. 3.3) over every cell of the
+    workload (default: trace-like, 1024 jobs x 4 types x 35 counts); the
+    exhaustive estimate of the same round scores its plans."""
+    import numpy as np
+    import torch
+
+    from paper_2403_16125_amd import arena, workcount, workloads
+
+    name = args.workload if args.workload != "full" or args.proxy_full else "trace"
+    w = workloads.make(name)
+    ops = workcount.proxy_ops(w, args.n_ops)
+    log(f"proxy planner on {args_workload_name(w)}: {w.n_cells} cells, {ops:.4g} ops per launch")
+    dev = torch.device("cuda", 0)
+    est = arena.Estimator(w, device=0)
+    stream = torch.cuda.current_stream(dev)
+    for i in range(args.warmup):
+        est.proxy_estimate(f_ref=workloads.F_REF, n_ops=args.n_ops)
+        torch.cuda.synchronize(dev)
+        log(f"warmup {i + 1}/{args.warmup} done")
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        est.proxy_estimate(f_ref=workloads.F_REF, n_ops=args.n_ops)
+        ends[i].record(stream)
+        torch.cuda.synchronize(dev)
+        log(f"step {i + 1}/{args.steps}: {starts[i].elapsed_time(ends[i]):.1f} ms")
+    wall = time.perf_counter() - t0
+    launch_ms = [a.elapsed_time(b) for a, b in zip(starts, ends)]
+    step_s = float(np.mean(launch_ms)) / 1e3
+    pr = est.proxy_results()
+    est.estimate()
+    ex = est.results()
+    est.close()
+    both = np.isfinite(pr["t_iter"]) & np.isfinite(ex["t_iter"])
+    ratio = ex["t_iter"][both].astype(np.float64) / pr["t_iter"][both].astype(np.float64)
+    achieved = ops / step_s
+    line = {
+        "metric": "(job,grid) cells/sec (proxy planner)",
+        "value": w.n_cells / step_s,
+        "unit": "cells/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"{args_workload_name(w)}: {w.n_cells} cells, {args.n_ops} operators per job, "
+                               "every pipeline degree and microbatch count"},
+        "proxy_score": {
+            "what": "exhaustive best T / proxy T per cell (1 = the proxy is as fast as the exhaustive optimum)",
+            "mean": float(ratio.mean()), "median": float(np.median(ratio)),
+            "frac_faster_than_exhaustive": float((ratio > 1).mean()),
+            "cells": int(both.sum()),
+            "proxy_only_feasible": int((np.isfinite(pr["t_iter"]) & ~np.isfinite(ex["t_iter"])).sum()),
+        },
+        "roofline": {
+            "bound": "alu",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_LANE_OPS / 1e12,
+            "unit": "Top/s",
+            "frac": achieved / PEAK_LANE_OPS,
+            "traffic": None,
+            "ops_per_launch": ops,
+            "launch_ms": step_s * 1e3,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the proxy oracle on a sample")
+        line["cpu_baseline"] = proxy_cpu_baseline(w, args.proxy_cpu_every)
+    log(f"timed {args.steps} launches in {wall:.2f} s wall")
+    print(json.dumps(line), flush=True)
+    return 0
 
 
 def bench_schedule(args) -> int:
@@ -177,6 +278,11 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", action="store_true",
                     help="time the scheduling step that consumes the throughput matrix instead")
+    ap.add_argument("--proxy", action="store_true",
+                    help="time the proxy-plan planner instead (trace-like workload unless --proxy-full)")
+    ap.add_argument("--proxy-full", action="store_true", help="with --proxy, run it on the full round")
+    ap.add_argument("--n-ops", type=int, default=16, help="operators per job for the proxy planner")
+    ap.add_argument("--proxy-cpu-every", type=int, default=199, help="proxy oracle sample: every k-th cell")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain elementwise copy of known size (HBM counter calibration)")
     args = ap.parse_args()
@@ -190,6 +296,8 @@ def main() -> int:
 
     if args.schedule:
         return bench_schedule(args)
+    if args.proxy:
+        return bench_proxy(args)
 
     import numpy as np
     import torch

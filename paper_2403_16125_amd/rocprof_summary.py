@@ -28,6 +28,9 @@ KERNEL_SOURCES = {
     "schedule_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
                         "paper_2403_16125_amd/csrc/arena_host.cpp",
                         "paper_2403_16125_amd/csrc/arena_sched.hip"),
+    "proxy_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
+                     "paper_2403_16125_amd/csrc/arena_host.cpp",
+                     "paper_2403_16125_amd/csrc/arena_proxy.hip"),
 }
 
 

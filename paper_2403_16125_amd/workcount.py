@@ -90,3 +90,50 @@ def count(w, kappa_round: int = 0) -> dict:
         tot["problem_ops"] += mult * pops
     tot["ops"] = tot["plan_ops"] + tot["problem_ops"]
     return tot
+
+
+# ------------------------------------------------------------ proxy planner
+
+@lru_cache(maxsize=None)
+def _pow2_splits(n: int, s: int, maxp: int) -> int:
+    """Multisets of s powers of two (each <= maxp) summing to n."""
+    if s == 0:
+        return 1 if n == 0 else 0
+    if n < s:
+        return 0
+    tot, p = 0, maxp
+    while p >= 1:
+        if p <= n - (s - 1):
+            tot += _pow2_splits(n - p, s - 1, p)
+        p //= 2
+    return tot
+
+
+@lru_cache(maxsize=None)
+def _proxy_cell_ops(n: int, O: int, n_m: int) -> int:
+    """Work of the proxy planner on one cell with O operators and n GPUs:
+    every grouping of every grid normalised against every power-of-two
+    multiset (3 fp64 ops -- subtract, multiply, add -- per stage and
+    multiset), plus a memory test per stage and microbatch count (8 ops)."""
+    from math import comb
+    top = 1 << (n.bit_length() - 1)
+    ops = 0
+    for s in range(1, min(O, n) + 1):
+        K = _pow2_splits(n, s, top)
+        if K == 0:
+            continue
+        ops += comb(O - 1, s - 1) * (3 * s * K + 8 * s * n_m)
+    return ops
+
+
+def proxy_ops(w, n_ops: int = 16) -> int:
+    """Algorithmic operations of one proxy-planner launch over every cell."""
+    L = np.diff(np.asarray(w.layer_offset))
+    per_job_ops = {}
+    total = 0
+    for Lj in L:
+        O = int(min(int(Lj), n_ops))
+        if O not in per_job_ops:
+            per_job_ops[O] = sum(_proxy_cell_ops(int(n), O, len(w.m_values)) for n in w.counts)
+        total += per_job_ops[O] * w.n_types
+    return int(total)
