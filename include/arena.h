@@ -293,10 +293,17 @@ typedef struct arena_sched_desc {
     int32_t* launched;           /* DEVICE [n_queue] out: 1 if the job launched */
     int32_t* result;             /* DEVICE [8] out: status (0 ok; 1 the running jobs exceed the
                                     capacity; 2 an index out of range, a queued job running or listed
-                                    twice, or a negative class -- nothing is changed then), scale-downs
-                                    kept, launches, scale-ups, decisions taken (launch, scale-down and
-                                    scale-up searches), candidates they examined (64-bit: low word,
-                                    high word), 0 */
+                                    twice, a negative class or a bad deadline value -- nothing is
+                                    changed then), scale-downs kept, launches, scale-ups, decisions
+                                    taken (launch, scale-down and scale-up searches), candidates they
+                                    examined (64-bit: low word, high word), 0 */
+    /* Deadline constraint (Eq. 6), optional: all three NULL to schedule without it.  With it, a grid
+     * is open to job i only if batch_i iters_i / thr <= deadline_i (fp64): launches, scale-downs (the
+     * largest smaller count still meeting it) and scale-ups (a larger count meeting it) consider open
+     * grids only, and the usable types of a queued job are those with an open grid. */
+    const int32_t* batch;        /* DEVICE [n_jobs] global batch size, > 0 */
+    const float* iters;          /* DEVICE [n_jobs] remaining iterations, finite >= 0 */
+    const float* deadline;       /* DEVICE [n_jobs] seconds left to the deadline, > 0 (+inf: none) */
 } arena_sched_desc;
 
 /* Host checks (sizes, pointers, counts, capacity, depth) return an error

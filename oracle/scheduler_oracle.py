@@ -28,6 +28,14 @@ S6  Then in-flight jobs are scaled up (GetOptimalScaleUp): each job's best
     (n' - n) (ties: the smaller n'); the job with the largest such gain moves
     (ties: the lower job id); at most D moves.
 
+S8  Deadline constraint (Eq. 6), when per-job batch B_i, remaining
+    iterations N_i and deadline DDL_i are given: a grid of throughput thr is
+    open to job i only if thr > 0 and B_i N_i / thr <= DDL_i (float64).
+    Every step above uses open grids only: launches (S2), the usable types
+    and the scale-down target (S3: the largest smaller count still open) and
+    scale-ups (S6: a larger open count).  A running job outside its deadline
+    is not moved for it.
+
 Returns the new allocation, which queued jobs launched, the move counts
 (scale-downs kept, launches, scale-ups) and the number of searches made
 (launch, scale-down and scale-up: the decisions of the step).
@@ -44,29 +52,36 @@ def _free(thr, counts, capacity, alloc_type, alloc_count):
     return free
 
 
-def launch_grid(thr_j, counts, free):
+def _open(v, work, ddl):
+    """S8: a grid of throughput v is open (work = B N; ddl None: no deadline)."""
+    return v > 0.0 and (ddl is None or work / v <= ddl)
+
+
+def launch_grid(thr_j, counts, free, work=0.0, ddl=None):
     """S2: best grid of one job under the free GPUs, or None."""
     best = None
     for g in range(len(free)):
         for c in range(len(counts)):
             v = float(thr_j[g][c])
-            if v > 0.0 and int(counts[c]) <= free[g]:
+            if _open(v, work, ddl) and int(counts[c]) <= free[g]:
                 key = (-v, int(counts[c]), g)
                 if best is None or key < best[0]:
                     best = (key, g, c)
     return None if best is None else (best[1], best[2])
 
 
-def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types):
-    """S3: (cost, job, new count index) of the cheapest scale-down, or None."""
+def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types, dl=None):
+    """S3: (cost, job, new count index) of the cheapest scale-down, or None.
+    dl(i) -> (work, deadline) of job i under S8."""
     best = None
     for i in range(len(alloc_type)):
         g = int(alloc_type[i])
         if g < 0 or g not in usable_types:
             continue
+        work, ddl = dl(i) if dl else (0.0, None)
         c = int(alloc_count[i])
         c2 = c - 1
-        while c2 >= 0 and not float(thr[i][g][c2]) > 0.0:
+        while c2 >= 0 and not _open(float(thr[i][g][c2]), work, ddl):
             c2 -= 1
         if c2 < 0:
             continue
@@ -76,13 +91,14 @@ def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types):
     return best
 
 
-def scale_up_move(thr, counts, alloc_type, alloc_count, free):
+def scale_up_move(thr, counts, alloc_type, alloc_count, free, dl=None):
     """S6: (gain, job, new count index) of the best scale-up, or None."""
     best = None
     for i in range(len(alloc_type)):
         g = int(alloc_type[i])
         if g < 0:
             continue
+        work, ddl = dl(i) if dl else (0.0, None)
         c = int(alloc_count[i])
         n, t = int(counts[c]), float(thr[i][g][c])
         mine = None
@@ -91,7 +107,7 @@ def scale_up_move(thr, counts, alloc_type, alloc_count, free):
             if dn > free[g]:
                 break
             t2 = float(thr[i][g][c2])
-            if t2 > t:
+            if t2 > t and _open(t2, work, ddl):
                 gain = (t2 - t) / float(dn)
                 if mine is None or gain > mine[0]:
                     mine = (gain, c2)
@@ -100,8 +116,9 @@ def scale_up_move(thr, counts, alloc_type, alloc_count, free):
     return best
 
 
-def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, depth):
-    """One scheduling step (Algorithm 1, readings S1-S6)."""
+def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, depth,
+             batch=None, iters=None, deadline=None):
+    """One scheduling step (Algorithm 1, readings S1-S6; S8 with deadlines)."""
     alloc_type = [int(v) for v in alloc_type]
     alloc_count = [int(v) for v in alloc_count]
     for k in range(1, len(counts)):
@@ -114,6 +131,16 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
         raise ValueError("queued jobs must be distinct and not running")
     if any(int(p) < 0 for p in priority):
         raise ValueError("priority classes must be >= 0")
+    given = [v is not None for v in (batch, iters, deadline)]
+    if any(given) and not all(given):
+        raise ValueError("give batch, iters and deadline together or none")
+    dl = None
+    if all(given):
+        for i in range(len(alloc_type)):
+            b, it, d = int(batch[i]), float(iters[i]), float(deadline[i])
+            if b <= 0 or not (it >= 0.0) or it == float("inf") or not (d > 0.0):
+                raise ValueError("bad deadline values")
+        dl = lambda i: (float(int(batch[i])) * float(iters[i]), float(deadline[i]))
     n_types = len(free)
     launched = [0] * len(queue)
     kept_down = launches = 0
@@ -121,10 +148,11 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
     lam = max((int(p) for p in priority), default=0) + 1
     for q in range(len(queue)):
         j = int(queue[q])
-        usable = {g for g in range(n_types) if any(float(v) > 0.0 for v in thr[j][g])}
+        work, ddl = dl(j) if dl else (0.0, None)
+        usable = {g for g in range(n_types) if any(_open(float(v), work, ddl) for v in thr[j][g])}
         log = []
         while True:
-            grid = launch_grid(thr[j], counts, free)
+            grid = launch_grid(thr[j], counts, free, work, ddl)
             decisions += 1
             if grid is not None:
                 g, c = grid
@@ -137,7 +165,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
             if len(log) >= depth:
                 grid = None
             else:
-                mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable)
+                mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable, dl)
                 decisions += 1
                 if mv is not None:
                     _, i, c2 = mv
@@ -159,7 +187,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
                 break
     ups = 0
     while ups < depth:
-        mv = scale_up_move(thr, counts, alloc_type, alloc_count, free)
+        mv = scale_up_move(thr, counts, alloc_type, alloc_count, free, dl)
         decisions += 1
         if mv is None:
             break

@@ -77,7 +77,8 @@ class SchedDesc(ctypes.Structure):
                 ("alloc_type", ctypes.c_void_p), ("alloc_count", ctypes.c_void_p),
                 ("queue", ctypes.c_void_p), ("priority", ctypes.c_void_p),
                 ("n_queue", ctypes.c_int32), ("depth", ctypes.c_int32),
-                ("launched", ctypes.c_void_p), ("result", ctypes.c_void_p)]
+                ("launched", ctypes.c_void_p), ("result", ctypes.c_void_p),
+                ("batch", ctypes.c_void_p), ("iters", ctypes.c_void_p), ("deadline", ctypes.c_void_p)]
 
 
 class SpaceSize(ctypes.Structure):
@@ -262,14 +263,16 @@ def unpack_proxy_plan(words):
 
 
 def arena_schedule(ctx, n_jobs, n_types, n_counts, thr, counts, capacity, alloc_type, alloc_count,
-                   queue, priority, n_queue, depth, launched, result, stream=None) -> None:
-    """thr, alloc_type, alloc_count, queue, priority, launched and result are
-    device tensors (or pointers); counts and capacity are host int32 arrays."""
+                   queue, priority, n_queue, depth, launched, result, stream=None,
+                   batch=None, iters=None, deadline=None) -> None:
+    """thr, alloc_type, alloc_count, queue, priority, launched, result and the
+    optional deadline arrays are device tensors (or pointers); counts and
+    capacity are host int32 arrays."""
     counts = np.ascontiguousarray(counts, np.int32)
     capacity = np.ascontiguousarray(capacity, np.int32)
     d = SchedDesc(int(n_jobs), int(n_types), int(n_counts), _ptr(thr), _ptr(counts), _ptr(capacity),
                   _ptr(alloc_type), _ptr(alloc_count), _ptr(queue), _ptr(priority), int(n_queue),
-                  int(depth), _ptr(launched), _ptr(result))
+                  int(depth), _ptr(launched), _ptr(result), _ptr(batch), _ptr(iters), _ptr(deadline))
     sp = 0 if stream is None else int(stream)
     _check(ctx, load().arena_schedule(ctx, ctypes.byref(d), sp))
 
@@ -400,7 +403,7 @@ class Scheduler:
     device memory: `thr` is a float32 [J, T, NC] array or device tensor (the
     thr output of an estimate, viewed as [J, T, NC], serves directly)."""
 
-    def __init__(self, thr, counts, capacity, device: int = 0):
+    def __init__(self, thr, counts, capacity, device: int = 0, batch=None, iters=None, deadline=None):
         import torch
         self.torch = torch
         self.dev = torch.device("cuda", device)
@@ -427,9 +430,23 @@ class Scheduler:
             self.launched = torch.empty(max(1, self.n_jobs), **i32)
             self.result = torch.empty(8, **i32)
             self.n_queue = 0
+            self.batch = self.iters = self.deadline = None
+            if batch is not None or iters is not None or deadline is not None:
+                self.set_deadlines(batch, iters, deadline)
         except Exception:
             self.close()
             raise
+
+    def set_deadlines(self, batch, iters, deadline) -> None:
+        """Per-job batch, remaining iterations and deadline (Eq. 6), or all None."""
+        torch = self.torch
+        if batch is None and iters is None and deadline is None:
+            self.batch = self.iters = self.deadline = None
+            return
+        self.batch = torch.as_tensor(np.ascontiguousarray(batch, np.int32)).to(self.dev)
+        self.iters = torch.as_tensor(np.ascontiguousarray(iters, np.float32)).to(self.dev)
+        self.deadline = torch.as_tensor(np.ascontiguousarray(deadline, np.float32)).to(self.dev)
+        torch.cuda.synchronize(self.dev)
 
     def load_state(self, alloc_type, alloc_count, queue, priority) -> None:
         """Copy a cluster state (allocation and queue) to the device (synchronously)."""
@@ -456,7 +473,8 @@ class Scheduler:
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
         arena_schedule(self.ctx, self.n_jobs, self.n_types, self.n_counts, self.thr, self.counts,
                        self.capacity, self.alloc_type, self.alloc_count, self.queue, self.priority,
-                       self.n_queue, depth, self.launched, self.result, s.cuda_stream)
+                       self.n_queue, depth, self.launched, self.result, s.cuda_stream,
+                       self.batch, self.iters, self.deadline)
 
     def results(self) -> dict:
         """Synchronise and copy the state after the last step to the host."""

@@ -784,6 +784,9 @@ arena_status arena_schedule(arena_ctx* c, const arena_sched_desc* d, void* strea
     if (!d->result || (d->n_jobs > 0 && (!d->thr || !d->alloc_type || !d->alloc_count)) ||
         (d->n_queue > 0 && (!d->queue || !d->priority || !d->launched)))
         return fail(c, ARENA_ERR_INVALID_ARG, "schedule: a device array is NULL");
+    const int n_ddl = (d->batch != nullptr) + (d->iters != nullptr) + (d->deadline != nullptr);
+    if (n_ddl != 0 && n_ddl != 3)
+        return fail(c, ARENA_ERR_INVALID_ARG, "schedule: give batch, iters and deadline together or none");
     for (int i = 0; i < d->n_counts; ++i) {
         const int n = d->counts[i];
         if (n < 1 || n > ARENA_MAX_GPU_COUNT)
@@ -832,6 +835,11 @@ arena_status arena_schedule(arena_ctx* c, const arena_sched_desc* d, void* strea
     A.n_counts = d->n_counts;
     A.n_queue = d->n_queue;
     A.depth = d->depth;
+    if (n_ddl == 3 && d->n_jobs > 0) {
+        A.batch = d->batch;
+        A.iters = d->iters;
+        A.ddl = d->deadline;
+    }
     if ((e = arena::launch_schedule(A, stream))) return hip_fail(c, e, "schedule launch");
     return ARENA_OK;
 }

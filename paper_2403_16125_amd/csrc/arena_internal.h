@@ -106,8 +106,13 @@ struct SchedArgs {
     const int32_t* queue;         // [Q]
     const int32_t* priority;      // [Q]
     int32_t* launched;            // [Q] out
-    int32_t* result;              // [4] out: status, scale-downs kept, launches, scale-ups
+    int32_t* result;              // [8] out: status, moves, decisions, candidates examined
     int32_t n_jobs, n_types, n_counts, n_queue, depth;
+    // deadline constraint (Eq. 6): all null, or per job batch, remaining
+    // iterations and time left to the deadline
+    const int32_t* batch;
+    const float* iters;
+    const float* ddl;
 };
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);

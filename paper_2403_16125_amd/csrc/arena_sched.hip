@@ -67,7 +67,7 @@ struct SchedLds {
     int32_t log_slot[kMaxSchedDepth];
     double log_cost[kMaxSchedDepth];
     int32_t log_info[kMaxSchedDepth];
-    unsigned long long usable;      // types where the queued job has a grid with throughput > 0
+    unsigned long long usable;      // types where the queued job has an open grid
     int32_t bad;
     int32_t pmax;                   // largest priority class in the queue
     int32_t n_run;                  // running jobs in the list
@@ -232,15 +232,41 @@ __device__ __forceinline__ unsigned long long block_min64(unsigned long long k, 
     return r;
 }
 
+// Work of job i to finish (batch x remaining iterations) and its deadline;
+// dl < 0 when there is no deadline constraint.
+template <bool DDL>
+__device__ __forceinline__ void job_deadline(const SchedArgs& A, int i, double& bn, double& dl)
+{
+    if (DDL) {
+        bn = (double)A.batch[i] * (double)A.iters[i];
+        dl = (double)A.ddl[i];
+    } else {
+        bn = 0.0;
+        dl = -1.0;
+    }
+}
+
+// A grid of throughput v is open to the job: v > 0 and, under the deadline
+// constraint (Eq. 6), the remaining work finishes in time at v.
+template <bool DDL>
+__device__ __forceinline__ bool open_grid(float v, double bn, double dl)
+{
+    if (!DDL) return v > 0.0f;
+    return v > 0.0f && bn / (double)v <= dl;
+}
+
 // S2: the fastest grid of job j that fits the free GPUs (payload the grid
 // index g*NC + c, -1 if none fits), and on the first pass of a visit the
-// types where j has a grid with throughput > 0.  A staged row is read from
+// types where j has an open grid.  A staged row is read from
 // LDS buffer `buf` with each thread's grids (type, count index, GPU count)
 // decoded once in `eg`; a larger row is read from memory and decoded here.
+template <bool DDL>
 __device__ __forceinline__ Best launch_grid(const SchedArgs& A, SchedLds& S, int j, int buf, bool first, int& phase,
                             unsigned long long& usable, const int (&eg)[kRowUnroll])
 {
     unsigned long long best = ~0ull, m = 0ull;
+    double bn, dl;
+    job_deadline<DDL>(A, j, bn, dl);
     const int nc = A.n_counts, ng = A.n_types * nc;
     if (ng <= kRowBuf) {
         float v[kRowUnroll];
@@ -252,7 +278,7 @@ __device__ __forceinline__ Best launch_grid(const SchedArgs& A, SchedLds& S, int
         }
 #pragma unroll
         for (int u = 0; u < kRowUnroll; ++u) {
-            if (eg[u] >= 0 && v[u] > 0.0f) {
+            if (eg[u] >= 0 && open_grid<DDL>(v[u], bn, dl)) {
                 const int g = eg[u] & 63;
                 m |= 1ull << g;
                 if ((eg[u] >> 15) <= fr[u]) {
@@ -273,7 +299,7 @@ __device__ __forceinline__ Best launch_grid(const SchedArgs& A, SchedLds& S, int
 #pragma unroll
             for (int u = 0; u < kRowUnroll; ++u) {
                 const int e = base + u * kSchedThreads;
-                if (e < ng && v[u] > 0.0f) {
+                if (e < ng && open_grid<DDL>(v[u], bn, dl)) {
                     const int g = e / nc, c = e - g * nc;
                     m |= 1ull << g;
                     if (S.counts[c] <= S.free[g]) {
@@ -294,16 +320,19 @@ __device__ __forceinline__ Best launch_grid(const SchedArgs& A, SchedLds& S, int
     return r;
 }
 
-// S3 for one running job: the largest smaller count with throughput > 0 and
-// the throughput lost per GPU freed; c2 = -1 if there is none.
+// S3 for one running job: the largest smaller count open to it and the
+// throughput lost per GPU freed; c2 = -1 if there is none.
+template <bool DDL>
 __device__ __forceinline__ double down_cost(const SchedArgs& A, const SchedLds& S, int i, int g, int c,
                                             int& c2)
 {
     const float* row = A.thr + ((size_t)i * A.n_types + g) * A.n_counts;
+    double bn, dl;
+    job_deadline<DDL>(A, i, bn, dl);
     const float tc = row[c];
     c2 = c - 1;
     float t2 = c2 >= 0 ? row[c2] : 0.0f;
-    while (c2 >= 0 && !(t2 > 0.0f)) {
+    while (c2 >= 0 && !open_grid<DDL>(t2, bn, dl)) {
         --c2;
         t2 = c2 >= 0 ? row[c2] : 0.0f;
     }
@@ -314,16 +343,18 @@ __device__ __forceinline__ double down_cost(const SchedArgs& A, const SchedLds& 
 }
 
 // Refreshes the cached scale-down of list slot k from S.ralloc[k] (one thread).
+template <bool DDL>
 __device__ __forceinline__ void cache_slot(const SchedArgs& A, SchedLds& S, int k)
 {
     const int al = S.ralloc[k], g = al >> 16;
     int c2;
-    const double cost = down_cost(A, S, S.run[k], g, al & 0xffff, c2);
+    const double cost = down_cost<DDL>(A, S, S.run[k], g, al & 0xffff, c2);
     S.dcost[k] = cost;
     S.dinfo[k] = c2 < 0 ? -1 : (c2 | (g << 16));
 }
 
 // S3: the cheapest scale-down on a type the queued job can use.
+template <bool DDL>
 __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
 {
     Best b{kInfD, kNone, -1, -1};
@@ -341,7 +372,7 @@ __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
             const int g = A.alloc_type[i];
             if (g < 0 || !((usable >> g) & 1ull)) continue;
             int c2;
-            const double cost = down_cost(A, S, i, g, A.alloc_count[i], c2);
+            const double cost = down_cost<DDL>(A, S, i, g, A.alloc_count[i], c2);
             if (c2 < 0) continue;
             if (better(cost, i, b.key, b.idx)) b = Best{cost, i, c2, -1};
         }
@@ -351,10 +382,13 @@ __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
 
 // S6 for one running job (type g, count index c): its best scale-up within
 // the free GPUs (gain per added GPU; ties to the smaller count).
+template <bool DDL>
 __device__ __forceinline__ void up_move(const SchedArgs& A, const SchedLds& S, int i, int g, int c, int k,
                                         Best& b)
 {
     const float* row = A.thr + ((size_t)i * A.n_types + g) * A.n_counts;
+    double bn, dl;
+    job_deadline<DDL>(A, i, bn, dl);
     const int n = S.counts[c];
     const int fr = S.free[g];
     const double t = (double)row[c];
@@ -363,8 +397,9 @@ __device__ __forceinline__ void up_move(const SchedArgs& A, const SchedLds& S, i
     for (int c2 = c + 1; c2 < A.n_counts; ++c2) {
         const int dn = S.counts[c2] - n;
         if (dn > fr) break;
-        const double t2 = (double)row[c2];
-        if (t2 > t) {
+        const float v2 = row[c2];
+        const double t2 = (double)v2;
+        if (t2 > t && open_grid<DDL>(v2, bn, dl)) {
             const double gain = (t2 - t) / (double)dn;
             if (gain > gbest) {
                 gbest = gain;
@@ -377,23 +412,25 @@ __device__ __forceinline__ void up_move(const SchedArgs& A, const SchedLds& S, i
 }
 
 // S6: the scale-up with the largest gain per GPU (key -gain).
+template <bool DDL>
 __device__ Best scale_up(const SchedArgs& A, SchedLds& S, int& phase)
 {
     Best b{kInfD, kNone, -1, -1};
     if (S.use_list) {
         for (int k = threadIdx.x; k < S.n_run; k += kSchedThreads) {
             const int al = S.ralloc[k];
-            up_move(A, S, S.run[k], al >> 16, al & 0xffff, k, b);
+            up_move<DDL>(A, S, S.run[k], al >> 16, al & 0xffff, k, b);
         }
     } else {
         for (int i = threadIdx.x; i < A.n_jobs; i += kSchedThreads) {
             const int g = A.alloc_type[i];
-            if (g >= 0) up_move(A, S, i, g, A.alloc_count[i], -1, b);
+            if (g >= 0) up_move<DDL>(A, S, i, g, A.alloc_count[i], -1, b);
         }
     }
     return block_min(b, S, phase);
 }
 
+template <bool DDL>
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
 {
     __shared__ SchedLds S;
@@ -424,6 +461,12 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             }
         }
     }
+    if (DDL)
+        for (int i = tid; i < A.n_jobs; i += kSchedThreads) {
+            const float it = A.iters[i], dd = A.ddl[i];
+            if (A.batch[i] <= 0 || !(it >= 0.0f) || it == __builtin_huge_valf() || !(dd > 0.0f))
+                atomicOr(&S.bad, 2);
+        }
     for (int q = tid; q < A.n_queue; q += kSchedThreads) {
         const int j = A.queue[q];
         if (j < 0 || j >= A.n_jobs || A.alloc_type[j] >= 0 || A.priority[q] < 0) {
@@ -445,7 +488,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
     for (int q = tid; q < A.n_queue; q += kSchedThreads) A.launched[q] = 0;
     const bool fits = S.n_run <= kMaxRun;
     if (fits)
-        for (int k = tid; k < S.n_run; k += kSchedThreads) cache_slot(A, S, k);
+        for (int k = tid; k < S.n_run; k += kSchedThreads) cache_slot<DDL>(A, S, k);
     __syncthreads();
     if (tid == 0) S.use_list = fits ? 1 : 0;
     __syncthreads();
@@ -503,7 +546,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
         bool ok = false;
         for (;;) {
             unsigned long long usable = 0ull;
-            const Best lg = launch_grid(A, S, j, buf, nlog == 0, phase, usable, eg);
+            const Best lg = launch_grid<DDL>(A, S, j, buf, nlog == 0, phase, usable, eg);
             ++passes;
             scanned += (unsigned long long)ng;
             if (lg.aux >= 0) {
@@ -517,7 +560,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
                             const int k = S.n_run++;
                             S.run[k] = j;
                             S.ralloc[k] = c | (g << 16);
-                            cache_slot(A, S, k);
+                            cache_slot<DDL>(A, S, k);
                         } else {
                             S.use_list = 0;
                         }
@@ -531,7 +574,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             __syncthreads();
             ++passes;
             scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
-            const Best sd = scale_down(A, S, phase);
+            const Best sd = scale_down<DDL>(A, S, phase);
             if (sd.aux < 0) break;
             if (tid == 0) {
                 const int i = sd.idx;
@@ -553,7 +596,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
                     S.log_cost[nlog] = S.dcost[sd.slot];
                     S.log_info[nlog] = S.dinfo[sd.slot];
                     S.ralloc[sd.slot] = sd.aux | (g << 16);
-                    cache_slot(A, S, sd.slot);
+                    cache_slot<DDL>(A, S, sd.slot);
                 }
             }
             ++nlog;
@@ -600,7 +643,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
     while (ups < A.depth) {              // S6
         ++passes;
         scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
-        const Best su = scale_up(A, S, phase);
+        const Best su = scale_up<DDL>(A, S, phase);
         if (su.aux < 0) break;
         if (tid == 0) {
             const int i = su.idx;
@@ -617,7 +660,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             A.alloc_count[i] = su.aux;
             if (su.slot >= 0) {
                 S.ralloc[su.slot] = su.aux | (g << 16);
-                cache_slot(A, S, su.slot);
+                cache_slot<DDL>(A, S, su.slot);
             }
         }
         ++ups;
@@ -639,7 +682,10 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
 
 hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream)
 {
-    hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), 0, stream, args);
+    if (args.ddl)
+        hipLaunchKernelGGL(schedule_kernel<true>, dim3(1), dim3(kSchedThreads), 0, stream, args);
+    else
+        hipLaunchKernelGGL(schedule_kernel<false>, dim3(1), dim3(kSchedThreads), 0, stream, args);
     return hipGetLastError();
 }
 

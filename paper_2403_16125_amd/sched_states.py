@@ -99,3 +99,22 @@ def full_round(seed: int = 11) -> SchedState:
     thr = synthetic_thr(seed, 16384, 8, counts)
     return random_state(seed, thr, counts, [160] * 8, running_frac=0.5, queued_frac=0.02,
                         n_classes=3, depth=3, max_count=32)
+
+
+def deadlines(seed: int, thr: np.ndarray, slack=(0.8, 6.0), none_frac: float = 0.3):
+    """Per-job batch, remaining iterations and seconds left to the deadline:
+    batch from {64, 128, 256, 512}, iterations log-uniform on [1e3, 1e5], and
+    the deadline the time to finish at the job's best throughput times a
+    slack drawn uniformly from `slack` (below 1: no grid meets it); a share
+    `none_frac` of jobs has no deadline (+inf)."""
+    J = thr.shape[0]
+    rng = _stream(seed, 1 << 21)
+    u = rng.uniform(4 * J)
+    batch = np.asarray([64, 128, 256, 512], np.int32)[(u[0::4] * 4).astype(np.int64) % 4]
+    iters = np.exp(np.log(1e3) + u[1::4] * (np.log(1e5) - np.log(1e3))).astype(np.float32)
+    best = thr.reshape(J, -1).max(axis=1).astype(np.float64)
+    fac = slack[0] + u[2::4] * (slack[1] - slack[0])
+    with np.errstate(divide="ignore"):
+        ddl = np.where(best > 0, batch * iters.astype(np.float64) / np.where(best > 0, best, 1.0) * fac, 1.0)
+    ddl = np.where(u[3::4] < none_frac, np.inf, ddl).astype(np.float32)
+    return batch.astype(np.int32), iters, ddl

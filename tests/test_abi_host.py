@@ -247,6 +247,8 @@ def test_schedule_validation(ctx):
     assert call(result=None) == arena.ARENA_ERR_INVALID_ARG
     assert call(queue=None) == arena.ARENA_ERR_INVALID_ARG
     assert call(launched=None) == arena.ARENA_ERR_INVALID_ARG
+    assert call(batch=fake) == arena.ARENA_ERR_INVALID_ARG           # deadline arrays: all or none
+    assert call(batch=fake, iters=fake) == arena.ARENA_ERR_INVALID_ARG
 
 
 def test_proxy_desc_layout(tmp_path):

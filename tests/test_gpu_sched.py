@@ -11,9 +11,11 @@ import pytest
 from oracle import scheduler_oracle as so
 from paper_2403_16125_amd import sched_states as ss
 
-def _gpu(st):
+def _gpu(st, ddl=None):
     from paper_2403_16125_amd import arena
     s = arena.Scheduler(st.thr, st.counts, st.capacity)
+    if ddl is not None:
+        s.set_deadlines(*ddl)
     try:
         s.load_state(st.alloc_type, st.alloc_count, st.queue, st.priority)
         s.step(st.depth)
@@ -22,12 +24,13 @@ def _gpu(st):
         s.close()
 
 
-def _check(st):
+def _check(st, ddl=None):
     print(f"schedule: J={st.n_jobs} T={st.thr.shape[1]} NC={st.thr.shape[2]} Q={len(st.queue)} "
-          f"D={st.depth}", flush=True)
+          f"D={st.depth} deadlines={ddl is not None}", flush=True)
+    kw = {} if ddl is None else dict(batch=ddl[0], iters=ddl[1], deadline=ddl[2])
     want = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
-                       st.priority, st.depth)
-    got = _gpu(st)
+                       st.priority, st.depth, **kw)
+    got = _gpu(st, ddl)
     assert got["status"] == 0
     assert got["moves"] == want["moves"]
     assert got["decisions"] == want["decisions"]
@@ -246,5 +249,77 @@ def test_repeated_steps_on_device_state():
             keep = [k for k in range(len(queue)) if not want["launched"][k]]
             queue, prio = [queue[k] for k in keep], [prio[k] for k in keep]
             s.load_queue(queue, prio)
+    finally:
+        s.close()
+
+
+# ---------------------------------------------------------------- deadlines (Eq. 6)
+
+DDL_HAND = {
+    "launch_gate": (({0: [[10, 18, 30]]}, [1, 2, 4], [2], [-1], [0], [0], [0], 4),
+                    ([10], [30.0], [12.0])),
+    "launch_open": (({0: [[10, 18, 30]]}, [1, 2, 4], [4], [-1], [0], [0], [0], 4),
+                    ([10], [30.0], [12.0])),
+    "scale_down_protected": (({0: [[0, 50, 80]], 1: [[10, 19, 0]], 2: [[3, 20, 0]]}, [1, 2, 4], [4],
+                              [-1, 0, 0], [0, 1, 1], [0], [0], 4), ([1, 1, 1], [1.0, 100.0, 1.0], [1e9, 6.0, 1e9])),
+    "scale_up_steered": (({0: [[1, 2, 4]]}, [1, 2, 4], [4], [0], [0], [], [], 1), ([1], [10.0], [3.0])),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", sorted(DDL_HAND))
+def test_deadline_hand_cases(name):
+    args, ddl = DDL_HAND[name]
+    _check(_state(*args), tuple(np.asarray(v) for v in ddl))
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", RANDOM[:6], ids=[f"seed{c[0]}_J{c[1]}" for c in RANDOM[:6]])
+def test_deadline_random_states(case):
+    seed, J, T, counts, cap, rf, qf, ncls, depth, mc = case
+    thr = ss.synthetic_thr(seed, J, T, counts)
+    st = ss.random_state(seed, thr, counts, cap, running_frac=rf, queued_frac=qf, n_classes=ncls,
+                         depth=depth, max_count=mc)
+    _check(st, ss.deadlines(seed, st.thr))
+
+
+@pytest.mark.gpu
+def test_deadline_full_round():
+    st = ss.full_round()
+    _check(st, ss.deadlines(11, st.thr, slack=(0.9, 4.0)))
+
+
+@pytest.mark.gpu
+def test_infinite_deadlines_change_nothing():
+    counts = [1, 2, 4, 8, 16]
+    thr = ss.synthetic_thr(12, 300, 4, counts)
+    st = ss.random_state(12, thr, counts, [64, 48, 32, 16], running_frac=0.7, queued_frac=0.25, depth=3)
+    a = _gpu(st)
+    b = _gpu(st, (np.full(300, 128, np.int32), np.full(300, 1e4, np.float32), np.full(300, np.inf, np.float32)))
+    assert a["moves"] == b["moves"] and (a["alloc_count"] == b["alloc_count"]).all()
+    assert (a["launched"] == b["launched"]).all()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("bad", ["batch", "iters", "deadline"])
+def test_bad_deadline_values_leave_everything_unchanged(bad):
+    from paper_2403_16125_amd import arena
+    thr = np.full((3, 1, 3), 5.0, np.float32)
+    B, N, D = np.full(3, 8, np.int32), np.full(3, 10.0, np.float32), np.full(3, 100.0, np.float32)
+    if bad == "batch":
+        B[1] = 0
+    elif bad == "iters":
+        N[2] = np.nan
+    else:
+        D[0] = -1.0
+    s = arena.Scheduler(thr, [1, 2, 4], [4], batch=B, iters=N, deadline=D)
+    try:
+        s.load_state([0, -1, -1], [1, 0, 0], [1, 2], [0, 1])
+        s.launched.fill_(-7)
+        s.step(2)
+        r = s.results()
+        assert r["status"] == 2
+        assert list(r["alloc_type"]) == [0, -1, -1] and list(r["alloc_count"]) == [1, 0, 0]
+        assert (r["launched"] == -7).all()
     finally:
         s.close()

@@ -138,3 +138,75 @@ def test_invariants_on_random_states(seed):
     assert r["moves"][2] <= st.depth
     for q, j in enumerate(st.queue):
         assert (r["alloc_type"][j] >= 0) == bool(r["launched"][q])
+
+
+def test_deadline_gates_the_launch():
+    # B N = 300: 1, 2, 4 GPUs finish in 30, 16.7, 10 s; a 12 s deadline opens only 4 GPUs
+    thr = _thr({0: [[10, 18, 30]]})
+    kw = dict(batch=[10], iters=[30.0], deadline=[12.0])
+    r = so.schedule(thr, [1, 2, 4], [4], [-1], [0], [0], [0], 4, **kw)
+    assert r["launched"] == [1] and r["alloc_count"] == [2]
+    r = so.schedule(thr, [1, 2, 4], [2], [-1], [0], [0], [0], 4, **kw)     # 2 GPUs fit, but too slow
+    assert r["launched"] == [0] and r["alloc_type"] == [-1]
+    r = so.schedule(thr, [1, 2, 4], [2], [-1], [0], [0], [0], 4)           # no deadline: launches on 2
+    assert r["launched"] == [1] and r["alloc_count"] == [1]
+
+
+def test_deadline_protects_a_scale_down():
+    # the scale-down case with job 1 (the cheapest to shrink) unable to finish on 1 GPU in
+    # time: only job 2 may shrink, which frees one GPU, not enough, so job 0 waits and the
+    # move is undone; with a roomier deadline for job 1 the original two scale-downs return
+    thr, counts, cap, at, ac, q, p = _scale_down_case()
+    base = dict(batch=[1, 1, 1], iters=[1.0, 100.0, 1.0])
+    r = so.schedule(thr, counts, cap, at, ac, q, p, 4, deadline=[1e9, 6.0, 1e9], **base)
+    # job 1 on 1 GPU needs 100 / 10 = 10 s > 6 s: not open; job 2 to 1 GPU frees one GPU only
+    assert r["launched"] == [0] and r["alloc_count"] == [0, 1, 1] and r["moves"] == [0, 0, 0]
+    r = so.schedule(thr, counts, cap, at, ac, q, p, 4, deadline=[1e9, 20.0, 1e9], **base)
+    assert r["launched"] == [1] and r["alloc_count"] == [1, 0, 0] and r["moves"] == [2, 1, 0]
+
+
+def test_deadline_steers_a_scale_up():
+    # 1 -> 2 and 1 -> 4 GPUs gain 1 sample/s per GPU alike (tie: the smaller count); a
+    # deadline that only 4 GPUs meet makes 4 the move
+    thr = _thr({0: [[1, 2, 4]]})
+    r = so.schedule(thr, [1, 2, 4], [4], [0], [0], [], [], 1)
+    assert r["alloc_count"] == [1]
+    r = so.schedule(thr, [1, 2, 4], [4], [0], [0], [], [], 1, batch=[1], iters=[10.0], deadline=[3.0])
+    assert r["alloc_count"] == [2]
+
+
+def test_deadline_values_checked_and_infinite_is_none():
+    thr = _thr({0: [[1, 2]], 1: [[1, 2]]})
+    for bad in (dict(batch=[0, 1], iters=[1.0, 1.0], deadline=[1.0, 1.0]),
+                dict(batch=[1, 1], iters=[-1.0, 1.0], deadline=[1.0, 1.0]),
+                dict(batch=[1, 1], iters=[1.0, 1.0], deadline=[0.0, 1.0]),
+                dict(batch=[1, 1], iters=[1.0, 1.0], deadline=[float("nan"), 1.0]),
+                dict(batch=[1, 1], iters=[1.0, 1.0])):
+        with pytest.raises(ValueError):
+            so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [0], [0], 1, **bad)
+    counts = [1, 2, 4, 8, 16, 32]
+    thr = ss.synthetic_thr(9, 80, 3, counts)
+    st = ss.random_state(9, thr, counts, [40, 24, 16], running_frac=0.6, queued_frac=0.3, depth=3)
+    a = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue, st.priority, 3)
+    inf = np.full(80, np.inf, np.float32)
+    b = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue, st.priority, 3,
+                    batch=np.full(80, 64, np.int32), iters=np.full(80, 1e4, np.float32), deadline=inf)
+    assert a == b
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_deadline_invariants_on_random_states(seed):
+    counts = [1, 2, 4, 8, 16, 32]
+    thr = ss.synthetic_thr(seed, 80, 3, counts)
+    st = ss.random_state(seed, thr, counts, [40, 24, 16], running_frac=0.6, queued_frac=0.3, depth=4)
+    B, N, D = ss.deadlines(seed, st.thr)
+    r = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue, st.priority,
+                    st.depth, batch=B, iters=N, deadline=D)
+    for q, j in enumerate(st.queue):
+        if r["launched"][q]:       # every launch meets its deadline
+            v = float(st.thr[j, r["alloc_type"][j], r["alloc_count"][j]])
+            assert float(B[j]) * float(N[j]) / v <= float(D[j])
+    for j in range(st.n_jobs):      # every moved running job sits on an open grid
+        if st.alloc_type[j] >= 0 and r["alloc_count"][j] != st.alloc_count[j]:
+            v = float(st.thr[j, r["alloc_type"][j], r["alloc_count"][j]])
+            assert float(B[j]) * float(N[j]) / v <= float(D[j])
