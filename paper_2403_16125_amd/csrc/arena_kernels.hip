@@ -48,6 +48,8 @@ struct WaveLds {
     uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
 
+constexpr int kStageCells = 136;   // counts whose outputs a block stages in LDS
+
 template <int SLOTS>
 struct BlockLds {
     float t[kLmax];
@@ -69,6 +71,11 @@ struct BlockLds {
     int32_t next_cell;
     int32_t uniform;              // one kappa for every count of this type
     int32_t moe;
+    // the block's output row (its cells are contiguous in every output
+    // array), written out once all counts are done when it fits
+    float st_t[kStageCells];
+    float st_thr[kStageCells];
+    uint32_t st_plan[kStageCells];
     WaveLds w[kWavesPerBlock];
 };
 
@@ -713,6 +720,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     WaveLds& Wv = B.w[wid];
 
     const int item = A.item_order[blockIdx.x];
+    const bool stage = A.n_counts <= kStageCells;
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
     const int off = A.layer_offset[j];
@@ -945,9 +953,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (!(tmin < kInf)) {
             tally(Wv, lane, kInfeasible, 1);
             if (lane == 0) {
-                A.t_iter[cidx] = __builtin_huge_valf();
-                A.thr[cidx] = 0.0f;
-                A.plan[cidx] = 0u;
+                if (stage) {
+                    B.st_t[ci] = __builtin_huge_valf();
+                    B.st_thr[ci] = 0.0f;
+                    B.st_plan[ci] = 0u;
+                } else {
+                    A.t_iter[cidx] = __builtin_huge_valf();
+                    A.thr[cidx] = 0.0f;
+                    A.plan[cidx] = 0u;
+                }
             }
             if (A.cuts) {
                 uint8_t* row = A.cuts + cidx * A.cuts_stride;
@@ -972,10 +986,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const int m = (int)(kbest & 0x7Fu);
         const int dp = cell.n / (tp * pp);
         if (lane == 0) {
-            A.t_iter[cidx] = (float)Tb;
-            A.thr[cidx] = (float)((double)jb.Bg / Tb);
-            A.plan[cidx] = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) |
-                           ((unsigned)m << 24) | (1u << 31);
+            const float tt = (float)Tb, th = (float)((double)jb.Bg / Tb);
+            const uint32_t pw = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) |
+                                ((unsigned)m << 24) | (1u << 31);
+            if (stage) {
+                B.st_t[ci] = tt;
+                B.st_thr[ci] = th;
+                B.st_plan[ci] = pw;
+            } else {
+                A.t_iter[cidx] = tt;
+                A.thr[cidx] = th;
+                A.plan[cidx] = pw;
+            }
         }
         if (A.cuts && Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf) {
             // the winner is the degree kept while pricing (cuts depend on tp and pp only)
@@ -1020,6 +1042,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         wave_sync();
     }
 
+    if (stage) {
+        __syncthreads();
+        const long long base = ((long long)j * A.n_types + g) * A.n_counts;
+        for (int e = tid; e < A.n_counts; e += 256) {
+            A.t_iter[base + e] = B.st_t[e];
+            A.thr[base + e] = B.st_thr[e];
+            A.plan[base + e] = B.st_plan[e];
+        }
+    }
     if (lane == 0) {
         if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
         const unsigned long long* t = Wv.tally;
