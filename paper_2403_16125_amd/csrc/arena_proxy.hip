@@ -50,6 +50,7 @@ struct ProxyLds {
     double oP[kProxyMaxOps], oA[kProxyMaxOps], oxl[kProxyMaxOps], oload[kProxyMaxOps];
     int32_t binom[16][16];
     int32_t mval[kMaxM];
+    double bt[11][kMaxM];                        // replica samples at dp = 2^e, m_values[k]; -1: not a divisor
     double gT[kProxyMaxOps + 1][kMaxM];          // T of each grid's proxy (inf: none fits)
     int32_t gR[kProxyMaxOps + 1][kMaxM];         // its grouping rank
     unsigned long long gD[kProxyMaxOps + 1][kMaxM];   // its stage GPU exponents
@@ -127,6 +128,23 @@ __device__ __forceinline__ unsigned unrank(int r, int O, int s, const ProxyLds& 
     return mask;
 }
 
+// The grouping after `mask` in lexicographic order of cut vectors (t cuts
+// among operators 1..O-1): the last cut moves up if it can; otherwise the
+// cuts packed against the end follow the highest cut that can still move.
+__device__ __forceinline__ unsigned next_grouping(unsigned mask, int O, int t)
+{
+    const int top = O - 1;
+    int r = 0;
+    while (r < t && ((mask >> (top - r)) & 1u)) ++r;
+    if (r == 0) {
+        const int c = 31 - __clz(mask);
+        return mask ^ (1u << c) ^ (1u << (c + 1));
+    }
+    const unsigned rest = mask & ~(((1u << r) - 1u) << (top - r + 1));
+    const int c = 31 - __clz(rest);
+    return (rest ^ (1u << c)) | (1u << (c + 1)) | (((1u << r) - 1u) << (c + 2));
+}
+
 // End (exclusive) of the stage starting at `lo`: the next stage start, or O.
 __device__ __forceinline__ int stage_end(unsigned mask, int lo, int O)
 {
@@ -170,17 +188,19 @@ __device__ __forceinline__ void shares(unsigned mask, int s, int O, const ProxyL
 }
 
 // Squared bias of multiset m (exponents at bits 4p, largest first) with
-// stage j taking position q_j, summed over the stages in stage order.
-__device__ __forceinline__ double bias(unsigned long long m, const double (&D)[16], const int (&q)[16], int s)
+// stage j taking position q_j, summed over the stages in stage order (S
+// stages, a compile-time count so the sum has no branches).
+template <int S>
+__device__ __forceinline__ double bias(unsigned long long m, const double (&D)[16], const int (&q)[16])
 {
+    const unsigned lo = (unsigned)m, hi = (unsigned)(m >> 32);
     double cost = 0.0;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        if (j < s) {
-            const long long e = (long long)((m >> (4 * q[j])) & 15ull);
-            const double diff = __longlong_as_double((1023ll + e) << 52) - D[j];   // 2^e - share
-            cost += diff * diff;
-        }
+    for (int j = 0; j < S; ++j) {
+        // the exponent of position q_j, then 2^e from its exponent field (e <= 10)
+        const unsigned e = __builtin_amdgcn_ubfe(q[j] < 8 ? lo : hi, (unsigned)(4 * q[j]) & 31u, 4u);
+        const double diff = __hiloint2double((int)((e << 20) + 0x3ff00000u), 0) - D[j];   // 2^e - share
+        cost += diff * diff;
     }
     return cost;
 }
@@ -188,19 +208,79 @@ __device__ __forceinline__ double bias(unsigned long long m, const double (&D)[1
 // The least bias over multisets k = first, first + step, ... below K (the
 // table is lexicographically descending, so among equal costs the smallest k
 // wins) and that k (-1 if none).
-__device__ __forceinline__ double normalise(const double (&D)[16], const int (&q)[16], int s, int K, int first,
-                                            int step, const ProxyLds& S, int& bk)
+template <int S>
+__device__ __forceinline__ double normalise_s(const double (&D)[16], const int (&q)[16], int K, int first,
+                                              int step, const ProxyLds& Ls, int& bk)
 {
     double best = kInfP;
     bk = -1;
-    for (int k = first; k < K; k += step) {
-        const double cost = bias(S.ms[k], D, q, s);
-        if (cost < best) {
-            best = cost;
+    // two multisets per iteration (independent sums), compared in order
+    int k = first;
+    for (; k + step < K; k += 2 * step) {
+        const unsigned long long m0 = Ls.ms[k], m1 = Ls.ms[k + step];
+        const double c0 = bias<S>(m0, D, q);
+        const double c1 = bias<S>(m1, D, q);
+        if (c0 < best) {
+            best = c0;
+            bk = k;
+        }
+        if (c1 < best) {
+            best = c1;
+            bk = k + step;
+        }
+    }
+    if (k < K) {
+        const double c0 = bias<S>(Ls.ms[k], D, q);
+        if (c0 < best) {
+            best = c0;
             bk = k;
         }
     }
     return best;
+}
+
+// shares() for a compile-time stage count.
+template <int S>
+__device__ __forceinline__ void shares_s(unsigned mask, int O, const ProxyLds& Ls, double (&D)[16], int (&q)[16])
+{
+    int lo = 0;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+        const int hi = stage_end(mask, lo, O);
+        D[j] = ssum(Ls, kQd, lo, hi);
+        lo = hi;
+    }
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+        int r = 0;
+#pragma unroll
+        for (int i = 0; i < S; ++i)
+            if (i != j && (D[i] > D[j] || (D[i] == D[j] && i < j))) ++r;
+        q[j] = r;
+    }
+}
+
+// One grouping's shares, ranks and least bias (over its lane's multisets).
+template <int S>
+__device__ __forceinline__ double group_bias(unsigned mask, int O, int K, int first, int step, const ProxyLds& Ls,
+                                             double (&D)[16], int (&q)[16], int& bk)
+{
+    shares_s<S>(mask, O, Ls, D, q);
+    return normalise_s<S>(D, q, K, first, step, Ls, bk);
+}
+
+__device__ __forceinline__ double group_bias(int s, unsigned mask, int O, int K, int first, int step,
+                                             const ProxyLds& Ls, double (&D)[16], int (&q)[16], int& bk)
+{
+    switch (s) {
+#define ARENA_PX_CASE(n) case n: return group_bias<n>(mask, O, K, first, step, Ls, D, q, bk);
+        ARENA_PX_CASE(1) ARENA_PX_CASE(2) ARENA_PX_CASE(3) ARENA_PX_CASE(4)
+        ARENA_PX_CASE(5) ARENA_PX_CASE(6) ARENA_PX_CASE(7) ARENA_PX_CASE(8)
+        ARENA_PX_CASE(9) ARENA_PX_CASE(10) ARENA_PX_CASE(11) ARENA_PX_CASE(12)
+        ARENA_PX_CASE(13) ARENA_PX_CASE(14) ARENA_PX_CASE(15) ARENA_PX_CASE(16)
+#undef ARENA_PX_CASE
+        default: bk = -1; return kInfP;
+    }
 }
 
 // The stage exponents (4 bits per stage, stage order) multiset m assigns.
@@ -380,6 +460,10 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
         S.binom[a][b] = v;
     }
     if (tid < A.n_m) S.mval[tid] = A.m_values[tid];
+    if (tid < 11 * A.n_m) {
+        const int e = tid / A.n_m, k = tid - e * A.n_m;
+        S.bt[e][k] = replica_batch(c.Bg, 1 << e, 1, A.m_values[k]);
+    }
     for (int z = tid; z < (kProxyMaxOps + 1) * kMaxM; z += kPxThreads) {
         (&S.gT[0][0])[z] = kInfP;
         (&S.gR[0][0])[z] = -1;
@@ -404,7 +488,7 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
     __syncthreads();
 
     const int smax = S.no_load ? 0 : (c.O < c.n ? c.O : c.n);
-    const int gpn_pow2 = c.gpn & -c.gpn;          // largest power of two dividing the node size
+    const int gpe = __ffs(c.gpn) - 1;             // log2 of the largest power of two dividing the node size
     for (int s = 1; s <= smax; ++s) {
         const int mo = A.mset_off[ci * 17 + s];
         const int K = A.mset_off[ci * 17 + s + 1] - mo;
@@ -419,19 +503,21 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
         while (tpg < 64 && tpg * 2 * nparts <= kPxThreads) tpg *= 2;
         const int sub = tid & (tpg - 1);
         const int slots = kPxThreads / tpg;
-        for (int base = 0; base < nparts; base += slots) {
-            const int r = base + tid / tpg;
+        // each slot takes a run of consecutive ranks: unrank the first, step to the next
+        const int chunk = (nparts + slots - 1) / slots;
+        const int r0 = (tid / tpg) * chunk;
+        unsigned mask = 0u;
+        for (int it = 0; it < chunk; ++it) {
+            const int r = r0 + it;
             const bool live = r < nparts;
-            unsigned mask = 0u;
             double D[16];
             int q[16];
             double best = kInfP;
             int bk = 0x7fffffff;
             if (live) {
-                mask = unrank(r, c.O, s, S);
-                shares(mask, s, c.O, S, D, q);
+                mask = it == 0 ? unrank(r, c.O, s, S) : next_grouping(mask, c.O, s - 1);
                 int kk;
-                best = normalise(D, q, s, K, sub, tpg, S, kk);
+                best = group_bias(s, mask, c.O, K, sub, tpg, S, D, q, kk);
                 if (kk >= 0) bk = kk;
             }
             for (int off = 1; off < tpg; off <<= 1) {
@@ -445,19 +531,25 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
             if (live && sub == 0) {
                 const unsigned long long dexp = stage_exps(S.ms[bk], q, s);
                 // memory test per B at the largest admissible tensor degree
+                // (replica samples from the per-cell table; dividing by the
+                // power-of-two tp is scaling by its exact reciprocal, so the
+                // memory is bitwise the plain formula's)
                 unsigned fm = (1u << A.n_m) - 1u;
                 int lo = 0;
-                for (int j = 0; j < s; ++j) {
+                for (int j = 0; j < s && fm; ++j) {
                     const int hi = stage_end(mask, lo, c.O);
-                    const int Dj = 1 << (int)((dexp >> (4 * j)) & 15ull);
-                    const int tp = Dj < gpn_pow2 ? Dj : gpn_pow2;
+                    const int ej = (int)((dexp >> (4 * j)) & 15ull);
+                    const int te = ej < gpe ? ej : gpe;                  // log2 of the largest tp
+                    const double itp = __hiloint2double((1023 - te) << 20, 0);
                     const double P = ssum(S, kQP, lo, hi), Aj = ssum(S, kQA, lo, hi);
+                    const double pmem = 4.0 * P * itp;
+                    const double* bt = S.bt[ej - te];
                     for (int k = 0; k < A.n_m; ++k) {
                         if (!((fm >> k) & 1u)) continue;
                         const int B = S.mval[k];
-                        const double b = replica_batch(c.Bg, Dj, tp, B);
+                        const double b = bt[k];
                         const int inflight = B < s - j ? B : s - j;
-                        if (b < 0.0 || stage_mem(P, Aj, tp, b, inflight) > c.mem) fm &= ~(1u << k);
+                        if (b < 0.0 || pmem + (double)inflight * b * Aj * itp > c.mem) fm &= ~(1u << k);
                     }
                     lo = hi;
                 }
