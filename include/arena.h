@@ -243,7 +243,10 @@ arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
  *                    each stage's tensor degree, same layout.  All zero when
  *                    infeasible.
  * Asynchronous on `stream`.  A job whose operators all have zero load has no
- * proxy plan. */
+ * proxy plan.  Host checks (jobs, grids and plan space bound; hbm_bw, f_ref
+ * and n_ops in range; output pointers; at most 2^31 - 1 cells; at most 1280
+ * power-of-two splits of one count into one stage count) return an error
+ * before anything is enqueued. */
 typedef struct arena_proxy_desc {
     const float* hbm_bw;   /* HOST [n_types] memory bandwidth of each type, bytes/s, finite > 0; copied */
     double f_ref;          /* FLOP/s of a speed-1.0 GPU, finite > 0 */
