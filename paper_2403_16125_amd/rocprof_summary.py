@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sqlite3
@@ -34,14 +35,21 @@ KERNEL_SOURCES = {
 }
 
 
+def _code_only(text: str) -> str:
+    """C/C++ source without its comments (edits to documentation do not
+    change what a kernel does)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.sub(r"//[^\n]*", "", text)
+
+
 def kernel_source_sha(kernel: str = "estimate_kernel") -> str:
-    """Hash of the source files one kernel is built from."""
+    """Hash of the code (comments removed) of the files one kernel is built from."""
     files = [os.path.join(ROOT, f) for f in KERNEL_SOURCES[kernel]]
     h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
