@@ -15,7 +15,9 @@
  *     slowest-stage time (the balanced-stage criterion of Sec. 3.2: a
  *     pipeline is bottlenecked by its slowest stage), found by the textbook
  *     recursion over prefixes, and the canonical (lexicographically smallest)
- *     optimal cut vector;
+ *     optimal cut vector; under the memory-constrained rule the same
+ *     criterion restricted to the cut vectors whose every stage fits the
+ *     GPU's memory (Sec. 3.3 chooses within memory limits);
  *   - the plan's iteration time: the 1F1B model of Sec. 3.4 (first
  *     microbatch through every stage, plus B-1 further microbatches on the
  *     slowest stage with point-to-point overlapped), stage latency as the sum
@@ -142,6 +144,149 @@ void oracle_canonical_cuts(const double* U, int L, int pp, double W, int* cuts)
 }
 
 /* ------------------------------------------------------------------ */
+/* Memory-constrained stage partition                                  */
+/* ------------------------------------------------------------------ */
+
+/* One plan's memory model seen from the partition: stage k (0-based) of a
+ * pp-stage 1F1B pipeline over layers [lo, hi) needs
+ *   4 P/tp + min(m, pp-k) b A/tp  bytes,
+ * P and A the parameter and activation bytes of its layers (summed left to
+ * right in double), and fits when that is at most mem. */
+typedef struct {
+    const double* p;   /* per-layer parameter bytes */
+    const double* a;   /* per-layer activation bytes per sample */
+    int L, m, tp;
+    double b, mem;
+} omem;
+
+static int fits_sums(const omem* M, double P, double A, int k, int pp)
+{
+    int inflight = M->m < pp - k ? M->m : pp - k;
+    double Mem = 4.0 * P / (double)M->tp + (double)inflight * M->b * A / (double)M->tp;
+    return Mem <= M->mem;
+}
+
+static int stage_fits(const omem* M, int lo, int hi, int k, int pp)
+{
+    double P = 0.0, A = 0.0;
+    for (int l = lo; l < hi; ++l) { P += M->p[l]; A += M->a[l]; }
+    return fits_sums(M, P, A, k, pp);
+}
+
+/* Brute force: every cut vector in lexicographic order; among those whose
+ * every stage fits, the least largest segment and the first vector attaining
+ * it.  +inf (cuts untouched) when no vector fits.  Small L only. */
+typedef struct {
+    const double* U;
+    const omem* M;
+    int L, pp;
+    int cur[ORACLE_MAX_L + 1];
+    int best[ORACLE_MAX_L + 1];
+    double best_w;
+} bfm_state;
+
+static void bfm_rec(bfm_state* s, int k, double run_max)
+{
+    /* stages 0..k-2 are placed and fit; cur[k-1] starts stage k-1 */
+    if (k == s->pp) {
+        if (!stage_fits(s->M, s->cur[k - 1], s->L, k - 1, s->pp)) return;
+        double w = seg(s->U, s->cur[k - 1], s->L);
+        double m = run_max > w ? run_max : w;
+        if (m < s->best_w) {
+            s->best_w = m;
+            memcpy(s->best, s->cur, sizeof(int) * (size_t)(s->pp + 1));
+        }
+        return;
+    }
+    for (int c = s->cur[k - 1] + 1; c <= s->L - (s->pp - k); ++c) {
+        if (!stage_fits(s->M, s->cur[k - 1], c, k - 1, s->pp)) continue;
+        double w = seg(s->U, s->cur[k - 1], c);
+        double m = run_max > w ? run_max : w;
+        s->cur[k] = c;
+        bfm_rec(s, k + 1, m);
+    }
+}
+
+static double bottleneck_mem_bruteforce(const double* U, const omem* M, int pp, int* cuts)
+{
+    bfm_state s;
+    s.U = U; s.M = M; s.L = M->L; s.pp = pp; s.best_w = INFINITY;
+    s.cur[0] = 0;
+    bfm_rec(&s, 1, -INFINITY);
+    if (cuts && s.best_w < INFINITY)
+        for (int k = 1; k < pp; ++k) cuts[k - 1] = s.best[k];
+    return s.best_w;
+}
+
+/* Recursion over suffixes, stages counted from the back (a stage's number of
+ * in-flight microbatches, min(m, pp-k), depends only on how many stages
+ * follow it, so suffix problems do not depend on pp):
+ *   G_0(L) = -inf, G_0(i) = +inf for i < L;
+ *   G_t(i) = min over e in (i, L] with layers [i, e) fitting as the t-th
+ *            stage from the back of max(U_e - U_i, G_{t-1}(e)).
+ * G_t(i) is the least largest segment over the splits of [i, L) into t
+ * non-empty stages that all fit.  G has (pp+1)(L+1) entries.  O(pp L^2): the
+ * memory sums of [i, e) grow with e one layer at a time (the same left-to-
+ * right sums as stage_fits). */
+static void mem_recursion(const double* U, const omem* M, int pp, double* G)
+{
+    int L = M->L, L1 = L + 1;
+    for (int i = 0; i <= L; ++i) G[i] = (i == L) ? -INFINITY : INFINITY;
+    for (int t = 1; t <= pp; ++t) {
+        for (int i = 0; i <= L; ++i) {
+            double best = INFINITY, P = 0.0, A = 0.0;
+            for (int e = i + 1; e <= L; ++e) {
+                P += M->p[e - 1];
+                A += M->a[e - 1];
+                /* as the t-th stage from the back it is stage pp - t */
+                if (!fits_sums(M, P, A, pp - t, pp)) continue;
+                double g = G[(t - 1) * L1 + e], w = seg(U, i, e);
+                double v = w > g ? w : g;
+                if (v < best) best = v;
+            }
+            G[t * L1 + i] = best;
+        }
+    }
+}
+
+/* W*_mem(pp) = G_pp(0) and the lexicographically smallest cut vector that
+ * attains it with every stage fitting: each cut, left to right, is the
+ * smallest position such that the stage it closes fits, is at most W, and
+ * the rest of the layers still split into the remaining stages within W.
+ * +inf (cuts untouched) when no split fits. */
+static double bottleneck_mem(const double* U, const omem* M, int pp, int* cuts)
+{
+    int L = M->L, L1 = L + 1;
+    double* G = (double*)malloc(sizeof(double) * (size_t)(pp + 1) * (size_t)L1);
+    mem_recursion(U, M, pp, G);
+    double W = G[pp * L1 + 0];
+    if (cuts && W < INFINITY) {
+        int prev = 0;
+        for (int k = 1; k < pp; ++k) {
+            int c = prev + 1;
+            while (!(seg(U, prev, c) <= W && stage_fits(M, prev, c, k - 1, pp) &&
+                     G[(pp - k) * L1 + c] <= W))
+                ++c;
+            cuts[k - 1] = c;
+            prev = c;
+        }
+    }
+    free(G);
+    return W;
+}
+
+/* Exposed for tests: p, a per-layer bytes, b samples per microbatch.
+ * Returns W (+inf if no split fits); cuts receives pp - 1 cuts. */
+double oracle_bottleneck_mem(const double* U, const double* p, const double* a, int L, int pp,
+                             int m, double b, int tp, double mem, int brute, int* cuts)
+{
+    if (L < 1 || pp < 1 || pp > L || L > ORACLE_MAX_L || m < 1 || tp < 1) return NAN;
+    omem M;
+    M.p = p; M.a = a; M.L = L; M.m = m; M.tp = tp; M.b = b; M.mem = mem;
+    return brute ? bottleneck_mem_bruteforce(U, &M, pp, cuts) : bottleneck_mem(U, &M, pp, cuts);
+}
+
+/* ------------------------------------------------------------------ */
 /* Plan pricing                                                        */
 /* ------------------------------------------------------------------ */
 
@@ -255,15 +400,38 @@ static int build_views(int j, int g, const int32_t* off, const float* t, const f
  * stages 1..pp-1) is priced as given.  out[0..3] = T, mem_max, s_max,
  * feasible; cuts_out (nullable) receives the cuts used.  Returns 0 on
  * success. */
+/* The stage cuts of plan (dp, tp, pp, m) under partition rule `rule`:
+ * 0 = the canonical balanced partition (memory checked after pricing),
+ * 1 = the canonical balanced partition among those whose every stage fits.
+ * Returns 0, or -1 when rule 1 finds no split that fits. */
+static int plan_cuts(const ojob* jb, const otype* ty, int rule, int dp, int tp, int pp, int m,
+                     const double* U, int* cuts)
+{
+    if (rule == 0) {
+        double W = oracle_bottleneck_dp(U, jb->L, pp);
+        oracle_canonical_cuts(U, jb->L, pp, W, cuts);
+        return 0;
+    }
+    double pd[ORACLE_MAX_L], ad[ORACLE_MAX_L];
+    for (int l = 0; l < jb->L; ++l) { pd[l] = (double)jb->p[l]; ad[l] = (double)jb->a[l]; }
+    omem M;
+    M.p = pd; M.a = ad; M.L = jb->L; M.m = m; M.tp = tp;
+    M.b = (double)jb->Bg / (double)(dp * m);
+    M.mem = ty->mem;
+    return bottleneck_mem(U, &M, pp, cuts) < INFINITY ? 0 : -1;
+}
+
 int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, int m,
                      const int32_t* off, const float* t, const float* p, const float* a,
                      const float* x, const float* a2a, const int32_t* batch,
                      const float* speed, const float* mem, const float* bwi, const float* bwe,
-                     const int32_t* gpn, const int32_t* cuts_in, int32_t* cuts_out, double* out)
+                     const int32_t* gpn, const int32_t* cuts_in, int32_t* cuts_out, double* out,
+                     int rule)
 {
     ojob jb; otype ty;
     if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
     if (dp < 1 || tp < 1 || pp < 1 || m < 1 || dp * tp * pp != n || pp > jb.L) return -1;
+    if (rule != 0 && rule != 1) return -1;
     double u[ORACLE_MAX_L], U[ORACLE_MAX_L + 1];
     int cuts[ORACLE_MAX_L];
     layer_costs(&jb, &ty, kappa, dp, tp, u);
@@ -274,9 +442,10 @@ int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, 
             int prevc = k == 0 ? 0 : cuts[k - 1];
             if (cuts[k] <= prevc || cuts[k] >= jb.L) return -1;
         }
-    } else {
-        double W = oracle_bottleneck_dp(U, jb.L, pp);
-        oracle_canonical_cuts(U, jb.L, pp, W, cuts);
+    } else if (plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) != 0) {
+        /* rule 1 and no split fits memory */
+        out[0] = INFINITY; out[1] = INFINITY; out[2] = INFINITY; out[3] = 0.0;
+        return 0;
     }
     oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
     out[0] = r.T; out[1] = r.mem_max; out[2] = r.s_max; out[3] = (double)r.feasible;
@@ -307,7 +476,7 @@ static int key_less(const ocand* a, const ocand* b)
  * pp divides n/tp and is at most the layer count, dp = n/(tp pp), and m is a
  * listed microbatch count with dp*m dividing the global batch (the global
  * batch is fixed under scaling, Sec. 3.5).  Each plan is priced with its
- * balanced partition.  The cell's answer is the smallest (pp, tp, m) among
+ * balanced partition under `rule` (see plan_cuts).  The cell's answer is the smallest (pp, tp, m) among
  * feasible plans whose T is within a factor (1 + tie_eps) of the smallest
  * feasible T.
  * res[0] = T (inf if none), res[1] = throughput (samples/s, 0 if none);
@@ -318,7 +487,7 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
                 const float* speed, const float* mem, const float* bwi, const float* bwe,
                 const int32_t* gpn, const int32_t* counts, const float* kappa_grid, int n_counts,
                 const int32_t* m_values, int n_m, double tie_eps,
-                double* res, int32_t* plan, int32_t* cuts_out)
+                double* res, int32_t* plan, int32_t* cuts_out, int rule)
 {
     ojob jb; otype ty;
     if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
@@ -342,15 +511,19 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
             if (!any) continue;
             layer_costs(&jb, &ty, kappa, dp, tp, u);
             oracle_prefix(u, L, U);
-            double W = oracle_bottleneck_dp(U, L, pp);
-            oracle_canonical_cuts(U, L, pp, W, cuts);
             for (int mi = 0; mi < n_m; ++mi) {
                 int m = m_values[mi];
                 if (jb.Bg % (dp * m) != 0) continue;
-                oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
                 if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
-                cand[nc].T = r.T; cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp;
-                cand[nc].m = m; cand[nc].feasible = r.feasible;
+                cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp; cand[nc].m = m;
+                if (plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) == 0) {
+                    oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
+                    cand[nc].T = r.T;
+                    cand[nc].feasible = r.feasible;
+                } else {
+                    cand[nc].T = INFINITY;
+                    cand[nc].feasible = 0;
+                }
                 ++nc;
             }
         }
@@ -378,8 +551,7 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
         if (cuts_out) {
             layer_costs(&jb, &ty, kappa, w->dp, w->tp, u);
             oracle_prefix(u, L, U);
-            double W = oracle_bottleneck_dp(U, L, w->pp);
-            oracle_canonical_cuts(U, L, w->pp, W, cuts);
+            plan_cuts(&jb, &ty, rule, w->dp, w->tp, w->pp, w->m, U, cuts);
             for (int k = 0; k < w->pp - 1; ++k) cuts_out[k] = cuts[k];
         }
     }
@@ -396,8 +568,10 @@ int oracle_cells(int n_sel, const int64_t* cells, int n_types, int n_counts,
                  const float* speed, const float* mem, const float* bwi, const float* bwe,
                  const int32_t* gpn, const int32_t* counts, const float* kappa_grid,
                  const int32_t* m_values, int n_m, double tie_eps,
-                 double* res, int32_t* plan, int32_t* cuts, int cuts_stride, int32_t* nplans)
+                 double* res, int32_t* plan, int32_t* cuts, int cuts_stride, int32_t* nplans,
+                 int rule)
 {
+    if (rule != 0 && rule != 1) return -1;
     for (int s = 0; s < n_sel; ++s) {
         int64_t c = cells[s];
         int ci = (int)(c % n_counts);
@@ -408,7 +582,7 @@ int oracle_cells(int n_sel, const int64_t* cells, int n_types, int n_counts,
             for (int k = 0; k < cuts_stride; ++k) crow[k] = -1;
         int np = oracle_cell(j, g, ci, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn,
                              counts, kappa_grid, n_counts, m_values, n_m, tie_eps,
-                             res + 2 * s, plan + 4 * s, crow);
+                             res + 2 * s, plan + 4 * s, crow, rule);
         if (np < 0) return -1;
         nplans[s] = np;
     }

@@ -53,11 +53,14 @@ def load():
     lib.oracle_canonical_cuts.argtypes = [_f64p, c_int, c_int, c_double, _i32p]
     lib.oracle_canonical_cuts.restype = None
     tables = [_i32p, _f32p, _f32p, _f32p, _f32p, _f32p, _i32p, _f32p, _f32p, _f32p, _f32p, _i32p]
+    lib.oracle_bottleneck_mem.argtypes = [_f64p, _f64p, _f64p, c_int, c_int, c_int, c_double, c_int,
+                                          c_double, c_int, _i32p]
+    lib.oracle_bottleneck_mem.restype = c_double
     lib.oracle_eval_plan.argtypes = [c_int, c_int, c_int, c_double, c_int, c_int, c_int, c_int] + tables + [
-        ctypes.c_void_p, ctypes.c_void_p, _f64p]
+        ctypes.c_void_p, ctypes.c_void_p, _f64p, c_int]
     lib.oracle_eval_plan.restype = c_int
     lib.oracle_cells.argtypes = [c_int, _i64p, c_int, c_int] + tables + [
-        _i32p, _f32p, _i32p, c_int, c_double, _f64p, _i32p, _i32p, c_int, _i32p]
+        _i32p, _f32p, _i32p, c_int, c_double, _f64p, _i32p, _i32p, c_int, _i32p, c_int]
     lib.oracle_cells.restype = c_int
     lib.oracle_layer_costs.argtypes = [c_int, c_int, c_double, c_int, c_int] + tables + [_f64p]
     lib.oracle_layer_costs.restype = None
@@ -94,6 +97,21 @@ def canonical_cuts(U, pp: int, W: float):
     return [int(c) for c in cuts[:pp - 1]]
 
 
+def bottleneck_mem(U, p, a, pp: int, m: int, b: float, tp: int, mem: float, brute: bool = False):
+    """(W*_mem, cuts) of the partition whose every stage fits memory: stage k of
+    pp holds 4 P/tp + min(m, pp-k) b A/tp bytes <= mem.  W = inf and cuts None
+    when no split fits.  brute=True enumerates every cut vector."""
+    U = np.ascontiguousarray(U, np.float64)
+    p = np.ascontiguousarray(p, np.float64)
+    a = np.ascontiguousarray(a, np.float64)
+    cuts = np.zeros(max(pp - 1, 1), np.int32)
+    w = load().oracle_bottleneck_mem(U, p, a, len(U) - 1, int(pp), int(m), float(b), int(tp), float(mem),
+                                     int(bool(brute)), cuts)
+    if not np.isfinite(w):
+        return w, None
+    return w, [int(c) for c in cuts[:pp - 1]]
+
+
 # ------------------------------------------------------------ workload access
 
 def _tables(w):
@@ -112,9 +130,10 @@ def layer_costs(w, j, g, kappa, dp, tp) -> np.ndarray:
     return u
 
 
-def eval_plan(w, j, g, n, kappa, dp, tp, pp, m, cuts=None):
-    """Price one plan.  cuts=None uses the canonical balanced partition.
-    Returns dict(T, mem_max, s_max, feasible, cuts)."""
+def eval_plan(w, j, g, n, kappa, dp, tp, pp, m, cuts=None, rule: int = 0):
+    """Price one plan.  cuts=None uses the canonical balanced partition of the
+    partition rule (0: balanced, memory checked after; 1: balanced among the
+    splits that fit memory).  Returns dict(T, mem_max, s_max, feasible, cuts)."""
     out = np.zeros(4, np.float64)
     cuts_out = np.zeros(max(pp - 1, 1), np.int32)
     cin = None
@@ -123,15 +142,16 @@ def eval_plan(w, j, g, n, kappa, dp, tp, pp, m, cuts=None):
         keep = np.ascontiguousarray(np.asarray(list(cuts) + [0], np.int32))
         cin = keep.ctypes.data
     rc = load().oracle_eval_plan(int(j), int(g), int(n), float(kappa), int(dp), int(tp), int(pp),
-                                 int(m), *_tables(w), cin, cuts_out.ctypes.data, out)
+                                 int(m), *_tables(w), cin, cuts_out.ctypes.data, out, int(rule))
     if rc != 0:
         raise ValueError("oracle_eval_plan rejected the plan")
     return dict(T=out[0], mem_max=out[1], s_max=out[2], feasible=bool(out[3]),
                 cuts=[int(c) for c in cuts_out[:pp - 1]])
 
 
-def cells(w, cell_ids, kappa_round: int = 0, cuts_stride: int = 128):
-    """Best plan of each listed cell (flat index (j*T + g)*NC + ci).
+def cells(w, cell_ids, kappa_round: int = 0, cuts_stride: int = 128, rule: int = 0):
+    """Best plan of each listed cell (flat index (j*T + g)*NC + ci) under
+    partition rule `rule` (see eval_plan).
     Returns dict of arrays: T (f64), thr (f64), dp, tp, pp, m (i32), cuts (i32, -1 padded),
     nplans (i32)."""
     ids = np.ascontiguousarray(np.asarray(cell_ids, np.int64))
@@ -144,7 +164,7 @@ def cells(w, cell_ids, kappa_round: int = 0, cuts_stride: int = 128):
     rc = load().oracle_cells(n, ids, int(w.n_types), int(w.n_counts), *_tables(w),
                              np.ascontiguousarray(w.counts, np.int32), kap,
                              np.ascontiguousarray(w.m_values, np.int32), len(w.m_values),
-                             float(w.tie_eps), res, plan, cuts, cuts_stride, nplans)
+                             float(w.tie_eps), res, plan, cuts, cuts_stride, nplans, int(rule))
     if rc != 0:
         raise ValueError("oracle_cells rejected the input")
     res = res[:2 * n].reshape(n, 2)
