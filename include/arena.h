@@ -129,7 +129,9 @@ typedef struct arena_counters {
     int64_t alg_ops;          /* algorithmic operations of the work done: 8 per layer of each
                                  solved problem (layer costs and prefix), 8 per recursion entry,
                                  4 L per priced pipeline degree (cuts), 12 pp + 40 per priced
-                                 plan */
+                                 plan; under ARENA_PARTITION_MEMORY also 4 L per memory-only
+                                 split test and per memory-rule cut vector */
+    int64_t mem_partitions;   /* memory-rule partitions solved (ARENA_PARTITION_MEMORY) */
 } arena_counters;
 
 /* Exact size of the plan space of the bound tables (host-side count). */
@@ -180,6 +182,25 @@ arena_status arena_set_plan_space(arena_ctx* ctx, const int32_t* m_values, int32
  * wanted.  The results are identical either way; only the work differs (see
  * plans_skipped).  0 turns it off, any other value on. */
 arena_status arena_set_bound_pruning(arena_ctx* ctx, int32_t enabled);
+
+/* Partition rules (arena_set_partition_rule). */
+#define ARENA_PARTITION_BALANCED 0
+#define ARENA_PARTITION_MEMORY 1
+
+/* Which stage partition prices a plan (default ARENA_PARTITION_BALANCED).
+ *   BALANCED  the canonical balanced partition (Sec. 3.2: a pipeline runs at
+ *             its slowest stage, so the stages minimise the largest stage
+ *             cost), then the memory check; a plan whose balanced stages do
+ *             not fit is infeasible.
+ *   MEMORY    the same criterion over the splits whose every stage fits
+ *             memory (Sec. 3.3 picks parallelism within memory limits):
+ *             stage k of pp holds 4 P_k/tp + min(m, pp-k) b A_k/tp bytes, at
+ *             most mem; the lexicographically smallest such split of least
+ *             largest stage cost.  A plan is infeasible only when no split
+ *             fits.  Plans whose balanced split fits are priced as under
+ *             BALANCED, so no cell gets slower; cut rows follow the rule.
+ * Takes effect at the next arena_estimate; INVALID_ARG for other values. */
+arena_status arena_set_partition_rule(arena_ctx* ctx, int32_t rule);
 
 /* Size of the plan space of the bound tables (host computation, no HIP
  * call).  Needs jobs, grids and plan space bound. */

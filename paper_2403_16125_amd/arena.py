@@ -30,8 +30,11 @@ EXPORTED = (
     "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
-    "arena_schedule", "arena_proxy_estimate",
+    "arena_schedule", "arena_proxy_estimate", "arena_set_partition_rule",
 )
+
+PARTITION_BALANCED = 0
+PARTITION_MEMORY = 1
 
 MAX_PROXY_OPS = 16
 
@@ -64,7 +67,7 @@ class Counters(ctypes.Structure):
     _fields_ = [("cells", ctypes.c_int64), ("plans", ctypes.c_int64),
                 ("problems", ctypes.c_int64), ("dp_entries", ctypes.c_int64),
                 ("infeasible_cells", ctypes.c_int64), ("plans_skipped", ctypes.c_int64),
-                ("alg_ops", ctypes.c_int64)]
+                ("alg_ops", ctypes.c_int64), ("mem_partitions", ctypes.c_int64)]
 
 
 class ProxyDesc(ctypes.Structure):
@@ -121,6 +124,8 @@ def load():
     lib.arena_set_plan_space.restype = st
     lib.arena_set_bound_pruning.argtypes = [vp, i32]
     lib.arena_set_bound_pruning.restype = st
+    lib.arena_set_partition_rule.argtypes = [vp, i32]
+    lib.arena_set_partition_rule.restype = st
     lib.arena_space_size_get.argtypes = [vp, ctypes.POINTER(SpaceSize)]
     lib.arena_space_size_get.restype = st
     lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
@@ -215,6 +220,10 @@ def arena_set_bound_pruning(ctx, enabled: bool) -> None:
     _check(ctx, load().arena_set_bound_pruning(ctx, 1 if enabled else 0))
 
 
+def arena_set_partition_rule(ctx, rule: int) -> None:
+    _check(ctx, load().arena_set_partition_rule(ctx, int(rule)))
+
+
 def arena_space_size_get(ctx) -> dict:
     s = SpaceSize()
     _check(ctx, load().arena_space_size_get(ctx, ctypes.byref(s)))
@@ -233,7 +242,8 @@ def arena_get_counters(ctx) -> dict:
     c = Counters()
     _check(ctx, load().arena_get_counters(ctx, ctypes.byref(c)))
     return dict(cells=c.cells, plans=c.plans, problems=c.problems, dp_entries=c.dp_entries,
-                infeasible_cells=c.infeasible_cells, plans_skipped=c.plans_skipped, alg_ops=c.alg_ops)
+                infeasible_cells=c.infeasible_cells, plans_skipped=c.plans_skipped, alg_ops=c.alg_ops,
+                mem_partitions=c.mem_partitions)
 
 
 def arena_proxy_estimate(ctx, hbm_bw, f_ref: float, n_ops: int, t_iter, thr, plan, stream=None) -> None:
@@ -291,7 +301,8 @@ class Estimator:
 
     `workload` is any object with the attributes of workloads.Workload."""
 
-    def __init__(self, workload, device: int = 0, with_cuts: bool = False, prune: bool = True):
+    def __init__(self, workload, device: int = 0, with_cuts: bool = False, prune: bool = True,
+                 rule: int = PARTITION_BALANCED):
         import torch
         self.torch = torch
         self.w = workload
@@ -311,6 +322,7 @@ class Estimator:
             arena_set_plan_space(self.ctx, workload.m_values, workload.tie_eps)
             arena_set_kappa(self.ctx, workload.kappa[0])
             arena_set_bound_pruning(self.ctx, prune)
+            arena_set_partition_rule(self.ctx, rule)
             C = workload.n_cells
             self.n_cells = C
             self.t_iter = torch.empty(C, dtype=torch.float32, device=self.dev)
@@ -327,6 +339,9 @@ class Estimator:
 
     def set_kappa(self, kappa) -> None:
         arena_set_kappa(self.ctx, kappa)
+
+    def set_partition_rule(self, rule: int) -> None:
+        arena_set_partition_rule(self.ctx, rule)
 
     def estimate(self, stream=None) -> None:
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream

@@ -44,6 +44,7 @@ struct arena_ctx {
     std::vector<int32_t> m_values;
     double tie_eps = 1e-6;
     bool prune = true;
+    int32_t partition_rule = ARENA_PARTITION_BALANCED;
 
     // cached space size
     bool size_valid = false;
@@ -548,6 +549,16 @@ arena_status arena_set_bound_pruning(arena_ctx* c, int32_t enabled)
     return ARENA_OK;
 }
 
+arena_status arena_set_partition_rule(arena_ctx* c, int32_t rule)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (rule != ARENA_PARTITION_BALANCED && rule != ARENA_PARTITION_MEMORY)
+        return fail(c, ARENA_ERR_INVALID_ARG, "partition rule: %d is neither BALANCED (0) nor MEMORY (1)", rule);
+    c->partition_rule = rule;
+    return ARENA_OK;
+}
+
 arena_status arena_space_size_get(const arena_ctx* cc, arena_space_size* out)
 {
     arena_ctx* c = const_cast<arena_ctx*>(cc);
@@ -605,6 +616,7 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     for (int i = 0; i < A.n_m; ++i) A.m_values[i] = ms[i];
     A.tie_eps = c->tie_eps;
     A.prune = c->prune ? 1 : 0;
+    A.mem_rule = c->partition_rule == ARENA_PARTITION_MEMORY ? 1 : 0;
     A.t_iter = t_iter;
     A.thr = thr;
     A.plan = plan;
@@ -637,6 +649,7 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     out->infeasible_cells = (int64_t)h[arena::kInfeasible];
     out->plans_skipped = (int64_t)h[arena::kSkipped];
     out->alg_ops = (int64_t)h[arena::kAlgOps];
+    out->mem_partitions = (int64_t)h[arena::kMemParts];
     if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");
     return ARENA_OK;
 }

@@ -22,7 +22,8 @@ struct TypeDev {
 };
 
 // Device tallies, zeroed before each estimate.
-enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kSkipped, kAlgOps, kNumCounters };
+enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kSkipped, kAlgOps, kMemParts,
+               kNumCounters };
 
 struct EstimateArgs {
     const int32_t* layer_offset;  // [J+1]
@@ -43,6 +44,7 @@ struct EstimateArgs {
     int32_t m_values[kMaxM];
     double tie_eps;
     int32_t prune;                // bound pruning on
+    int32_t mem_rule;             // partition rule 1: balanced among the splits that fit memory
     float* t_iter;
     float* thr;
     uint32_t* plan;

@@ -41,9 +41,11 @@ struct WaveLds {
     int32_t mq[kMaxM];            // those microbatch counts
     double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
     uint8_t tq[64];               // a problem's requested degrees, compacted
-    uint8_t cutrow[kLmax];        // with cuts on: the cut row of the degree holding the best time
+    uint8_t cutrow[kLmax];        // with cuts on: the cut row of the plan holding the best time
     double cut_T;                 //   that time (+inf: none yet)
     int32_t cut_tp, cut_pp;       //   and its degrees
+    int32_t cut_m;                //   memory rule: its m if the row fits only under the rule, else 0
+    int32_t cut_mfit;             //   the smallest m the balanced row fits
     unsigned long long tally[kNumCounters];   // the wave's work tallies (lane 0 updates)
     uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
 };
@@ -522,18 +524,226 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     return r;
 }
 
+// ------------------------------------------------------------ memory-constrained partition
+
+// Stage [j, e) fits when 4 P + ib A <= cap, ib = in-flight microbatches x
+// samples per microbatch and cap = mem x tp (the memory check of the pricing,
+// same operation order).
+__device__ __forceinline__ bool seg_fits(double Pe, double Ae, double Pj, double Aj, double ib, double cap)
+{
+    return 4.0 * (Pe - Pj) + ib * (Ae - Aj) <= cap;
+}
+
+// Stage bounds of a cut vector held as c_k in lane k (cA) and lane k - 64
+// (cB), c_0 = 0 and c_pp = L set here; as canonical_stages returns them.
+__device__ __forceinline__ Stages stages_from_cuts(int cA, int cB, int lane, int L, int pp)
+{
+    cA = (lane >= 1 && lane < pp) ? cA : 0;
+    cA = lane == pp ? L : cA;
+    cB = lane + 64 < pp ? cB : 0;
+    cB = lane + 64 == pp ? L : cB;
+    Stages r;
+    r.lo0 = cA;
+    r.hi0 = from_next_lane(cA, __builtin_amdgcn_readlane(cB, 0));
+    r.lo1 = cB;
+    r.hi1 = from_next_lane(cB, pp == 128 ? L : 0);
+    return r;
+}
+
+// Do the stages of sg all fit with m microbatches of b samples?  Stage s
+// holds min(m, pp - s) microbatches.
+__device__ __forceinline__ bool stages_fit(const Stages& sg, const double* Pp, const double* Ap, int lane,
+                                           int pp, int m, double b, double cap)
+{
+    bool bad = false;
+    if (lane < pp) {
+        const int r = pp - lane;
+        bad = !seg_fits(Pp[sg.hi0], Ap[sg.hi0], Pp[sg.lo0], Ap[sg.lo0], (double)(m < r ? m : r) * b, cap);
+    }
+    if (lane + 64 < pp) {
+        const int r = pp - lane - 64;
+        bad |= !seg_fits(Pp[sg.hi1], Ap[sg.hi1], Pp[sg.lo1], Ap[sg.lo1], (double)(m < r ? m : r) * b, cap);
+    }
+    return __ballot(bad) == 0ull;
+}
+
+// Lexicographically smallest cut vector of pp stages whose every stage fits
+// (stage k holds min(m, pp - k) microbatches of b samples) and costs at most
+// W, if there is one (W = +inf: memory alone).  From the back, the t-th stage
+// starts at r_t, the leftmost start whose stage up to r_{t-1} fits and costs
+// at most W (both hold on a suffix of starts: cost and memory only grow as a
+// stage extends left); then c_k = max(k, r_{pp-k}).  If any split fits
+// within W, no cut of it lies left of this vector's, and this vector fits
+// too: a stage the clamp leaves as one layer holds no more microbatches than
+// the stage holding that layer in the other split.  So the split exists iff
+// the vector passes the final check.  Lane l tests starts l and l + 64.
+template <int S>
+__device__ bool mem_cuts(const double* U, const double* Pp, const double* Ap, int lane, int L, int pp, int m,
+                         double b, double cap, double W, Stages& sg)
+{
+    const int j0 = lane, j1 = lane + 64;
+    const double Uj0 = U[j0 * S], Uj1 = U[j1 * S];
+    const double Pj0 = Pp[j0], Aj0 = Ap[j0];
+    const double Pj1 = j1 <= kLmax ? Pp[j1] : 0.0, Aj1 = j1 <= kLmax ? Ap[j1] : 0.0;
+    int cA = 0, cB = 0;
+    int e = L;
+    for (int t = 1; t < pp; ++t) {
+        int r = 0;
+        if (e > 0) {
+            const double ib = (double)(m < t ? m : t) * b;
+            const double Ue = U[e * S], Pe = Pp[e], Ae = Ap[e];
+            const bool p0 = j0 < e && Ue - Uj0 <= W && seg_fits(Pe, Ae, Pj0, Aj0, ib, cap);
+            const bool p1 = j1 < e && Ue - Uj1 <= W && seg_fits(Pe, Ae, Pj1, Aj1, ib, cap);
+            const unsigned long long b0 = __ballot(p0), b1 = __ballot(p1);
+            if (b0) r = __ffsll((long long)b0) - 1;
+            else if (b1) r = 63 + __ffsll((long long)b1);
+            else return false;        // not even the last layer alone: no split
+        }
+        const int k = pp - t;
+        const int c = r > k ? r : k;
+        cA = lane == k ? c : cA;
+        cB = lane + 64 == k ? c : cB;
+        e = r;
+    }
+    sg = stages_from_cuts(cA, cB, lane, L, pp);
+    bool bad = false;
+    if (lane < pp) {
+        const int r = pp - lane;
+        bad = !(sg.hi0 > sg.lo0) || !(U[sg.hi0 * S] - U[sg.lo0 * S] <= W) ||
+              !seg_fits(Pp[sg.hi0], Ap[sg.hi0], Pp[sg.lo0], Ap[sg.lo0], (double)(m < r ? m : r) * b, cap);
+    }
+    if (lane + 64 < pp) {
+        const int r = pp - lane - 64;
+        bad |= !(sg.hi1 > sg.lo1) || !(U[sg.hi1 * S] - U[sg.lo1 * S] <= W) ||
+               !seg_fits(Pp[sg.hi1], Ap[sg.hi1], Pp[sg.lo1], Ap[sg.lo1], (double)(m < r ? m : r) * b, cap);
+    }
+    return __ballot(bad) == 0ull;
+}
+
+// Smallest starting position j in [0, i] of a stage ending at i that fits
+// with ib (j = i, the empty stage, always does).
+__device__ __forceinline__ int fit_start(const double* Pp, const double* Ap, int i, double Pi, double Ai,
+                                         double ib, double cap)
+{
+    int lo = 0, hi = i;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (seg_fits(Pi, Ai, Pp[mid], Ap[mid], ib, cap)) hi = mid; else lo = mid + 1;
+    }
+    return lo;
+}
+
+// One entry of row k of the memory-constrained recursion (R holds row k-1
+// and receives row k in place, as in dp_entry):
+//   D_k(i) = min over j in [a, i-1] of max(D_{k-1}(j), U_i - U_j),
+// a = max(k-1, the first start whose stage up to i fits as stage k-1).
+// D_{k-1} is non-decreasing in j also under the memory limits (dropping the
+// last layer of a prefix, or splitting a stage to keep k-1 of them, moves
+// stages only towards the back, where they hold fewer microbatches), so the
+// minimum sits at the crossing c, the first j >= a with D_{k-1}(j) >=
+// U_i - U_j (i itself counts as passing): min(D_{k-1}(c), U_i - U_{c-1}),
+// each term only where its position lies in the window.
+template <int S>
+__device__ __forceinline__ void mem_entry(const double* U, double* R, int k, int L, int i, double Ui, int fs)
+{
+    double v = kInf;
+    const bool act = i <= L;
+    if (act) {
+        const int a = fs > k - 1 ? fs : k - 1;
+        if (i >= k && a < i) {
+            int lo = a, hi = i;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (R[mid] >= Ui - U[mid * S]) hi = mid; else lo = mid + 1;
+            }
+            v = lo < i ? R[lo] : kInf;
+            if (lo > a) v = fmin(v, Ui - U[(lo - 1) * S]);
+        }
+    }
+    __asm__ volatile("" ::: "memory");
+    if (act) R[i] = v;
+}
+
+// Bottleneck of pp stages over the splits whose every stage fits (stage k
+// holds min(m, pp - k) microbatches of b samples): D_pp(L), +inf if none.
+// R: the wave's row of kLmax + 1 doubles.  Lane l owns i = 1 + l and 65 + l.
+template <int S>
+__device__ double mem_bottleneck(const double* U, const double* Pp, const double* Ap, double* R, int lane,
+                                 int L, int pp, int m, double b, double cap, unsigned& entries)
+{
+    const int i0 = 1 + lane, i1 = 65 + lane;
+    const double Ui0 = U[i0 * S], Ui1 = U[i1 * S];
+    const double Pi0 = Pp[i0], Ai0 = Ap[i0];
+    const double Pi1 = i1 <= kLmax ? Pp[i1] : 0.0, Ai1 = i1 <= kLmax ? Ap[i1] : 0.0;
+    const bool two = L > 64;
+    // row 1: the first stage holds min(m, pp) microbatches
+    int rcur = m < pp ? m : pp;
+    double ib = (double)rcur * b;
+    int fs0 = i0 <= L ? fit_start(Pp, Ap, i0, Pi0, Ai0, ib, cap) : 0;
+    int fs1 = (two && i1 <= L) ? fit_start(Pp, Ap, i1, Pi1, Ai1, ib, cap) : 0;
+    if (lane == 0) R[0] = kInf;
+    if (i0 <= L) R[i0] = fs0 == 0 ? Ui0 - U[0] : kInf;
+    if (two && i1 <= L) R[i1] = fs1 == 0 ? Ui1 - U[0] : kInf;
+    unsigned n = (unsigned)L;
+    wave_sync();
+    for (int k = 2; k <= pp; ++k) {
+        const int r = m < pp - k + 1 ? m : pp - k + 1;
+        if (r != rcur) {
+            rcur = r;
+            ib = (double)r * b;
+            fs0 = i0 <= L ? fit_start(Pp, Ap, i0, Pi0, Ai0, ib, cap) : 0;
+            fs1 = (two && i1 <= L) ? fit_start(Pp, Ap, i1, Pi1, Ai1, ib, cap) : 0;
+        }
+        if (two) mem_entry<S>(U, R, k, L, i1, Ui1, fs1);   // high half first: reads only lower positions
+        mem_entry<S>(U, R, k, L, i0, Ui0, fs0);
+        n += (unsigned)(L - k + 1);
+        wave_sync();
+    }
+    entries += n;
+    const double W = R[L];
+    wave_sync();
+    return W;
+}
+
+// Per-sample p2p bytes and largest stage parameters of the stages in sg
+// (as the pricing sums them).
+__device__ __forceinline__ void stage_sums(const Stages& sg, const float* x, const double* Pp, int lane, int pp,
+                                           double& sumX, double& pmax)
+{
+    double P0 = 0.0, P1 = 0.0, sx = 0.0;
+    if (lane < pp) {
+        P0 = Pp[sg.hi0] - Pp[sg.lo0];
+        if (lane < pp - 1) sx = (double)x[sg.hi0 - 1];
+    }
+    if (lane + 64 < pp) {
+        P1 = Pp[sg.hi1] - Pp[sg.lo1];
+        if (lane + 64 < pp - 1) sx += (double)x[sg.hi1 - 1];
+    }
+    double rs[1] = {sx}, rm[1] = {fmax(P0, P1)};
+    wave_reduce<OpSum, 1>(rs);
+    wave_reduce<OpMax, 1>(rm);
+    sumX = rs[0];
+    pmax = rm[0];
+}
+
 // Price every admissible microbatch count of plan (dp, tp, pp) with the
 // canonical stages of bottleneck W; appends to the wave's plan buffer.  Lane
 // mi < n_m holds m_values[mi] (ascending) in `mv`: the lanes price one count
 // each.  A stage's memory is non-increasing in m (min(m, pp-k) b is the batch
 // share Bg/dp while m <= pp-k and falls after), so the counts that fit are the
-// top of the admissible list; the first one is found by bisection.  Returns
-// the iteration time of the largest admissible count if it fits (+inf if
-// not): a plan of the cell, so an upper bound of the cell's best time.
-template <int SLOTS, int S>
+// top of the admissible list; the first one is found by bisection.  Under
+// the memory rule (MEM) each count below those, largest first, gets the
+// balanced partition among the splits that fit (R: the wave's row for its
+// recursion); counts stop once none fits (memory only grows as m falls) and,
+// with `prune`, are skipped when a lower bound of their time lies past the
+// tie window (tie_eps) of `best` or of a count priced here.  Returns the
+// least time of the plans priced that fit (+inf if none): a plan of the
+// cell, so an upper bound of the cell's best time.
+template <int SLOTS, int S, bool MEM>
 __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
-                               double W, int& np, bool keep_cuts)
+                               double W, int& np, bool keep_cuts, double* R, double best, double tie_eps,
+                               bool prune)
 {
     const Stages sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
@@ -610,21 +820,72 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
             Wv.planKey[slot] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)mv;
         }
     }
+    const int base = np;
     np += nadm;
     if (np > kMaxPlans) {
         tally(Wv, lane, kOverflow, 1);
         np = kMaxPlans;
     }
-    if (lo >= nadm) return kInf;
-    const double best_t = bcast(T, 63 - __clzll(amask));   // the largest admissible count fits
-    if (keep_cuts && best_t < Wv.cut_T) {
-        // the cell's best time so far: keep this degree's cut row for the output
-        if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sg.hi0;
-        if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sg.hi1;
-        if (lane == 0) {
-            Wv.cut_T = best_t;
-            Wv.cut_tp = tp;
-            Wv.cut_pp = pp;
+    double best_t = kInf;
+    if (lo < nadm) {
+        best_t = bcast(T, 63 - __clzll(amask));   // the largest admissible count fits
+        if (keep_cuts && best_t < Wv.cut_T) {
+            // the cell's best time so far: keep this degree's cut row for the output
+            if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sg.hi0;
+            if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sg.hi1;
+            if (lane == 0) {
+                Wv.cut_T = best_t;
+                Wv.cut_tp = tp;
+                Wv.cut_pp = pp;
+                Wv.cut_m = 0;
+                Wv.cut_mfit = Wv.mq[lo];
+            }
+        }
+    }
+    if constexpr (MEM) {
+        if (lo > 0) {
+            wave_sync();
+            // a count whose lower bound with any split (as target_bound, with
+            // the unconstrained bottleneck) lies past the window is not solved
+            double lim_c = prune ? fmin(best, best_t) * (1.0 + tie_eps) : kInf;
+            const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
+            const double c_ar = (dp > 1) ? cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp)
+                                         : 0.0;
+            const double fill_lb = sumS + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
+            for (int rk = lo - 1; rk >= 0; --rk) {
+                const double bm = Wv.bq[rk];
+                const int m = Wv.mq[rk];
+                if (lim_c < kInf &&
+                    (bm * fill_lb + (double)(m - 1) * (bm * W) + plb * c_ar) * (1.0 - 1e-9) > lim_c)
+                    continue;
+                Stages sm;
+                tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
+                if (!mem_cuts<S>(U, B.Pp, B.Ap, lane, jb.L, pp, m, bm, cap, kInf, sm)) break;
+                unsigned ent = 0;
+                const double Wm = mem_bottleneck<S>(U, B.Pp, B.Ap, R, lane, jb.L, pp, m, bm, cap, ent);
+                tally(Wv, lane, kDpEntries, ent);
+                tally(Wv, lane, kMemParts, 1);
+                tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
+                if (!(Wm < kInf) || !mem_cuts<S>(U, B.Pp, B.Ap, lane, jb.L, pp, m, bm, cap, Wm, sm)) continue;
+                double sX, pm;
+                stage_sums(sm, B.x, B.Pp, lane, pp, sX, pm);
+                const double Tm = bm * (sumS + cell.c_p2p * sX) + (double)(m - 1) * (bm * Wm) +
+                                  ((dp > 1) ? pm * c_ar : 0.0);
+                if (lane == 0 && base + rk < kMaxPlans) Wv.planT[base + rk] = Tm;
+                best_t = fmin(best_t, Tm);
+                if (prune) lim_c = fmin(lim_c, Tm * (1.0 + tie_eps));
+                if (keep_cuts && Tm < Wv.cut_T) {
+                    if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sm.hi0;
+                    if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sm.hi1;
+                    if (lane == 0) {
+                        Wv.cut_T = Tm;
+                        Wv.cut_tp = tp;
+                        Wv.cut_pp = pp;
+                        Wv.cut_m = m;
+                    }
+                }
+                wave_sync();
+            }
         }
     }
     return best_t;
@@ -710,14 +971,18 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
 
 // ------------------------------------------------------------ the kernel
 
-template <int SLOTS>
+// MEM: the memory-constrained partition rule (each wave has one more LDS
+// row for its recursion).
+template <int SLOTS, bool MEM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
 {
     __shared__ BlockLds<SLOTS> B;
+    __shared__ double memrows[MEM ? kWavesPerBlock * (kLmax + 1) : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
     WaveLds& Wv = B.w[wid];
+    double* const R = MEM ? memrows + wid * (kLmax + 1) : nullptr;
 
     const int item = A.item_order[blockIdx.x];
     const bool stage = A.n_counts <= kStageCells;
@@ -878,8 +1143,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / pp - 1]);
                         continue;
                     }
-                    best = fmin(best, price_target<SLOTS, 1>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
-                                                             B.Wtab[0][pp], np, A.cuts != nullptr));
+                    best = fmin(best, price_target<SLOTS, 1, MEM>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
+                                                                  B.Wtab[0][pp], np, A.cuts != nullptr, R, best,
+                                                                  A.tie_eps, A.prune != 0));
                 }
             }
         }
@@ -923,13 +1189,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
                         continue;
                     }
-                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, B.Wtab[slot][pp],
-                                                   np, A.cuts != nullptr));
+                    best = fmin(best, price_target<SLOTS, 2, MEM>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp,
+                                                                  B.Wtab[slot][pp], np, A.cuts != nullptr, R, best,
+                                                                  A.tie_eps, A.prune != 0));
                 }
             } else {
                 solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
-                    best = fmin(best, price_target<SLOTS, 2>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W, np,
-                                                             A.cuts != nullptr));
+                    best = fmin(best, price_target<SLOTS, 2, MEM>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W,
+                                                                  np, A.cuts != nullptr, R, best, A.tie_eps,
+                                                                  A.prune != 0));
                     const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
@@ -999,8 +1267,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 A.plan[cidx] = pw;
             }
         }
-        if (A.cuts && Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf) {
-            // the winner is the degree kept while pricing (cuts depend on tp and pp only)
+        const bool kept = Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf &&
+                          (!MEM || (Wv.cut_m == 0 ? m >= Wv.cut_mfit : Wv.cut_m == m));
+        if (A.cuts && kept) {
+            // the winner is the plan kept while pricing (balanced cuts depend on
+            // tp and pp only; memory-rule cuts also on m)
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
             for (int e = lane; e < A.cuts_stride; e += 64)
                 row[e] = (e < pp - 1) ? Wv.cutrow[e] : (uint8_t)0xFF;
@@ -1029,7 +1300,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 });
                 if (lane == 0) Wv.tally[kDpEntries] = e0;
             }
-            const Stages sg = canonical_stages<2>(U, Wv.J, lane, jb.L, pp, W);
+            Stages sg = canonical_stages<2>(U, Wv.J, lane, jb.L, pp, W);
+            if constexpr (MEM) {
+                // the balanced split if it fits with the winner's m, else the rule's
+                const double dm = (double)(dp * m);
+                const double bw = rint((double)jb.Bg / dm);
+                const double cap = ty.mem * (double)tp;
+                if (!stages_fit(sg, B.Pp, B.Ap, lane, pp, m, bw, cap)) {
+                    unsigned ent = 0;
+                    const double Wm = mem_bottleneck<2>(U, B.Pp, B.Ap, R, lane, jb.L, pp, m, bw, cap, ent);
+                    mem_cuts<2>(U, B.Pp, B.Ap, lane, jb.L, pp, m, bw, cap, Wm, sg);
+                }
+            }
             uint8_t* row = A.cuts + cidx * A.cuts_stride;
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
@@ -1060,6 +1342,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
         if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
         atomicAdd(&A.counters[kSkipped], t[kSkipped]);
+        atomicAdd(&A.counters[kMemParts], t[kMemParts]);
         atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
     }
 }
@@ -1093,10 +1376,18 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
 {
     const long long blocks = (long long)args.n_jobs * args.n_types;
     if (blocks <= 0) return hipSuccess;
-    if (args.share_tp)
-        hipLaunchKernelGGL(estimate_kernel<kSlotsShared>, dim3((unsigned)blocks), dim3(256), 0, stream, args);
-    else
-        hipLaunchKernelGGL(estimate_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, stream, args);
+    const dim3 grid((unsigned)blocks), block(256);
+    if (args.mem_rule) {
+        if (args.share_tp)
+            hipLaunchKernelGGL((estimate_kernel<kSlotsShared, true>), grid, block, 0, stream, args);
+        else
+            hipLaunchKernelGGL((estimate_kernel<1, true>), grid, block, 0, stream, args);
+    } else {
+        if (args.share_tp)
+            hipLaunchKernelGGL((estimate_kernel<kSlotsShared, false>), grid, block, 0, stream, args);
+        else
+            hipLaunchKernelGGL((estimate_kernel<1, false>), grid, block, 0, stream, args);
+    }
     return hipGetLastError();
 }
 

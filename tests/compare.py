@@ -22,12 +22,13 @@ def decode(w, ids):
     return j, g, ci
 
 
-def compare(w, gpu, ids, oracle, kappa_round=0, ref=None):
-    """gpu: dict with t_iter, thr, dp, tp, pp, m, feasible, cuts (u8 rows) for `ids`.
+def compare(w, gpu, ids, oracle, kappa_round=0, ref=None, rule=0):
+    """gpu: dict with t_iter, thr, dp, tp, pp, m, feasible, cuts (u8 rows) for `ids`,
+    estimated under partition rule `rule`.
     Returns a report dict; report['mismatch'] lists failing cells."""
     ids = np.asarray(ids, np.int64)
     if ref is None:
-        ref = oracle.cells(w, ids, kappa_round=kappa_round)
+        ref = oracle.cells(w, ids, kappa_round=kappa_round, rule=rule)
     J, G, CI = decode(w, ids)
     rep = dict(n=len(ids), exact=0, near_tie=0, mismatch=[], max_rel_T=0.0, max_rel_thr=0.0,
                infeasible=0)
@@ -79,7 +80,7 @@ def compare(w, gpu, ids, oracle, kappa_round=0, ref=None):
         if g_inf:
             # the oracle found a feasible plan; near-tie only if it sits on the memory limit
             e = oracle.eval_plan(w, j, g, n, kap, int(ref["dp"][s]), int(ref["tp"][s]),
-                                 int(ref["pp"][s]), int(ref["m"][s]))
+                                 int(ref["pp"][s]), int(ref["m"][s]), rule=rule)
             if abs(e["mem_max"] - float(w.mem[g])) <= REL_T * float(w.mem[g]):
                 rep["near_tie"] += 1
             else:

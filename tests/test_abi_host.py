@@ -179,6 +179,18 @@ def test_bound_pruning_switch(ctx):
     arena.arena_set_bound_pruning(ctx, True)
 
 
+def test_partition_rule_switch(ctx):
+    lib = arena.load()
+    assert lib.arena_set_partition_rule(None, 0) == arena.ARENA_ERR_INVALID_ARG
+    for bad in (-1, 2, 7):
+        _expect(arena.ARENA_ERR_INVALID_ARG, arena.arena_set_partition_rule, ctx, bad, match="partition rule")
+    arena.arena_set_partition_rule(ctx, arena.PARTITION_MEMORY)
+    arena.arena_set_partition_rule(ctx, arena.PARTITION_BALANCED)
+    src = open(HEADER).read()
+    assert re.search(r"#define ARENA_PARTITION_BALANCED 0\b", src)
+    assert re.search(r"#define ARENA_PARTITION_MEMORY 1\b", src)
+
+
 def test_unsorted_microbatch_counts_accepted(ctx):
     # the library sorts them for the kernel; the caller's order is free
     arena.arena_set_plan_space(ctx, [8, 1, 4, 2], 1e-6)
