@@ -12,6 +12,9 @@ matrix (Algorithm 1 with the throughput objective) on a 1280-GPU cluster
 state over the same 16384 x 8 x 131 shape, and prints that line.  With
 --proxy it times the proxy-plan planner (Sec. 3.3) over every cell of the
 trace-like workload and scores its plans against the exhaustive estimate.
+With --partition memory the estimate prices each plan with the balanced
+partition among the stage splits that fit memory instead of the balanced
+partition followed by the memory check.
 """
 from __future__ import annotations
 
@@ -47,9 +50,10 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, every: int, kappa_round: int = 0) -> dict:
+def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0) -> dict:
     """The oracle (single-threaded C, fp64) on a bounded sample of the same
-    workload: jobs j = 0, every, 2*every, ... times every grid of one round."""
+    workload: jobs j = 0, every, 2*every, ... times every grid of one round,
+    under partition rule `rule`."""
     import numpy as np
     from oracle import oracle as oracle_c
     oracle_c.load()
@@ -57,7 +61,7 @@ def cpu_baseline(w, every: int, kappa_round: int = 0) -> dict:
     jobs = list(range(0, w.n_jobs, every))
     ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)
     t0 = time.perf_counter()
-    oracle_c.cells(w, ids, kappa_round=kappa_round)
+    oracle_c.cells(w, ids, kappa_round=kappa_round, rule=rule)
     dt = time.perf_counter() - t0
     return {"value": len(ids) / dt, "unit": "cells/s", "cores": 1, "kind": "oracle",
             "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, round {kappa_round}: "
@@ -274,7 +278,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="full", choices=["tiny", "small", "trace", "moe", "full"])
     ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
-    ap.add_argument("--cpu-every", type=int, default=256, help="oracle sample: every k-th job")
+    ap.add_argument("--cpu-every", type=int, default=None,
+                    help="oracle sample: every k-th job (default 256; 2048 with --partition memory)")
+    ap.add_argument("--partition", default="balanced", choices=["balanced", "memory"],
+                    help="stage partition rule of the estimate")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", action="store_true",
                     help="time the scheduling step that consumes the throughput matrix instead")
@@ -323,7 +330,8 @@ def main() -> int:
         f"{work['problems']} partition problems")
 
     dev = torch.device("cuda", 0)
-    est = arena.Estimator(w, device=0, with_cuts=args.cuts)
+    rule = arena.PARTITION_MEMORY if args.partition == "memory" else arena.PARTITION_BALANCED
+    est = arena.Estimator(w, device=0, with_cuts=args.cuts, rule=rule)
     size = est.space_size()
     assert size["plans"] == work["plans"]
     stream = torch.cuda.current_stream(dev)
@@ -381,6 +389,7 @@ def main() -> int:
                         f"({w.n_cells} cells, {work['plans']} plans per round), per-grid contention "
                         "redrawn every round",
             "cuts": bool(args.cuts),
+            "partition": args.partition,
             "rounds_per_step": 1,
         },
         "plans_per_s": plans_per_s,
@@ -390,9 +399,9 @@ def main() -> int:
             "peak": PEAK_LANE_OPS / 1e12,
             "unit": "Top/s",
             "frac": achieved / PEAK_LANE_OPS,
-            "traffic": stored_traffic(args.workload),
+            "traffic": stored_traffic(args.workload) if rule == arena.PARTITION_BALANCED else None,
             "ops_per_launch": float(np.mean(ops_done)),
-            "ops_exhaustive": work["ops"],
+            "ops_exhaustive": work["ops"] if rule == arena.PARTITION_BALANCED else None,
             "launch_ms": avg_launch_s * 1e3,
         },
         "device_tallies": cnt,
@@ -400,7 +409,8 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_every)
+        every = args.cpu_every or (2048 if rule == arena.PARTITION_MEMORY else 256)
+        line["cpu_baseline"] = cpu_baseline(w, every, rule=rule)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -726,6 +726,68 @@ __device__ __forceinline__ void stage_sums(const Stages& sg, const float* x, con
     pmax = rm[0];
 }
 
+// The memory rule's counts of one degree: ranks lo-1 down to 0 of the
+// wave's admissible list (bq, mq), whose balanced split does not fit.  Each
+// is skipped when a lower bound of its time with any split (as target_bound,
+// with the unconstrained bottleneck W) lies past lim_c; otherwise its
+// fitting splits are tested (none: no smaller count fits either, stop), its
+// bottleneck solved and its lexicographically smallest cuts priced into plan
+// slot base + rank.  Out of line so that its registers do not add to those
+// live around the pricing.  Returns the least of best_t and the times priced.
+template <class T>
+using Lds = __attribute__((address_space(3))) T;
+
+template <int S>
+__device__ __noinline__ double mem_counts(const Lds<double>* Ul, const Lds<double>* Ppl, const Lds<double>* Apl,
+                                          const Lds<float>* xl, Lds<double>* Rl, Lds<WaveLds>* Wpl, int lane, int L,
+                                          int tp, int pp, int dp, int lo, int base, double W, double cap,
+                                          double sumS, double c_p2p, double c_ar, double plb, double x_min,
+                                          double best_t, double lim_c, double tie_eps, bool prune, bool keep_cuts)
+{
+    // the pointers arrive typed as LDS so that the accesses below stay LDS
+    // accesses in this out-of-line function
+    const double* U = (const double*)Ul;
+    const double* Pp = (const double*)Ppl;
+    const double* Ap = (const double*)Apl;
+    const float* x = (const float*)xl;
+    double* R = (double*)Rl;
+    WaveLds& Wv = *(WaveLds*)Wpl;
+    const double fill_lb = sumS + c_p2p * ((double)(pp - 1) * x_min);
+    for (int rk = lo - 1; rk >= 0; --rk) {
+        const double bm = Wv.bq[rk];
+        const int m = Wv.mq[rk];
+        if (lim_c < kInf && (bm * fill_lb + (double)(m - 1) * (bm * W) + plb * c_ar) * (1.0 - 1e-9) > lim_c)
+            continue;
+        Stages sm;
+        tally(Wv, lane, kAlgOps, 4ull * (unsigned)L);
+        if (!mem_cuts<S>(U, Pp, Ap, lane, L, pp, m, bm, cap, kInf, sm)) break;
+        unsigned ent = 0;
+        const double Wm = mem_bottleneck<S>(U, Pp, Ap, R, lane, L, pp, m, bm, cap, ent);
+        tally(Wv, lane, kDpEntries, ent);
+        tally(Wv, lane, kMemParts, 1);
+        tally(Wv, lane, kAlgOps, 4ull * (unsigned)L);
+        if (!(Wm < kInf) || !mem_cuts<S>(U, Pp, Ap, lane, L, pp, m, bm, cap, Wm, sm)) continue;
+        double sX, pm;
+        stage_sums(sm, x, Pp, lane, pp, sX, pm);
+        const double Tm = bm * (sumS + c_p2p * sX) + (double)(m - 1) * (bm * Wm) + ((dp > 1) ? pm * c_ar : 0.0);
+        if (lane == 0 && base + rk < kMaxPlans) Wv.planT[base + rk] = Tm;
+        best_t = fmin(best_t, Tm);
+        if (prune) lim_c = fmin(lim_c, Tm * (1.0 + tie_eps));
+        if (keep_cuts && Tm < Wv.cut_T) {
+            if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sm.hi0;
+            if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sm.hi1;
+            if (lane == 0) {
+                Wv.cut_T = Tm;
+                Wv.cut_tp = tp;
+                Wv.cut_pp = pp;
+                Wv.cut_m = m;
+            }
+        }
+        wave_sync();
+    }
+    return best_t;
+}
+
 // Price every admissible microbatch count of plan (dp, tp, pp) with the
 // canonical stages of bottleneck W; appends to the wave's plan buffer.  Lane
 // mi < n_m holds m_values[mi] (ascending) in `mv`: the lanes price one count
@@ -845,47 +907,14 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     if constexpr (MEM) {
         if (lo > 0) {
             wave_sync();
-            // a count whose lower bound with any split (as target_bound, with
-            // the unconstrained bottleneck) lies past the window is not solved
-            double lim_c = prune ? fmin(best, best_t) * (1.0 + tie_eps) : kInf;
-            const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
             const double c_ar = (dp > 1) ? cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp)
                                          : 0.0;
-            const double fill_lb = sumS + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
-            for (int rk = lo - 1; rk >= 0; --rk) {
-                const double bm = Wv.bq[rk];
-                const int m = Wv.mq[rk];
-                if (lim_c < kInf &&
-                    (bm * fill_lb + (double)(m - 1) * (bm * W) + plb * c_ar) * (1.0 - 1e-9) > lim_c)
-                    continue;
-                Stages sm;
-                tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
-                if (!mem_cuts<S>(U, B.Pp, B.Ap, lane, jb.L, pp, m, bm, cap, kInf, sm)) break;
-                unsigned ent = 0;
-                const double Wm = mem_bottleneck<S>(U, B.Pp, B.Ap, R, lane, jb.L, pp, m, bm, cap, ent);
-                tally(Wv, lane, kDpEntries, ent);
-                tally(Wv, lane, kMemParts, 1);
-                tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
-                if (!(Wm < kInf) || !mem_cuts<S>(U, B.Pp, B.Ap, lane, jb.L, pp, m, bm, cap, Wm, sm)) continue;
-                double sX, pm;
-                stage_sums(sm, B.x, B.Pp, lane, pp, sX, pm);
-                const double Tm = bm * (sumS + cell.c_p2p * sX) + (double)(m - 1) * (bm * Wm) +
-                                  ((dp > 1) ? pm * c_ar : 0.0);
-                if (lane == 0 && base + rk < kMaxPlans) Wv.planT[base + rk] = Tm;
-                best_t = fmin(best_t, Tm);
-                if (prune) lim_c = fmin(lim_c, Tm * (1.0 + tie_eps));
-                if (keep_cuts && Tm < Wv.cut_T) {
-                    if (lane < pp - 1) Wv.cutrow[lane] = (uint8_t)sm.hi0;
-                    if (lane + 64 < pp - 1) Wv.cutrow[lane + 64] = (uint8_t)sm.hi1;
-                    if (lane == 0) {
-                        Wv.cut_T = Tm;
-                        Wv.cut_tp = tp;
-                        Wv.cut_pp = pp;
-                        Wv.cut_m = m;
-                    }
-                }
-                wave_sync();
-            }
+            best_t = mem_counts<S>((const Lds<double>*)U, (const Lds<double>*)B.Pp, (const Lds<double>*)B.Ap,
+                                   (const Lds<float>*)B.x, (Lds<double>*)R, (Lds<WaveLds>*)&Wv, lane, jb.L, tp, pp,
+                                   dp, lo, base, W, cap, sumS,
+                                   cell.c_p2p, c_ar, fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max), B.x_layer_min,
+                                   best_t, prune ? fmin(best, best_t) * (1.0 + tie_eps) : kInf, tie_eps, prune,
+                                   keep_cuts);
         }
     }
     return best_t;
@@ -974,7 +1003,7 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
 // MEM: the memory-constrained partition rule (each wave has one more LDS
 // row for its recursion).
 template <int SLOTS, bool MEM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
+__device__ __forceinline__ void estimate_body(const EstimateArgs& A)
 {
     __shared__ BlockLds<SLOTS> B;
     __shared__ double memrows[MEM ? kWavesPerBlock * (kLmax + 1) : 1];
@@ -1347,6 +1376,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
 }
 
+template <int SLOTS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
+{
+    estimate_body<SLOTS, false>(A);
+}
+
+// The memory rule's out-of-line solve raises register use: its kernel aims at
+// three waves per SIMD (three blocks per CU, as its LDS allows) and spills the
+// rest, which measured faster than two waves without spills.
+template <int SLOTS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void estimate_mem_kernel(EstimateArgs A)
+{
+    estimate_body<SLOTS, true>(A);
+}
+
 __global__ void zero_kernel(unsigned long long* p, int n)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1379,14 +1423,14 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
     const dim3 grid((unsigned)blocks), block(256);
     if (args.mem_rule) {
         if (args.share_tp)
-            hipLaunchKernelGGL((estimate_kernel<kSlotsShared, true>), grid, block, 0, stream, args);
+            hipLaunchKernelGGL((estimate_mem_kernel<kSlotsShared>), grid, block, 0, stream, args);
         else
-            hipLaunchKernelGGL((estimate_kernel<1, true>), grid, block, 0, stream, args);
+            hipLaunchKernelGGL((estimate_mem_kernel<1>), grid, block, 0, stream, args);
     } else {
         if (args.share_tp)
-            hipLaunchKernelGGL((estimate_kernel<kSlotsShared, false>), grid, block, 0, stream, args);
+            hipLaunchKernelGGL((estimate_kernel<kSlotsShared>), grid, block, 0, stream, args);
         else
-            hipLaunchKernelGGL((estimate_kernel<1, false>), grid, block, 0, stream, args);
+            hipLaunchKernelGGL((estimate_kernel<1>), grid, block, 0, stream, args);
     }
     return hipGetLastError();
 }
