@@ -511,12 +511,14 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
             if (!any) continue;
             layer_costs(&jb, &ty, kappa, dp, tp, u);
             oracle_prefix(u, L, U);
+            /* the balanced partition does not depend on m: solved once per degree */
+            if (rule == 0) plan_cuts(&jb, &ty, 0, dp, tp, pp, 1, U, cuts);
             for (int mi = 0; mi < n_m; ++mi) {
                 int m = m_values[mi];
                 if (jb.Bg % (dp * m) != 0) continue;
                 if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
                 cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp; cand[nc].m = m;
-                if (plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) == 0) {
+                if (rule == 0 || plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) == 0) {
                     oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
                     cand[nc].T = r.T;
                     cand[nc].feasible = r.feasible;
