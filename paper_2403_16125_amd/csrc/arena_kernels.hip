@@ -47,7 +47,10 @@ struct WaveLds {
     int32_t cut_m;                //   memory rule: its m if the row fits only under the rule, else 0
     int32_t cut_mfit;             //   the smallest m the balanced row fits
     unsigned long long tally[kNumCounters];   // the wave's work tallies (lane 0 updates)
-    uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
+    union {
+        uint8_t J[kLevels * kLevelStride];   // successor tables of the canonical cuts
+        double R[kLmax + 1];                 // memory rule: its recursion row (never live with J)
+    };
 };
 
 constexpr int kStageCells = 136;   // counts whose outputs a block stages in LDS
@@ -1006,12 +1009,11 @@ template <int SLOTS, bool MEM>
 __device__ __forceinline__ void estimate_body(const EstimateArgs& A)
 {
     __shared__ BlockLds<SLOTS> B;
-    __shared__ double memrows[MEM ? kWavesPerBlock * (kLmax + 1) : 1];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
     WaveLds& Wv = B.w[wid];
-    double* const R = MEM ? memrows + wid * (kLmax + 1) : nullptr;
+    double* const R = MEM ? Wv.R : nullptr;
 
     const int item = A.item_order[blockIdx.x];
     const bool stage = A.n_counts <= kStageCells;
@@ -1382,11 +1384,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     estimate_body<SLOTS, false>(A);
 }
 
-// The memory rule's out-of-line solve raises register use: its kernel aims at
-// three waves per SIMD (three blocks per CU, as its LDS allows) and spills the
-// rest, which measured faster than two waves without spills.
+// The memory rule's out-of-line solve raises register use; its kernel still
+// aims at four waves per SIMD (its recursion row shares LDS with the cut
+// tables, so four blocks fit a CU) and spills the rest, which measured faster
+// than three or two waves with fewer spills.
 template <int SLOTS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void estimate_mem_kernel(EstimateArgs A)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_mem_kernel(EstimateArgs A)
 {
     estimate_body<SLOTS, true>(A);
 }
