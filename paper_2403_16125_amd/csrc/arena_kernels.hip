@@ -647,10 +647,10 @@ __device__ __forceinline__ int fit_start(const double* Pp, const double* Ap, int
 // U_i - U_j (i itself counts as passing): min(D_{k-1}(c), U_i - U_{c-1}),
 // each term only where its position lies in the window.
 template <int S>
-__device__ __forceinline__ void mem_entry(const double* U, double* R, int k, int L, int i, double Ui, int fs)
+__device__ __forceinline__ void mem_entry(const double* U, double* R, int k, int hk, int i, double Ui, int fs)
 {
     double v = kInf;
-    const bool act = i <= L;
+    const bool act = i <= hk;
     if (act) {
         const int a = fs > k - 1 ? fs : k - 1;
         if (i >= k && a < i) {
@@ -670,6 +670,8 @@ __device__ __forceinline__ void mem_entry(const double* U, double* R, int k, int
 // Bottleneck of pp stages over the splits whose every stage fits (stage k
 // holds min(m, pp - k) microbatches of b samples): D_pp(L), +inf if none.
 // R: the wave's row of kLmax + 1 doubles.  Lane l owns i = 1 + l and 65 + l.
+// Row k is needed only up to i = L - (pp - k) (each later stage takes a
+// layer), which is also as far as row k + 1 reads it.
 template <int S>
 __device__ double mem_bottleneck(const double* U, const double* Pp, const double* Ap, double* R, int lane,
                                  int L, int pp, int m, double b, double cap, unsigned& entries)
@@ -684,10 +686,11 @@ __device__ double mem_bottleneck(const double* U, const double* Pp, const double
     double ib = (double)rcur * b;
     int fs0 = i0 <= L ? fit_start(Pp, Ap, i0, Pi0, Ai0, ib, cap) : 0;
     int fs1 = (two && i1 <= L) ? fit_start(Pp, Ap, i1, Pi1, Ai1, ib, cap) : 0;
+    const int h1 = L - pp + 1;
     if (lane == 0) R[0] = kInf;
-    if (i0 <= L) R[i0] = fs0 == 0 ? Ui0 - U[0] : kInf;
-    if (two && i1 <= L) R[i1] = fs1 == 0 ? Ui1 - U[0] : kInf;
-    unsigned n = (unsigned)L;
+    if (i0 <= h1) R[i0] = fs0 == 0 ? Ui0 - U[0] : kInf;
+    if (two && i1 <= h1) R[i1] = fs1 == 0 ? Ui1 - U[0] : kInf;
+    unsigned n = (unsigned)h1;
     wave_sync();
     for (int k = 2; k <= pp; ++k) {
         const int r = m < pp - k + 1 ? m : pp - k + 1;
@@ -697,9 +700,10 @@ __device__ double mem_bottleneck(const double* U, const double* Pp, const double
             fs0 = i0 <= L ? fit_start(Pp, Ap, i0, Pi0, Ai0, ib, cap) : 0;
             fs1 = (two && i1 <= L) ? fit_start(Pp, Ap, i1, Pi1, Ai1, ib, cap) : 0;
         }
-        if (two) mem_entry<S>(U, R, k, L, i1, Ui1, fs1);   // high half first: reads only lower positions
-        mem_entry<S>(U, R, k, L, i0, Ui0, fs0);
-        n += (unsigned)(L - k + 1);
+        const int hk = L - pp + k;
+        if (hk >= 65) mem_entry<S>(U, R, k, hk, i1, Ui1, fs1);   // high half first: reads only lower positions
+        mem_entry<S>(U, R, k, hk, i0, Ui0, fs0);
+        n += (unsigned)(hk - k + 1);
         wave_sync();
     }
     entries += n;
