@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9   # CUs x SIMDs x lanes x clock: one unpacked VALU op per lane per clock
+PUBLISHED_FP32 = 157.3e12                # MI355X fp32 vector, as published
 COPY_BYTES = 1 << 30                    # calibration copy: 1 GiB read + 1 GiB written
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_estimate_full.json")
 
@@ -368,6 +369,7 @@ def main() -> int:
     res = est.results(np.arange(0, w.n_cells, 9973))
     est.close()
 
+    traffic = stored_traffic(args.workload) if rule == arena.PARTITION_BALANCED else None
     cells_per_s = w.n_cells * args.steps / wall
     plans_per_s = work["plans"] * args.steps / wall       # every plan of the space is decided
     achieved = float(np.sum(ops_done)) / (float(np.sum(launch_ms)) / 1e3)
@@ -399,10 +401,14 @@ def main() -> int:
             "peak": PEAK_LANE_OPS / 1e12,
             "unit": "Top/s",
             "frac": achieved / PEAK_LANE_OPS,
-            "traffic": stored_traffic(args.workload) if rule == arena.PARTITION_BALANCED else None,
+            "traffic": traffic,
             "ops_per_launch": float(np.mean(ops_done)),
             "ops_exhaustive": work["ops"] if rule == arena.PARTITION_BALANCED else None,
             "launch_ms": avg_launch_s * 1e3,
+            # for transparency: against the published fp32 vector rate (FMA and packed pairs
+            # counted twice each), and the measured HBM rate when the counters are current
+            "frac_of_published_fp32": achieved / PUBLISHED_FP32,
+            "hbm_GBps": (traffic / avg_launch_s / 1e9) if traffic else None,
         },
         "device_tallies": cnt,
         "feasible_fraction_sampled": float(np.mean(res["feasible"])),
