@@ -8,6 +8,15 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+# A copy of the oracle library to test the pins against (tests/test_oracle_mutants.py
+# builds copies with planted mistakes and runs the pins in a child process).
+_ORACLE_LIB = os.environ.get("ARENA_ORACLE_LIB")
+if _ORACLE_LIB:
+    from oracle import oracle as _oracle_mod
+    _oracle_mod._LIB = _ORACLE_LIB
+    _oracle_mod._lib = None
+
+
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (runs the HIP library)")
 

@@ -244,3 +244,31 @@ def test_microbatch_order_irrelevant():
     b, _, _ = _run(w2)
     for k in ("t_iter", "thr", "plan", "cuts"):
         assert np.array_equal(a[k], b[k]), k
+
+
+def test_hand_tie_and_link_cells():
+    """The hand-derived cells of the oracle's pins, through the HIP path: an exact
+    three-way tie decided by the key (pp, tp, m) with tie tolerance 1e-6 and 0,
+    the p2p of a stage boundary carrying the stage's last layer, and a data-
+    parallel group that fits a node without dividing it (inter-node link)."""
+    tie_job = dict(t=[1.0, 1.0], p=[0.0, 10.0], a=[0.0, 0.0], x=[0.0, 0.0625], a2a=[0.0, 0.0], batch=2)
+    ty2 = dict(speed=1.0, mem=1e12, bw_intra=1.0, bw_inter=1.0, gpus_per_node=2)
+    for eps in (1e-6, 0.0):
+        _say(f"hand tie cell, tie_eps {eps}")
+        w = wl.from_lists([tie_job], [ty2], [2], [1, 2], kappa=1.0, tie_eps=eps)
+        res, _, _ = _run(w)
+        assert (res["dp"][0], res["tp"][0], res["pp"][0], res["m"][0]) == (1, 2, 1, 1)
+        assert res["t_iter"][0] == 1.5
+    _say("hand p2p and dp-link cells")
+    p2p_job = dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.5, 0.25], a2a=[0.0, 0.0], batch=1)
+    w = wl.from_lists([p2p_job], [ty2], [2], [1], kappa=1.0)
+    res, _, _ = _run(w)
+    # (1, 1, 2, 1) costs 3 (p2p 1 after layer 0); (1, 2, 1, 1) costs 1 + 4 x (0.5 + 0.25) = 4
+    assert (res["dp"][0], res["tp"][0], res["pp"][0], res["m"][0]) == (1, 1, 2, 1)
+    assert res["t_iter"][0] == 3.0 and list(res["cuts"][0][:2]) == [1, 0xFF]
+    dp_job = dict(t=[3.0], p=[3e9], a=[0.0], x=[0.0], a2a=[0.0], batch=3)
+    ty4 = dict(speed=1.0, mem=1e12, bw_intra=1e10, bw_inter=1e9, gpus_per_node=4)
+    w = wl.from_lists([dp_job], [ty4], [3], [1], kappa=1.0)
+    res, _, _ = _run(w)
+    assert (res["dp"][0], res["tp"][0], res["pp"][0], res["m"][0]) == (3, 1, 1, 1)
+    assert res["t_iter"][0] == pytest.approx(5.0, rel=1e-6)

@@ -1,4 +1,4 @@
-"""The memory-constrained partition's pins catch plausible mistakes (CPU only).
+"""The oracle's pins catch plausible mistakes (CPU only).
 
 Each case plants one mistake in a copy of the oracle's C source (an in-flight
 count off by one, the tensor degree dropped from the activations, a strict
@@ -8,7 +8,8 @@ few, a sum where the recursion takes a maximum), builds it with gcc into a
 temporary library, and runs the pins of test_oracle_memory_partition.py
 against it in a child process: some pin must fail (an assertion, or a crash
 or time-out of the broken copy).  The unmodified copy, built the same way,
-must pass them all.
+must pass them all.  The same is done for the balanced partition, the layer
+costs, the plan price and the per-cell choice with their own pins.
 """
 import os
 import subprocess
@@ -89,11 +90,59 @@ def _run_pins(lib):
 
 
 def test_unmodified_copy_passes(tmp_path):
-    rc, out = _run_pins(_build(tmp_path, "control", None))
+    lib = _build(tmp_path, "control", None)
+    rc, out = _run_pins(lib)
+    assert rc == 0, out
+    rc, out = _run_pin_files(lib)
     assert rc == 0, out
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_planted_mistake_is_caught(tmp_path, name):
     rc, out = _run_pins(_build(tmp_path, name, MUTANTS[name]))
+    assert rc != 0, f"mistake {name} survived every pin: {out}"
+
+
+# Mistakes in the balanced partition, the layer costs, the plan price and the
+# per-cell choice, against the pins of test_oracle_partition.py and
+# test_oracle_pricing.py (run by pytest in a child process on the copy).
+CORE_MUTANTS = {
+    "tp_comm_without_kappa": ("v += kappa * 8.0 * (double)(tp - 1) / (double)tp * (double)jb->x[l] / ty->bw_intra;",
+                              "v += 8.0 * (double)(tp - 1) / (double)tp * (double)jb->x[l] / ty->bw_intra;"),
+    "all_to_all_only_with_tp": ("if (dp * tp > 1)", "if (tp > 1)"),
+    "p2p_of_the_next_layer": ("p2p = kappa * 2.0 * b * (double)jb->x[hi - 1] / B_pp;",
+                              "p2p = kappa * 2.0 * b * (double)jb->x[hi] / B_pp;"),
+    "allreduce_factor_halved": ("AR = kappa * 2.0 * (double)(dp - 1)", "AR = kappa * (double)(dp - 1)"),
+    "pricing_inflight_off_by_one": ("int inflight = m < pp - k ? m : pp - k;",
+                                    "int inflight = m < pp - k - 1 ? m : pp - k - 1;"),
+    "steady_state_m_microbatches": ("r.T = fill + (double)(m - 1) * w_max + ar_max;",
+                                    "r.T = fill + (double)m * w_max + ar_max;"),
+    "pipeline_link_strict": ("double B_pp = (n <= ty->gpn)", "double B_pp = (n < ty->gpn)"),
+    "dp_link_ignores_divisibility": ("(grp <= ty->gpn && ty->gpn % grp == 0)", "(grp <= ty->gpn)"),
+    "recursion_skips_first_split": ("for (int j = k - 1; j <= i - 1; ++j)", "for (int j = k; j <= i - 1; ++j)"),
+    "canonical_cut_tie_wrong_way": ("while (c < next - 1 && seg(U, c, next) > W) ++c;",
+                                    "while (c < next - 1 && seg(U, c, next) >= W) ++c;"),
+    "tie_window_strict": ("if (!cand[i].feasible || !(cand[i].T <= lim)) continue;",
+                          "if (!cand[i].feasible || !(cand[i].T < lim)) continue;"),
+    "key_tp_before_pp": ("if (a->pp != b->pp) return a->pp < b->pp;", "if (a->tp != b->tp) return a->tp < b->tp;"),
+    "admissibility_ignores_dp": ("if (jb.Bg % (dp * m) != 0) continue;", "if (jb.Bg % m != 0) continue;"),
+    "weights_counted_twice_not_four_times": ("double Mem = 4.0 * Pk / (double)tp", "double Mem = 2.0 * Pk / (double)tp"),
+}
+
+
+def _run_pin_files(lib):
+    env = dict(os.environ, ARENA_ORACLE_LIB=lib)
+    files = [os.path.join(ROOT, "tests", f) for f in ("test_oracle_partition.py", "test_oracle_pricing.py")]
+    try:
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                            "-p", "no:xdist"] + files, capture_output=True, text=True, timeout=300, env=env,
+                           cwd=ROOT)
+    except subprocess.TimeoutExpired:
+        return None, "timed out"
+    return r.returncode, (r.stdout + r.stderr)[-2000:]
+
+
+@pytest.mark.parametrize("name", sorted(CORE_MUTANTS))
+def test_planted_core_mistake_is_caught(tmp_path, name):
+    rc, out = _run_pin_files(_build(tmp_path, name, CORE_MUTANTS[name]))
     assert rc != 0, f"mistake {name} survived every pin: {out}"

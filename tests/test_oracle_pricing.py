@@ -244,3 +244,52 @@ def test_enumeration_and_choice(oracle, name):
         cand = sorted((p for p in priced if p[0] <= tmin * (1 + w.tie_eps)), key=lambda p: p[1])
         assert (r["dp"][s], r["tp"][s], r["pp"][s], r["m"][s]) == cand[0][2]
         assert r["T"][s] == cand[0][0]
+
+
+# ---------------------------------------------------------------- hand-derived tie-breaks and links
+
+def _cell(job, ty, n, m_values, tie_eps=1e-6):
+    return wl.from_lists([job], [ty], [n], m_values, kappa=1.0, tie_eps=tie_eps)
+
+
+@pytest.mark.parametrize("tie_eps", [1e-6, 0.0])
+def test_tie_prefers_fewer_stages_then_less_tp(oracle, tie_eps):
+    """Two layers of time 1 (whole batch of 2), boundary activations x = [0, 1/16],
+    weights 0 and 10 bytes, 2 GPUs on one node of 2, links of 1 byte/s, m in {1, 2}.
+      (dp, tp, pp) = (1, 2, 1): u_l = 1/(2*2) + 8 (1/2) x_l = 0.25, 0.5; T = Bg sum u
+        = 2 x 0.75 = 1.5 for m = 1 and m = 2 (b = 2/m, m b = 2);
+      (1, 1, 2): u = 0.5, 0.5, cuts [1], p2p carries x_0 = 0: m = 2 gives
+        (0.5 + 0.5) + (2 - 1) x 0.5 = 1.5, m = 1 gives 2;
+      (2, 1, 1): T = 1 + all-reduce 2 (1/2) 10 / 1 = 11 (m = 1 only).
+    Three plans tie at exactly 1.5; the key (pp, tp, m) picks (1, 2, 1) over
+    (pp 2, tp 1).  With a zero tie tolerance the best plan itself still counts."""
+    job = dict(t=[1.0, 1.0], p=[0.0, 10.0], a=[0.0, 0.0], x=[0.0, 0.0625], a2a=[0.0, 0.0], batch=2)
+    ty = dict(speed=1.0, mem=1e12, bw_intra=1.0, bw_inter=1.0, gpus_per_node=2)
+    r = oracle.cells(_cell(job, ty, 2, [1, 2], tie_eps), [0])
+    assert (r["dp"][0], r["tp"][0], r["pp"][0], r["m"][0]) == (1, 2, 1, 1)
+    assert r["T"][0] == 1.5
+    w = _cell(job, ty, 2, [1, 2], tie_eps)
+    assert oracle.eval_plan(w, 0, 0, 2, 1.0, 1, 1, 2, 2)["T"] == 1.5
+    assert oracle.eval_plan(w, 0, 0, 2, 1.0, 2, 1, 1, 1)["T"] == 11.0
+
+
+def test_p2p_carries_the_last_layer_of_the_stage(oracle):
+    """Two layers of time 1 (batch 1), x = [0.5, 0.25], 2 GPUs on one node of 2,
+    links of 1 byte/s; plan (1, 1, 2, 1): b = 1, stages [0,1) [1,2) of time 1 each,
+    the boundary after layer 0 carries 2 x 1 x x_0 = 1 (activation out, gradient
+    back): T = (1 + 1) + 1 = 3."""
+    job = dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.5, 0.25], a2a=[0.0, 0.0], batch=1)
+    ty = dict(speed=1.0, mem=1e12, bw_intra=1.0, bw_inter=1.0, gpus_per_node=2)
+    e = oracle.eval_plan(_cell(job, ty, 2, [1]), 0, 0, 2, 1.0, 1, 1, 2, 1)
+    assert e["cuts"] == [1] and e["T"] == 3.0
+
+
+def test_dp_group_not_dividing_the_node_uses_the_inter_node_link(oracle):
+    """One layer of time 3 (batch 3), 3e9 bytes of weights, nodes of 4 GPUs,
+    intra 1e10 and inter 1e9 bytes/s; plan (3, 1, 1, 1): b = 1, compute 3/3 = 1;
+    the dp group of 3 fits a node but does not divide it, so its gradient
+    all-reduce 2 (2/3) 3e9 crosses the inter-node link: 4 s; T = 5."""
+    job = dict(t=[3.0], p=[3e9], a=[0.0], x=[0.0], a2a=[0.0], batch=3)
+    ty = dict(speed=1.0, mem=1e12, bw_intra=1e10, bw_inter=1e9, gpus_per_node=4)
+    e = oracle.eval_plan(_cell(job, ty, 3, [1]), 0, 0, 3, 1.0, 3, 1, 1, 1)
+    assert e["T"] == pytest.approx(5.0, rel=1e-15)
