@@ -15,6 +15,11 @@ if _ORACLE_LIB:
     from oracle import oracle as _oracle_mod
     _oracle_mod._LIB = _ORACLE_LIB
     _oracle_mod._lib = None
+_PROXY_ORACLE_LIB = os.environ.get("ARENA_PROXY_ORACLE_LIB")
+if _PROXY_ORACLE_LIB:
+    from oracle import proxy as _proxy_mod
+    _proxy_mod._LIB = _PROXY_ORACLE_LIB
+    _proxy_mod._lib = None
 
 
 def pytest_configure(config):

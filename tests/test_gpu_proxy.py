@@ -123,3 +123,27 @@ def test_full_round_jobs_every_grid():
     w = wl.make("full").subset_jobs(range(0, 16384, 683))
     ids = np.arange(0, w.n_cells, 97)
     _compare(w, ids, kappa_round=3)
+
+
+def _hand(layers, batch, counts, m_values, gpn, bw):
+    ty = dict(speed=1.0, mem=1e15, bw_intra=bw, bw_inter=bw, gpus_per_node=gpn)
+    w = wl.from_lists([dict(batch=batch, **layers)], [ty], counts, m_values, kappa=1.0)
+    w.hbm = np.asarray([1e30], np.float32)
+    return w
+
+
+def test_hand_tie_workloads():
+    """The hand-derived tie cases of the oracle's pins (a bias tie decided by the
+    pipeline term of the communication load, a full tie kept by the first
+    grouping, equal intra-stage costs keeping the smaller tp, p2p between
+    unequal stages) as whole cells over several GPU counts."""
+    three = lambda a2a: dict(t=[1.0, 2.0, 1.0], p=[0.0] * 3, a=[0.0] * 3, x=[1e9] * 3, a2a=a2a)
+    cases = [
+        _hand(three([0.0, 1e9, 2e9]), 8, [2, 3, 4], [1, 2], 2, 1e9),
+        _hand(three([0.0, 0.0, 0.0]), 8, [2, 3, 4], [1, 2], 2, 1e9),
+        _hand(dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.0, 0.0], a2a=[0.0, 0.0]), 2, [1, 2], [1], 2, 1e9),
+        _hand(dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.25, 0.0], a2a=[0.0, 0.0]), 4, [2, 3, 4], [1, 2],
+              4, 1.0),
+    ]
+    for w in cases:
+        _compare(w, np.arange(w.n_cells))

@@ -9,7 +9,8 @@ temporary library, and runs the pins of test_oracle_memory_partition.py
 against it in a child process: some pin must fail (an assertion, or a crash
 or time-out of the broken copy).  The unmodified copy, built the same way,
 must pass them all.  The same is done for the balanced partition, the layer
-costs, the plan price and the per-cell choice with their own pins.
+costs, the plan price and the per-cell choice, and for the proxy-plan
+planner's oracle, each with its own pins.
 """
 import os
 import subprocess
@@ -66,8 +67,8 @@ sys.exit(1 if failed else 0)
 """
 
 
-def _build(tmp_path, name, patch):
-    src = open(SRC).read()
+def _build(tmp_path, name, patch, source=SRC):
+    src = open(source).read()
     if patch is not None:
         old, new = patch
         assert src.count(old) == 1, (name, old)
@@ -145,4 +146,50 @@ def _run_pin_files(lib):
 @pytest.mark.parametrize("name", sorted(CORE_MUTANTS))
 def test_planted_core_mistake_is_caught(tmp_path, name):
     rc, out = _run_pin_files(_build(tmp_path, name, CORE_MUTANTS[name]))
+    assert rc != 0, f"mistake {name} survived every pin: {out}"
+
+
+# Mistakes in the proxy-plan planner's oracle, against test_oracle_proxy.py.
+PROXY_SRC = os.path.join(ROOT, "oracle", "proxy_oracle.c")
+PROXY_MUTANTS = {
+    "roofline_min_not_max": ("o->load[i] = compute > memory ? compute : memory;",
+                             "o->load[i] = compute < memory ? compute : memory;"),
+    "traffic_without_batch": ("M += (double)jb->p[l] + (double)jb->Bg * (double)jb->a[l];",
+                              "M += (double)jb->p[l] + (double)jb->a[l];"),
+    "operator_bounds_rounded_up": ("o->lo[i] = (int)(((long long)i * jb->L) / O);",
+                                   "o->lo[i] = (int)(((long long)i * jb->L + O - 1) / O);"),
+    "bias_tie_smaller_multiset": ("(cost == st->best_cost && lex_greater(st->cur, st->best, st->s))",
+                                  "(cost == st->best_cost && lex_greater(st->best, st->cur, st->s))"),
+    "pairing_in_stage_order": ("double diff = (double)(1 << st->cur[st->pos[j]]) - st->D[j];",
+                               "double diff = (double)(1 << st->cur[j]) - st->D[j];"),
+    "lcomm_without_pipeline_term": ("*lcomm = (double)(pl->B - 1) * cmax + csum + arsum;",
+                                    "*lcomm = csum + arsum;"),
+    "intra_stage_tie_larger_tp": ("if (best == 0 || cost < best_cost)", "if (best == 0 || cost <= best_cost)"),
+    "p2p_with_larger_dp": ("int dmin = dp < dpn ? dp : dpn;", "int dmin = dp > dpn ? dp : dpn;"),
+    "proxy_tie_later_grouping": ("(b2 == bq->b2 && lcomm < bq->lcomm)", "(b2 == bq->b2 && lcomm <= bq->lcomm)"),
+    "stage_allreduce_not_split_by_tp": (
+        "*AR = kappa * 2.0 * (double)(dp - 1) / (double)dp * (P / (double)tp) / B_dp;",
+        "*AR = kappa * 2.0 * (double)(dp - 1) / (double)dp * P / B_dp;"),
+}
+
+
+def _run_proxy_pins(lib):
+    env = dict(os.environ, ARENA_PROXY_ORACLE_LIB=lib)
+    try:
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                            "-p", "no:xdist", os.path.join(ROOT, "tests", "test_oracle_proxy.py")],
+                           capture_output=True, text=True, timeout=300, env=env, cwd=ROOT)
+    except subprocess.TimeoutExpired:
+        return None, "timed out"
+    return r.returncode, (r.stdout + r.stderr)[-2000:]
+
+
+def test_unmodified_proxy_copy_passes(tmp_path):
+    rc, out = _run_proxy_pins(_build(tmp_path, "proxy_control", None, PROXY_SRC))
+    assert rc == 0, out
+
+
+@pytest.mark.parametrize("name", sorted(PROXY_MUTANTS))
+def test_planted_proxy_mistake_is_caught(tmp_path, name):
+    rc, out = _run_proxy_pins(_build(tmp_path, "proxy_" + name, PROXY_MUTANTS[name], PROXY_SRC))
     assert rc != 0, f"mistake {name} survived every pin: {out}"

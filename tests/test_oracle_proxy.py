@@ -249,3 +249,60 @@ def test_uniform_proxies_price_as_the_uniform_oracle():
         assert r["T"][q] == pytest.approx(ref["T"], rel=1e-12)
         checked += 1
     assert checked > 10
+
+
+# ---------------------------------------------------------------- hand-derived tie-breaks
+
+def test_bias_tie_takes_the_larger_multiset():
+    # shares (3, 1.5, 1.5) on 6 GPUs: {4, 1, 1} and {2, 2, 2} both have squared
+    # bias 1 + 0.25 + 0.25 = 1.5; the lexicographically larger sorted multiset wins
+    b2, m = px.normalize([3.0, 1.5, 1.5], 6)
+    assert b2 == 1.5 and list(m) == [4, 1, 1]
+
+
+def _three_ops(a2a):
+    # three layers (= operators) of compute time 1, 2, 1: shares 1, 2, 1 of 4
+    # GPUs; no memory traffic, no weights; huge TP volume so tp 1 is chosen
+    return _workload(dict(t=[1.0, 2.0, 1.0], p=[0.0] * 3, a=[0.0] * 3, x=[1e9] * 3, a2a=a2a), 8, [4], [2],
+                     bwi=1e9, bwe=1e9, gpn=2, mem=1e15, hbm=1e30)
+
+
+def test_communication_load_breaks_a_bias_tie_with_its_pipeline_term():
+    """Groupings {0}{1,2} and {0,1}{2} both get 2 + 2 GPUs (shares (1, 3) and
+    (3, 1): squared bias 2 each).  With B = 2 each stage is dp 2 x tp 1 with
+    b = 8 / (2 x 2) = 2 samples per microbatch and all-to-all volumes
+    (0, 1e9, 2e9) at 1e9 B/s: C = 2 x (sum a2a) / 1e9.
+      {0}{1,2}:  C = (0, 6): l_comm = (2-1) x 6 + 6 = 12
+      {0,1}{2}:  C = (2, 4): l_comm = (2-1) x 4 + 6 = 10
+    The sums tie; the (B-1) max C term picks the second grouping."""
+    g = px.grid(_three_ops([0.0, 1e9, 2e9]), 0, 0, 4, 1.0, 2, 2, F_REF)
+    assert g["ok"] and g["b2"] == 2.0
+    assert list(g["bounds"]) == [0, 2, 3] and list(g["Dn"]) == [2, 2] and list(g["tp"]) == [1, 1]
+    assert g["lcomm"] == pytest.approx(10.0, rel=1e-12)
+
+
+def test_full_tie_keeps_the_first_grouping():
+    # no communication at all: both groupings have bias 2 and l_comm 0; the
+    # lexicographically smallest cut vector ({0}{1,2}) is the proxy
+    g = px.grid(_three_ops([0.0, 0.0, 0.0]), 0, 0, 4, 1.0, 2, 2, F_REF)
+    assert g["ok"] and list(g["bounds"]) == [0, 1, 3] and g["lcomm"] == 0.0
+
+
+def test_equal_intra_stage_costs_take_the_smaller_tp():
+    # one stage of 2 GPUs (node of 2) with no communication of any kind: tp 1
+    # and tp 2 cost 0 each; the smaller tensor degree is kept
+    w = _workload(dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.0, 0.0], a2a=[0.0, 0.0]), 2, [2], [1],
+                  bwi=1e9, bwe=1e9, gpn=2, mem=1e15, hbm=1e30)
+    g = px.grid(w, 0, 0, 2, 1.0, 1, 1, F_REF)
+    assert g["ok"] and list(g["Dn"]) == [2] and list(g["tp"]) == [1]
+
+
+def test_p2p_between_unequal_stages_carries_the_smaller_replica_count():
+    """Two layers of time 1, batch 4, B = 2; stage 0 on 2 GPUs (dp 2, b = 1),
+    stage 1 on 1 GPU (b = 2); x = (0.25, 0) at 1 B/s inside a node of 4.
+    W0 = 1 x 1/4, W1 = 2 x 1/4; the boundary carries the samples of the smaller
+    dp: 2 x (4 / (1 x 2)) x 0.25 = 1.  T = (0.25 + 1) + 0.5 + (2-1) x 0.5 = 2.25."""
+    w = _workload(dict(t=[1.0, 1.0], p=[0.0, 0.0], a=[0.0, 0.0], x=[0.25, 0.0], a2a=[0.0, 0.0]), 4, [3], [2],
+                  bwi=1.0, bwe=1.0, gpn=4, mem=1e15, hbm=1e30)
+    T, feas, _ = px.price(w, 0, 0, 3, 1.0, [0, 1, 2], [2, 1], [1, 1], 2, F_REF)
+    assert feas and T == 2.25
