@@ -22,6 +22,17 @@ if _PROXY_ORACLE_LIB:
     _proxy_mod._lib = None
 
 
+_SCHED_ORACLE_SRC = os.environ.get("ARENA_SCHED_ORACLE_SRC")
+if _SCHED_ORACLE_SRC:
+    import importlib.util
+    import oracle as _oracle_pkg
+    _spec = importlib.util.spec_from_file_location("oracle.scheduler_oracle", _SCHED_ORACLE_SRC)
+    _sched_mod = importlib.util.module_from_spec(_spec)
+    _spec.loader.exec_module(_sched_mod)
+    sys.modules["oracle.scheduler_oracle"] = _sched_mod
+    _oracle_pkg.scheduler_oracle = _sched_mod
+
+
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (runs the HIP library)")
 

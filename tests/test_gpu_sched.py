@@ -69,6 +69,9 @@ HAND = {
     "scale_up": ({0: [[5, 9, 16, 20]], 1: [[4, 10, 19, 30]]}, [1, 2, 4, 8], [8], [0, 0], [1, 1],
                  [], [], 8),
     "scale_up_best_step": ({0: [[10, 11, 40]]}, [1, 2, 4], [4], [0], [0], [], [], 4),
+    "scale_down_per_gpu": ({0: [[0, 50, 80]], 1: [[5, 20, 30]], 2: [[2, 10, 0]]}, [1, 2, 4], [6],
+                           [-1, 0, 0], [0, 2, 1], [0], [0], 4),
+    "allowance": ({0: [[0, 0, 50]], 1: [[10, 0, 0]]}, [1, 2, 4], [2], [-1, -1], [0, 0], [0, 1], [1, 1], 4),
 }
 
 
@@ -263,6 +266,7 @@ DDL_HAND = {
     "scale_down_protected": (({0: [[0, 50, 80]], 1: [[10, 19, 0]], 2: [[3, 20, 0]]}, [1, 2, 4], [4],
                               [-1, 0, 0], [0, 1, 1], [0], [0], 4), ([1, 1, 1], [1.0, 100.0, 1.0], [1e9, 6.0, 1e9])),
     "scale_up_steered": (({0: [[1, 2, 4]]}, [1, 2, 4], [4], [0], [0], [], [], 1), ([1], [10.0], [3.0])),
+    "met_exactly": (({0: [[10, 20]]}, [1, 2], [2], [-1], [0], [0], [0], 4), ([4], [10.0], [2.0])),
 }
 
 

@@ -9,8 +9,8 @@ temporary library, and runs the pins of test_oracle_memory_partition.py
 against it in a child process: some pin must fail (an assertion, or a crash
 or time-out of the broken copy).  The unmodified copy, built the same way,
 must pass them all.  The same is done for the balanced partition, the layer
-costs, the plan price and the per-cell choice, and for the proxy-plan
-planner's oracle, each with its own pins.
+costs, the plan price and the per-cell choice, for the proxy-plan planner's
+oracle and for the scheduler's, each with its own pins.
 """
 import os
 import subprocess
@@ -192,4 +192,56 @@ def test_unmodified_proxy_copy_passes(tmp_path):
 @pytest.mark.parametrize("name", sorted(PROXY_MUTANTS))
 def test_planted_proxy_mistake_is_caught(tmp_path, name):
     rc, out = _run_proxy_pins(_build(tmp_path, "proxy_" + name, PROXY_MUTANTS[name], PROXY_SRC))
+    assert rc != 0, f"mistake {name} survived every pin: {out}"
+
+
+# Mistakes in the scheduler's oracle (Python), against test_oracle_scheduler.py.
+SCHED_SRC = os.path.join(ROOT, "oracle", "scheduler_oracle.py")
+SCHED_MUTANTS = {
+    "launch_tie_larger_count": ("key = (-v, int(counts[c]), g)", "key = (-v, -int(counts[c]), g)"),
+    "launch_needs_spare_gpu": ("if _open(v, work, ddl) and int(counts[c]) <= free[g]:",
+                               "if _open(v, work, ddl) and int(counts[c]) < free[g]:"),
+    "scale_down_cost_not_per_gpu": ("/ float(int(counts[c]) - int(counts[c2]))", "/ 1.0"),
+    "scale_down_any_type": ("if g < 0 or g not in usable_types:", "if g < 0:"),
+    "scale_up_gain_not_per_gpu": ("gain = (t2 - t) / float(dn)", "gain = (t2 - t)"),
+    "priority_rule_strict": ("if int(priority[q]) <= lam:", "if int(priority[q]) < lam:"),
+    "depth_off_by_one": ("if len(log) >= depth:", "if len(log) > depth:"),
+    "undo_frees_instead": ("free[g] -= int(counts[c_old]) - int(counts[alloc_count[i]])",
+                           "free[g] += int(counts[c_old]) - int(counts[alloc_count[i]])"),
+    "deadline_strict": ("work / v <= ddl", "work / v < ddl"),
+    "scale_up_to_equal_throughput": ("if t2 > t and _open(t2, work, ddl):", "if t2 >= t and _open(t2, work, ddl):"),
+    "no_priority_allowance": ("lam = max((int(p) for p in priority), default=0) + 1", "lam = 0"),
+}
+
+
+def _run_sched_pins(src):
+    env = dict(os.environ, ARENA_SCHED_ORACLE_SRC=src)
+    try:
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                            "-p", "no:xdist", os.path.join(ROOT, "tests", "test_oracle_scheduler.py")],
+                           capture_output=True, text=True, timeout=300, env=env, cwd=ROOT)
+    except subprocess.TimeoutExpired:
+        return None, "timed out"
+    return r.returncode, (r.stdout + r.stderr)[-2000:]
+
+
+def _sched_copy(tmp_path, name, patch):
+    src = open(SCHED_SRC).read()
+    if patch is not None:
+        old, new = patch
+        assert src.count(old) == 1, (name, old)
+        src = src.replace(old, new)
+    path = tmp_path / f"sched_{name}.py"
+    path.write_text(src)
+    return str(path)
+
+
+def test_unmodified_scheduler_copy_passes(tmp_path):
+    rc, out = _run_sched_pins(_sched_copy(tmp_path, "control", None))
+    assert rc == 0, out
+
+
+@pytest.mark.parametrize("name", sorted(SCHED_MUTANTS))
+def test_planted_scheduler_mistake_is_caught(tmp_path, name):
+    rc, out = _run_sched_pins(_sched_copy(tmp_path, name, SCHED_MUTANTS[name]))
     assert rc != 0, f"mistake {name} survived every pin: {out}"

@@ -70,9 +70,41 @@ def test_scale_down_only_on_types_the_queued_job_can_use():
     # job 1 (type 0, useless to job 0) is never touched
     assert r["launched"] == [0]
     assert r["alloc_count"] == [0, 1, 1]
-    # with 3 GPUs of type 1 the one freed GPU is enough
+    # with 3 GPUs of type 1 the one freed GPU is enough: one scale-down (job 2),
+    # one launch, no scale-up, and job 1 never moved (stepping it down and back
+    # up again would end in the same allocation, so the moves are checked too)
     r = so.schedule(thr, [1, 2], [2, 3], [-1, 0, 1], [0, 1, 1], [0], [0], 4)
     assert r["launched"] == [1] and r["alloc_count"][2] == 0 and r["alloc_count"][1] == 1
+    assert r["moves"] == [1, 1, 0] and r["decisions"] == 4
+
+
+def test_scale_down_cost_is_per_freed_gpu():
+    # one type of 6 GPUs, counts 1, 2, 4; job 1 runs on 4 (4 -> 2 loses 30 - 20
+    # = 10 for 2 GPUs: 5 per GPU), job 2 on 2 (2 -> 1 loses 10 - 2 = 8 for 1 GPU:
+    # 8 per GPU); queued job 0 needs 2.  Per freed GPU, job 1 is cheaper: one
+    # scale-down, job 0 launches on 2, nothing left to scale up
+    thr = _thr({0: [[0, 50, 80]], 1: [[5, 20, 30]], 2: [[2, 10, 0]]})
+    r = so.schedule(thr, [1, 2, 4], [6], [-1, 0, 0], [0, 2, 1], [0], [0], 4)
+    assert r["launched"] == [1]
+    assert r["alloc_count"] == [1, 1, 1] and r["moves"] == [1, 1, 0] and r["decisions"] == 4
+
+
+def test_first_failed_launch_sets_the_allowance():
+    # queue: job 0 (class 1) needs 4 GPUs of the 2 there are and fails, which
+    # allows class <= 1 from then on; job 1 (class 1) fits on one GPU
+    thr = _thr({0: [[0, 0, 50]], 1: [[10, 0, 0]]})
+    r = so.schedule(thr, [1, 2, 4], [2], [-1, -1], [0, 0], [0, 1], [1, 1], 4)
+    assert r["launched"] == [0, 1] and r["alloc_type"] == [-1, 0] and r["alloc_count"] == [0, 0]
+
+
+def test_deadline_met_exactly_is_open():
+    # batch 4 x 10 iterations = 40 samples; at 20 samples/s (2 GPUs) the job
+    # finishes in exactly its 2 s deadline: open; at 10 samples/s (1 GPU) not
+    thr = _thr({0: [[10, 20]]})
+    r = so.schedule(thr, [1, 2], [2], [-1], [0], [0], [0], 4, batch=[4], iters=[10.0], deadline=[2.0])
+    assert r["launched"] == [1] and r["alloc_count"] == [1]
+    r = so.schedule(thr, [1, 2], [2], [-1], [0], [0], [0], 4, batch=[4], iters=[10.0], deadline=[1.999])
+    assert r["launched"] == [0]
 
 
 def test_priority_rule_stops_after_a_failed_class():
