@@ -26,7 +26,10 @@
  *     (Eq. 4's once-per-iteration term), latency proportional to volume
  *     (Sec. 3.4), memory limits (Sec. 3.3);
  *   - the best plan of the cell, its iteration time T and throughput
- *     Bg / T: one entry of the throughput matrix of Eq. 5.
+ *     Bg / T: one entry of the throughput matrix of Eq. 5;
+ *   - optionally (the *_tab entries) communication latency interpolated in
+ *     per-link tables of profiled (volume, latency) samples (Sec. 3.4)
+ *     instead of volume / bandwidth.
  *
  * Readings where the paper leaves the model open (units, memory model,
  * link choice, tie-breaks) are listed in the repository's design notes;
@@ -601,4 +604,256 @@ void oracle_layer_costs(int j, int g, double kappa, int dp, int tp,
     ojob jb; otype ty;
     if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return;
     layer_costs(&jb, &ty, kappa, dp, tp, u);
+}
+
+/* ------------------------------------------------------------------ */
+/* Interpolated communication latency                                  */
+/* ------------------------------------------------------------------ */
+
+/* A communication primitive's latency is profiled at sampled volumes on the
+ * target interconnect and interpolated by volume online (Sec. 3.4).  One
+ * table per GPU type and link (0 inside a node, 1 across nodes): K points
+ * vol[0] = 0 < vol[1] < ... < vol[K-1] bytes with latencies lat[k] seconds
+ * (non-decreasing).  Nothing moved costs nothing; otherwise the latency is
+ * linear between the samples around v and extended by the first or last
+ * segment outside them. */
+typedef struct {
+    int K;
+    const double* vol;
+    const double* lat;
+} otab;
+
+static double tab_lat(const otab* tb, double v)
+{
+    if (!(v > 0.0)) return 0.0;
+    int k = 1;
+    while (k < tb->K - 1 && v > tb->vol[k]) ++k;
+    return tb->lat[k - 1] + (v - tb->vol[k - 1]) * (tb->lat[k] - tb->lat[k - 1]) / (tb->vol[k] - tb->vol[k - 1]);
+}
+
+double oracle_tab_latency(int K, const double* vol, const double* lat, double v)
+{
+    otab tb;
+    tb.K = K; tb.vol = vol; tb.lat = lat;
+    return tab_lat(&tb, v);
+}
+
+/* Per-microbatch cost of each layer on one GPU of plan (dp, tp, m) with b
+ * samples per microbatch: compute as in layer_costs times b; four tensor-
+ * parallel ring all-reduces each moving 2 (tp-1)/tp b x_l bytes on the
+ * intra-node link; the MoE all-to-all of b a2a_l bytes on the inter-node
+ * link; communication scaled by kappa.  With a table linear through the
+ * origin this is b times the per-sample cost of layer_costs. */
+static void layer_costs_tab(const ojob* jb, const otype* ty, const otab* tabs, double kappa, int dp, int tp,
+                            double b, double* c)
+{
+    for (int l = 0; l < jb->L; ++l) {
+        double v = b * ((double)jb->t[l] / ((double)jb->Bg * ty->speed * (double)tp));
+        if (tp > 1)
+            v += kappa * (4.0 * tab_lat(&tabs[0], 2.0 * (double)(tp - 1) / (double)tp * b * (double)jb->x[l]));
+        if (dp * tp > 1)
+            v += kappa * tab_lat(&tabs[1], b * (double)jb->a2a[l]);
+        c[l] = v;
+    }
+}
+
+/* Price plan (dp, tp, pp, m) with stage cuts over the per-microbatch cost
+ * prefix U:
+ *   W_k   = U_{c_{k+1}} - U_{c_k}
+ *   p2p_k = kappa 2 f_pp(b x_{last layer of k})      (k < pp-1), activation out
+ *                                                     and gradient back
+ *   AR_k  = kappa [dp>1] f_dp(2 (dp-1)/dp P_k/tp)     gradient ring all-reduce
+ *   Mem_k as in price_plan
+ *   T     = sum_k (W_k + p2p_k) + (m-1) max_k W_k + max_k AR_k
+ * f_pp and f_dp are the tables of the links price_plan picks. */
+static oplan price_plan_tab(const ojob* jb, const otype* ty, const otab* tabs, int n, double kappa,
+                            int dp, int tp, int pp, int m, const double* U, const int* cuts)
+{
+    oplan r;
+    int bound[ORACLE_MAX_L + 2];
+    bound[0] = 0;
+    for (int k = 1; k < pp; ++k) bound[k] = cuts[k - 1];
+    bound[pp] = jb->L;
+
+    double b = (double)jb->Bg / (double)(dp * m);
+    const otab* t_pp = (n <= ty->gpn) ? &tabs[0] : &tabs[1];
+    int grp = dp * tp;
+    const otab* t_dp = (grp <= ty->gpn && ty->gpn % grp == 0) ? &tabs[0] : &tabs[1];
+
+    double fill = 0.0, w_max = 0.0, ar_max = 0.0, mem_max = 0.0;
+    for (int k = 0; k < pp; ++k) {
+        int lo = bound[k], hi = bound[k + 1];
+        double W = seg(U, lo, hi);
+        double Pk = 0.0, Ak = 0.0;
+        for (int l = lo; l < hi; ++l) { Pk += (double)jb->p[l]; Ak += (double)jb->a[l]; }
+        double p2p = 0.0;
+        if (k < pp - 1) p2p = kappa * (2.0 * tab_lat(t_pp, b * (double)jb->x[hi - 1]));
+        double AR = 0.0;
+        if (dp > 1) AR = kappa * tab_lat(t_dp, 2.0 * (double)(dp - 1) / (double)dp * (Pk / (double)tp));
+        int inflight = m < pp - k ? m : pp - k;
+        double Mem = 4.0 * Pk / (double)tp + (double)inflight * b * Ak / (double)tp;
+        fill += W + p2p;
+        if (W > w_max) w_max = W;
+        if (AR > ar_max) ar_max = AR;
+        if (Mem > mem_max) mem_max = Mem;
+    }
+    r.T = fill + (double)(m - 1) * w_max + ar_max;
+    r.mem_max = mem_max;
+    r.s_max = w_max;
+    r.feasible = (mem_max <= ty->mem) ? 1 : 0;
+    return r;
+}
+
+/* The tables of type g: tab[g][link] at vol/lat + (g*2 + link)*K. */
+static void type_tabs(int g, int K, const double* vol, const double* lat, otab* tabs)
+{
+    for (int link = 0; link < 2; ++link) {
+        tabs[link].K = K;
+        tabs[link].vol = vol + ((size_t)g * 2 + (size_t)link) * (size_t)K;
+        tabs[link].lat = lat + ((size_t)g * 2 + (size_t)link) * (size_t)K;
+    }
+}
+
+/* Balanced partition of plan (dp, tp, pp, m) under the tables: its own
+ * per-microbatch costs (they are no longer b times a per-sample cost, so
+ * every microbatch count has its own partition), prefix, W* and canonical
+ * cuts. */
+static void plan_tab_partition(const ojob* jb, const otype* ty, const otab* tabs, double kappa, int dp, int tp,
+                               int pp, int m, double* U, int* cuts)
+{
+    double c[ORACLE_MAX_L];
+    double b = (double)jb->Bg / (double)(dp * m);
+    layer_costs_tab(jb, ty, tabs, kappa, dp, tp, b, c);
+    oracle_prefix(c, jb->L, U);
+    double W = oracle_bottleneck_dp(U, jb->L, pp);
+    oracle_canonical_cuts(U, jb->L, pp, W, cuts);
+}
+
+/* Price one plan under the tables (vol, lat: [T][2][K]); as oracle_eval_plan. */
+int oracle_eval_plan_tab(int j, int g, int n, double kappa, int dp, int tp, int pp, int m,
+                         const int32_t* off, const float* t, const float* p, const float* a,
+                         const float* x, const float* a2a, const int32_t* batch,
+                         const float* speed, const float* mem, const float* bwi, const float* bwe,
+                         const int32_t* gpn, int K, const double* vol, const double* lat,
+                         const int32_t* cuts_in, int32_t* cuts_out, double* out)
+{
+    ojob jb; otype ty;
+    if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
+    if (dp < 1 || tp < 1 || pp < 1 || m < 1 || dp * tp * pp != n || pp > jb.L || K < 2) return -1;
+    otab tabs[2];
+    type_tabs(g, K, vol, lat, tabs);
+    double U[ORACLE_MAX_L + 1];
+    int cuts[ORACLE_MAX_L];
+    if (cuts_in) {
+        double c[ORACLE_MAX_L];
+        layer_costs_tab(&jb, &ty, tabs, kappa, dp, tp, (double)jb.Bg / (double)(dp * m), c);
+        oracle_prefix(c, jb.L, U);
+        for (int k = 0; k < pp - 1; ++k) {
+            cuts[k] = cuts_in[k];
+            int prevc = k == 0 ? 0 : cuts[k - 1];
+            if (cuts[k] <= prevc || cuts[k] >= jb.L) return -1;
+        }
+    } else {
+        plan_tab_partition(&jb, &ty, tabs, kappa, dp, tp, pp, m, U, cuts);
+    }
+    oplan r = price_plan_tab(&jb, &ty, tabs, n, kappa, dp, tp, pp, m, U, cuts);
+    out[0] = r.T; out[1] = r.mem_max; out[2] = r.s_max; out[3] = (double)r.feasible;
+    if (cuts_out)
+        for (int k = 0; k < pp - 1; ++k) cuts_out[k] = cuts[k];
+    return 0;
+}
+
+/* Best plan of cell (j, g, counts[ci]) under the tables: the plan space,
+ * feasibility, tie window and key of oracle_cell; every plan priced with the
+ * balanced partition of its own per-microbatch costs. */
+static int oracle_cell_tab(int j, int g, int ci, const int32_t* off, const float* t, const float* p,
+                           const float* a, const float* x, const float* a2a, const int32_t* batch,
+                           const float* speed, const float* mem, const float* bwi, const float* bwe,
+                           const int32_t* gpn, const int32_t* counts, const float* kappa_grid, int n_counts,
+                           const int32_t* m_values, int n_m, double tie_eps, int K, const double* vol,
+                           const double* lat, double* res, int32_t* plan, int32_t* cuts_out)
+{
+    ojob jb; otype ty;
+    if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
+    int n = counts[ci];
+    double kappa = (double)kappa_grid[g * n_counts + ci];
+    int L = jb.L;
+    otab tabs[2];
+    type_tabs(g, K, vol, lat, tabs);
+
+    int cap = 64, nc = 0;
+    ocand* cand = (ocand*)malloc(sizeof(ocand) * (size_t)cap);
+    double U[ORACLE_MAX_L + 1];
+    int cuts[ORACLE_MAX_L];
+    for (int tp = 1; tp <= n; ++tp) {
+        if (n % tp != 0 || tp > ty.gpn || ty.gpn % tp != 0) continue;
+        for (int pp = 1; pp <= n / tp; ++pp) {
+            if ((n / tp) % pp != 0 || pp > L) continue;
+            int dp = n / (tp * pp);
+            for (int mi = 0; mi < n_m; ++mi) {
+                int m = m_values[mi];
+                if (jb.Bg % (dp * m) != 0) continue;
+                plan_tab_partition(&jb, &ty, tabs, kappa, dp, tp, pp, m, U, cuts);
+                oplan r = price_plan_tab(&jb, &ty, tabs, n, kappa, dp, tp, pp, m, U, cuts);
+                if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
+                cand[nc].T = r.T; cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp;
+                cand[nc].m = m; cand[nc].feasible = r.feasible;
+                ++nc;
+            }
+        }
+    }
+    double tmin = INFINITY;
+    for (int i = 0; i < nc; ++i)
+        if (cand[i].feasible && cand[i].T < tmin) tmin = cand[i].T;
+    int win = -1;
+    if (tmin < INFINITY) {
+        double lim = tmin * (1.0 + tie_eps);
+        for (int i = 0; i < nc; ++i) {
+            if (!cand[i].feasible || !(cand[i].T <= lim)) continue;
+            if (win < 0 || key_less(&cand[i], &cand[win])) win = i;
+        }
+    }
+    if (win < 0) {
+        res[0] = INFINITY; res[1] = 0.0;
+        plan[0] = plan[1] = plan[2] = plan[3] = 0;
+    } else {
+        ocand* w = &cand[win];
+        res[0] = w->T;
+        res[1] = (double)jb.Bg / w->T;
+        plan[0] = w->dp; plan[1] = w->tp; plan[2] = w->pp; plan[3] = w->m;
+        if (cuts_out) {
+            plan_tab_partition(&jb, &ty, tabs, kappa, w->dp, w->tp, w->pp, w->m, U, cuts);
+            for (int k = 0; k < w->pp - 1; ++k) cuts_out[k] = cuts[k];
+        }
+    }
+    free(cand);
+    return nc;
+}
+
+/* Batch driver under the tables (vol, lat: [n_types][2][K]); as oracle_cells. */
+int oracle_cells_tab(int n_sel, const int64_t* cells, int n_types, int n_counts,
+                     const int32_t* off, const float* t, const float* p, const float* a,
+                     const float* x, const float* a2a, const int32_t* batch,
+                     const float* speed, const float* mem, const float* bwi, const float* bwe,
+                     const int32_t* gpn, const int32_t* counts, const float* kappa_grid,
+                     const int32_t* m_values, int n_m, double tie_eps, int K, const double* vol,
+                     const double* lat, double* res, int32_t* plan, int32_t* cuts, int cuts_stride,
+                     int32_t* nplans)
+{
+    if (K < 2) return -1;
+    for (int s = 0; s < n_sel; ++s) {
+        int64_t c = cells[s];
+        int ci = (int)(c % n_counts);
+        int g = (int)((c / n_counts) % n_types);
+        int j = (int)(c / ((int64_t)n_counts * n_types));
+        int32_t* crow = cuts ? cuts + (int64_t)s * cuts_stride : NULL;
+        if (crow)
+            for (int k = 0; k < cuts_stride; ++k) crow[k] = -1;
+        int np = oracle_cell_tab(j, g, ci, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn,
+                                 counts, kappa_grid, n_counts, m_values, n_m, tie_eps, K, vol, lat,
+                                 res + 2 * s, plan + 4 * s, crow);
+        if (np < 0) return -1;
+        nplans[s] = np;
+    }
+    return 0;
 }

@@ -64,6 +64,14 @@ def load():
     lib.oracle_cells.restype = c_int
     lib.oracle_layer_costs.argtypes = [c_int, c_int, c_double, c_int, c_int] + tables + [_f64p]
     lib.oracle_layer_costs.restype = None
+    lib.oracle_tab_latency.argtypes = [c_int, _f64p, _f64p, c_double]
+    lib.oracle_tab_latency.restype = c_double
+    lib.oracle_eval_plan_tab.argtypes = [c_int, c_int, c_int, c_double, c_int, c_int, c_int, c_int] + tables + [
+        c_int, _f64p, _f64p, ctypes.c_void_p, ctypes.c_void_p, _f64p]
+    lib.oracle_eval_plan_tab.restype = c_int
+    lib.oracle_cells_tab.argtypes = [c_int, _i64p, c_int, c_int] + tables + [
+        _i32p, _f32p, _i32p, c_int, c_double, c_int, _f64p, _f64p, _f64p, _i32p, _i32p, c_int, _i32p]
+    lib.oracle_cells_tab.restype = c_int
     _lib = lib
     return lib
 
@@ -167,6 +175,65 @@ def cells(w, cell_ids, kappa_round: int = 0, cuts_stride: int = 128, rule: int =
                              float(w.tie_eps), res, plan, cuts, cuts_stride, nplans, int(rule))
     if rc != 0:
         raise ValueError("oracle_cells rejected the input")
+    res = res[:2 * n].reshape(n, 2)
+    plan = plan[:4 * n].reshape(n, 4)
+    return dict(T=res[:, 0], thr=res[:, 1], dp=plan[:, 0], tp=plan[:, 1], pp=plan[:, 2],
+                m=plan[:, 3], cuts=cuts[:n * cuts_stride].reshape(n, cuts_stride),
+                nplans=nplans[:n])
+
+
+# ------------------------------------------------------------ interpolated communication tables
+
+def _tab_arrays(w, tables):
+    vol = np.ascontiguousarray(tables[0], np.float64)
+    lat = np.ascontiguousarray(tables[1], np.float64)
+    assert vol.shape == lat.shape and vol.ndim == 3 and vol.shape[:2] == (int(w.n_types), 2)
+    return vol.shape[2], vol.ravel(), lat.ravel()
+
+
+def tab_latency(vol, lat, v: float) -> float:
+    """Latency of v bytes in one (volume, latency) table (0 when nothing moves)."""
+    vol = np.ascontiguousarray(vol, np.float64)
+    lat = np.ascontiguousarray(lat, np.float64)
+    return load().oracle_tab_latency(len(vol), vol, lat, float(v))
+
+
+def eval_plan_tab(w, j, g, n, kappa, dp, tp, pp, m, tables, cuts=None):
+    """Price one plan with communication latency from tables = (vol, lat), each
+    [n_types][2 links][K].  cuts=None: the balanced partition of the plan's own
+    per-microbatch costs.  Returns dict(T, mem_max, w_max, feasible, cuts)."""
+    K, vol, lat = _tab_arrays(w, tables)
+    out = np.zeros(4, np.float64)
+    cuts_out = np.zeros(max(pp - 1, 1), np.int32)
+    cin = None
+    keep = None
+    if cuts is not None:
+        keep = np.ascontiguousarray(np.asarray(list(cuts) + [0], np.int32))
+        cin = keep.ctypes.data
+    rc = load().oracle_eval_plan_tab(int(j), int(g), int(n), float(kappa), int(dp), int(tp), int(pp), int(m),
+                                     *_tables(w), K, vol, lat, cin, cuts_out.ctypes.data, out)
+    if rc != 0:
+        raise ValueError("oracle_eval_plan_tab rejected the plan")
+    return dict(T=out[0], mem_max=out[1], w_max=out[2], feasible=bool(out[3]),
+                cuts=[int(c) for c in cuts_out[:pp - 1]])
+
+
+def cells_tab(w, cell_ids, tables, kappa_round: int = 0, cuts_stride: int = 128):
+    """cells() with communication latency from tables = (vol, lat)."""
+    K, vol, lat = _tab_arrays(w, tables)
+    ids = np.ascontiguousarray(np.asarray(cell_ids, np.int64))
+    n = len(ids)
+    res = np.zeros(2 * max(n, 1), np.float64)
+    plan = np.zeros(4 * max(n, 1), np.int32)
+    cuts = np.zeros(max(n, 1) * cuts_stride, np.int32)
+    nplans = np.zeros(max(n, 1), np.int32)
+    kap = np.ascontiguousarray(w.kappa[kappa_round], np.float32)
+    rc = load().oracle_cells_tab(n, ids, int(w.n_types), int(w.n_counts), *_tables(w),
+                                 np.ascontiguousarray(w.counts, np.int32), kap,
+                                 np.ascontiguousarray(w.m_values, np.int32), len(w.m_values),
+                                 float(w.tie_eps), K, vol, lat, res, plan, cuts, cuts_stride, nplans)
+    if rc != 0:
+        raise ValueError("oracle_cells_tab rejected the input")
     res = res[:2 * n].reshape(n, 2)
     plan = plan[:4 * n].reshape(n, 4)
     return dict(T=res[:, 0], thr=res[:, 1], dp=plan[:, 0], tp=plan[:, 1], pp=plan[:, 2],

@@ -353,3 +353,45 @@ def from_lists(jobs, types, counts, m_values, kappa=None, tie_eps: float = 1e-6,
         gpus_per_node=np.asarray([ty["gpus_per_node"] for ty in types], np.int32),
         counts=np.asarray(counts, np.int32), m_values=np.asarray(m_values, np.int32),
         kappa=kap, tie_eps=tie_eps)
+
+
+# ------------------------------------------------------------ synthetic profiled communication
+
+COMM_VOLUMES = (0.0, 65536.0, 1048576.0, 16777216.0, 268435456.0, 4294967296.0)
+
+
+def comm_tables(w, volumes=COMM_VOLUMES, alpha=(1e-5, 2.5e-5), half=(262144.0, 1048576.0)):
+    """Synthetic stand-ins for profiled (volume, latency) samples of each GPU
+    type's intra-node (link 0) and inter-node (link 1) links: at volume v the
+    latency is alpha + v / (bw * v / (v + half)), i.e. a start-up cost plus the
+    volume over a bandwidth that small messages reach only in part.  Returns
+    (vol, lat), each float64 [n_types][2][K]."""
+    T, K = int(w.n_types), len(volumes)
+    vol = np.zeros((T, 2, K), np.float64)
+    lat = np.zeros((T, 2, K), np.float64)
+    for g in range(T):
+        for link, bw in enumerate((float(w.bw_intra[g]), float(w.bw_inter[g]))):
+            for k, v in enumerate(volumes):
+                vol[g, link, k] = v
+                if v == 0.0 or not np.isfinite(bw):
+                    lat[g, link, k] = alpha[link] if np.isfinite(bw) else 0.0
+                else:
+                    lat[g, link, k] = alpha[link] + (v + half[link]) / bw
+    return vol, lat
+
+
+def linear_tables(w, K: int = 2):
+    """Tables that reproduce volume / bandwidth: points (0, 0) and (bw, 1 s), and
+    K - 2 more on the same line."""
+    T = int(w.n_types)
+    vol = np.zeros((T, 2, K), np.float64)
+    lat = np.zeros((T, 2, K), np.float64)
+    for g in range(T):
+        for link, bw in enumerate((float(w.bw_intra[g]), float(w.bw_inter[g]))):
+            for k in range(K):
+                if np.isfinite(bw):
+                    vol[g, link, k] = bw * k / (K - 1)
+                    lat[g, link, k] = k / (K - 1)
+                else:                      # a free link: no latency at any volume
+                    vol[g, link, k] = float(k)
+    return vol, lat
