@@ -202,6 +202,38 @@ arena_status arena_set_bound_pruning(arena_ctx* ctx, int32_t enabled);
  * Takes effect at the next arena_estimate; INVALID_ARG for other values. */
 arena_status arena_set_partition_rule(arena_ctx* ctx, int32_t rule);
 
+#define ARENA_MAX_COMM_POINTS 16   /* samples per communication latency table */
+
+/* Communication latency interpolated in profiled tables instead of volume /
+ * bandwidth.  The paper profiles each communication primitive offline at
+ * sampled volumes on the target interconnect and, online, interpolates its
+ * latency by volume under the same primitive and topology (Sec. 3.4).  Here
+ * each GPU type has one table per link -- link 0 inside a node, link 1
+ * across nodes -- of n_points samples: volumes[(g*2 + link)*n_points + k]
+ * bytes (the first 0, strictly increasing, finite) with latencies[...]
+ * seconds (finite, >= 0, non-decreasing).  f(v) = 0 when nothing moves, else
+ * linear between the samples around v, extended by the first or last
+ * segment.  With tables set, every communication term takes its latency
+ * from its link's table, scaled by kappa:
+ *   tensor-parallel   4 f_intra(2 (tp-1)/tp b x_l)  per layer and microbatch
+ *   MoE all-to-all    f_inter(b a2a_l)              per layer and microbatch, dp tp > 1
+ *   p2p               2 f_pp(b x_last)              per stage boundary (fill term)
+ *   DP all-reduce     f_dp(2 (dp-1)/dp P_k/tp)      per iteration, dp > 1
+ * (b = Bg/(dp m); f_pp, f_dp on the links of the balanced model), and the
+ * stage costs are per microbatch: each plan (dp, tp, pp, m) gets the
+ * canonical balanced partition of its own per-microbatch layer costs, every
+ * plan is priced (bound pruning does not apply), and the per-cell choice,
+ * outputs and cut rows are as without tables.  Tables linear through the
+ * origin reproduce the volume / bandwidth model.  Host arrays, copied;
+ * uploaded by the next arena_estimate.  Needs grids bound (the tables follow
+ * their type count; rebinding grids with another type count makes
+ * arena_estimate return NOT_READY until tables are set again).  n_points = 0
+ * returns to volume / bandwidth.  With tables, arena_estimate returns
+ * UNSUPPORTED under ARENA_PARTITION_MEMORY.  INVALID_ARG on bad values,
+ * nothing kept. */
+arena_status arena_set_comm_tables(arena_ctx* ctx, int32_t n_points, const double* volumes,
+                                   const double* latencies);
+
 /* Size of the plan space of the bound tables (host computation, no HIP
  * call).  Needs jobs, grids and plan space bound. */
 arena_status arena_space_size_get(const arena_ctx* ctx, arena_space_size* out);

@@ -30,7 +30,7 @@ EXPORTED = (
     "arena_create", "arena_destroy", "arena_last_error", "arena_status_string",
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
-    "arena_schedule", "arena_proxy_estimate", "arena_set_partition_rule",
+    "arena_schedule", "arena_proxy_estimate", "arena_set_partition_rule", "arena_set_comm_tables",
 )
 
 PARTITION_BALANCED = 0
@@ -126,6 +126,8 @@ def load():
     lib.arena_set_bound_pruning.restype = st
     lib.arena_set_partition_rule.argtypes = [vp, i32]
     lib.arena_set_partition_rule.restype = st
+    lib.arena_set_comm_tables.argtypes = [vp, i32, vp, vp]
+    lib.arena_set_comm_tables.restype = st
     lib.arena_space_size_get.argtypes = [vp, ctypes.POINTER(SpaceSize)]
     lib.arena_space_size_get.restype = st
     lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
@@ -224,6 +226,19 @@ def arena_set_partition_rule(ctx, rule: int) -> None:
     _check(ctx, load().arena_set_partition_rule(ctx, int(rule)))
 
 
+def arena_set_comm_tables(ctx, volumes=None, latencies=None) -> None:
+    """volumes, latencies: float64 [n_types][2][K] host arrays, or None to return
+    to volume / bandwidth."""
+    if volumes is None:
+        _check(ctx, load().arena_set_comm_tables(ctx, 0, None, None))
+        return
+    v = np.ascontiguousarray(volumes, np.float64)
+    lt = np.ascontiguousarray(latencies, np.float64)
+    if v.shape != lt.shape or v.ndim != 3 or v.shape[1] != 2:
+        raise ValueError("comm tables: volumes and latencies must both be [n_types][2][K]")
+    _check(ctx, load().arena_set_comm_tables(ctx, int(v.shape[2]), v.ctypes.data, lt.ctypes.data))
+
+
 def arena_space_size_get(ctx) -> dict:
     s = SpaceSize()
     _check(ctx, load().arena_space_size_get(ctx, ctypes.byref(s)))
@@ -302,7 +317,7 @@ class Estimator:
     `workload` is any object with the attributes of workloads.Workload."""
 
     def __init__(self, workload, device: int = 0, with_cuts: bool = False, prune: bool = True,
-                 rule: int = PARTITION_BALANCED):
+                 rule: int = PARTITION_BALANCED, comm_tables=None):
         import torch
         self.torch = torch
         self.w = workload
@@ -323,6 +338,8 @@ class Estimator:
             arena_set_kappa(self.ctx, workload.kappa[0])
             arena_set_bound_pruning(self.ctx, prune)
             arena_set_partition_rule(self.ctx, rule)
+            if comm_tables is not None:
+                arena_set_comm_tables(self.ctx, *comm_tables)
             C = workload.n_cells
             self.n_cells = C
             self.t_iter = torch.empty(C, dtype=torch.float32, device=self.dev)
@@ -342,6 +359,13 @@ class Estimator:
 
     def set_partition_rule(self, rule: int) -> None:
         arena_set_partition_rule(self.ctx, rule)
+
+    def set_comm_tables(self, tables=None) -> None:
+        """tables = (volumes, latencies), each [n_types][2][K]; None: volume / bandwidth."""
+        if tables is None:
+            arena_set_comm_tables(self.ctx)
+        else:
+            arena_set_comm_tables(self.ctx, *tables)
 
     def estimate(self, stream=None) -> None:
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream

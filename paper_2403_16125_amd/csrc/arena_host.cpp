@@ -46,6 +46,13 @@ struct arena_ctx {
     bool prune = true;
     int32_t partition_rule = ARENA_PARTITION_BALANCED;
 
+    // interpolated communication latency: volumes then latencies, [T][2][K]
+    int32_t tab_k = 0, tab_types = 0;
+    std::vector<double> tab;
+    bool tab_dirty = false;
+    double* d_tab = nullptr;
+    size_t cap_tab = 0;
+
     // cached space size
     bool size_valid = false;
     arena_space_size size{};
@@ -140,6 +147,10 @@ void free_device(arena_ctx* c)
     (void)hipFree(c->d_msets);
     (void)hipFree(c->d_mset_off);
     (void)hipFree(c->d_hbm);
+    (void)hipFree(c->d_tab);
+    c->d_tab = nullptr;
+    c->cap_tab = 0;
+    c->tab_dirty = c->tab_k > 0;
     c->d_msets = nullptr;
     c->d_mset_off = nullptr;
     c->d_hbm = nullptr;
@@ -559,6 +570,43 @@ arena_status arena_set_partition_rule(arena_ctx* c, int32_t rule)
     return ARENA_OK;
 }
 
+arena_status arena_set_comm_tables(arena_ctx* c, int32_t n_points, const double* volumes,
+                                   const double* latencies)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    if (n_points == 0) {
+        c->tab_k = 0;
+        c->tab.clear();
+        return ARENA_OK;
+    }
+    if (!c->grids_bound) return fail(c, ARENA_ERR_NOT_READY, "comm tables: bind grids first");
+    if (n_points < 2 || n_points > ARENA_MAX_COMM_POINTS)
+        return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: %d points (2..%d)", n_points, ARENA_MAX_COMM_POINTS);
+    if (!volumes || !latencies) return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: NULL array");
+    const size_t nt = (size_t)c->n_types * 2, K = (size_t)n_points;
+    for (size_t q = 0; q < nt; ++q) {
+        const double* v = volumes + q * K;
+        const double* l = latencies + q * K;
+        if (v[0] != 0.0)
+            return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: table %zu does not start at volume 0", q);
+        for (size_t k = 0; k < K; ++k) {
+            if (!std::isfinite(v[k]) || !std::isfinite(l[k]) || !(l[k] >= 0.0))
+                return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: table %zu point %zu not finite or negative", q, k);
+            if (k > 0 && !(v[k] > v[k - 1]))
+                return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: table %zu volumes not increasing", q);
+            if (k > 0 && !(l[k] >= l[k - 1]))
+                return fail(c, ARENA_ERR_INVALID_ARG, "comm tables: table %zu latencies decrease", q);
+        }
+    }
+    c->tab.assign(volumes, volumes + nt * K);
+    c->tab.insert(c->tab.end(), latencies, latencies + nt * K);
+    c->tab_k = n_points;
+    c->tab_types = c->n_types;
+    c->tab_dirty = true;
+    return ARENA_OK;
+}
+
 arena_status arena_space_size_get(const arena_ctx* cc, arena_space_size* out)
 {
     arena_ctx* c = const_cast<arena_ctx*>(cc);
@@ -588,12 +636,29 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     if (c->size.max_plans_per_cell > arena::kMaxPlans)
         return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: a cell admits %d plans (max %d)",
                     c->size.max_plans_per_cell, arena::kMaxPlans);
+    if (c->tab_k > 0 && c->partition_rule != ARENA_PARTITION_BALANCED)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: comm tables with the memory partition rule");
+    if (c->tab_k > 0 && c->tab_types != c->n_types)
+        return fail(c, ARENA_ERR_NOT_READY, "estimate: comm tables were set for %d types, %d are bound",
+                    c->tab_types, c->n_types);
     hipStream_t stream = (hipStream_t)stream_ptr;
     DeviceGuard guard(c->device);
     if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
     arena_status st = ensure_device(c, stream);
     if (st != ARENA_OK) return st;
     if (c->order_dirty && (st = upload_orders(c, stream)) != ARENA_OK) return st;
+    hipError_t e;
+    if (c->tab_k > 0) {
+        if (c->tab_dirty) {
+            if ((e = ensure_capacity(&c->d_tab, &c->cap_tab, c->tab.size())))
+                return fail(c, ARENA_ERR_OUT_OF_MEMORY, "comm tables: %s", hipGetErrorString(e));
+            if ((e = hipMemcpyAsync(c->d_tab, c->tab.data(), sizeof(double) * c->tab.size(),
+                                    hipMemcpyHostToDevice, stream)) ||
+                (e = hipStreamSynchronize(stream)))
+                return hip_fail(c, e, "comm table upload");
+            c->tab_dirty = false;
+        }
+    }
 
     arena::EstimateArgs A;
     std::memset(&A, 0, sizeof(A));
@@ -617,13 +682,17 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.tie_eps = c->tie_eps;
     A.prune = c->prune ? 1 : 0;
     A.mem_rule = c->partition_rule == ARENA_PARTITION_MEMORY ? 1 : 0;
+    if (c->tab_k > 0) {
+        A.tab_k = c->tab_k;
+        A.tab_vol = c->d_tab;
+        A.tab_lat = c->d_tab + c->tab.size() / 2;
+    }
     A.t_iter = t_iter;
     A.thr = thr;
     A.plan = plan;
     A.cuts = cuts;
     A.cuts_stride = cuts ? cuts_stride : 0;
     A.counters = c->d_counters;
-    hipError_t e;
     if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)))
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");

@@ -13,6 +13,7 @@ constexpr int kMaxPlans = 256;      // plans per cell
 constexpr int kMaxM = 16;           // microbatch choices
 constexpr int kWavesPerBlock = 4;   // waves of one (job, type) block, each on its own cells
 constexpr int kMaxDp = 1024;        // largest data-parallel degree (counts are <= 1024)
+constexpr int kMaxTabPoints = 16;   // samples per communication latency table
 
 // GPU type as the kernels read it (doubles converted from the f32 inputs).
 struct TypeDev {
@@ -45,6 +46,11 @@ struct EstimateArgs {
     double tie_eps;
     int32_t prune;                // bound pruning on
     int32_t mem_rule;             // partition rule 1: balanced among the splits that fit memory
+    // interpolated communication latency: tab_k points per (type, link),
+    // volumes then latencies, each [T][2][tab_k]; tab_k = 0: volume / bandwidth
+    const double* tab_vol;
+    const double* tab_lat;
+    int32_t tab_k;
     float* t_iter;
     float* thr;
     uint32_t* plan;

@@ -1398,6 +1398,276 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     estimate_body<SLOTS, true>(A);
 }
 
+// ------------------------------------------------------------ interpolated communication latency
+
+// Latency of v bytes in one profiled (volume, latency) table of K samples
+// (vol[0] = 0, ascending): nothing moved costs nothing; otherwise linear
+// between the samples around v, extended by the first or last segment.
+__device__ __forceinline__ double tab_lat(const double* vol, const double* lat, int K, double v)
+{
+    if (!(v > 0.0)) return 0.0;
+    int k = 1;
+    while (k < K - 1 && v > vol[k]) ++k;
+    return lat[k - 1] + (v - vol[k - 1]) * (lat[k] - lat[k - 1]) / (vol[k] - vol[k - 1]);
+}
+
+struct TabBlockLds {
+    float t[kLmax];
+    float x[kLmax];
+    float q[kLmax];
+    double Pp[kLmax + 1];
+    double Ap[kLmax + 1];
+    double vol[2][kMaxTabPoints];     // link 0 inside a node, 1 across nodes
+    double lat[2][kMaxTabPoints];
+    int32_t next_cell;
+    WaveLds w[kWavesPerBlock];
+};
+
+// Per-microbatch cost of layers lane and lane+64 of plan (dp, tp) with b
+// samples per microbatch (0 past L): compute, four tensor-parallel ring
+// all-reduces of 2 (tp-1)/tp b x_l bytes on the intra-node link, the MoE
+// all-to-all of b a2a_l bytes on the inter-node link; comm scaled by kappa.
+__device__ __forceinline__ void tab_layer_costs(const TabBlockLds& B, int lane, const JobCtx& jb, const TypeDev& ty,
+                                                int K, double kappa, int dp, int tp, double b, double (&c)[2])
+{
+    const double denom = (double)jb.Bg * ty.speed * (double)tp;
+    const double ftp = 2.0 * (double)(tp - 1) / (double)tp;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const int l = lane + 64 * s;
+        c[s] = 0.0;
+        if (l < jb.L) {
+            double v = b * ((double)B.t[l] / denom);
+            if (tp > 1) v += kappa * (4.0 * tab_lat(B.vol[0], B.lat[0], K, ftp * b * (double)B.x[l]));
+            if (dp * tp > 1) v += kappa * tab_lat(B.vol[1], B.lat[1], K, b * (double)B.q[l]);
+            c[s] = v;
+        }
+    }
+}
+
+// The plan's per-microbatch costs, prefix (into Wv.UD), bottleneck of pp
+// stages (one-degree recursion) and canonical stages.
+__device__ __forceinline__ Stages tab_partition(const TabBlockLds& B, WaveLds& Wv, int lane, const JobCtx& jb,
+                                                const TypeDev& ty, int K, double kappa, int dp, int tp, int pp,
+                                                double b, double& W)
+{
+    double c[2];
+    tab_layer_costs(B, lane, jb, ty, K, kappa, dp, tp, b, c);
+    seq_prefix<2, 2>(c[0], c[1], jb.L, lane, Wv.UD, Wv.UD + 1, true);
+    Mask one;
+    one.lo = pp <= 64 ? (1ull << (pp - 1)) : 0ull;
+    one.hi = pp > 64 ? (1ull << (pp - 65)) : 0ull;
+    W = 0.0;
+    solve_dp(Wv, jb.L, one, lane, [&](int, double Wk, Mask mk) {
+        W = Wk;
+        return mk;
+    });
+    return canonical_stages<2>(Wv.UD, Wv.J, lane, jb.L, pp, W);
+}
+
+// Iteration time of plan (dp, tp, pp, m) on stages sg under the tables
+// (+inf if a stage does not fit):
+//   T = sum_k (W_k + p2p_k) + (m-1) max_k W_k + max_k AR_k,
+//   W_k the stage's per-microbatch cost, p2p_k = kappa 2 f_pp(b x_last)
+//   (k < pp-1), AR_k = kappa f_dp(2 (dp-1)/dp P_k/tp) (dp > 1), memory as in
+//   the balanced model.
+__device__ __forceinline__ double tab_price(const TabBlockLds& B, WaveLds& Wv, int lane, const JobCtx& jb,
+                                            const TypeDev& ty, int K, const Cell& cell, int dp, int tp, int pp,
+                                            int m, double b, const Stages& sg)
+{
+    const int lpp = cell.n <= ty.gpn ? 0 : 1;
+    const int grp = dp * tp;
+    const int ldp = (grp <= ty.gpn && ty.gpn % grp == 0) ? 0 : 1;
+    const double fdp = 2.0 * (double)(dp - 1) / (double)dp;
+    double fill = 0.0, wmax = 0.0, armax = 0.0, memmax = 0.0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int k = lane + 64 * h;
+        if (k < pp) {
+            const int lo = h == 0 ? sg.lo0 : sg.lo1;
+            const int hi = h == 0 ? sg.hi0 : sg.hi1;
+            const double Wk = Wv.UD[2 * hi] - Wv.UD[2 * lo];
+            const double Pk = B.Pp[hi] - B.Pp[lo];
+            const double Ak = B.Ap[hi] - B.Ap[lo];
+            double p2p = 0.0;
+            if (k < pp - 1) p2p = cell.kappa * (2.0 * tab_lat(B.vol[lpp], B.lat[lpp], K, b * (double)B.x[hi - 1]));
+            double AR = 0.0;
+            if (dp > 1) AR = cell.kappa * tab_lat(B.vol[ldp], B.lat[ldp], K, fdp * (Pk / (double)tp));
+            const int inflight = m < pp - k ? m : pp - k;
+            const double Mem = 4.0 * Pk / (double)tp + (double)inflight * b * Ak / (double)tp;
+            fill += Wk + p2p;
+            wmax = fmax(wmax, Wk);
+            armax = fmax(armax, AR);
+            memmax = fmax(memmax, Mem);
+        }
+    }
+    double rs[1] = {fill};
+    double rm[3] = {wmax, armax, memmax};
+    wave_reduce<OpSum, 1>(rs);
+    wave_reduce<OpMax, 3>(rm);
+    if (!(rm[2] <= ty.mem)) return kInf;
+    return rs[0] + (double)(m - 1) * rm[0] + rm[1];
+}
+
+// Every cell under interpolated communication latency: one block per (job,
+// type), its waves taking counts; every plan of a cell gets the balanced
+// partition of its own per-microbatch costs (no sharing across m or counts,
+// no bound pruning), then the cell's choice as in estimate_kernel.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
+{
+    __shared__ TabBlockLds B;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    WaveLds& Wv = B.w[wid];
+
+    const int item = A.item_order[blockIdx.x];
+    const int j = item / A.n_types;
+    const int g = item - j * A.n_types;
+    const int off = A.layer_offset[j];
+    JobCtx jb;
+    jb.L = A.layer_offset[j + 1] - off;
+    jb.Bg = A.batch[j];
+    jb.moe = false;
+    const TypeDev ty = A.types[g];
+    const int K = A.tab_k;
+
+    if (tid < jb.L) {
+        B.t[tid] = A.t[off + tid];
+        B.x[tid] = A.x[off + tid];
+        B.q[tid] = A.q[off + tid];
+    }
+    if (tid < 2 * K) {
+        const int link = tid / K, k = tid - link * K;
+        const long long base = ((long long)g * 2 + link) * K + k;
+        B.vol[link][k] = A.tab_vol[base];
+        B.lat[link][k] = A.tab_lat[base];
+    }
+    if (wid == 0 || wid == 1) {
+        const float* src = (wid == 0 ? A.p : A.a) + off;
+        const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
+        const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
+        seq_prefix<1, 2>(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.UD + 1, false);
+    }
+    if (tid == 0) B.next_cell = 0;
+    if (lane < kNumCounters) Wv.tally[lane] = 0ull;
+    __syncthreads();
+
+    for (;;) {
+        int cix = 0;
+        if (lane == 0) cix = atomicAdd(&B.next_cell, 1);
+        cix = __builtin_amdgcn_readfirstlane(cix);
+        if (cix >= A.n_counts) break;
+        const int ci = A.count_order[cix];
+        Cell cell;
+        cell.n = A.counts[ci];
+        cell.kappa = (double)A.kappa[g * A.n_counts + ci];
+        cell.B_pp = 0.0;
+        cell.c_p2p = 0.0;
+        int np = 0;
+        for (int tp = 1; tp <= cell.n && tp <= ty.gpn; ++tp) {
+            if (cell.n % tp != 0 || ty.gpn % tp != 0) continue;
+            const int qn = cell.n / tp;
+            for (int pp = 1; pp <= qn && pp <= jb.L; ++pp) {
+                if (qn % pp != 0) continue;
+                const int dp = qn / pp;
+                for (int mi = 0; mi < A.n_m; ++mi) {
+                    const int m = A.m_values[mi];
+                    const double dm = (double)(dp * m);
+                    const double bq = rint((double)jb.Bg / dm);
+                    if (!(bq * dm == (double)jb.Bg)) continue;
+                    double W;
+                    const Stages sg = tab_partition(B, Wv, lane, jb, ty, K, cell.kappa, dp, tp, pp, bq, W);
+                    const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp, pp, m, bq, sg);
+                    if (lane == 0 && np < kMaxPlans) {
+                        Wv.planT[np] = T;
+                        Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
+                    }
+                    ++np;
+                    tally(Wv, lane, kProblems, 1);
+                    tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L + 4ull * (unsigned)jb.L +
+                                             12ull * (unsigned)pp + 40ull);
+                    wave_sync();
+                }
+            }
+        }
+        if (np > kMaxPlans) {
+            tally(Wv, lane, kOverflow, 1);
+            np = kMaxPlans;
+        }
+        wave_sync();
+
+        double tl = kInf;
+        for (int e = lane; e < np; e += 64) tl = fmin(tl, Wv.planT[e]);
+        const double tmin = wave_reduce1<OpMin>(tl);
+        const long long cidx = ((long long)j * A.n_types + g) * A.n_counts + ci;
+        tally(Wv, lane, kPlans, (unsigned long long)np);
+        if (!(tmin < kInf)) {
+            tally(Wv, lane, kInfeasible, 1);
+            if (lane == 0) {
+                A.t_iter[cidx] = __builtin_huge_valf();
+                A.thr[cidx] = 0.0f;
+                A.plan[cidx] = 0u;
+            }
+            if (A.cuts) {
+                uint8_t* row = A.cuts + cidx * A.cuts_stride;
+                for (int e = lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
+            }
+            wave_sync();
+            continue;
+        }
+        const double tlim = tmin * (1.0 + A.tie_eps);
+        double kl = kInf;
+        for (int e = lane; e < np; e += 64)
+            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)Wv.planKey[e]);
+        const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
+        double il = -1.0;
+        for (int e = lane; e < np; e += 64)
+            if (Wv.planKey[e] == kbest) il = (double)e;
+        int ib = (int)wave_reduce1<OpMax>(il);
+        ib = ib < 0 ? 0 : (ib >= np ? np - 1 : ib);
+        const double Tb = Wv.planT[ib];
+        const int pp = (int)(kbest >> 12);
+        const int tp = (int)((kbest >> 7) & 0x1Fu);
+        const int m = (int)(kbest & 0x7Fu);
+        const int dp = cell.n / (tp * pp);
+        if (lane == 0) {
+            A.t_iter[cidx] = (float)Tb;
+            A.thr[cidx] = (float)((double)jb.Bg / Tb);
+            A.plan[cidx] = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) | ((unsigned)m << 24) |
+                           (1u << 31);
+        }
+        if (A.cuts) {
+            // re-derive the winner's stages (the recursion's entries are not tallied twice)
+            const unsigned long long e0 = Wv.tally[kDpEntries];
+            const double bw = rint((double)jb.Bg / (double)(dp * m));
+            double W;
+            const Stages sg = tab_partition(B, Wv, lane, jb, ty, K, cell.kappa, dp, tp, pp, bw, W);
+            if (lane == 0) Wv.tally[kDpEntries] = e0;
+            uint8_t* row = A.cuts + cidx * A.cuts_stride;
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                const int idx = lane + 64 * s;
+                const int en = s == 0 ? +sg.hi0 : +sg.hi1;
+                if (idx < A.cuts_stride) row[idx] = (idx < pp - 1) ? (uint8_t)en : (uint8_t)0xFF;
+            }
+            for (int e = 128 + lane; e < A.cuts_stride; e += 64) row[e] = 0xFF;
+        }
+        wave_sync();
+    }
+
+    if (lane == 0) {
+        if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
+        const unsigned long long* t = Wv.tally;
+        atomicAdd(&A.counters[kPlans], t[kPlans]);
+        atomicAdd(&A.counters[kProblems], t[kProblems]);
+        atomicAdd(&A.counters[kDpEntries], t[kDpEntries]);
+        atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
+        if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
+        atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
+    }
+}
+
 __global__ void zero_kernel(unsigned long long* p, int n)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1428,7 +1698,9 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
     const long long blocks = (long long)args.n_jobs * args.n_types;
     if (blocks <= 0) return hipSuccess;
     const dim3 grid((unsigned)blocks), block(256);
-    if (args.mem_rule) {
+    if (args.tab_k > 0) {
+        hipLaunchKernelGGL(estimate_tab_kernel, grid, block, 0, stream, args);
+    } else if (args.mem_rule) {
         if (args.share_tp)
             hipLaunchKernelGGL((estimate_mem_kernel<kSlotsShared>), grid, block, 0, stream, args);
         else

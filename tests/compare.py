@@ -22,13 +22,21 @@ def decode(w, ids):
     return j, g, ci
 
 
-def compare(w, gpu, ids, oracle, kappa_round=0, ref=None, rule=0):
+def compare(w, gpu, ids, oracle, kappa_round=0, ref=None, rule=0, tables=None):
     """gpu: dict with t_iter, thr, dp, tp, pp, m, feasible, cuts (u8 rows) for `ids`,
-    estimated under partition rule `rule`.
+    estimated under partition rule `rule`, or with communication latency from
+    `tables` = (volumes, latencies).
     Returns a report dict; report['mismatch'] lists failing cells."""
     ids = np.asarray(ids, np.int64)
     if ref is None:
-        ref = oracle.cells(w, ids, kappa_round=kappa_round, rule=rule)
+        ref = (oracle.cells(w, ids, kappa_round=kappa_round, rule=rule) if tables is None else
+               oracle.cells_tab(w, ids, tables, kappa_round=kappa_round))
+
+    def price(j, g, n, kap, dp, tp, pp, m, cuts=None):
+        if tables is None:
+            return oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m, cuts=cuts, rule=rule if cuts is None else 0)
+        return oracle.eval_plan_tab(w, j, g, n, kap, dp, tp, pp, m, tables, cuts=cuts)
+
     J, G, CI = decode(w, ids)
     rep = dict(n=len(ids), exact=0, near_tie=0, mismatch=[], max_rel_T=0.0, max_rel_thr=0.0,
                infeasible=0)
@@ -79,14 +87,13 @@ def compare(w, gpu, ids, oracle, kappa_round=0, ref=None, rule=0):
         # differing decision: price the GPU's choice in the oracle
         if g_inf:
             # the oracle found a feasible plan; near-tie only if it sits on the memory limit
-            e = oracle.eval_plan(w, j, g, n, kap, int(ref["dp"][s]), int(ref["tp"][s]),
-                                 int(ref["pp"][s]), int(ref["m"][s]), rule=rule)
+            e = price(j, g, n, kap, int(ref["dp"][s]), int(ref["tp"][s]), int(ref["pp"][s]), int(ref["m"][s]))
             if abs(e["mem_max"] - float(w.mem[g])) <= REL_T * float(w.mem[g]):
                 rep["near_tie"] += 1
             else:
                 rep["mismatch"].append((int(ids[s]), "GPU infeasible, oracle feasible"))
             continue
-        e = oracle.eval_plan(w, j, g, n, kap, *plan, cuts=gc)
+        e = price(j, g, n, kap, *plan, cuts=gc)
         on_mem_edge = abs(e["mem_max"] - float(w.mem[g])) <= REL_T * float(w.mem[g])
         if not e["feasible"] and not on_mem_edge:
             rep["mismatch"].append((int(ids[s]), f"GPU plan {plan} does not fit"))

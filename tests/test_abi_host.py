@@ -191,6 +191,46 @@ def test_partition_rule_switch(ctx):
     assert re.search(r"#define ARENA_PARTITION_MEMORY 1\b", src)
 
 
+def test_comm_tables_validation(ctx):
+    lib = arena.load()
+    assert lib.arena_set_comm_tables(None, 0, None, None) == arena.ARENA_ERR_INVALID_ARG
+    good_v = np.array([[[0.0, 1e6, 1e9]] * 2], np.float64)        # 1 type x 2 links x 3 points
+    good_l = np.array([[[1e-5, 2e-5, 1e-2]] * 2], np.float64)
+    _expect(arena.ARENA_ERR_NOT_READY, arena.arena_set_comm_tables, ctx, good_v, good_l, match="grids")
+    w = wl.tiny()
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    T = int(w.n_types)
+    v = np.broadcast_to(good_v[0], (T, 2, 3)).copy()
+    lt = np.broadcast_to(good_l[0], (T, 2, 3)).copy()
+    arena.arena_set_comm_tables(ctx, v, lt)
+    arena.arena_set_comm_tables(ctx)                                # back to volume / bandwidth
+    bad = []
+    x = v.copy(); x[0, 0, 0] = 1.0; bad.append((x, lt, "volume 0"))
+    x = v.copy(); x[0, 1, 2] = x[0, 1, 1]; bad.append((x, lt, "not increasing"))
+    y = lt.copy(); y[0, 0, 2] = 1e-6; bad.append((v, y, "decrease"))
+    y = lt.copy(); y[0, 0, 0] = -1.0; bad.append((v, y, "negative"))
+    y = lt.copy(); y[0, 0, 1] = np.nan; bad.append((v, y, "not finite"))
+    for vv, ll, msg in bad:
+        _expect(arena.ARENA_ERR_INVALID_ARG, arena.arena_set_comm_tables, ctx, vv, ll, match=msg)
+    one_v, one_l = v[:, :, :1].copy(), lt[:, :, :1].copy()
+    _expect(arena.ARENA_ERR_INVALID_ARG, arena.arena_set_comm_tables, ctx, one_v, one_l, match="points")
+    many_v = np.cumsum(np.ones((T, 2, 17)), axis=2) - 1.0
+    _expect(arena.ARENA_ERR_INVALID_ARG, arena.arena_set_comm_tables, ctx, many_v, np.ones((T, 2, 17)),
+            match="points")
+    assert lib.arena_set_comm_tables(ctx, 3, None, None) == arena.ARENA_ERR_INVALID_ARG
+
+
+def test_comm_tables_rejected_with_the_memory_rule(ctx):
+    # host-side: the estimate refuses the combination before touching a device
+    w = wl.tiny()
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    arena.arena_set_plan_space(ctx, w.m_values, 1e-6)
+    arena.arena_bind_jobs(ctx, w.layer_offset, w.batch, FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_set_comm_tables(ctx, *wl.comm_tables(w))
+    arena.arena_set_partition_rule(ctx, arena.PARTITION_MEMORY)
+    _expect(arena.ARENA_ERR_UNSUPPORTED, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="comm tables")
+
+
 def test_unsorted_microbatch_counts_accepted(ctx):
     # the library sorts them for the kernel; the caller's order is free
     arena.arena_set_plan_space(ctx, [8, 1, 4, 2], 1e-6)
