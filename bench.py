@@ -14,7 +14,9 @@ state over the same 16384 x 8 x 131 shape, and prints that line.  With
 trace-like workload and scores its plans against the exhaustive estimate.
 With --partition memory the estimate prices each plan with the balanced
 partition among the stage splits that fit memory instead of the balanced
-partition followed by the memory check.
+partition followed by the memory check.  With --comm-tables communication
+latency is interpolated in synthetic profiled (volume, latency) tables per
+link instead of volume / bandwidth.
 """
 from __future__ import annotations
 
@@ -51,10 +53,10 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0) -> dict:
+def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None) -> dict:
     """The oracle (single-threaded C, fp64) on a bounded sample of the same
     workload: jobs j = 0, every, 2*every, ... times every grid of one round,
-    under partition rule `rule`."""
+    under partition rule `rule` or with communication latency from `tables`."""
     import numpy as np
     from oracle import oracle as oracle_c
     oracle_c.load()
@@ -62,7 +64,10 @@ def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0) -> dict:
     jobs = list(range(0, w.n_jobs, every))
     ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)
     t0 = time.perf_counter()
-    oracle_c.cells(w, ids, kappa_round=kappa_round, rule=rule)
+    if tables is None:
+        oracle_c.cells(w, ids, kappa_round=kappa_round, rule=rule)
+    else:
+        oracle_c.cells_tab(w, ids, tables, kappa_round=kappa_round)
     dt = time.perf_counter() - t0
     return {"value": len(ids) / dt, "unit": "cells/s", "cores": 1, "kind": "oracle",
             "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, round {kappa_round}: "
@@ -280,9 +285,12 @@ def main() -> int:
     ap.add_argument("--workload", default="full", choices=["tiny", "small", "trace", "moe", "full"])
     ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
     ap.add_argument("--cpu-every", type=int, default=None,
-                    help="oracle sample: every k-th job (default 256; 2048 with --partition memory)")
+                    help="oracle sample: every k-th job (default 256; 2048 with --partition memory, "
+                         "1024 with --comm-tables)")
     ap.add_argument("--partition", default="balanced", choices=["balanced", "memory"],
                     help="stage partition rule of the estimate")
+    ap.add_argument("--comm-tables", action="store_true",
+                    help="communication latency from synthetic profiled tables (interpolated by volume)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", action="store_true",
                     help="time the scheduling step that consumes the throughput matrix instead")
@@ -332,7 +340,12 @@ def main() -> int:
 
     dev = torch.device("cuda", 0)
     rule = arena.PARTITION_MEMORY if args.partition == "memory" else arena.PARTITION_BALANCED
-    est = arena.Estimator(w, device=0, with_cuts=args.cuts, rule=rule)
+    tables = workloads.comm_tables(w) if args.comm_tables else None
+    if tables is not None and rule != arena.PARTITION_BALANCED:
+        print("--comm-tables works with the balanced partition only", file=sys.stderr, flush=True)
+        return 2
+    est = arena.Estimator(w, device=0, with_cuts=args.cuts, rule=rule, comm_tables=tables)
+    plain = rule == arena.PARTITION_BALANCED and tables is None
     size = est.space_size()
     assert size["plans"] == work["plans"]
     stream = torch.cuda.current_stream(dev)
@@ -369,7 +382,7 @@ def main() -> int:
     res = est.results(np.arange(0, w.n_cells, 9973))
     est.close()
 
-    traffic = stored_traffic(args.workload) if rule == arena.PARTITION_BALANCED else None
+    traffic = stored_traffic(args.workload) if plain else None
     cells_per_s = w.n_cells * args.steps / wall
     plans_per_s = work["plans"] * args.steps / wall       # every plan of the space is decided
     achieved = float(np.sum(ops_done)) / (float(np.sum(launch_ms)) / 1e3)
@@ -392,6 +405,7 @@ def main() -> int:
                         "redrawn every round",
             "cuts": bool(args.cuts),
             "partition": args.partition,
+            "comm": "interpolated tables" if tables is not None else "volume / bandwidth",
             "rounds_per_step": 1,
         },
         "plans_per_s": plans_per_s,
@@ -403,7 +417,7 @@ def main() -> int:
             "frac": achieved / PEAK_LANE_OPS,
             "traffic": traffic,
             "ops_per_launch": float(np.mean(ops_done)),
-            "ops_exhaustive": work["ops"] if rule == arena.PARTITION_BALANCED else None,
+            "ops_exhaustive": work["ops"] if plain else None,
             "launch_ms": avg_launch_s * 1e3,
             # for transparency: against the published fp32 vector rate (FMA and packed pairs
             # counted twice each), and the measured HBM rate when the counters are current
@@ -415,8 +429,8 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
-        every = args.cpu_every or (2048 if rule == arena.PARTITION_MEMORY else 256)
-        line["cpu_baseline"] = cpu_baseline(w, every, rule=rule)
+        every = args.cpu_every or (256 if plain else (1024 if tables is not None else 2048))
+        line["cpu_baseline"] = cpu_baseline(w, every, rule=rule, tables=tables)
     print(json.dumps(line), flush=True)
     return 0
 

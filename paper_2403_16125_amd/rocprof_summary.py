@@ -29,6 +29,9 @@ KERNEL_SOURCES = {
     "estimate_mem_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
                             "paper_2403_16125_amd/csrc/arena_host.cpp",
                             "paper_2403_16125_amd/csrc/arena_kernels.hip"),
+    "estimate_tab_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
+                            "paper_2403_16125_amd/csrc/arena_host.cpp",
+                            "paper_2403_16125_amd/csrc/arena_kernels.hip"),
     "schedule_kernel": ("include/arena.h", "paper_2403_16125_amd/csrc/arena_internal.h",
                         "paper_2403_16125_amd/csrc/arena_host.cpp",
                         "paper_2403_16125_amd/csrc/arena_sched.hip"),

@@ -86,6 +86,16 @@ def test_full_size_sampled(oracle, name, k):
     assert cnt["cells"] == w.n_cells and cnt["plans"] == size["plans"]
 
 
+def test_full_round_sampled(oracle):
+    w = wl.full()
+    tabs = wl.comm_tables(w)
+    ids = _sample(w, 300, seed=43)
+    _say(f"full round: {w.n_cells} cells on the GPU, {len(ids)} compared")
+    res, cnt, size = _run(w, tabs, ids=ids)
+    _check(compare(w, res, ids, oracle, tables=tabs), "full")
+    assert cnt["cells"] == w.n_cells and cnt["plans"] == size["plans"]
+
+
 def test_edge_cases(oracle):
     sys.path.insert(0, __file__.rsplit("/", 1)[0])
     from test_gpu_parity import _edge_workload
