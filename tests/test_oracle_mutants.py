@@ -9,8 +9,9 @@ temporary library, and runs the pins of test_oracle_memory_partition.py
 against it in a child process: some pin must fail (an assertion, or a crash
 or time-out of the broken copy).  The unmodified copy, built the same way,
 must pass them all.  The same is done for the balanced partition, the layer
-costs, the plan price and the per-cell choice, for the proxy-plan planner's
-oracle and for the scheduler's, each with its own pins.
+costs, the plan price and the per-cell choice, the interpolated communication
+latency, the proxy-plan planner's oracle and the scheduler's, each with its own
+pins.
 """
 import os
 import subprocess
@@ -246,4 +247,49 @@ def test_unmodified_scheduler_copy_passes(tmp_path):
 @pytest.mark.parametrize("name", sorted(SCHED_MUTANTS))
 def test_planted_scheduler_mistake_is_caught(tmp_path, name):
     rc, out = _run_sched_pins(_sched_copy(tmp_path, name, SCHED_MUTANTS[name]))
+    assert rc != 0, f"mistake {name} survived every pin: {out}"
+
+
+# Mistakes in the interpolated communication latency, against test_oracle_comm_tables.py.
+TAB_MUTANTS = {
+    # (moving to the next segment at a sample volume is no mistake: the
+    # interpolant is continuous there; skipping the search is)
+    "first_segment_everywhere": ("while (k < tb->K - 1 && v > tb->vol[k]) ++k;", "(void)k;"),
+    "start_up_cost_when_nothing_moves": ("if (!(v > 0.0)) return 0.0;", "if (!(v >= 0.0)) return 0.0;"),
+    "tp_allreduce_count_two": (
+        "v += kappa * (4.0 * tab_lat(&tabs[0], 2.0 * (double)(tp - 1) / (double)tp * b * (double)jb->x[l]));",
+        "v += kappa * (2.0 * tab_lat(&tabs[0], 2.0 * (double)(tp - 1) / (double)tp * b * (double)jb->x[l]));"),
+    "all_to_all_on_intra_link": ("v += kappa * tab_lat(&tabs[1], b * (double)jb->a2a[l]);",
+                                 "v += kappa * tab_lat(&tabs[0], b * (double)jb->a2a[l]);"),
+    "p2p_one_direction": ("if (k < pp - 1) p2p = kappa * (2.0 * tab_lat(t_pp, b * (double)jb->x[hi - 1]));",
+                          "if (k < pp - 1) p2p = kappa * tab_lat(t_pp, b * (double)jb->x[hi - 1]);"),
+    "allreduce_volume_not_split_by_tp": (
+        "if (dp > 1) AR = kappa * tab_lat(t_dp, 2.0 * (double)(dp - 1) / (double)dp * (Pk / (double)tp));",
+        "if (dp > 1) AR = kappa * tab_lat(t_dp, 2.0 * (double)(dp - 1) / (double)dp * Pk);"),
+    "pipeline_link_always_intra": ("const otab* t_pp = (n <= ty->gpn) ? &tabs[0] : &tabs[1];",
+                                   "const otab* t_pp = &tabs[0];"),
+    "partition_with_m_ignored": ("double b = (double)jb->Bg / (double)(dp * m);\n    layer_costs_tab",
+                                 "double b = (double)jb->Bg / (double)dp;\n    layer_costs_tab"),
+}
+
+
+def _run_tab_pins(lib):
+    env = dict(os.environ, ARENA_ORACLE_LIB=lib)
+    try:
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                            "-p", "no:xdist", os.path.join(ROOT, "tests", "test_oracle_comm_tables.py")],
+                           capture_output=True, text=True, timeout=300, env=env, cwd=ROOT)
+    except subprocess.TimeoutExpired:
+        return None, "timed out"
+    return r.returncode, (r.stdout + r.stderr)[-2000:]
+
+
+def test_unmodified_copy_passes_the_table_pins(tmp_path):
+    rc, out = _run_tab_pins(_build(tmp_path, "tab_control", None))
+    assert rc == 0, out
+
+
+@pytest.mark.parametrize("name", sorted(TAB_MUTANTS))
+def test_planted_table_mistake_is_caught(tmp_path, name):
+    rc, out = _run_tab_pins(_build(tmp_path, "tab_" + name, TAB_MUTANTS[name]))
     assert rc != 0, f"mistake {name} survived every pin: {out}"
