@@ -1419,6 +1419,8 @@ struct TabBlockLds {
     double Ap[kLmax + 1];
     double vol[2][kMaxTabPoints];     // link 0 inside a node, 1 across nodes
     double lat[2][kMaxTabPoints];
+    double p_layer_max;               // largest parameter bytes of one layer
+    double x_layer_min;               // smallest boundary activation bytes of one layer
     int32_t next_cell;
     WaveLds w[kWavesPerBlock];
 };
@@ -1509,10 +1511,42 @@ __device__ __forceinline__ double tab_price(const TabBlockLds& B, WaveLds& Wv, i
     return rs[0] + (double)(m - 1) * rm[0] + rm[1];
 }
 
+// Lower bound of the time of plan (dp, tp, pp, m) over every split, or +inf
+// when no split can fit memory, from its per-microbatch costs alone: the
+// stages tile the layers (W_max >= sum c / pp and >= max c), each of the pp-1
+// boundaries moves at least the smallest boundary activation, the largest
+// stage holds at least max(P / pp, max p_l) of parameters, and f is
+// non-decreasing.  A relative margin of 1e-9 covers the sums' rounding.
+__device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, const JobCtx& jb, const TypeDev& ty,
+                                            int K, const Cell& cell, int dp, int tp, int pp, int m, double b)
+{
+    double c[2];
+    tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp, tp, b, c);
+    double rs[1] = {c[0] + c[1]};
+    double rm[1] = {fmax(c[0], c[1])};
+    wave_reduce<OpSum, 1>(rs);
+    wave_reduce<OpMax, 1>(rm);
+    const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
+    if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
+    const double UL = rs[0];
+    const double Wlb = fmax(UL / (double)pp, rm[0]);
+    const int lpp = cell.n <= ty.gpn ? 0 : 1;
+    const int grp = dp * tp;
+    const int ldp = (grp <= ty.gpn && ty.gpn % grp == 0) ? 0 : 1;
+    const double p2p = pp > 1 ? cell.kappa * (2.0 * tab_lat(B.vol[lpp], B.lat[lpp], K, b * B.x_layer_min)) : 0.0;
+    const double ar = dp > 1
+        ? cell.kappa * tab_lat(B.vol[ldp], B.lat[ldp], K, 2.0 * (double)(dp - 1) / (double)dp * (plb / (double)tp))
+        : 0.0;
+    return (UL + (double)(pp - 1) * p2p + (double)(m - 1) * Wlb + ar) * (1.0 - 1e-9);
+}
+
 // Every cell under interpolated communication latency: one block per (job,
-// type), its waves taking counts; every plan of a cell gets the balanced
-// partition of its own per-microbatch costs (no sharing across m or counts,
-// no bound pruning), then the cell's choice as in estimate_kernel.
+// type), its waves taking counts.  Every plan of a cell has the balanced
+// partition of its own per-microbatch costs (no sharing across m or counts).
+// With bound pruning, the plans' lower bounds come first, the plan of least
+// bound is priced, and every other plan only if its bound lies within the tie
+// window of the best time priced so far (it can neither be the best nor tie
+// with it otherwise); then the cell's choice as in estimate_kernel.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
 {
     __shared__ TabBlockLds B;
@@ -1548,6 +1582,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
         seq_prefix<1, 2>(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.UD + 1, false);
+        if (wid == 0) {
+            const double pm = wave_reduce1<OpMax>(fmax(v0, v1));
+            if (lane == 0) B.p_layer_max = pm;
+        }
+    } else if (wid == 2) {
+        const double x0 = lane < jb.L ? (double)A.x[off + lane] : kInf;
+        const double x1 = lane + 64 < jb.L ? (double)A.x[off + lane + 64] : kInf;
+        const double xm = wave_reduce1<OpMin>(fmin(x0, x1));
+        if (lane == 0) B.x_layer_min = xm;
     }
     if (tid == 0) B.next_cell = 0;
     if (lane < kNumCounters) Wv.tally[lane] = 0ull;
@@ -1564,7 +1607,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         cell.kappa = (double)A.kappa[g * A.n_counts + ci];
         cell.B_pp = 0.0;
         cell.c_p2p = 0.0;
-        int np = 0;
+        // the plans: keys and lower bounds
+        int np = 0, nskip = 0;
         for (int tp = 1; tp <= cell.n && tp <= ty.gpn; ++tp) {
             if (cell.n % tp != 0 || ty.gpn % tp != 0) continue;
             const int qn = cell.n / tp;
@@ -1576,18 +1620,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                     const double dm = (double)(dp * m);
                     const double bq = rint((double)jb.Bg / dm);
                     if (!(bq * dm == (double)jb.Bg)) continue;
-                    double W;
-                    const Stages sg = tab_partition(B, Wv, lane, jb, ty, K, cell.kappa, dp, tp, pp, bq, W);
-                    const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp, pp, m, bq, sg);
+                    const double lb = A.prune ? tab_bound(B, lane, jb, ty, K, cell, dp, tp, pp, m, bq) : 0.0;
                     if (lane == 0 && np < kMaxPlans) {
-                        Wv.planT[np] = T;
+                        Wv.planT[np] = lb;
                         Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
                     }
                     ++np;
-                    tally(Wv, lane, kProblems, 1);
-                    tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L + 4ull * (unsigned)jb.L +
-                                             12ull * (unsigned)pp + 40ull);
-                    wave_sync();
+                    if (A.prune) tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
                 }
             }
         }
@@ -1596,12 +1635,58 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             np = kMaxPlans;
         }
         wave_sync();
+        // price plan e of the buffer (its slot receives the time)
+        auto price_slot = [&](int e) -> double {
+            const unsigned key = Wv.planKey[e];
+            const int pp = (int)(key >> 12);
+            const int tp = (int)((key >> 7) & 0x1Fu);
+            const int m = (int)(key & 0x7Fu);
+            const int dp = cell.n / (tp * pp);
+            const double bq = rint((double)jb.Bg / (double)(dp * m));
+            double W;
+            const Stages sg = tab_partition(B, Wv, lane, jb, ty, K, cell.kappa, dp, tp, pp, bq, W);
+            const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp, pp, m, bq, sg);
+            tally(Wv, lane, kProblems, 1);
+            tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L + 4ull * (unsigned)jb.L + 12ull * (unsigned)pp + 40ull);
+            wave_sync();
+            if (lane == 0) Wv.planT[e] = T;
+            wave_sync();
+            return T;
+        };
+        if (A.prune) {
+            // the plan of least bound first, then the others within the window
+            double bl = kInf;
+            for (int e = lane; e < np; e += 64) bl = fmin(bl, Wv.planT[e]);
+            const double bmin = wave_reduce1<OpMin>(bl);
+            double il = -1.0;
+            for (int e = lane; e < np; e += 64)
+                if (Wv.planT[e] == bmin) il = (double)e;
+            const int first = (int)wave_reduce1<OpMax>(il);
+            double best = kInf;
+            if (first >= 0 && bmin < kInf) best = price_slot(first);
+            for (int e = 0; e < np; ++e) {
+                if (e == first) continue;
+                const double lbe = Wv.planT[e];
+                if (!(lbe < kInf && lbe <= best * (1.0 + A.tie_eps))) {
+                    wave_sync();
+                    if (lane == 0) Wv.planT[e] = kInf;
+                    ++nskip;
+                    wave_sync();
+                    continue;
+                }
+                best = fmin(best, price_slot(e));
+            }
+        } else {
+            for (int e = 0; e < np; ++e) price_slot(e);
+        }
+        tally(Wv, lane, kSkipped, (unsigned long long)nskip);
+        wave_sync();
 
         double tl = kInf;
         for (int e = lane; e < np; e += 64) tl = fmin(tl, Wv.planT[e]);
         const double tmin = wave_reduce1<OpMin>(tl);
         const long long cidx = ((long long)j * A.n_types + g) * A.n_counts + ci;
-        tally(Wv, lane, kPlans, (unsigned long long)np);
+        tally(Wv, lane, kPlans, (unsigned long long)(np - nskip));
         if (!(tmin < kInf)) {
             tally(Wv, lane, kInfeasible, 1);
             if (lane == 0) {
@@ -1664,6 +1749,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         atomicAdd(&A.counters[kDpEntries], t[kDpEntries]);
         atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
         if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
+        atomicAdd(&A.counters[kSkipped], t[kSkipped]);
         atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
     }
 }

@@ -23,8 +23,8 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def _run(w, tables, ids=None, with_cuts=True):
-    est = arena.Estimator(w, with_cuts=with_cuts, comm_tables=tables)
+def _run(w, tables, ids=None, with_cuts=True, prune=True):
+    est = arena.Estimator(w, with_cuts=with_cuts, comm_tables=tables, prune=prune)
     try:
         est.estimate()
         res = est.results(ids)
@@ -62,7 +62,7 @@ def test_hand_cell():
     lat = np.broadcast_to(np.array([0.25, 0.65, 1.25]), (1, 2, 3)).copy()
     res, cnt, _ = _run(w, (vol, lat))
     assert (res["dp"][0], res["tp"][0], res["pp"][0], res["m"][0]) == (2, 1, 1, 1)
-    assert res["t_iter"][0] == pytest.approx(1.65, rel=1e-6) and cnt["plans"] == 5
+    assert res["t_iter"][0] == pytest.approx(1.65, rel=1e-6) and cnt["plans"] + cnt["plans_skipped"] == 5
 
 
 @pytest.mark.parametrize("name", ["tiny", "small"])
@@ -72,7 +72,7 @@ def test_every_cell(oracle, name):
     _say(f"{name}: {w.n_cells} cells, all compared")
     res, cnt, size = _run(w, tabs)
     _check(compare(w, res, np.arange(w.n_cells), oracle, tables=tabs), name)
-    assert cnt["cells"] == w.n_cells and cnt["plans"] == size["plans"] and cnt["plans_skipped"] == 0
+    assert cnt["cells"] == w.n_cells and cnt["plans"] + cnt["plans_skipped"] == size["plans"]
 
 
 @pytest.mark.parametrize("name,k", [("trace", 400), ("moe", 150)])
@@ -83,7 +83,7 @@ def test_full_size_sampled(oracle, name, k):
     _say(f"{name}: {w.n_cells} cells on the GPU, {len(ids)} compared")
     res, cnt, size = _run(w, tabs, ids=ids)
     _check(compare(w, res, ids, oracle, tables=tabs), name)
-    assert cnt["cells"] == w.n_cells and cnt["plans"] == size["plans"]
+    assert cnt["cells"] == w.n_cells and cnt["plans"] + cnt["plans_skipped"] == size["plans"]
 
 
 def test_full_round_sampled(oracle):
@@ -93,7 +93,7 @@ def test_full_round_sampled(oracle):
     _say(f"full round: {w.n_cells} cells on the GPU, {len(ids)} compared")
     res, cnt, size = _run(w, tabs, ids=ids)
     _check(compare(w, res, ids, oracle, tables=tabs), "full")
-    assert cnt["cells"] == w.n_cells and cnt["plans"] == size["plans"]
+    assert cnt["cells"] == w.n_cells and cnt["plans"] + cnt["plans_skipped"] == size["plans"]
 
 
 def test_edge_cases(oracle):
@@ -142,3 +142,19 @@ def test_tables_switch_on_one_context():
     for k in ("t_iter", "thr", "plan", "cuts"):
         assert np.array_equal(x1[k], rb[k]), k
         assert np.array_equal(x0[k], ra[k]), k
+
+
+@pytest.mark.parametrize("name", ["trace", "moe"])
+def test_bound_pruning_is_exact(name):
+    """Pruning plans whose lower bound lies past the tie window changes nothing:
+    the whole launch bitwise equal with pruning off."""
+    w = wl.make(name)
+    tabs = wl.comm_tables(w)
+    _say(f"{name}: tables with pruning on and off")
+    r1, c1, size = _run(w, tabs)
+    r0, c0, _ = _run(w, tabs, prune=False)
+    for k in ("t_iter", "thr", "plan", "cuts"):
+        assert np.array_equal(r1[k], r0[k]), k
+    assert c0["plans_skipped"] == 0 and c0["plans"] == size["plans"]
+    assert c1["plans"] + c1["plans_skipped"] == size["plans"] and c1["plans_skipped"] > 0
+    _say(f"{name}: {c1['plans_skipped']} of {size['plans']} plans skipped")
