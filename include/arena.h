@@ -221,8 +221,9 @@ arena_status arena_set_partition_rule(arena_ctx* ctx, int32_t rule);
  *   DP all-reduce     f_dp(2 (dp-1)/dp P_k/tp)      per iteration, dp > 1
  * (b = Bg/(dp m); f_pp, f_dp on the links of the balanced model), and the
  * stage costs are per microbatch: each plan (dp, tp, pp, m) gets the
- * canonical balanced partition of its own per-microbatch layer costs, every
- * plan is priced (bound pruning does not apply), and the per-cell choice,
+ * canonical balanced partition of its own per-microbatch layer costs (with
+ * bound pruning, a plan whose lower bound lies past the tie window of a plan
+ * already priced is skipped; the results are the same), and the per-cell choice,
  * outputs and cut rows are as without tables.  Tables linear through the
  * origin reproduce the volume / bandwidth model.  Host arrays, copied;
  * uploaded by the next arena_estimate.  Needs grids bound (the tables follow
