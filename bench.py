@@ -306,7 +306,7 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}): "
-              "the estimator shards by job rows, but this build measures a single GPU.",
+              "the estimator shards by job rows, but this benchmark measures a single GPU.",
               file=sys.stderr, flush=True)
         return 2
 
