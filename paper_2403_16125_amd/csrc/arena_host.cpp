@@ -72,6 +72,8 @@ struct arena_ctx {
     bool order_dirty = true;
     unsigned long long* d_counters = nullptr;
     unsigned long long* h_counters = nullptr;   // pinned
+    unsigned long long* d_queue = nullptr;      // the estimate kernels' item queue
+    int n_cus = 0;
     float* h_kappa[2] = {nullptr, nullptr};     // pinned staging, double-buffered
     hipEvent_t kappa_done[2] = {nullptr, nullptr};
     size_t cap_hkappa = 0;
@@ -144,6 +146,8 @@ void free_device(arena_ctx* c)
     (void)hipFree(c->d_count_order);
     (void)hipFree(c->d_counters);
     (void)hipHostFree(c->h_counters);
+    (void)hipFree(c->d_queue);
+    c->d_queue = nullptr;
     (void)hipFree(c->d_msets);
     (void)hipFree(c->d_mset_off);
     (void)hipFree(c->d_hbm);
@@ -214,6 +218,10 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
             return e == hipErrorOutOfMemory ? fail(c, ARENA_ERR_OUT_OF_MEMORY, "counters") : hip_fail(c, e, "hipMalloc");
         if ((e = hipHostMalloc((void**)&c->h_counters, sizeof(unsigned long long) * arena::kNumCounters, 0)))
             return hip_fail(c, e, "hipHostMalloc");
+        if ((e = hipMalloc((void**)&c->d_queue, sizeof(unsigned long long))))
+            return e == hipErrorOutOfMemory ? fail(c, ARENA_ERR_OUT_OF_MEMORY, "queue") : hip_fail(c, e, "hipMalloc");
+        if ((e = hipDeviceGetAttribute(&c->n_cus, hipDeviceAttributeMultiprocessorCount, c->device)))
+            return hip_fail(c, e, "hipDeviceGetAttribute");
         for (int i = 0; i < 2; ++i)
             if ((e = hipEventCreateWithFlags(&c->kappa_done[i], hipEventDisableTiming)))
                 return hip_fail(c, e, "hipEventCreate");
@@ -318,6 +326,8 @@ arena_status upload_orders(arena_ctx* c, hipStream_t stream)
         }
         for (int g = 0; g < c->n_types; ++g) icost[(size_t)j * c->n_types + g] = it->second[g];
     }
+    // the kernels' resident blocks take items from a queue in this order:
+    // heaviest first, so the last items to start are the light ones
     std::vector<int32_t> iorder(items);
     std::iota(iorder.begin(), iorder.end(), 0);
     std::stable_sort(iorder.begin(), iorder.end(), [&](int a, int b) { return icost[a] > icost[b]; });
@@ -673,6 +683,10 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.n_counts = c->n_counts;
     A.item_order = c->d_item_order;
     A.count_order = c->d_count_order;
+    A.queue = c->d_queue;
+    A.n_items = c->n_jobs * c->n_types;
+    // one block per resident slot (four per CU); each takes items from the queue
+    A.n_blocks = std::min(A.n_items, 4 * std::max(c->n_cus, 1));
     A.share_tp = kappa_shared(c) ? 1 : 0;
     // ascending: the kernel bisects the microbatch counts for the memory limit
     std::vector<int32_t> ms(c->m_values);
@@ -693,7 +707,8 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.cuts = cuts;
     A.cuts_stride = cuts ? cuts_stride : 0;
     A.counters = c->d_counters;
-    if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)))
+    if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)) ||
+        (e = arena::launch_zero_counters(c->d_queue, 1, stream)))
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     return ARENA_OK;

@@ -38,6 +38,9 @@ struct EstimateArgs {
     const int32_t* counts;        // [NC]
     const float* kappa;           // [T*NC]
     const int32_t* item_order;    // [J*T] (job, type) items, most work first
+    unsigned long long* queue;    // [1] next item to take (zeroed before each launch)
+    int32_t n_items;              // J * T
+    int32_t n_blocks;             // resident blocks launched; each takes items until none is left
     const int32_t* count_order;   // [NC] count indices, largest count first
     int32_t n_jobs, n_types, n_counts;
     int32_t share_tp;             // some type has one kappa for all its counts: share tp problems

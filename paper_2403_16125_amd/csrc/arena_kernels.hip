@@ -1,6 +1,8 @@
 // HIP kernels of the plan-space estimator (gfx950 / CDNA4).
 //
-// A block of four 64-lane wavefronts owns one (job, GPU type) pair.
+// A block of four 64-lane wavefronts works on one (job, GPU type) pair at a
+// time; one block per resident slot is launched and each takes pairs from a
+// device queue, heaviest first, until none is left.
 //   set-up   the job's layer tables, parameter/activation prefix sums and the
 //            pure-compute cost prefix are staged in LDS once;
 //   shared   stage-partition problems that do not depend on the GPU count
@@ -1010,7 +1012,7 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
 // MEM: the memory-constrained partition rule (each wave has one more LDS
 // row for its recursion).
 template <int SLOTS, bool MEM>
-__device__ __forceinline__ void estimate_body(const EstimateArgs& A)
+__device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 {
     __shared__ BlockLds<SLOTS> B;
     const int tid = threadIdx.x;
@@ -1019,7 +1021,6 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A)
     WaveLds& Wv = B.w[wid];
     double* const R = MEM ? Wv.R : nullptr;
 
-    const int item = A.item_order[blockIdx.x];
     const bool stage = A.n_counts <= kStageCells;
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
@@ -1382,10 +1383,30 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A)
     }
 }
 
+// The (job, type) item a block works on next: the queue hands items out in
+// the host's order (heaviest first) to whichever resident block is free, so
+// the work balances over the CUs whatever the items really cost.  Returns
+// the item, or -1 once the queue is empty (every block then leaves).
+__device__ __forceinline__ int take_item(const EstimateArgs& A, int* slot)
+{
+    if (threadIdx.x == 0) {
+        const unsigned long long q = atomicAdd(A.queue, 1ull);
+        *slot = q < (unsigned long long)A.n_items ? A.item_order[q] : -1;
+    }
+    __syncthreads();
+    const int item = *slot;
+    __syncthreads();
+    return item;
+}
+
 template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
 {
-    estimate_body<SLOTS, false>(A);
+    __shared__ int slot;
+    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
+        estimate_body<SLOTS, false>(A, item);
+        __syncthreads();
+    }
 }
 
 // The memory rule's out-of-line solve raises register use; its kernel still
@@ -1395,7 +1416,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_mem_kernel(EstimateArgs A)
 {
-    estimate_body<SLOTS, true>(A);
+    __shared__ int slot;
+    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
+        estimate_body<SLOTS, true>(A, item);
+        __syncthreads();
+    }
 }
 
 // ------------------------------------------------------------ interpolated communication latency
@@ -1540,14 +1565,14 @@ __device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, cons
     return (UL + (double)(pp - 1) * p2p + (double)(m - 1) * Wlb + ar) * (1.0 - 1e-9);
 }
 
-// Every cell under interpolated communication latency: one block per (job,
-// type), its waves taking counts.  Every plan of a cell has the balanced
+// Every cell under interpolated communication latency: a block works on one
+// (job, type) at a time (taken from the queue), its waves taking counts.  Every plan of a cell has the balanced
 // partition of its own per-microbatch costs (no sharing across m or counts).
 // With bound pruning, the plans' lower bounds come first, the plan of least
 // bound is priced, and every other plan only if its bound lies within the tie
 // window of the best time priced so far (it can neither be the best nor tie
 // with it otherwise); then the cell's choice as in estimate_kernel.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
+__device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int item)
 {
     __shared__ TabBlockLds B;
     const int tid = threadIdx.x;
@@ -1555,7 +1580,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int wid = tid >> 6;
     WaveLds& Wv = B.w[wid];
 
-    const int item = A.item_order[blockIdx.x];
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
     const int off = A.layer_offset[j];
@@ -1754,6 +1778,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
 }
 
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
+{
+    __shared__ int slot;
+    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
+        estimate_tab_body(A, item);
+        __syncthreads();
+    }
+}
+
 __global__ void zero_kernel(unsigned long long* p, int n)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1781,9 +1814,8 @@ __global__ __launch_bounds__(64) void validate_kernel(ValidateArgs V)
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
 {
-    const long long blocks = (long long)args.n_jobs * args.n_types;
-    if (blocks <= 0) return hipSuccess;
-    const dim3 grid((unsigned)blocks), block(256);
+    if (args.n_items <= 0 || args.n_blocks <= 0) return hipSuccess;
+    const dim3 grid((unsigned)args.n_blocks), block(256);
     if (args.tab_k > 0) {
         hipLaunchKernelGGL(estimate_tab_kernel, grid, block, 0, stream, args);
     } else if (args.mem_rule) {
