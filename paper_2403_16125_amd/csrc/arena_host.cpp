@@ -72,7 +72,7 @@ struct arena_ctx {
     bool order_dirty = true;
     unsigned long long* d_counters = nullptr;
     unsigned long long* h_counters = nullptr;   // pinned
-    unsigned long long* d_queue = nullptr;      // the estimate kernels' item queue
+    unsigned long long* d_queue = nullptr;      // the estimate and proxy kernels' item queue
     int n_cus = 0;
     float* h_kappa[2] = {nullptr, nullptr};     // pinned staging, double-buffered
     hipEvent_t kappa_done[2] = {nullptr, nullptr};
@@ -855,6 +855,10 @@ arena_status arena_proxy_estimate(arena_ctx* c, const arena_proxy_desc* d, float
     A.t_iter = t_iter;
     A.thr = thr;
     A.plan = (unsigned long long*)plan;
+    A.queue = c->d_queue;
+    A.n_cus = c->n_cus;
+    if ((e = arena::launch_zero_counters(c->d_queue, 1, stream)))
+        return hip_fail(c, e, "proxy queue reset");
     if ((e = arena::launch_proxy(A, stream))) return hip_fail(c, e, "proxy launch");
     return ARENA_OK;
 }

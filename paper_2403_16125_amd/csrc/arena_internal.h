@@ -98,6 +98,8 @@ struct ProxyArgs {
     float* t_iter;
     float* thr;
     unsigned long long* plan;     // [C * kProxyPlanWords]
+    unsigned long long* queue;    // [1] next cell to take (zeroed before each launch)
+    int32_t n_cus;                // compute units: one launch fills them with resident blocks
 };
 
 hipError_t launch_proxy(const ProxyArgs& args, hipStream_t stream);

@@ -705,14 +705,22 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
     }
 }
 
-// Cells in a grid-stride loop: a launch covers at most kProxyMaxBlocks
-// workgroups (the dispatch's work-item count is a 32-bit quantity).
-constexpr int kProxyMaxBlocks = 1 << 20;
-
+// Resident blocks take cells from a device queue until none is left: a
+// dispatcher that places block b on XCD b % 8 in order would otherwise leave
+// CUs idle while a block waits for room on its XCD.
 __global__ __launch_bounds__(kPxThreads) void proxy_kernel(ProxyArgs A, int n_cells)
 {
     __shared__ ProxyLds S;
-    for (int cell = blockIdx.x; cell < n_cells; cell += gridDim.x) {
+    __shared__ int slot;
+    for (;;) {
+        if (threadIdx.x == 0) {
+            const unsigned long long q = atomicAdd(A.queue, 1ull);
+            slot = q < (unsigned long long)n_cells ? (int)q : -1;
+        }
+        __syncthreads();
+        const int cell = slot;
+        __syncthreads();
+        if (cell < 0) break;
         proxy_cell(A, S, cell);
         __syncthreads();          // the next cell reuses the LDS
     }
@@ -724,7 +732,11 @@ hipError_t launch_proxy(const ProxyArgs& args, hipStream_t stream)
 {
     const long long cells = (long long)args.n_jobs * args.n_types * args.n_counts;
     if (cells <= 0) return hipSuccess;
-    const unsigned blocks = (unsigned)(cells < kProxyMaxBlocks ? cells : kProxyMaxBlocks);
+    int per_cu = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, proxy_kernel, kPxThreads, 0);
+    if (e != hipSuccess) return e;
+    const long long resident = (long long)(args.n_cus > 0 ? args.n_cus : 1) * (per_cu > 0 ? per_cu : 1);
+    const unsigned blocks = (unsigned)(cells < resident ? cells : resident);
     hipLaunchKernelGGL(proxy_kernel, dim3(blocks), dim3(kPxThreads), 0, stream, args, (int)cells);
     return hipGetLastError();
 }
