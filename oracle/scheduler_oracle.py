@@ -36,6 +36,21 @@ S8  Deadline constraint (Eq. 6), when per-job batch B_i, remaining
     scale-ups (S6: a larger open count).  A running job outside its deadline
     is not moved for it.
 
+S9  Finish-time fairness objective (Eq. 7), when asked for, with per-job
+    batch B_i and remaining iterations N_i (deadlines optional): the
+    allocation indicator in the denominator is read as selecting the job's
+    grid, and the resource measure Q of a grid as its GPU count, so a job
+    running at throughput thr on n GPUs has rho = N_i T / n with T = B_i /
+    thr, i.e. rho = B_i N_i / (thr n) in float64 (+inf at thr = 0).  The
+    objective minimises the largest rho, so the two searches of Algorithm 1
+    change their keys: GetOptimalScaleDown moves the job whose rho after
+    its step down is smallest (same candidates as S3; ties: the lower job
+    id); GetOptimalScaleUp takes, for each running job, the larger count
+    within the free GPUs (and open, under S8) that minimises its rho (ties:
+    the smaller count), kept only if that rho is below its current one, and
+    moves the job whose current rho is largest (ties: the lower job id).
+    Launches (S2) and everything else are unchanged.
+
 Returns the new allocation, which queued jobs launched, the move counts
 (scale-downs kept, launches, scale-ups) and the number of searches made
 (launch, scale-down and scale-up: the decisions of the step).
@@ -70,9 +85,15 @@ def launch_grid(thr_j, counts, free, work=0.0, ddl=None):
     return None if best is None else (best[1], best[2])
 
 
-def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types, dl=None):
+def _rho(v, n, work):
+    """S9: B N / (thr n) of a job with work B N at throughput v on n GPUs."""
+    return work / (v * float(n)) if v > 0.0 else float("inf")
+
+
+def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types, dl=None, fair=False):
     """S3: (cost, job, new count index) of the cheapest scale-down, or None.
-    dl(i) -> (work, deadline) of job i under S8."""
+    dl(i) -> (work, deadline) of job i under S8 (deadline None: none); with
+    fair (S9) the cost is the job's rho after the step."""
     best = None
     for i in range(len(alloc_type)):
         g = int(alloc_type[i])
@@ -85,14 +106,18 @@ def scale_down_move(thr, counts, alloc_type, alloc_count, usable_types, dl=None)
             c2 -= 1
         if c2 < 0:
             continue
-        cost = (float(thr[i][g][c]) - float(thr[i][g][c2])) / float(int(counts[c]) - int(counts[c2]))
+        if fair:
+            cost = _rho(float(thr[i][g][c2]), int(counts[c2]), work)
+        else:
+            cost = (float(thr[i][g][c]) - float(thr[i][g][c2])) / float(int(counts[c]) - int(counts[c2]))
         if best is None or cost < best[0]:
             best = (cost, i, c2)
     return best
 
 
-def scale_up_move(thr, counts, alloc_type, alloc_count, free, dl=None):
-    """S6: (gain, job, new count index) of the best scale-up, or None."""
+def scale_up_move(thr, counts, alloc_type, alloc_count, free, dl=None, fair=False):
+    """S6: (gain, job, new count index) of the best scale-up, or None; with
+    fair (S9): (current rho, job, new count index) of the job moved."""
     best = None
     for i in range(len(alloc_type)):
         g = int(alloc_type[i])
@@ -102,6 +127,19 @@ def scale_up_move(thr, counts, alloc_type, alloc_count, free, dl=None):
         c = int(alloc_count[i])
         n, t = int(counts[c]), float(thr[i][g][c])
         mine = None
+        if fair:
+            r0 = _rho(t, n, work)
+            for c2 in range(c + 1, len(counts)):
+                if int(counts[c2]) - n > free[g]:
+                    break
+                t2 = float(thr[i][g][c2])
+                if _open(t2, work, ddl):
+                    r2 = _rho(t2, int(counts[c2]), work)
+                    if mine is None or r2 < mine[0]:
+                        mine = (r2, c2)
+            if mine is not None and mine[0] < r0 and (best is None or r0 > best[0]):
+                best = (r0, i, mine[1])
+            continue
         for c2 in range(c + 1, len(counts)):
             dn = int(counts[c2]) - n
             if dn > free[g]:
@@ -117,8 +155,9 @@ def scale_up_move(thr, counts, alloc_type, alloc_count, free, dl=None):
 
 
 def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, depth,
-             batch=None, iters=None, deadline=None):
-    """One scheduling step (Algorithm 1, readings S1-S6; S8 with deadlines)."""
+             batch=None, iters=None, deadline=None, objective="throughput"):
+    """One scheduling step (Algorithm 1, readings S1-S6; S8 with deadlines;
+    S9 with objective "fairness", which needs batch and iters)."""
     alloc_type = [int(v) for v in alloc_type]
     alloc_count = [int(v) for v in alloc_count]
     for k in range(1, len(counts)):
@@ -131,16 +170,26 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
         raise ValueError("queued jobs must be distinct and not running")
     if any(int(p) < 0 for p in priority):
         raise ValueError("priority classes must be >= 0")
+    if objective not in ("throughput", "fairness"):
+        raise ValueError("objective must be 'throughput' or 'fairness'")
+    fair = objective == "fairness"
     given = [v is not None for v in (batch, iters, deadline)]
-    if any(given) and not all(given):
+    if fair and not (given[0] and given[1]):
+        raise ValueError("the fairness objective needs batch and iters")
+    if not fair and any(given) and not all(given):
         raise ValueError("give batch, iters and deadline together or none")
     dl = None
-    if all(given):
+    if given[0] and given[1]:
         for i in range(len(alloc_type)):
-            b, it, d = int(batch[i]), float(iters[i]), float(deadline[i])
-            if b <= 0 or not (it >= 0.0) or it == float("inf") or not (d > 0.0):
+            b, it = int(batch[i]), float(iters[i])
+            if b <= 0 or not (it >= 0.0) or it == float("inf"):
                 raise ValueError("bad deadline values")
-        dl = lambda i: (float(int(batch[i])) * float(iters[i]), float(deadline[i]))
+            if deadline is not None and not (float(deadline[i]) > 0.0):
+                raise ValueError("bad deadline values")
+        if deadline is not None:
+            dl = lambda i: (float(int(batch[i])) * float(iters[i]), float(deadline[i]))
+        else:
+            dl = lambda i: (float(int(batch[i])) * float(iters[i]), None)
     n_types = len(free)
     launched = [0] * len(queue)
     kept_down = launches = 0
@@ -165,7 +214,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
             if len(log) >= depth:
                 grid = None
             else:
-                mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable, dl)
+                mv = scale_down_move(thr, counts, alloc_type, alloc_count, usable, dl, fair)
                 decisions += 1
                 if mv is not None:
                     _, i, c2 = mv
@@ -187,7 +236,7 @@ def schedule(thr, counts, capacity, alloc_type, alloc_count, queue, priority, de
                 break
     ups = 0
     while ups < depth:
-        mv = scale_up_move(thr, counts, alloc_type, alloc_count, free, dl)
+        mv = scale_up_move(thr, counts, alloc_type, alloc_count, free, dl, fair)
         decisions += 1
         if mv is None:
             break

@@ -214,6 +214,14 @@ SCHED_MUTANTS = {
     "deadline_strict": ("work / v <= ddl", "work / v < ddl"),
     "scale_up_to_equal_throughput": ("if t2 > t and _open(t2, work, ddl):", "if t2 >= t and _open(t2, work, ddl):"),
     "no_priority_allowance": ("lam = max((int(p) for p in priority), default=0) + 1", "lam = 0"),
+    "fair_up_helps_the_best_off": ("(best is None or r0 > best[0])", "(best is None or r0 < best[0])"),
+    "fair_up_without_improvement": ("if mine is not None and mine[0] < r0 and", "if mine is not None and"),
+    "fair_rho_not_per_gpu": ("return work / (v * float(n)) if v > 0.0", "return work / v if v > 0.0"),
+    "fair_target_tie_larger": ("if mine is None or r2 < mine[0]:", "if mine is None or r2 <= mine[0]:"),
+    "fair_down_rho_before_the_step": ("cost = _rho(float(thr[i][g][c2]), int(counts[c2]), work)",
+                                      "cost = _rho(float(thr[i][g][c]), int(counts[c]), work)"),
+    "fair_down_throughput_cost": ("        if fair:\n            cost = _rho(", "        if not fair:\n            cost = _rho("),
+    "fair_up_ignores_deadline": ("if _open(t2, work, ddl):\n                    r2", "if t2 > 0.0:\n                    r2"),
 }
 
 

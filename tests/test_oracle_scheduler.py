@@ -242,3 +242,119 @@ def test_deadline_invariants_on_random_states(seed):
         if st.alloc_type[j] >= 0 and r["alloc_count"][j] != st.alloc_count[j]:
             v = float(st.thr[j, r["alloc_type"][j], r["alloc_count"][j]])
             assert float(B[j]) * float(N[j]) / v <= float(D[j])
+
+
+# ---------------------------------------------------------------- Eq. 7 (S9)
+# rho = B N / (thr n): the finish-time-fairness ratio of a job on n GPUs.
+
+def test_fairness_scale_up_helps_the_worst_job():
+    # job 0: B N = 100 at 10 samples/s on 1 GPU -> rho 10; job 1: B N = 20 at 1/s -> rho 20.
+    # Eq. 5 moves job 0 first (gain 9/GPU to 2 GPUs vs job 1's 0.5); Eq. 7 moves job 1, the
+    # worst, to the count with its least rho: 2 GPUs 20 / 3 = 6.67, 4 GPUs 20 / 7.2 = 2.78.
+    thr = _thr({0: [[10, 19, 36]], 1: [[1, 1.5, 1.8]]})
+    kw = dict(batch=[1, 1], iters=[100.0, 20.0])
+    r = so.schedule(thr, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 1)
+    assert r["alloc_count"] == [1, 0]
+    r = so.schedule(thr, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 1, objective="fairness", **kw)
+    assert r["alloc_count"] == [0, 2] and r["moves"] == [0, 0, 1] and r["free"] == [1]
+    # depth 3: then job 0 (rho 10) takes the last GPU (100 / 38 = 2.63); job 1 (2.78) is now
+    # the worst but at its largest count, and nothing is free: the third search finds nothing
+    r = so.schedule(thr, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 3, objective="fairness", **kw)
+    assert r["alloc_count"] == [1, 2] and r["moves"] == [0, 0, 2] and r["free"] == [0]
+    assert r["decisions"] == 3
+
+
+def test_fairness_scale_down_takes_from_the_least_harmed():
+    # 8 GPUs all busy, job 2 needs 1.  Eq. 5 shrinks job 0 (loses 0.5/GPU vs job 1's 0.6/GPU);
+    # Eq. 7 shrinks the job whose rho after the step is smallest: job 1, 137.6 / (40 * 2) = 1.720
+    # against job 0's 100 / (29 * 2) = 1.724 -- though job 1's rho before the step is the larger
+    # (137.6 / (41.2 * 4) = 0.835 vs 100 / (30 * 4) = 0.833).  Job 2 then launches on 2 GPUs.
+    thr = _thr({0: [[10, 29, 30]], 1: [[5, 40, 41.2]], 2: [[1, 2, 3]]})
+    args = ([1, 2, 4], [8], [0, 0, -1], [2, 2, 0], [2], [0], 4)
+    r = so.schedule(thr, *args)
+    assert r["alloc_count"][:2] == [1, 2]
+    r = so.schedule(thr, *args, batch=[1, 1, 1], iters=[100.0, 137.6, 5.0], objective="fairness")
+    assert r["alloc_count"] == [2, 1, 1] and r["alloc_type"] == [0, 0, 0]
+    assert r["launched"] == [1] and r["moves"] == [1, 1, 0] and r["decisions"] == 4
+
+
+def test_fairness_target_ties_go_to_the_smaller_count():
+    # thr * n = 4, 6, 6: rho on 2 and on 4 GPUs is exactly 1 (B N = 6): the smaller count
+    thr = _thr({0: [[4, 3, 1.5]]})
+    r = so.schedule(thr, [1, 2, 4], [4], [0], [0], [], [], 1, batch=[2], iters=[3.0], objective="fairness")
+    assert r["alloc_count"] == [1] and r["moves"] == [0, 0, 1]
+
+
+def test_fairness_moves_only_when_rho_falls_and_ties_go_to_the_lower_job():
+    # no work left (N = 0): rho is 0 on every grid, nothing improves, nothing moves
+    thr = _thr({0: [[1, 2, 4]], 1: [[1, 2, 4]]})
+    r = so.schedule(thr, [1, 2, 4], [8], [0, 0], [0, 0], [], [], 4, batch=[1, 1], iters=[0.0, 0.0],
+                    objective="fairness")
+    assert r["alloc_count"] == [0, 0] and r["moves"] == [0, 0, 0]
+    # equal rho (B N = 8 on 1 GPU at 1/s): job 0 moves first, to 4 GPUs (rho 0.5); one GPU is
+    # left, so job 1 goes to 2 GPUs (rho 2) -- 4 would need 3 more
+    r = so.schedule(thr, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 4, batch=[1, 1], iters=[8.0, 8.0],
+                    objective="fairness")
+    assert r["alloc_count"] == [2, 1] and r["moves"] == [0, 0, 2]
+
+
+def test_fairness_with_a_deadline_scales_up_within_it():
+    # the tie of the previous test broken by a deadline: job 1 may only finish in time on 4 GPUs
+    # (8 / 4 = 2 s <= 2.5 s), which does not fit after job 0's move; with 6 free it would
+    thr = _thr({0: [[1, 2, 4]], 1: [[1, 2, 4]]})
+    kw = dict(batch=[1, 1], iters=[8.0, 8.0], deadline=[1e9, 2.5], objective="fairness")
+    r = so.schedule(thr, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 4, **kw)
+    assert r["alloc_count"] == [2, 0] and r["moves"] == [0, 0, 1]
+
+
+def test_fairness_needs_work_and_checks_the_objective():
+    thr = _thr({0: [[1, 2]], 1: [[1, 2]]})
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [0], [0], 1, objective="fairness")
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [0], [0], 1, batch=[1, 1], objective="fairness")
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [0], [0], 1, objective="makespan")
+    with pytest.raises(ValueError):
+        so.schedule(thr, [1, 2], [4], [-1, -1], [0, 0], [0], [0], 1, batch=[1, 1], iters=[-1.0, 1.0],
+                    objective="fairness")
+
+
+def _rho_all(st, r, B, N):
+    out = []
+    for j in range(st.n_jobs):
+        g = r["alloc_type"][j]
+        if g >= 0:
+            v = float(st.thr[j, g, r["alloc_count"][j]])
+            out.append(float(B[j]) * float(N[j]) / (v * st.counts[r["alloc_count"][j]]) if v > 0 else np.inf)
+    return out
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_fairness_invariants_on_random_states(seed):
+    counts = [1, 2, 4, 8, 16, 32]
+    thr = ss.synthetic_thr(seed, 80, 3, counts)
+    st = ss.random_state(seed, thr, counts, [40, 24, 16], running_frac=0.6, queued_frac=0.3, depth=4)
+    B, N, _ = ss.deadlines(seed, st.thr)
+    r = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue, st.priority,
+                    st.depth, batch=B, iters=N, objective="fairness")
+    used = np.zeros(3, np.int64)
+    for j in range(st.n_jobs):
+        g = r["alloc_type"][j]
+        if g >= 0:
+            used[g] += counts[r["alloc_count"][j]]
+            if st.alloc_type[j] >= 0:
+                assert g == st.alloc_type[j]
+    assert list(used + np.asarray(r["free"])) == list(st.capacity) and min(r["free"]) >= 0
+    # without a queue every move lowers the rho of one job: the largest rho never rises
+    r0 = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, [], [], 1,
+                     batch=B, iters=N, objective="fairness")
+    before = _rho_all(st, dict(alloc_type=list(st.alloc_type), alloc_count=list(st.alloc_count)), B, N)
+    prev = max(before)
+    for d in range(1, 6):
+        rd = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, [], [], d,
+                         batch=B, iters=N, objective="fairness")
+        now = max(_rho_all(st, rd, B, N))
+        assert now <= prev
+        prev = now
+    assert r0["moves"][2] in (0, 1)
