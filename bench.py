@@ -8,8 +8,9 @@ device memory before timing starts.  Prints one JSON line on stdout; progress
 goes to stderr.
 
 With --schedule it times instead the scheduling step that consumes such a
-matrix (Algorithm 1 with the throughput objective) on a 1280-GPU cluster
-state over the same 16384 x 8 x 131 shape, and prints that line.  With
+matrix (Algorithm 1 with the throughput objective, or with --objective
+fairness the finish-time fairness objective) on a 1280-GPU cluster state over
+the same 16384 x 8 x 131 shape, and prints that line.  With
 --proxy it times the proxy-plan planner (Sec. 3.3) over every cell of the
 trace-like workload and scores its plans against the exhaustive estimate.
 With --partition memory the estimate prices each plan with the balanced
@@ -74,14 +75,15 @@ def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None
                       f"{len(ids)} cells in {dt:.1f} s"}
 
 
-def schedule_cpu_baseline(st, min_seconds: float = 10.0) -> dict:
+def schedule_cpu_baseline(st, min_seconds: float = 10.0, objective: str = "throughput", work=None) -> dict:
     """The scheduler oracle (single-threaded Python) on the same state,
     repeated until about min_seconds of CPU work."""
     from oracle import scheduler_oracle as so
+    kw = {} if work is None else dict(batch=work[0], iters=work[1])
     n, t0 = 0, time.perf_counter()
     while True:
         so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
-                    st.priority, st.depth)
+                    st.priority, st.depth, objective=objective, **kw)
         n += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds and n >= 2:
@@ -190,8 +192,9 @@ def bench_proxy(args) -> int:
 
 
 def bench_schedule(args) -> int:
-    """One step = one scheduling step (Algorithm 1, throughput objective) on
-    the full-round state, from the same starting allocation every time."""
+    """One step = one scheduling step (Algorithm 1, throughput or fairness
+    objective) on the full-round state, from the same starting allocation
+    every time."""
     import numpy as np
     import torch
 
@@ -203,7 +206,13 @@ def bench_schedule(args) -> int:
     log(f"{J} jobs x {T} types x {NC} counts, {int((st.alloc_type >= 0).sum())} running, "
         f"{len(st.queue)} queued, depth {st.depth}")
     dev = torch.device("cuda", 0)
-    sch = arena.Scheduler(st.thr, st.counts, st.capacity, device=0)
+    sch = arena.Scheduler(st.thr, st.counts, st.capacity, device=0, objective=args.objective)
+    work = None
+    if args.objective == "fairness":
+        # each job's batch and remaining iterations (the deadline recipe's; no deadline)
+        B, N, _ = sched_states.deadlines(11, st.thr, slack=(0.9, 4.0))
+        work = (B, N)
+        sch.set_deadlines(B, N, None)
     sch.load_state(st.alloc_type, st.alloc_count, st.queue, st.priority)
     at0, ac0 = sch.alloc_type.clone(), sch.alloc_count.clone()
     stream = torch.cuda.current_stream(dev)
@@ -254,6 +263,8 @@ def bench_schedule(args) -> int:
             "workload": f"scheduling step over the full-round throughput matrix: {J} jobs x {T} GPU types "
                         f"x {NC} GPU counts, 1280-GPU cluster, {int((st.alloc_type >= 0).sum())} running, "
                         f"{len(st.queue)} queued in 3 classes, search depth {st.depth}",
+            "objective": "throughput (Eq. 5)" if args.objective == "throughput" else
+                         "finish-time fairness (Eq. 7)",
         },
         "decisions": res["decisions"],
         "ns_per_decision": step_s / max(1, res["decisions"]) * 1e9,
@@ -272,7 +283,7 @@ def bench_schedule(args) -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the scheduler oracle on the same state")
-        line["cpu_baseline"] = schedule_cpu_baseline(st)
+        line["cpu_baseline"] = schedule_cpu_baseline(st, objective=args.objective, work=work)
     print(json.dumps(line), flush=True)
     return 0
 
@@ -294,6 +305,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedule", action="store_true",
                     help="time the scheduling step that consumes the throughput matrix instead")
+    ap.add_argument("--objective", default="throughput", choices=["throughput", "fairness"],
+                    help="with --schedule, the scheduling objective")
     ap.add_argument("--proxy", action="store_true",
                     help="time the proxy-plan planner instead (trace-like workload unless --proxy-full)")
     ap.add_argument("--proxy-full", action="store_true", help="with --proxy, run it on the full round")

@@ -318,6 +318,10 @@ arena_status arena_proxy_estimate(arena_ctx* ctx, const arena_proxy_desc* d, flo
 #define ARENA_MAX_SCHED_DEPTH 256
 #define ARENA_MAX_SCHED_CAPACITY (1 << 24)   /* GPUs of one type */
 
+/* Scheduling objectives (arena_sched_desc.objective). */
+#define ARENA_SCHED_THROUGHPUT 0   /* Eq. 5: maximise the summed throughput */
+#define ARENA_SCHED_FAIRNESS 1     /* Eq. 7: minimise the largest finish-time-fairness ratio */
+
 /* One scheduling step over a throughput matrix (for instance the thr output
  * of arena_estimate): event-driven scheduling with the throughput objective
  * (Sec. 3.5, Algorithm 1, Eq. 5).  Queued jobs are visited in queue order;
@@ -361,6 +365,14 @@ typedef struct arena_sched_desc {
     const int32_t* batch;        /* DEVICE [n_jobs] global batch size, > 0 */
     const float* iters;          /* DEVICE [n_jobs] remaining iterations, finite >= 0 */
     const float* deadline;       /* DEVICE [n_jobs] seconds left to the deadline, > 0 (+inf: none) */
+    /* Objective: ARENA_SCHED_THROUGHPUT (the searches above) or ARENA_SCHED_FAIRNESS (Eq. 7, which
+     * needs batch and iters; deadline may then be NULL).  Under fairness a job at throughput thr on n
+     * GPUs has rho = batch iters / (thr n) (fp64; the grid's GPU count is the resource measure Q), and
+     * the searches rank by it: a scale-down moves the job whose rho after the step is least (ties:
+     * lower job id); a scale-up takes each running job's larger count within the free GPUs (and open,
+     * with deadlines) of least rho (ties: smaller count), if below its current rho, and moves the job
+     * whose current rho is largest (ties: lower job id).  Launches are as above. */
+    int32_t objective;
 } arena_sched_desc;
 
 /* Host checks (sizes, pointers, counts, capacity, depth) return an error

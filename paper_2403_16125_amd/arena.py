@@ -35,6 +35,9 @@ EXPORTED = (
 
 PARTITION_BALANCED = 0
 PARTITION_MEMORY = 1
+SCHED_THROUGHPUT = 0
+SCHED_FAIRNESS = 1
+_OBJECTIVES = {"throughput": SCHED_THROUGHPUT, "fairness": SCHED_FAIRNESS}
 
 MAX_PROXY_OPS = 16
 
@@ -81,7 +84,8 @@ class SchedDesc(ctypes.Structure):
                 ("queue", ctypes.c_void_p), ("priority", ctypes.c_void_p),
                 ("n_queue", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("launched", ctypes.c_void_p), ("result", ctypes.c_void_p),
-                ("batch", ctypes.c_void_p), ("iters", ctypes.c_void_p), ("deadline", ctypes.c_void_p)]
+                ("batch", ctypes.c_void_p), ("iters", ctypes.c_void_p), ("deadline", ctypes.c_void_p),
+                ("objective", ctypes.c_int32)]
 
 
 class SpaceSize(ctypes.Structure):
@@ -289,15 +293,17 @@ def unpack_proxy_plan(words):
 
 def arena_schedule(ctx, n_jobs, n_types, n_counts, thr, counts, capacity, alloc_type, alloc_count,
                    queue, priority, n_queue, depth, launched, result, stream=None,
-                   batch=None, iters=None, deadline=None) -> None:
+                   batch=None, iters=None, deadline=None, objective=0) -> None:
     """thr, alloc_type, alloc_count, queue, priority, launched, result and the
-    optional deadline arrays are device tensors (or pointers); counts and
-    capacity are host int32 arrays."""
+    optional batch / iters / deadline arrays are device tensors (or pointers);
+    counts and capacity are host int32 arrays.  objective: SCHED_THROUGHPUT or
+    SCHED_FAIRNESS."""
     counts = np.ascontiguousarray(counts, np.int32)
     capacity = np.ascontiguousarray(capacity, np.int32)
     d = SchedDesc(int(n_jobs), int(n_types), int(n_counts), _ptr(thr), _ptr(counts), _ptr(capacity),
                   _ptr(alloc_type), _ptr(alloc_count), _ptr(queue), _ptr(priority), int(n_queue),
-                  int(depth), _ptr(launched), _ptr(result), _ptr(batch), _ptr(iters), _ptr(deadline))
+                  int(depth), _ptr(launched), _ptr(result), _ptr(batch), _ptr(iters), _ptr(deadline),
+                  int(objective))
     sp = 0 if stream is None else int(stream)
     _check(ctx, load().arena_schedule(ctx, ctypes.byref(d), sp))
 
@@ -442,7 +448,8 @@ class Scheduler:
     device memory: `thr` is a float32 [J, T, NC] array or device tensor (the
     thr output of an estimate, viewed as [J, T, NC], serves directly)."""
 
-    def __init__(self, thr, counts, capacity, device: int = 0, batch=None, iters=None, deadline=None):
+    def __init__(self, thr, counts, capacity, device: int = 0, batch=None, iters=None, deadline=None,
+                 objective: str = "throughput"):
         import torch
         self.torch = torch
         self.dev = torch.device("cuda", device)
@@ -469,6 +476,7 @@ class Scheduler:
             self.launched = torch.empty(max(1, self.n_jobs), **i32)
             self.result = torch.empty(8, **i32)
             self.n_queue = 0
+            self.set_objective(objective)
             self.batch = self.iters = self.deadline = None
             if batch is not None or iters is not None or deadline is not None:
                 self.set_deadlines(batch, iters, deadline)
@@ -476,15 +484,23 @@ class Scheduler:
             self.close()
             raise
 
+    def set_objective(self, objective: str) -> None:
+        """"throughput" (Eq. 5) or "fairness" (Eq. 7; needs batch and iters)."""
+        if objective not in _OBJECTIVES:
+            raise ValueError(f"objective must be one of {sorted(_OBJECTIVES)}")
+        self.objective = _OBJECTIVES[objective]
+
     def set_deadlines(self, batch, iters, deadline) -> None:
-        """Per-job batch, remaining iterations and deadline (Eq. 6), or all None."""
+        """Per-job batch, remaining iterations and deadline (Eq. 6), or all
+        None; deadline alone may be None (the fairness objective's work)."""
         torch = self.torch
         if batch is None and iters is None and deadline is None:
             self.batch = self.iters = self.deadline = None
             return
         self.batch = torch.as_tensor(np.ascontiguousarray(batch, np.int32)).to(self.dev)
         self.iters = torch.as_tensor(np.ascontiguousarray(iters, np.float32)).to(self.dev)
-        self.deadline = torch.as_tensor(np.ascontiguousarray(deadline, np.float32)).to(self.dev)
+        self.deadline = (None if deadline is None else
+                         torch.as_tensor(np.ascontiguousarray(deadline, np.float32)).to(self.dev))
         torch.cuda.synchronize(self.dev)
 
     def load_state(self, alloc_type, alloc_count, queue, priority) -> None:
@@ -513,7 +529,7 @@ class Scheduler:
         arena_schedule(self.ctx, self.n_jobs, self.n_types, self.n_counts, self.thr, self.counts,
                        self.capacity, self.alloc_type, self.alloc_count, self.queue, self.priority,
                        self.n_queue, depth, self.launched, self.result, s.cuda_stream,
-                       self.batch, self.iters, self.deadline)
+                       self.batch, self.iters, self.deadline, self.objective)
 
     def results(self) -> dict:
         """Synchronise and copy the state after the last step to the host."""

@@ -885,9 +885,16 @@ arena_status arena_schedule(arena_ctx* c, const arena_sched_desc* d, void* strea
     if (!d->result || (d->n_jobs > 0 && (!d->thr || !d->alloc_type || !d->alloc_count)) ||
         (d->n_queue > 0 && (!d->queue || !d->priority || !d->launched)))
         return fail(c, ARENA_ERR_INVALID_ARG, "schedule: a device array is NULL");
+    if (d->objective != ARENA_SCHED_THROUGHPUT && d->objective != ARENA_SCHED_FAIRNESS)
+        return fail(c, ARENA_ERR_INVALID_ARG, "schedule: objective=%d is neither throughput (0) nor fairness (1)",
+                    d->objective);
     const int n_ddl = (d->batch != nullptr) + (d->iters != nullptr) + (d->deadline != nullptr);
-    if (n_ddl != 0 && n_ddl != 3)
+    if (d->objective == ARENA_SCHED_FAIRNESS) {
+        if (!d->batch || !d->iters)
+            return fail(c, ARENA_ERR_INVALID_ARG, "schedule: the fairness objective needs batch and iters");
+    } else if (n_ddl != 0 && n_ddl != 3) {
         return fail(c, ARENA_ERR_INVALID_ARG, "schedule: give batch, iters and deadline together or none");
+    }
     for (int i = 0; i < d->n_counts; ++i) {
         const int n = d->counts[i];
         if (n < 1 || n > ARENA_MAX_GPU_COUNT)
@@ -936,11 +943,12 @@ arena_status arena_schedule(arena_ctx* c, const arena_sched_desc* d, void* strea
     A.n_counts = d->n_counts;
     A.n_queue = d->n_queue;
     A.depth = d->depth;
-    if (n_ddl == 3 && d->n_jobs > 0) {
+    if (d->n_jobs > 0 && (n_ddl == 3 || d->objective == ARENA_SCHED_FAIRNESS)) {
         A.batch = d->batch;
         A.iters = d->iters;
-        A.ddl = d->deadline;
+        A.ddl = d->deadline;        // NULL: no deadline constraint
     }
+    A.objective = d->objective;
     if ((e = arena::launch_schedule(A, stream))) return hip_fail(c, e, "schedule launch");
     return ARENA_OK;
 }

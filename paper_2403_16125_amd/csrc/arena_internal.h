@@ -126,6 +126,7 @@ struct SchedArgs {
     const int32_t* batch;
     const float* iters;
     const float* ddl;
+    int32_t objective;            // 0 throughput (Eq. 5), 1 finish-time fairness (Eq. 7)
 };
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);

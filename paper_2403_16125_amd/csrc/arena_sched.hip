@@ -4,7 +4,10 @@
 // Algorithm 1, Eq. 5): queued jobs launch on the fastest grid that fits,
 // cheapest scale-downs of running jobs (throughput lost per GPU freed) make
 // room within the search depth, and the best scale-ups (throughput gained
-// per GPU) use what is left.  The step is a chain of dependent decisions,
+// per GPU) use what is left.  Under the finish-time fairness objective
+// (Eq. 7) the two searches rank by rho = B N / (thr n) instead: the job
+// whose rho after its scale-down is least, and the worst-off job moved to
+// its least-rho count.  The step is a chain of dependent decisions,
 // each an arg-min over the running jobs or over one job's grids, so one
 // workgroup runs the whole step and each decision is a block-wide reduction
 // of (key, index) pairs -- index breaking ties -- over per-thread candidates.
@@ -232,18 +235,21 @@ __device__ __forceinline__ unsigned long long block_min64(unsigned long long k, 
     return r;
 }
 
-// Work of job i to finish (batch x remaining iterations) and its deadline;
-// dl < 0 when there is no deadline constraint.
-template <bool DDL>
+// Work of job i to finish (batch x remaining iterations, when the deadline
+// constraint or the fairness objective needs it) and its deadline; dl < 0
+// when there is no deadline constraint.
+template <bool DDL, bool FAIR = false>
 __device__ __forceinline__ void job_deadline(const SchedArgs& A, int i, double& bn, double& dl)
 {
-    if (DDL) {
-        bn = (double)A.batch[i] * (double)A.iters[i];
-        dl = (double)A.ddl[i];
-    } else {
-        bn = 0.0;
-        dl = -1.0;
-    }
+    bn = (DDL || FAIR) ? (double)A.batch[i] * (double)A.iters[i] : 0.0;
+    dl = DDL ? (double)A.ddl[i] : -1.0;
+}
+
+// Finish-time-fairness ratio (Eq. 7) of a job with work bn at throughput v
+// on n GPUs: the remaining time bn / v per GPU; +inf at v = 0.
+__device__ __forceinline__ double fair_rho(float v, int n, double bn)
+{
+    return v > 0.0f ? bn / ((double)v * (double)n) : kInfD;
 }
 
 // A grid of throughput v is open to the job: v > 0 and, under the deadline
@@ -321,14 +327,15 @@ __device__ __forceinline__ Best launch_grid(const SchedArgs& A, SchedLds& S, int
 }
 
 // S3 for one running job: the largest smaller count open to it and the
-// throughput lost per GPU freed; c2 = -1 if there is none.
-template <bool DDL>
+// throughput lost per GPU freed (under fairness: the job's rho there);
+// c2 = -1 if there is none.
+template <bool DDL, bool FAIR>
 __device__ __forceinline__ double down_cost(const SchedArgs& A, const SchedLds& S, int i, int g, int c,
                                             int& c2)
 {
     const float* row = A.thr + ((size_t)i * A.n_types + g) * A.n_counts;
     double bn, dl;
-    job_deadline<DDL>(A, i, bn, dl);
+    job_deadline<DDL, FAIR>(A, i, bn, dl);
     const float tc = row[c];
     c2 = c - 1;
     float t2 = c2 >= 0 ? row[c2] : 0.0f;
@@ -337,24 +344,25 @@ __device__ __forceinline__ double down_cost(const SchedArgs& A, const SchedLds& 
         t2 = c2 >= 0 ? row[c2] : 0.0f;
     }
     if (c2 < 0) return kInfD;
+    if (FAIR) return fair_rho(t2, S.counts[c2], bn);
     const double cost = ((double)tc - (double)t2) / (double)(S.counts[c] - S.counts[c2]);
     if (cost != cost) c2 = -1;      // not a number (infinite throughputs): no candidate
     return cost;
 }
 
 // Refreshes the cached scale-down of list slot k from S.ralloc[k] (one thread).
-template <bool DDL>
+template <bool DDL, bool FAIR>
 __device__ __forceinline__ void cache_slot(const SchedArgs& A, SchedLds& S, int k)
 {
     const int al = S.ralloc[k], g = al >> 16;
     int c2;
-    const double cost = down_cost<DDL>(A, S, S.run[k], g, al & 0xffff, c2);
+    const double cost = down_cost<DDL, FAIR>(A, S, S.run[k], g, al & 0xffff, c2);
     S.dcost[k] = cost;
     S.dinfo[k] = c2 < 0 ? -1 : (c2 | (g << 16));
 }
 
 // S3: the cheapest scale-down on a type the queued job can use.
-template <bool DDL>
+template <bool DDL, bool FAIR>
 __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
 {
     Best b{kInfD, kNone, -1, -1};
@@ -372,7 +380,7 @@ __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
             const int g = A.alloc_type[i];
             if (g < 0 || !((usable >> g) & 1ull)) continue;
             int c2;
-            const double cost = down_cost<DDL>(A, S, i, g, A.alloc_count[i], c2);
+            const double cost = down_cost<DDL, FAIR>(A, S, i, g, A.alloc_count[i], c2);
             if (c2 < 0) continue;
             if (better(cost, i, b.key, b.idx)) b = Best{cost, i, c2, -1};
         }
@@ -381,16 +389,37 @@ __device__ Best scale_down(const SchedArgs& A, SchedLds& S, int& phase)
 }
 
 // S6 for one running job (type g, count index c): its best scale-up within
-// the free GPUs (gain per added GPU; ties to the smaller count).
-template <bool DDL>
+// the free GPUs (gain per added GPU; ties to the smaller count).  Under
+// fairness: the count with the least rho, a candidate only if that is below
+// the current rho, keyed by -(current rho) so the worst-off job wins.
+template <bool DDL, bool FAIR>
 __device__ __forceinline__ void up_move(const SchedArgs& A, const SchedLds& S, int i, int g, int c, int k,
                                         Best& b)
 {
     const float* row = A.thr + ((size_t)i * A.n_types + g) * A.n_counts;
     double bn, dl;
-    job_deadline<DDL>(A, i, bn, dl);
+    job_deadline<DDL, FAIR>(A, i, bn, dl);
     const int n = S.counts[c];
     const int fr = S.free[g];
+    if (FAIR) {
+        const double r0 = fair_rho(row[c], n, bn);
+        double rbest = kInfD;
+        int cb = -1;
+        for (int c2 = c + 1; c2 < A.n_counts; ++c2) {
+            const int n2 = S.counts[c2];
+            if (n2 - n > fr) break;
+            const float v2 = row[c2];
+            if (open_grid<DDL>(v2, bn, dl)) {
+                const double r2 = fair_rho(v2, n2, bn);
+                if (cb < 0 || r2 < rbest) {
+                    rbest = r2;
+                    cb = c2;
+                }
+            }
+        }
+        if (cb >= 0 && rbest < r0 && better(-r0, i, b.key, b.idx)) b = Best{-r0, i, cb, k};
+        return;
+    }
     const double t = (double)row[c];
     double gbest = -kInfD;
     int cbest = -1;
@@ -412,25 +441,25 @@ __device__ __forceinline__ void up_move(const SchedArgs& A, const SchedLds& S, i
 }
 
 // S6: the scale-up with the largest gain per GPU (key -gain).
-template <bool DDL>
+template <bool DDL, bool FAIR>
 __device__ Best scale_up(const SchedArgs& A, SchedLds& S, int& phase)
 {
     Best b{kInfD, kNone, -1, -1};
     if (S.use_list) {
         for (int k = threadIdx.x; k < S.n_run; k += kSchedThreads) {
             const int al = S.ralloc[k];
-            up_move<DDL>(A, S, S.run[k], al >> 16, al & 0xffff, k, b);
+            up_move<DDL, FAIR>(A, S, S.run[k], al >> 16, al & 0xffff, k, b);
         }
     } else {
         for (int i = threadIdx.x; i < A.n_jobs; i += kSchedThreads) {
             const int g = A.alloc_type[i];
-            if (g >= 0) up_move<DDL>(A, S, i, g, A.alloc_count[i], -1, b);
+            if (g >= 0) up_move<DDL, FAIR>(A, S, i, g, A.alloc_count[i], -1, b);
         }
     }
     return block_min(b, S, phase);
 }
 
-template <bool DDL>
+template <bool DDL, bool FAIR>
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
 {
     __shared__ SchedLds S;
@@ -461,10 +490,10 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             }
         }
     }
-    if (DDL)
+    if (DDL || FAIR)
         for (int i = tid; i < A.n_jobs; i += kSchedThreads) {
-            const float it = A.iters[i], dd = A.ddl[i];
-            if (A.batch[i] <= 0 || !(it >= 0.0f) || it == __builtin_huge_valf() || !(dd > 0.0f))
+            const float it = A.iters[i];
+            if (A.batch[i] <= 0 || !(it >= 0.0f) || it == __builtin_huge_valf() || (DDL && !(A.ddl[i] > 0.0f)))
                 atomicOr(&S.bad, 2);
         }
     for (int q = tid; q < A.n_queue; q += kSchedThreads) {
@@ -488,7 +517,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
     for (int q = tid; q < A.n_queue; q += kSchedThreads) A.launched[q] = 0;
     const bool fits = S.n_run <= kMaxRun;
     if (fits)
-        for (int k = tid; k < S.n_run; k += kSchedThreads) cache_slot<DDL>(A, S, k);
+        for (int k = tid; k < S.n_run; k += kSchedThreads) cache_slot<DDL, FAIR>(A, S, k);
     __syncthreads();
     if (tid == 0) S.use_list = fits ? 1 : 0;
     __syncthreads();
@@ -560,7 +589,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
                             const int k = S.n_run++;
                             S.run[k] = j;
                             S.ralloc[k] = c | (g << 16);
-                            cache_slot<DDL>(A, S, k);
+                            cache_slot<DDL, FAIR>(A, S, k);
                         } else {
                             S.use_list = 0;
                         }
@@ -574,7 +603,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             __syncthreads();
             ++passes;
             scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
-            const Best sd = scale_down<DDL>(A, S, phase);
+            const Best sd = scale_down<DDL, FAIR>(A, S, phase);
             if (sd.aux < 0) break;
             if (tid == 0) {
                 const int i = sd.idx;
@@ -596,7 +625,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
                     S.log_cost[nlog] = S.dcost[sd.slot];
                     S.log_info[nlog] = S.dinfo[sd.slot];
                     S.ralloc[sd.slot] = sd.aux | (g << 16);
-                    cache_slot<DDL>(A, S, sd.slot);
+                    cache_slot<DDL, FAIR>(A, S, sd.slot);
                 }
             }
             ++nlog;
@@ -643,7 +672,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
     while (ups < A.depth) {              // S6
         ++passes;
         scanned += (unsigned long long)(S.use_list ? S.n_run : A.n_jobs);
-        const Best su = scale_up<DDL>(A, S, phase);
+        const Best su = scale_up<DDL, FAIR>(A, S, phase);
         if (su.aux < 0) break;
         if (tid == 0) {
             const int i = su.idx;
@@ -660,7 +689,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
             A.alloc_count[i] = su.aux;
             if (su.slot >= 0) {
                 S.ralloc[su.slot] = su.aux | (g << 16);
-                cache_slot<DDL>(A, S, su.slot);
+                cache_slot<DDL, FAIR>(A, S, su.slot);
             }
         }
         ++ups;
@@ -682,10 +711,14 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs A)
 
 hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream)
 {
-    if (args.ddl)
-        hipLaunchKernelGGL(schedule_kernel<true>, dim3(1), dim3(kSchedThreads), 0, stream, args);
-    else
-        hipLaunchKernelGGL(schedule_kernel<false>, dim3(1), dim3(kSchedThreads), 0, stream, args);
+    const dim3 grid(1), block(kSchedThreads);
+    if (args.objective == 1) {
+        if (args.ddl) hipLaunchKernelGGL((schedule_kernel<true, true>), grid, block, 0, stream, args);
+        else hipLaunchKernelGGL((schedule_kernel<false, true>), grid, block, 0, stream, args);
+    } else {
+        if (args.ddl) hipLaunchKernelGGL((schedule_kernel<true, false>), grid, block, 0, stream, args);
+        else hipLaunchKernelGGL((schedule_kernel<false, false>), grid, block, 0, stream, args);
+    }
     return hipGetLastError();
 }
 

@@ -301,6 +301,14 @@ def test_schedule_validation(ctx):
     assert call(launched=None) == arena.ARENA_ERR_INVALID_ARG
     assert call(batch=fake) == arena.ARENA_ERR_INVALID_ARG           # deadline arrays: all or none
     assert call(batch=fake, iters=fake) == arena.ARENA_ERR_INVALID_ARG
+    assert call(objective=2) == arena.ARENA_ERR_INVALID_ARG            # neither objective
+    assert "objective" in arena.arena_last_error(ctx)
+    assert call(objective=-1) == arena.ARENA_ERR_INVALID_ARG
+    # the fairness objective needs batch and iters (a deadline is optional)
+    assert call(objective=arena.SCHED_FAIRNESS) == arena.ARENA_ERR_INVALID_ARG
+    assert call(objective=arena.SCHED_FAIRNESS, batch=fake) == arena.ARENA_ERR_INVALID_ARG
+    assert call(objective=arena.SCHED_FAIRNESS, iters=fake, deadline=fake) == arena.ARENA_ERR_INVALID_ARG
+    assert "batch and iters" in arena.arena_last_error(ctx)
 
 
 def test_proxy_desc_layout(tmp_path):

@@ -1,5 +1,7 @@
 """Parity of the HIP scheduling step (arena_schedule) with the CPU oracle of
-Algorithm 1 under the throughput objective (Sec. 3.5, Eq. 5), through the C ABI.
+Algorithm 1 under the throughput objective (Sec. 3.5, Eq. 5), the deadline
+constraint (Eq. 6) and the finish-time fairness objective (Eq. 7), through the
+C ABI.
 
 Both sides take every decision in float64 from the same float32 throughput
 matrix, so the agreement is exact: the new allocation of every job, which
@@ -11,9 +13,9 @@ import pytest
 from oracle import scheduler_oracle as so
 from paper_2403_16125_amd import sched_states as ss
 
-def _gpu(st, ddl=None):
+def _gpu(st, ddl=None, objective="throughput"):
     from paper_2403_16125_amd import arena
-    s = arena.Scheduler(st.thr, st.counts, st.capacity)
+    s = arena.Scheduler(st.thr, st.counts, st.capacity, objective=objective)
     if ddl is not None:
         s.set_deadlines(*ddl)
     try:
@@ -24,13 +26,13 @@ def _gpu(st, ddl=None):
         s.close()
 
 
-def _check(st, ddl=None):
+def _check(st, ddl=None, objective="throughput"):
     print(f"schedule: J={st.n_jobs} T={st.thr.shape[1]} NC={st.thr.shape[2]} Q={len(st.queue)} "
-          f"D={st.depth} deadlines={ddl is not None}", flush=True)
+          f"D={st.depth} deadlines={ddl is not None and ddl[2] is not None} objective={objective}", flush=True)
     kw = {} if ddl is None else dict(batch=ddl[0], iters=ddl[1], deadline=ddl[2])
     want = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
-                       st.priority, st.depth, **kw)
-    got = _gpu(st, ddl)
+                       st.priority, st.depth, objective=objective, **kw)
+    got = _gpu(st, ddl, objective)
     assert got["status"] == 0
     assert got["moves"] == want["moves"]
     assert got["decisions"] == want["decisions"]
@@ -317,6 +319,131 @@ def test_bad_deadline_values_leave_everything_unchanged(bad):
     else:
         D[0] = -1.0
     s = arena.Scheduler(thr, [1, 2, 4], [4], batch=B, iters=N, deadline=D)
+    try:
+        s.load_state([0, -1, -1], [1, 0, 0], [1, 2], [0, 1])
+        s.launched.fill_(-7)
+        s.step(2)
+        r = s.results()
+        assert r["status"] == 2
+        assert list(r["alloc_type"]) == [0, -1, -1] and list(r["alloc_count"]) == [1, 0, 0]
+        assert (r["launched"] == -7).all()
+    finally:
+        s.close()
+
+
+# ---------------------------------------------------------------- finish-time fairness (Eq. 7)
+
+FAIR_HAND = {
+    "up_worst_first": (({0: [[10, 19, 36]], 1: [[1, 1.5, 1.8]]}, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 3),
+                       ([1, 1], [100.0, 20.0], None)),
+    "down_least_harmed": (({0: [[10, 29, 30]], 1: [[5, 40, 41.2]], 2: [[1, 2, 3]]}, [1, 2, 4], [8],
+                           [0, 0, -1], [2, 2, 0], [2], [0], 4), ([1, 1, 1], [100.0, 137.6, 5.0], None)),
+    "target_tie": (({0: [[4, 3, 1.5]]}, [1, 2, 4], [4], [0], [0], [], [], 1), ([2], [3.0], None)),
+    "no_work_left": (({0: [[1, 2, 4]], 1: [[1, 2, 4]]}, [1, 2, 4], [8], [0, 0], [0, 0], [], [], 4),
+                     ([1, 1], [0.0, 0.0], None)),
+    "job_tie": (({0: [[1, 2, 4]], 1: [[1, 2, 4]]}, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 4),
+                ([1, 1], [8.0, 8.0], None)),
+    "with_deadline": (({0: [[1, 2, 4]], 1: [[1, 2, 4]]}, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 4),
+                      ([1, 1], [8.0, 8.0], [1e9, 2.5])),
+    "zero_throughput_running": (({0: [[0, 2, 4]], 1: [[1, 2, 4]]}, [1, 2, 4], [6], [0, 0], [0, 0], [], [], 2),
+                                ([1, 1], [8.0, 8.0], None)),
+}
+
+
+def _fair_args(ddl):
+    B, N, D = ddl
+    return (np.asarray(B, np.int32), np.asarray(N, np.float32),
+            None if D is None else np.asarray(D, np.float32))
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", sorted(FAIR_HAND))
+def test_fairness_hand_cases(name):
+    args, ddl = FAIR_HAND[name]
+    _check(_state(*args), _fair_args(ddl), "fairness")
+
+
+@pytest.mark.gpu
+def test_fairness_hand_case_values():
+    # the GPU reproduces the hand-derived outcomes the oracle is pinned to
+    args, ddl = FAIR_HAND["up_worst_first"]
+    got = _gpu(_state(*args), _fair_args(ddl), "fairness")
+    assert list(got["alloc_count"]) == [1, 2] and got["moves"] == [0, 0, 2] and got["decisions"] == 3
+    args, ddl = FAIR_HAND["down_least_harmed"]
+    got = _gpu(_state(*args), _fair_args(ddl), "fairness")
+    assert list(got["alloc_count"]) == [2, 1, 1] and got["moves"] == [1, 1, 0]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", RANDOM, ids=[f"seed{c[0]}_J{c[1]}" for c in RANDOM])
+def test_fairness_random_states(case):
+    seed, J, T, counts, cap, rf, qf, ncls, depth, mc = case
+    thr = ss.synthetic_thr(seed, J, T, counts)
+    st = ss.random_state(seed, thr, counts, cap, running_frac=rf, queued_frac=qf, n_classes=ncls,
+                         depth=depth, max_count=mc)
+    B, N, D = ss.deadlines(seed, st.thr)
+    _check(st, (B, N, None), "fairness")
+    if seed <= 3:
+        _check(st, (B, N, D), "fairness")
+
+
+def test_fairness_random_states_cover_every_move():
+    # CPU only: the fairness cases above exercise kept scale-downs, launches and scale-ups
+    seen = np.zeros(3, np.int64)
+    for seed, J, T, counts, cap, rf, qf, ncls, depth, mc in RANDOM:
+        thr = ss.synthetic_thr(seed, J, T, counts)
+        st = ss.random_state(seed, thr, counts, cap, running_frac=rf, queued_frac=qf,
+                             n_classes=ncls, depth=depth, max_count=mc)
+        B, N, _ = ss.deadlines(seed, st.thr)
+        r = so.schedule(st.thr, st.counts, st.capacity, st.alloc_type, st.alloc_count, st.queue,
+                        st.priority, st.depth, batch=B, iters=N, objective="fairness")
+        seen += r["moves"]
+    assert (seen > 0).all(), seen
+
+
+@pytest.mark.gpu
+def test_fairness_full_round():
+    st = ss.full_round()
+    B, N, D = ss.deadlines(11, st.thr, slack=(0.9, 4.0))
+    want = _check(st, (B, N, None), "fairness")
+    assert want["moves"][1] > 0
+    _check(st, (B, N, D), "fairness")
+
+
+@pytest.mark.gpu
+def test_fairness_many_running_jobs():
+    # more running jobs than the kernel's LDS list holds: the scan path
+    counts = [1, 2, 4, 8]
+    J = 5150
+    thr = ss.synthetic_thr(43, J, 2, counts)
+    at = np.full(J, -1, np.int32)
+    ac = np.zeros(J, np.int32)
+    used = np.zeros(2, np.int64)
+    for j in range(5000):
+        g = j % 2
+        c = int(np.argmax(thr[j, g] > 0))
+        at[j], ac[j] = g, c
+        used[g] += counts[c]
+    cap = (used + 64).astype(np.int32)
+    queue = np.arange(5000, J, dtype=np.int32)
+    st = ss.SchedState(thr=thr, counts=np.asarray(counts, np.int32), capacity=cap, alloc_type=at,
+                       alloc_count=ac, queue=queue, priority=np.zeros(len(queue), np.int32), depth=4)
+    B, N, _ = ss.deadlines(43, thr)
+    want = _check(st, (B, N, None), "fairness")
+    assert want["moves"][1] > 0
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("bad", ["batch", "iters"])
+def test_fairness_bad_values_leave_everything_unchanged(bad):
+    from paper_2403_16125_amd import arena
+    thr = np.full((3, 1, 3), 5.0, np.float32)
+    B, N = np.full(3, 8, np.int32), np.full(3, 10.0, np.float32)
+    if bad == "batch":
+        B[1] = -2
+    else:
+        N[2] = np.inf
+    s = arena.Scheduler(thr, [1, 2, 4], [4], batch=B, iters=N, objective="fairness")
     try:
         s.load_state([0, -1, -1], [1, 0, 0], [1, 2], [0, 1])
         s.launched.fill_(-7)
