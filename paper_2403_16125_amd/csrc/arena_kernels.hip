@@ -1565,13 +1565,25 @@ __device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, cons
     return (UL + (double)(pp - 1) * p2p + (double)(m - 1) * Wlb + ar) * (1.0 - 1e-9);
 }
 
+// Plan-buffer key of the interpolated-tables kernel: pp << 12 | tp << 7 | m,
+// with the top bit set once the plan is priced.
+constexpr unsigned kTabPriced = 1u << 31;
+constexpr unsigned kTabKeyMask = kTabPriced - 1u;
+
 // Every cell under interpolated communication latency: a block works on one
 // (job, type) at a time (taken from the queue), its waves taking counts.  Every plan of a cell has the balanced
-// partition of its own per-microbatch costs (no sharing across m or counts).
-// With bound pruning, the plans' lower bounds come first, the plan of least
-// bound is priced, and every other plan only if its bound lies within the tie
-// window of the best time priced so far (it can neither be the best nor tie
-// with it otherwise); then the cell's choice as in estimate_kernel.
+// partition of its own per-microbatch costs.  Those costs depend on the plan
+// only through tp, b and whether dp tp > 1, and for fixed tp and b each
+// pipeline degree fixes dp and hence m, so the plans of a cell sharing (tp, b,
+// dp tp > 1) form a group that differs only in pp: one recursion up to the
+// group's largest degree gives every member's bottleneck, and each member is
+// priced as soon as its row is done.  With bound pruning, the plans' lower
+// bounds come first, then the unpriced plan of least bound is priced with its
+// group, again and again, until every bound left lies past the tie window of
+// the best time priced so far (those plans can neither be the best nor tie
+// with it): a group takes only members within the window and drops the
+// degrees the window excludes as it tightens.  Then the cell's choice as in
+// estimate_kernel.
 __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int item)
 {
     __shared__ TabBlockLds B;
@@ -1659,49 +1671,94 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
             np = kMaxPlans;
         }
         wave_sync();
-        // price plan e of the buffer (its slot receives the time)
-        auto price_slot = [&](int e) -> double {
-            const unsigned key = Wv.planKey[e];
-            const int pp = (int)(key >> 12);
-            const int tp = (int)((key >> 7) & 0x1Fu);
-            const int m = (int)(key & 0x7Fu);
-            const int dp = cell.n / (tp * pp);
-            const double bq = rint((double)jb.Bg / (double)(dp * m));
-            double W;
-            const Stages sg = tab_partition(B, Wv, lane, jb, ty, K, cell.kappa, dp, tp, pp, bq, W);
-            const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp, pp, m, bq, sg);
+        // price plan e0 of the buffer and the unpriced plans of its group (each
+        // slot receives its time and the priced flag); returns the best time
+        // so far.  Wv.lbnd[d - 1] holds the member of degree d (-1: none).
+        auto price_group = [&](int e0, double best_in) -> double {
+            const unsigned key0 = Wv.planKey[e0] & kTabKeyMask;
+            const int pp0 = (int)(key0 >> 12);
+            const int tp0 = (int)((key0 >> 7) & 0x1Fu);
+            const int dp0 = cell.n / (tp0 * pp0);
+            const double bq0 = rint((double)jb.Bg / (double)(dp0 * (int)(key0 & 0x7Fu)));
+            const bool fl0 = dp0 * tp0 > 1;
+            const double lim0 = best_in * (1.0 + A.tie_eps);
+            Wv.lbnd[lane] = -1.0;
+            Wv.lbnd[lane + 64] = -1.0;
+            wave_sync();
+            for (int e = lane; e < np; e += 64) {
+                const unsigned k = Wv.planKey[e];
+                if (k & kTabPriced) continue;
+                const int pp = (int)(k >> 12);
+                const int tp = (int)((k >> 7) & 0x1Fu);
+                if (tp != tp0) continue;
+                const int dp = cell.n / (tp * pp);
+                if ((dp * tp > 1) != fl0 || rint((double)jb.Bg / (double)(dp * (int)(k & 0x7Fu))) != bq0) continue;
+                const double lbe = Wv.planT[e];
+                if (e != e0 && A.prune && !(lbe < kInf && lbe <= lim0)) continue;
+                Wv.lbnd[pp - 1] = (double)e;      // degrees of a group are distinct
+            }
+            wave_sync();
+            const Mask tm = ballot_mask(Wv.lbnd[lane] >= 0.0, Wv.lbnd[lane + 64] >= 0.0);
+            double c[2];
+            tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp0, tp0, bq0, c);
+            seq_prefix<2, 2>(c[0], c[1], jb.L, lane, Wv.UD, Wv.UD + 1, true);
             tally(Wv, lane, kProblems, 1);
-            tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L + 4ull * (unsigned)jb.L + 12ull * (unsigned)pp + 40ull);
-            wave_sync();
-            if (lane == 0) Wv.planT[e] = T;
-            wave_sync();
-            return T;
+            tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
+            double bst = best_in;
+            solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask mk) {
+                const int e = (int)Wv.lbnd[pp - 1];
+                const int dp = cell.n / (tp0 * pp);
+                const int m = (int)(Wv.planKey[e] & 0x7Fu);
+                const Stages sg = canonical_stages<2>(Wv.UD, Wv.J, lane, jb.L, pp, W);
+                const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp0, pp, m, bq0, sg);
+                tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L + 12ull * (unsigned)pp + 40ull);
+                wave_sync();
+                if (lane == 0) {
+                    Wv.planT[e] = T;
+                    Wv.planKey[e] |= kTabPriced;
+                }
+                wave_sync();
+                bst = fmin(bst, T);
+                Mask rest = mk;                      // degrees still to come
+                if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
+                if (!A.prune) return rest;
+                // members whose bound now lies past the window are left to the
+                // main loop, which skips them
+                const double lim = bst * (1.0 + A.tie_eps);
+                const int ea = (int)Wv.lbnd[lane], eb = (int)Wv.lbnd[lane + 64];
+                const bool ka = ea >= 0 && Wv.planT[ea] <= lim;
+                const bool kb = eb >= 0 && Wv.planT[eb] <= lim;
+                return rest & ballot_mask(ka, kb);
+            });
+            return bst;
         };
         if (A.prune) {
-            // the plan of least bound first, then the others within the window
-            double bl = kInf;
-            for (int e = lane; e < np; e += 64) bl = fmin(bl, Wv.planT[e]);
-            const double bmin = wave_reduce1<OpMin>(bl);
-            double il = -1.0;
-            for (int e = lane; e < np; e += 64)
-                if (Wv.planT[e] == bmin) il = (double)e;
-            const int first = (int)wave_reduce1<OpMax>(il);
+            // best first: the unpriced plan of least bound (and its group),
+            // until every bound left lies past the tie window of the best time
             double best = kInf;
-            if (first >= 0 && bmin < kInf) best = price_slot(first);
-            for (int e = 0; e < np; ++e) {
-                if (e == first) continue;
-                const double lbe = Wv.planT[e];
-                if (!(lbe < kInf && lbe <= best * (1.0 + A.tie_eps))) {
-                    wave_sync();
-                    if (lane == 0) Wv.planT[e] = kInf;
-                    ++nskip;
-                    wave_sync();
-                    continue;
-                }
-                best = fmin(best, price_slot(e));
+            for (;;) {
+                double bl = kInf;
+                for (int e = lane; e < np; e += 64)
+                    if (!(Wv.planKey[e] & kTabPriced)) bl = fmin(bl, Wv.planT[e]);
+                const double bmin = wave_reduce1<OpMin>(bl);
+                if (!(bmin < kInf && bmin <= best * (1.0 + A.tie_eps))) break;
+                double il = -1.0;
+                for (int e = lane; e < np; e += 64)
+                    if (!(Wv.planKey[e] & kTabPriced) && Wv.planT[e] == bmin) il = (double)e;
+                best = price_group((int)wave_reduce1<OpMax>(il), best);
             }
+            // the rest can neither be the best nor tie with it
+            double ns = 0.0;
+            for (int e = lane; e < np; e += 64)
+                if (!(Wv.planKey[e] & kTabPriced)) {
+                    Wv.planT[e] = kInf;
+                    ns += 1.0;
+                }
+            nskip = (int)wave_reduce1<OpSum>(ns);
+            wave_sync();
         } else {
-            for (int e = 0; e < np; ++e) price_slot(e);
+            for (int e = 0; e < np; ++e)
+                if (!(Wv.planKey[e] & kTabPriced)) price_group(e, kInf);
         }
         tally(Wv, lane, kSkipped, (unsigned long long)nskip);
         wave_sync();
@@ -1728,11 +1785,11 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         const double tlim = tmin * (1.0 + A.tie_eps);
         double kl = kInf;
         for (int e = lane; e < np; e += 64)
-            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)Wv.planKey[e]);
+            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)(Wv.planKey[e] & kTabKeyMask));
         const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
         double il = -1.0;
         for (int e = lane; e < np; e += 64)
-            if (Wv.planKey[e] == kbest) il = (double)e;
+            if ((Wv.planKey[e] & kTabKeyMask) == kbest) il = (double)e;
         int ib = (int)wave_reduce1<OpMax>(il);
         ib = ib < 0 ? 0 : (ib >= np ? np - 1 : ib);
         const double Tb = Wv.planT[ib];
