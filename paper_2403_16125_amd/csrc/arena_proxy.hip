@@ -35,7 +35,7 @@
 namespace arena {
 namespace {
 
-constexpr int kPxThreads = 512;
+constexpr int kPxThreads = 1024;
 constexpr int kPxWaves = kPxThreads / 64;
 constexpr int kMaxParts = 6435;           // C(15, 7): groupings of 16 operators
 constexpr double kInfP = __builtin_huge_val();
