@@ -54,25 +54,73 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def host_info() -> dict:
+    """The host the oracle is timed on: CPU model, the cores this process may
+    use (capped at 16, the host share of one GPU), the oracle's compiler."""
+    import platform
+    import subprocess
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    try:
+        cc = subprocess.run(["gcc", "--version"], capture_output=True, text=True).stdout.splitlines()[0]
+    except (OSError, IndexError):
+        cc = "gcc"
+    from oracle import oracle as oracle_c
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable,
+            "threads": max(1, min(16, usable)), "compiler": cc, "flags": " ".join(oracle_c.CFLAGS)}
+
+
+def _oracle_threads(fn, ids, threads: int) -> float:
+    """Wall time of fn over ids split in `threads` contiguous chunks, one
+    thread each (the oracle's C calls keep no global state and release the
+    interpreter lock)."""
+    import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
+    chunks = [c for c in np.array_split(ids, threads) if len(c)]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=len(chunks)) as ex:
+        list(ex.map(fn, chunks))
+    return time.perf_counter() - t0
+
+
 def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None) -> dict:
-    """The oracle (single-threaded C, fp64) on a bounded sample of the same
-    workload: jobs j = 0, every, 2*every, ... times every grid of one round,
-    under partition rule `rule` or with communication latency from `tables`."""
+    """The oracle (C, fp64, one cell at a time) on a bounded sample of the
+    same workload: jobs j = 0, every, 2*every, ... times every grid of one
+    round, under partition rule `rule` or with communication latency from
+    `tables`; timed on all usable host cores (jobs split over threads, each
+    thread single-threaded code) and on one core."""
     import numpy as np
     from oracle import oracle as oracle_c
     oracle_c.load()
+    info = host_info()
     per = w.n_types * w.n_counts
     jobs = list(range(0, w.n_jobs, every))
     ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)
-    t0 = time.perf_counter()
-    if tables is None:
-        oracle_c.cells(w, ids, kappa_round=kappa_round, rule=rule)
-    else:
-        oracle_c.cells_tab(w, ids, tables, kappa_round=kappa_round)
-    dt = time.perf_counter() - t0
-    return {"value": len(ids) / dt, "unit": "cells/s", "cores": 1, "kind": "oracle",
-            "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, round {kappa_round}: "
-                      f"{len(ids)} cells in {dt:.1f} s"}
+
+    def run(sub):
+        if tables is None:
+            oracle_c.cells(w, sub, kappa_round=kappa_round, rule=rule)
+        else:
+            oracle_c.cells_tab(w, sub, tables, kappa_round=kappa_round)
+
+    dt_all = _oracle_threads(run, ids, info["threads"])
+    dt_one = _oracle_threads(run, ids, 1)
+    return {"value": len(ids) / dt_all, "unit": "cells/s", "cores": info["threads"], "kind": "oracle",
+            "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, contention round {kappa_round}: "
+                      f"{len(ids)} cells, {dt_all:.1f} s on {info['threads']} threads, {dt_one:.1f} s on one",
+            "single_core": {"value": len(ids) / dt_one, "unit": "cells/s", "cores": 1},
+            "host": info}
 
 
 def schedule_cpu_baseline(st, min_seconds: float = 10.0, objective: str = "throughput", work=None) -> dict:
@@ -348,8 +396,9 @@ def main() -> int:
     log(f"{w.n_jobs} jobs, {w.n_types} types, {w.n_counts} counts, {w.n_cells} cells, "
         f"{w.n_rounds} rounds of contention factors")
     work = workcount.count(w, kappa_round=0)
-    log(f"exhaustive work per round: {work['ops']:.4g} ops, {work['plans']} plans, "
-        f"{work['problems']} partition problems")
+    log(f"work per round (survey convention): {work['ops']:.4g} ops ({work['dp_entries_full']:.4g} recursion "
+        f"entries), {work['plans']} plans, {work['problems']} partition problems; truncated rows "
+        f"{work['ops_truncated']:.4g} ops")
 
     dev = torch.device("cuda", 0)
     rule = arena.PARTITION_MEMORY if args.partition == "memory" else arena.PARTITION_BALANCED
@@ -386,19 +435,27 @@ def main() -> int:
         f"(min {min(launch_ms):.2f}, max {max(launch_ms):.2f})")
     # the work each timed launch did (bound pruning depends on the round's
     # contention factors): the device tallies of the same rounds, re-run untimed
-    ops_done = []
+    ops_done, counts_done = [], []
     for i in range(args.steps):
         est.set_round(i % w.n_rounds)
         est.estimate()
         cnt = est.counters()
         ops_done.append(cnt["alg_ops"])
+        counts_done.append(cnt)
     res = est.results(np.arange(0, w.n_cells, 9973))
     est.close()
 
     traffic = stored_traffic(args.workload) if plain else None
     cells_per_s = w.n_cells * args.steps / wall
-    plans_per_s = work["plans"] * args.steps / wall       # every plan of the space is decided
-    achieved = float(np.sum(ops_done)) / (float(np.sum(launch_ms)) / 1e3)
+    launch_s = float(np.sum(launch_ms)) / 1e3
+    # numerator: the survey's count of the method's work per round (8 L + 8 L P
+    # + 4 L |S| per distinct partition problem, 12 pp + 40 per plan); it does not
+    # depend on the contention round.  Beside it: the same units with
+    # truncated recursion rows, and the device's tally of the work it did.
+    ops_round = float(work["ops"]) if plain else None
+    achieved = ops_round * args.steps / launch_s if plain else float(np.sum(ops_done)) / launch_s
+    tally_rate = float(np.sum(ops_done)) / launch_s
+    priced = float(np.mean([c["plans"] for c in counts_done]))
     line = {
         "metric": "(job,grid) cells/sec",
         "value": cells_per_s,
@@ -421,7 +478,10 @@ def main() -> int:
             "comm": "interpolated tables" if tables is not None else "volume / bandwidth",
             "rounds_per_step": 1,
         },
-        "plans_per_s": plans_per_s,
+        # every plan of the space is decided each round: priced, or skipped by
+        # an exact bound
+        "plans_decided_per_s": work["plans"] * args.steps / launch_s,
+        "plans_priced_per_s": priced * args.steps / launch_s,
         "roofline": {
             "bound": "alu",
             "achieved": achieved / 1e12,
@@ -429,13 +489,18 @@ def main() -> int:
             "unit": "Top/s",
             "frac": achieved / PEAK_LANE_OPS,
             "traffic": traffic,
-            "ops_per_launch": float(np.mean(ops_done)),
-            "ops_exhaustive": work["ops"] if plain else None,
-            "launch_ms": avg_launch_s * 1e3,
+            "ops_per_launch": ops_round if plain else float(np.mean(ops_done)),
+            "ops_convention": ("survey: 8 L + 8 L P + 4 L |S| per distinct partition problem + 12 pp + 40 per plan"
+                               if plain else "device tally of the work done"),
+            "launch_ms": launch_s / args.steps * 1e3,
+            "frac_truncated_rows": (float(work["ops_truncated"]) * args.steps / launch_s / PEAK_LANE_OPS
+                                    if plain else None),
+            "frac_device_tally": tally_rate / PEAK_LANE_OPS,
+            "ops_device_tally": float(np.mean(ops_done)),
             # for transparency: against the published fp32 vector rate (FMA and packed pairs
             # counted twice each), and the measured HBM rate when the counters are current
             "frac_of_published_fp32": achieved / PUBLISHED_FP32,
-            "hbm_GBps": (traffic / avg_launch_s / 1e9) if traffic else None,
+            "hbm_GBps": (traffic / (launch_s / args.steps) / 1e9) if traffic else None,
         },
         "device_tallies": cnt,
         "feasible_fraction_sampled": float(np.mean(res["feasible"])),

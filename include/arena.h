@@ -251,6 +251,18 @@ arena_status arena_space_size_get(const arena_ctx* ctx, arena_space_size* out);
 arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t* plan,
                             uint8_t* cuts, int32_t cuts_stride, void* stream);
 
+/* Cap on the device memory the library allocates for this context: its
+ * copies of the job offsets, batches, grid tables and contention factors,
+ * the work order, the tallies and the communication tables (the caller's
+ * arrays are not counted).  bytes = 0 (the default) sets no cap.  An
+ * arena_estimate whose bound workload needs more returns
+ * ARENA_ERR_OUT_OF_MEMORY before anything is allocated, enqueued or written
+ * (the need is 4 (J+1) + 4 J + 40 T + 8 NC + 4 T NC + 4 J T bytes plus the
+ * tables and about 2 KB, for J jobs, T types and NC counts).  INVALID_ARG
+ * for a negative value.  arena_estimate also returns OUT_OF_MEMORY when a
+ * device allocation fails. */
+arena_status arena_set_workspace_limit(arena_ctx* ctx, int64_t bytes);
+
 /* Tallies of the last arena_estimate.  Synchronises the device. */
 arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
 

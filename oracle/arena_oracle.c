@@ -44,7 +44,21 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <stdio.h>
+
 #define ORACLE_MAX_L 128
+
+/* Allocation that cannot fail silently: a test oracle that ran out of memory
+ * must stop rather than return a partial answer. */
+static void* xrealloc(void* old, size_t bytes)
+{
+    void* p = realloc(old, bytes ? bytes : 1);
+    if (!p) {
+        fprintf(stderr, "arena oracle: out of memory (%zu bytes)\n", bytes);
+        abort();
+    }
+    return p;
+}
 
 /* ------------------------------------------------------------------ */
 /* Stage partition                                                     */
@@ -260,7 +274,7 @@ static void mem_recursion(const double* U, const omem* M, int pp, double* G)
 static double bottleneck_mem(const double* U, const omem* M, int pp, int* cuts)
 {
     int L = M->L, L1 = L + 1;
-    double* G = (double*)malloc(sizeof(double) * (size_t)(pp + 1) * (size_t)L1);
+    double* G = (double*)xrealloc(NULL, sizeof(double) * (size_t)(pp + 1) * (size_t)L1);
     mem_recursion(U, M, pp, G);
     double W = G[pp * L1 + 0];
     if (cuts && W < INFINITY) {
@@ -499,7 +513,7 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
     int L = jb.L;
 
     int cap = 64, nc = 0;
-    ocand* cand = (ocand*)malloc(sizeof(ocand) * (size_t)cap);
+    ocand* cand = (ocand*)xrealloc(NULL, sizeof(ocand) * (size_t)cap);
     double u[ORACLE_MAX_L], U[ORACLE_MAX_L + 1];
     int cuts[ORACLE_MAX_L];
 
@@ -519,7 +533,7 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
             for (int mi = 0; mi < n_m; ++mi) {
                 int m = m_values[mi];
                 if (jb.Bg % (dp * m) != 0) continue;
-                if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
+                if (nc == cap) { cap *= 2; cand = (ocand*)xrealloc(cand, sizeof(ocand) * (size_t)cap); }
                 cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp; cand[nc].m = m;
                 if (rule == 0 || plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) == 0) {
                     oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
@@ -782,7 +796,7 @@ static int oracle_cell_tab(int j, int g, int ci, const int32_t* off, const float
     type_tabs(g, K, vol, lat, tabs);
 
     int cap = 64, nc = 0;
-    ocand* cand = (ocand*)malloc(sizeof(ocand) * (size_t)cap);
+    ocand* cand = (ocand*)xrealloc(NULL, sizeof(ocand) * (size_t)cap);
     double U[ORACLE_MAX_L + 1];
     int cuts[ORACLE_MAX_L];
     for (int tp = 1; tp <= n; ++tp) {
@@ -795,7 +809,7 @@ static int oracle_cell_tab(int j, int g, int ci, const int32_t* off, const float
                 if (jb.Bg % (dp * m) != 0) continue;
                 plan_tab_partition(&jb, &ty, tabs, kappa, dp, tp, pp, m, U, cuts);
                 oplan r = price_plan_tab(&jb, &ty, tabs, n, kappa, dp, tp, pp, m, U, cuts);
-                if (nc == cap) { cap *= 2; cand = (ocand*)realloc(cand, sizeof(ocand) * (size_t)cap); }
+                if (nc == cap) { cap *= 2; cand = (ocand*)xrealloc(cand, sizeof(ocand) * (size_t)cap); }
                 cand[nc].T = r.T; cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp;
                 cand[nc].m = m; cand[nc].feasible = r.feasible;
                 ++nc;

@@ -27,15 +27,22 @@ CELL_WORDS = 52        # one cell: s, B, bounds[17], GPUs per stage[16], tp per 
 _lib = None
 
 
-def build() -> str:
-    """Compile with gcc: IEEE double, no contraction, no fast-math."""
-    os.makedirs(os.path.dirname(_LIB), exist_ok=True)
-    tmp = _LIB + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off",
-           "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+# gcc flags of the oracle: IEEE double, no contraction, no fast-math
+CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra"]
+
+
+def build(out: str = None, extra_flags=()) -> str:
+    """Compile with gcc: IEEE double, no contraction, no fast-math.
+
+    `extra_flags` (e.g. a sanitizer build for the tests) are appended;
+    `out` defaults to the library the wrappers load."""
+    out = out or _LIB
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    tmp = out + ".tmp"
+    cmd = ["gcc"] + CFLAGS + list(extra_flags) + ["-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB)
-    return _LIB
+    os.replace(tmp, out)
+    return out
 
 
 def load():

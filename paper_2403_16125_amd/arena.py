@@ -31,6 +31,7 @@ EXPORTED = (
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
     "arena_schedule", "arena_proxy_estimate", "arena_set_partition_rule", "arena_set_comm_tables",
+    "arena_set_workspace_limit",
 )
 
 PARTITION_BALANCED = 0
@@ -136,6 +137,8 @@ def load():
     lib.arena_space_size_get.restype = st
     lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     lib.arena_estimate.restype = st
+    lib.arena_set_workspace_limit.argtypes = [vp, ctypes.c_int64]
+    lib.arena_set_workspace_limit.restype = st
     lib.arena_get_counters.argtypes = [vp, ctypes.POINTER(Counters)]
     lib.arena_get_counters.restype = st
     lib.arena_proxy_estimate.argtypes = [vp, ctypes.POINTER(ProxyDesc), vp, vp, vp, vp]
@@ -255,6 +258,10 @@ def arena_estimate(ctx, t_iter, thr, plan, cuts=None, cuts_stride: int = 0, stre
     sp = 0 if stream is None else int(stream)
     _check(ctx, load().arena_estimate(ctx, _ptr(t_iter), _ptr(thr), _ptr(plan), _ptr(cuts),
                                       int(cuts_stride), sp))
+
+
+def arena_set_workspace_limit(ctx, nbytes: int) -> None:
+    _check(ctx, load().arena_set_workspace_limit(ctx, int(nbytes)))
 
 
 def arena_get_counters(ctx) -> dict:
@@ -377,6 +384,9 @@ class Estimator:
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
         arena_estimate(self.ctx, self.t_iter, self.thr, self.plan, self.cuts,
                        CUTS_STRIDE if self.cuts is not None else 0, s.cuda_stream)
+
+    def set_workspace_limit(self, nbytes: int) -> None:
+        arena_set_workspace_limit(self.ctx, nbytes)
 
     def proxy_estimate(self, f_ref: float = 1e14, n_ops: int = 16, hbm_bw=None, stream=None) -> None:
         """The proxy-plan planner over the same cells (outputs kept beside the

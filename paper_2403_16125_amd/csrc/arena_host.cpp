@@ -70,7 +70,11 @@ struct arena_ctx {
     int32_t* d_count_order = nullptr;
     size_t cap_items = 0, cap_corder = 0;
     bool order_dirty = true;
+    bool horder_valid = false;                  // host copies of the work order below are current
+    std::vector<int32_t> h_iorder, h_corder;
+    int64_t ws_limit = 0;                       // cap on library-owned device bytes, 0: none
     unsigned long long* d_counters = nullptr;
+    const unsigned long long* last_counters = nullptr;   // tallies of the last estimate
     unsigned long long* h_counters = nullptr;   // pinned
     unsigned long long* d_queue = nullptr;      // the estimate and proxy kernels' item queue
     int n_cus = 0;
@@ -302,10 +306,13 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
 
 // Work order: (job, type) blocks with the most estimated work first (so the
 // longest blocks do not form the tail), and within a block the largest GPU
-// counts first.  The estimate is plans x layers per cell.
-arena_status upload_orders(arena_ctx* c, hipStream_t stream)
+// counts first.  The estimate is plans x layers per cell.  Host copies,
+// rebuilt when the bindings change.
+void compute_orders(arena_ctx* c)
 {
-    std::vector<int32_t> corder((size_t)c->n_counts);
+    if (c->horder_valid) return;
+    std::vector<int32_t>& corder = c->h_corder;
+    corder.resize((size_t)c->n_counts);
     std::iota(corder.begin(), corder.end(), 0);
     std::stable_sort(corder.begin(), corder.end(),
                      [&](int a, int b) { return c->counts[a] > c->counts[b]; });
@@ -328,21 +335,55 @@ arena_status upload_orders(arena_ctx* c, hipStream_t stream)
     }
     // the kernels' resident blocks take items from a queue in this order:
     // heaviest first, so the last items to start are the light ones
-    std::vector<int32_t> iorder(items);
+    std::vector<int32_t>& iorder = c->h_iorder;
+    iorder.resize(items);
     std::iota(iorder.begin(), iorder.end(), 0);
     std::stable_sort(iorder.begin(), iorder.end(), [&](int a, int b) { return icost[a] > icost[b]; });
+    c->horder_valid = true;
+}
+
+arena_status upload_orders(arena_ctx* c, hipStream_t stream)
+{
+    compute_orders(c);
+    const size_t items = (size_t)c->n_jobs * c->n_types;
     hipError_t e;
     if ((e = ensure_capacity(&c->d_item_order, &c->cap_items, items)) ||
         (e = ensure_capacity(&c->d_count_order, &c->cap_corder, (size_t)c->n_counts)))
         return fail(c, ARENA_ERR_OUT_OF_MEMORY, "work order: %s", hipGetErrorString(e));
-    if ((e = hipMemcpyAsync(c->d_item_order, iorder.data(), sizeof(int32_t) * items,
+    if ((e = hipMemcpyAsync(c->d_item_order, c->h_iorder.data(), sizeof(int32_t) * items,
                             hipMemcpyHostToDevice, stream)) ||
-        (e = hipMemcpyAsync(c->d_count_order, corder.data(), sizeof(int32_t) * c->n_counts,
+        (e = hipMemcpyAsync(c->d_count_order, c->h_corder.data(), sizeof(int32_t) * c->n_counts,
                             hipMemcpyHostToDevice, stream)) ||
         (e = hipStreamSynchronize(stream)))
         return hip_fail(c, e, "work order upload");
     c->order_dirty = false;
     return ARENA_OK;
+}
+
+// Library-owned device memory of one estimate, section by section, each
+// section starting at a 256-byte boundary.
+struct Workspace {
+    size_t counters, queue, off, batch, types, counts, kappa, items, corder, tab, total;
+};
+
+Workspace workspace_layout(const arena_ctx* c)
+{
+    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    const size_t J = (size_t)c->n_jobs, T = (size_t)c->n_types, NC = (size_t)c->n_counts;
+    Workspace w;
+    size_t o = 0;
+    w.counters = o; o = up(o + sizeof(unsigned long long) * arena::kNumCounters);
+    w.queue = o;    o = up(o + sizeof(unsigned long long));
+    w.off = o;      o = up(o + sizeof(int32_t) * (J + 1));
+    w.batch = o;    o = up(o + sizeof(int32_t) * J);
+    w.types = o;    o = up(o + sizeof(TypeDev) * T);
+    w.counts = o;   o = up(o + sizeof(int32_t) * NC);
+    w.kappa = o;    o = up(o + sizeof(float) * T * NC);
+    w.items = o;    o = up(o + sizeof(int32_t) * J * T);
+    w.corder = o;   o = up(o + sizeof(int32_t) * NC);
+    w.tab = o;      o = up(o + (c->tab_k > 0 ? sizeof(double) * c->tab.size() : 0));
+    w.total = o;
+    return w;
 }
 
 // Some type has one contention factor for all its counts: the kernel then
@@ -461,6 +502,7 @@ arena_status arena_bind_jobs(arena_ctx* c, const arena_jobs_desc* d)
     c->jobs_checked = false;
     c->jobs_dirty = true;
     c->order_dirty = true;
+    c->horder_valid = false;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -516,6 +558,7 @@ arena_status arena_bind_grids(arena_ctx* c, const arena_grids_desc* d)
     c->msets_dirty = true;
     c->kappa_dirty = true;
     c->order_dirty = true;
+    c->horder_valid = false;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -558,6 +601,7 @@ arena_status arena_set_plan_space(arena_ctx* c, const int32_t* m_values, int32_t
     c->tie_eps = tie_eps;
     c->space_set = true;
     c->order_dirty = true;
+    c->horder_valid = false;
     c->size_valid = false;
     return ARENA_OK;
 }
@@ -630,11 +674,23 @@ arena_status arena_space_size_get(const arena_ctx* cc, arena_space_size* out)
     return ARENA_OK;
 }
 
-arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts,
-                            int32_t cuts_stride, void* stream_ptr)
+arena_status arena_set_workspace_limit(arena_ctx* c, int64_t bytes)
 {
     if (!c) return ARENA_ERR_INVALID_ARG;
     c->err.clear();
+    if (bytes < 0) return fail(c, ARENA_ERR_INVALID_ARG, "workspace limit: %lld bytes", (long long)bytes);
+    c->ws_limit = bytes;
+    return ARENA_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Host checks shared by both estimate entry points (nothing touches the device).
+arena_status check_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts,
+                            int32_t cuts_stride)
+{
     if (!c->jobs_bound || !c->grids_bound || !c->space_set)
         return fail(c, ARENA_ERR_NOT_READY, "estimate: bind jobs, grids and plan space first");
     if (!t_iter || !thr || !plan) return fail(c, ARENA_ERR_INVALID_ARG, "estimate: output array is NULL");
@@ -651,39 +707,31 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     if (c->tab_k > 0 && c->tab_types != c->n_types)
         return fail(c, ARENA_ERR_NOT_READY, "estimate: comm tables were set for %d types, %d are bound",
                     c->tab_types, c->n_types);
-    hipStream_t stream = (hipStream_t)stream_ptr;
-    DeviceGuard guard(c->device);
-    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
-    arena_status st = ensure_device(c, stream);
-    if (st != ARENA_OK) return st;
-    if (c->order_dirty && (st = upload_orders(c, stream)) != ARENA_OK) return st;
-    hipError_t e;
-    if (c->tab_k > 0) {
-        if (c->tab_dirty) {
-            if ((e = ensure_capacity(&c->d_tab, &c->cap_tab, c->tab.size())))
-                return fail(c, ARENA_ERR_OUT_OF_MEMORY, "comm tables: %s", hipGetErrorString(e));
-            if ((e = hipMemcpyAsync(c->d_tab, c->tab.data(), sizeof(double) * c->tab.size(),
-                                    hipMemcpyHostToDevice, stream)) ||
-                (e = hipStreamSynchronize(stream)))
-                return hip_fail(c, e, "comm table upload");
-            c->tab_dirty = false;
-        }
-    }
+    return ARENA_OK;
+}
 
+// Kernel arguments from the context, with the library-owned tables at the
+// given device addresses.
+arena::EstimateArgs estimate_args(const arena_ctx* c, const int32_t* d_off, const int32_t* d_batch,
+                                  const TypeDev* d_types, const int32_t* d_counts, const float* d_kappa,
+                                  const int32_t* d_items, const int32_t* d_corder, unsigned long long* d_queue,
+                                  const double* d_tab, unsigned long long* d_counters, float* t_iter, float* thr,
+                                  uint32_t* plan, uint8_t* cuts, int32_t cuts_stride)
+{
     arena::EstimateArgs A;
     std::memset(&A, 0, sizeof(A));
-    A.layer_offset = c->d_off;
-    A.batch = c->d_batch;
+    A.layer_offset = d_off;
+    A.batch = d_batch;
     A.t = c->t; A.p = c->p; A.a = c->a; A.x = c->x; A.q = c->q;
-    A.types = c->d_types;
-    A.counts = c->d_counts;
-    A.kappa = c->d_kappa;
+    A.types = d_types;
+    A.counts = d_counts;
+    A.kappa = d_kappa;
     A.n_jobs = c->n_jobs;
     A.n_types = c->n_types;
     A.n_counts = c->n_counts;
-    A.item_order = c->d_item_order;
-    A.count_order = c->d_count_order;
-    A.queue = c->d_queue;
+    A.item_order = d_items;
+    A.count_order = d_corder;
+    A.queue = d_queue;
     A.n_items = c->n_jobs * c->n_types;
     // one block per resident slot (four per CU); each takes items from the queue
     A.n_blocks = std::min(A.n_items, 4 * std::max(c->n_cus, 1));
@@ -698,19 +746,59 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     A.mem_rule = c->partition_rule == ARENA_PARTITION_MEMORY ? 1 : 0;
     if (c->tab_k > 0) {
         A.tab_k = c->tab_k;
-        A.tab_vol = c->d_tab;
-        A.tab_lat = c->d_tab + c->tab.size() / 2;
+        A.tab_vol = d_tab;
+        A.tab_lat = d_tab + c->tab.size() / 2;
     }
     A.t_iter = t_iter;
     A.thr = thr;
     A.plan = plan;
     A.cuts = cuts;
     A.cuts_stride = cuts ? cuts_stride : 0;
-    A.counters = c->d_counters;
+    A.counters = d_counters;
+    return A;
+}
+
+}  // namespace
+
+extern "C" {
+
+arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts,
+                            int32_t cuts_stride, void* stream_ptr)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    arena_status st = check_estimate(c, t_iter, thr, plan, cuts, cuts_stride);
+    if (st != ARENA_OK) return st;
+    const Workspace ws = workspace_layout(c);
+    if (c->ws_limit > 0 && ws.total > (size_t)c->ws_limit)
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "estimate: needs %zu bytes of device workspace (limit %lld)",
+                    ws.total, (long long)c->ws_limit);
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    st = ensure_device(c, stream);
+    if (st != ARENA_OK) return st;
+    if (c->order_dirty && (st = upload_orders(c, stream)) != ARENA_OK) return st;
+    hipError_t e;
+    if (c->tab_k > 0) {
+        if (c->tab_dirty) {
+            if ((e = ensure_capacity(&c->d_tab, &c->cap_tab, c->tab.size())))
+                return fail(c, ARENA_ERR_OUT_OF_MEMORY, "comm tables: %s", hipGetErrorString(e));
+            if ((e = hipMemcpyAsync(c->d_tab, c->tab.data(), sizeof(double) * c->tab.size(),
+                                    hipMemcpyHostToDevice, stream)) ||
+                (e = hipStreamSynchronize(stream)))
+                return hip_fail(c, e, "comm table upload");
+            c->tab_dirty = false;
+        }
+    }
+    const arena::EstimateArgs A =
+        estimate_args(c, c->d_off, c->d_batch, c->d_types, c->d_counts, c->d_kappa, c->d_item_order,
+                      c->d_count_order, c->d_queue, c->d_tab, c->d_counters, t_iter, thr, plan, cuts, cuts_stride);
     if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)) ||
         (e = arena::launch_zero_counters(c->d_queue, 1, stream)))
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
+    c->last_counters = c->d_counters;
     return ARENA_OK;
 }
 
@@ -719,13 +807,14 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     if (!c) return ARENA_ERR_INVALID_ARG;
     c->err.clear();
     if (!out) return fail(c, ARENA_ERR_INVALID_ARG, "counters: out is NULL");
-    if (!c->dev_ready) return fail(c, ARENA_ERR_NOT_READY, "counters: no estimate has run");
+    if (!c->last_counters) return fail(c, ARENA_ERR_NOT_READY, "counters: no estimate has run");
     DeviceGuard guard(c->device);
     if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
     hipError_t e;
     if ((e = hipDeviceSynchronize())) return hip_fail(c, e, "synchronise");
     unsigned long long h[arena::kNumCounters];
-    if ((e = hipMemcpy(h, c->d_counters, sizeof(h), hipMemcpyDeviceToHost))) return hip_fail(c, e, "counter copy");
+    if ((e = hipMemcpy(h, c->last_counters, sizeof(h), hipMemcpyDeviceToHost)))
+        return hip_fail(c, e, "counter copy");
     out->cells = (int64_t)h[arena::kCells];
     out->plans = (int64_t)h[arena::kPlans];
     out->problems = (int64_t)h[arena::kProblems];

@@ -130,6 +130,7 @@ struct SchedArgs {
 };
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);
+
 hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream);
 hipError_t launch_zero_counters(unsigned long long* counters, int n, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& args, hipStream_t stream);

@@ -8,14 +8,20 @@ schedules it:
   times divided by a scale, so it is one problem per job for every GPU type
   and count; every other vector is one per (job, type, tp, all-to-all flag,
   contention factor value);
-* the problem's requested degrees S are the union over the cells sharing it;
-  the recursion only needs row k at i in [k, L - tau(k) + k], tau(k) the
-  smallest requested degree >= k, so its entries are
-  E = sum_{k=1}^{max S} (L - tau(k) + 1);
-* ops(problem) = 8 L (cost vector and prefix) + 8 E (two subtracts, a
-  compare, a min/max and an amortised pointer step per entry)
+* the problem's requested degrees S are the union over the cells sharing it
+  and P its largest; the O(P L) bottleneck recursion fills P rows of L
+  entries, 8 operations each (two subtracts, a compare, a min/max and an
+  amortised pointer step);
+* ops(problem) = 8 L (cost vector and prefix) + 8 L P (the recursion)
   + 4 L |S| (canonical cuts);
 * ops(plan) = 12 pp + 40 (stage terms, memory check, reduction).
+
+This is the convention the roofline fraction is quoted in (`ops`).  Two
+smaller figures are kept beside it: `ops_truncated` counts only the entries
+a recursion needs when row k stops at i = L - tau(k) + k (tau(k) the
+smallest requested degree >= k), E = sum_{k=1}^{P} (L - tau(k) + 1); the
+kernel's own tally counts the entries and plans it evaluated after bound
+pruning.
 """
 from __future__ import annotations
 
@@ -55,7 +61,8 @@ def count(w, kappa_round: int = 0) -> dict:
         key = (int(Ls[j]), int(w.batch[j]), bool(moe_job[j]))
         groups[key] = groups.get(key, 0) + 1
 
-    tot = dict(cells=w.n_cells, plans=0, plan_ops=0, problems=0, dp_entries=0, problem_ops=0)
+    tot = dict(cells=w.n_cells, plans=0, plan_ops=0, problems=0, dp_entries=0, problem_ops=0,
+               dp_entries_full=0, problem_ops_full=0)
     for (L, Bg, moe), mult in groups.items():
         pure_targets = set()
         shared = {}                  # (g, tp, flag, kappa) -> target set
@@ -82,13 +89,19 @@ def count(w, kappa_round: int = 0) -> dict:
         probs = [pure_targets] if pure_targets else []
         probs += list(shared.values())
         ent = sum(_entries(L, tuple(sorted(s))) for s in probs)
-        pops = sum(8 * L + 4 * L * len(s) for s in probs) + 8 * ent
+        ent_full = sum(L * max(s) for s in probs)
+        base = sum(8 * L + 4 * L * len(s) for s in probs)
+        pops = base + 8 * ent
+        pops_full = base + 8 * ent_full
         tot["plans"] += mult * plans
         tot["plan_ops"] += mult * plan_ops
         tot["problems"] += mult * len(probs)
         tot["dp_entries"] += mult * ent
         tot["problem_ops"] += mult * pops
-    tot["ops"] = tot["plan_ops"] + tot["problem_ops"]
+        tot["dp_entries_full"] += mult * ent_full
+        tot["problem_ops_full"] += mult * pops_full
+    tot["ops"] = tot["plan_ops"] + tot["problem_ops_full"]
+    tot["ops_truncated"] = tot["plan_ops"] + tot["problem_ops"]
     return tot
 
 

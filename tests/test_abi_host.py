@@ -358,3 +358,35 @@ def test_proxy_validation(ctx):
     assert status(t_iter=None) == arena.ARENA_ERR_INVALID_ARG
     assert status(plan=None) == arena.ARENA_ERR_INVALID_ARG
     assert lib.arena_proxy_estimate(ctx, None, fake, fake, fake, None) == arena.ARENA_ERR_INVALID_ARG
+
+
+def _bind_host_only(ctx, n_jobs, L=4, n_types=8, n_counts=16):
+    """Jobs, grids and plan space bound with fake device pointers (never read:
+    every check below fails on the host first)."""
+    off = (np.arange(n_jobs + 1, dtype=np.int64) * L).astype(np.int32)
+    arena.arena_bind_jobs(ctx, off, np.full(n_jobs, 8, np.int32), FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_bind_grids(ctx, speed=[1.0] * n_types, mem_bytes=[8e10] * n_types, bw_intra=[3e11] * n_types,
+                           bw_inter=[2.5e10] * n_types, gpus_per_node=[8] * n_types,
+                           counts=[8 * (i + 1) for i in range(n_counts)])
+    arena.arena_set_plan_space(ctx, [1, 2, 4, 8], 1e-6)
+
+
+def test_workspace_limit_out_of_memory(ctx):
+    """A workload whose library-owned tables exceed the context's workspace cap
+    fails with OUT_OF_MEMORY before any device call (this runs without a GPU);
+    a negative cap is rejected."""
+    _expect(1, arena.arena_set_workspace_limit, ctx, -1, match="workspace")
+    _bind_host_only(ctx, 5000)
+    arena.arena_set_workspace_limit(ctx, 64 << 10)
+    _expect(2, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="limit 65536")
+    # J = 5000, T = 8, NC = 16: 4 J T + 8 J + ... bytes, the header's formula
+    msg = None
+    try:
+        arena.arena_estimate(ctx, FAKE, FAKE, FAKE)
+    except arena.ArenaError as e:
+        msg = e.message
+    need = int(msg.split("needs ")[1].split(" bytes")[0])
+    J, T, NC = 5000, 8, 16
+    approx = 4 * (J + 1) + 4 * J + 40 * T + 8 * NC + 4 * T * NC + 4 * J * T
+    assert approx <= need <= approx + 2560
+

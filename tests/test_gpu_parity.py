@@ -81,14 +81,40 @@ def test_full_size_sampled(oracle, name, k):
     assert cnt["cells"] == w.n_cells and cnt["plans"] + cnt["plans_skipped"] == size["plans"]
 
 
-@pytest.mark.parametrize("rnd", [0, 9])
-def test_full_round_sampled(oracle, rnd):
+@pytest.mark.parametrize("rnd,with_cuts", [(0, True), (9, True), (4, False)])
+def test_full_round_sampled(oracle, rnd, with_cuts):
+    """The full round on the GPU, compared with the oracle on sampled cells.
+    Without cut rows (4) this is exactly the launch the benchmark times (cut
+    rows off, bound pruning on); the oracle then checks time and plan."""
     w = wl.full()
     ids = _sample(w, 1200, seed=100 + rnd, whole_jobs=1)
-    _say(f"full round {rnd}: {w.n_cells} cells on the GPU, {len(ids)} compared")
-    res, cnt, size = _run(w, rnd=rnd, ids=ids)
+    _say(f"full round {rnd}, cut rows {'on' if with_cuts else 'off'}: {w.n_cells} cells on the GPU, "
+         f"{len(ids)} compared")
+    res, cnt, size = _run(w, rnd=rnd, with_cuts=with_cuts, ids=ids)
+    assert ("cuts" in res) == with_cuts
     _check(compare(w, res, ids, oracle, kappa_round=rnd), f"full r{rnd}")
     assert cnt["cells"] == w.n_cells and cnt["plans"] + cnt["plans_skipped"] == size["plans"]
+
+
+def test_full_round_timed_launch_bitwise_equals_cut_launch():
+    """The benchmark's launch (no cut rows) writes, on every one of the 17.2 M
+    cells of a full round, bitwise the times, throughputs and plans of the
+    launch with cut rows, whose cells the oracle checks above."""
+    import torch
+    w = wl.full()
+    _say(f"full round 6: {w.n_cells} cells with and without cut rows")
+    out = []
+    for with_cuts in (False, True):
+        est = arena.Estimator(w, with_cuts=with_cuts)
+        try:
+            est.set_round(6)
+            est.estimate()
+            torch.cuda.synchronize()
+            out.append((est.t_iter.clone(), est.thr.clone(), est.plan.clone()))
+        finally:
+            est.close()
+    for k, (a, b) in zip(("t_iter", "thr", "plan"), zip(*out)):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32)), k
 
 
 def _edge_workload():
@@ -159,6 +185,32 @@ def test_bitwise_deterministic_and_permutation_equivariant():
     rows = (perm[:, None] * per + np.arange(per)[None, :]).ravel()
     for k in ("t_iter", "thr", "plan", "cuts"):
         assert np.array_equal(rp[k], r1[k][rows]), k
+
+
+def test_grid_permutation_equivariant():
+    """Reordering the GPU types and the GPU counts of the grid (with their
+    contention factors) only reorders the matrix: every cell, cut row
+    included, is bitwise the same as the original cell it maps to."""
+    import dataclasses
+    w = wl.trace(n_jobs=64)
+    _say("grid permutation: trace[64 jobs], 4 types x 35 counts permuted")
+    r1, _, _ = _run(w)
+    rng = np.random.default_rng(9)
+    tperm = rng.permutation(w.n_types)
+    cperm = rng.permutation(w.n_counts)
+    kap = np.asarray(w.kappa).reshape(w.n_rounds, w.n_types, w.n_counts)[:, tperm][:, :, cperm]
+    wp = dataclasses.replace(
+        w, speed=w.speed[tperm].copy(), mem=w.mem[tperm].copy(), bw_intra=w.bw_intra[tperm].copy(),
+        bw_inter=w.bw_inter[tperm].copy(), gpus_per_node=w.gpus_per_node[tperm].copy(),
+        counts=w.counts[cperm].copy(), kappa=np.ascontiguousarray(kap.reshape(w.n_rounds, -1)),
+        hbm=None if w.hbm is None else w.hbm[tperm].copy())
+    rp, _, _ = _run(wp)
+    # cell (j, g', c') of the permuted grid is cell (j, tperm[g'], cperm[c'])
+    j = np.arange(w.n_jobs)[:, None, None]
+    src = (j * w.n_types + tperm[None, :, None]) * w.n_counts + cperm[None, None, :]
+    src = src.ravel()
+    for k in ("t_iter", "thr", "plan", "cuts"):
+        assert np.array_equal(rp[k], r1[k][src]), k
 
 
 def test_no_cuts_and_kappa_rounds_consistent():
