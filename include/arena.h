@@ -263,7 +263,30 @@ arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t*
  * device allocation fails. */
 arena_status arena_set_workspace_limit(arena_ctx* ctx, int64_t bytes);
 
-/* Tallies of the last arena_estimate.  Synchronises the device. */
+#define ARENA_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/* arena_estimate for callers that cannot allocate device memory (work under
+ * stream capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments, outputs and errors, but every
+ * library-owned device buffer of the call (job offsets and batches, grid
+ * tables, contention factors, work order, tallies, communication tables) is
+ * placed in one statically sized device array of ARENA_NOALLOC_SCRATCH_BYTES
+ * per GPU, which the library holds until the process ends; the call makes no
+ * device or pinned allocation (it copies the tables from the context's host
+ * copies into the array on `stream` each time, and on the first call for
+ * a set of job tables runs the value check, which synchronises the stream).
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * (the tallies of the last call, which arena_get_counters reads): calls that
+ * overlap on one GPU, from any context or stream, race and must be ordered by
+ * the caller.  Returns ARENA_ERR_OUT_OF_MEMORY, with nothing enqueued or
+ * written, when the bound workload's tables need more than the array (about
+ * 4 J T + 8 J + 4 T NC bytes; for example 16384 jobs x 8 types x 131 counts
+ * need 0.7 MB). */
+arena_status arena_estimate_noalloc(arena_ctx* ctx, float* t_iter, float* thr, uint32_t* plan,
+                                    uint8_t* cuts, int32_t cuts_stride, void* stream);
+
+/* Tallies of the last arena_estimate or arena_estimate_noalloc.
+ * Synchronises the device. */
 arena_status arena_get_counters(arena_ctx* ctx, arena_counters* out);
 
 /* ------------------------------------------------------------------ */

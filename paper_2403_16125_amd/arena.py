@@ -31,8 +31,10 @@ EXPORTED = (
     "arena_bind_jobs", "arena_bind_grids", "arena_set_kappa", "arena_set_plan_space",
     "arena_space_size_get", "arena_estimate", "arena_get_counters", "arena_set_bound_pruning",
     "arena_schedule", "arena_proxy_estimate", "arena_set_partition_rule", "arena_set_comm_tables",
-    "arena_set_workspace_limit",
+    "arena_set_workspace_limit", "arena_estimate_noalloc",
 )
+
+NOALLOC_SCRATCH_BYTES = 4 << 20
 
 PARTITION_BALANCED = 0
 PARTITION_MEMORY = 1
@@ -137,6 +139,8 @@ def load():
     lib.arena_space_size_get.restype = st
     lib.arena_estimate.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     lib.arena_estimate.restype = st
+    lib.arena_estimate_noalloc.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    lib.arena_estimate_noalloc.restype = st
     lib.arena_set_workspace_limit.argtypes = [vp, ctypes.c_int64]
     lib.arena_set_workspace_limit.restype = st
     lib.arena_get_counters.argtypes = [vp, ctypes.POINTER(Counters)]
@@ -260,6 +264,14 @@ def arena_estimate(ctx, t_iter, thr, plan, cuts=None, cuts_stride: int = 0, stre
                                       int(cuts_stride), sp))
 
 
+def arena_estimate_noalloc(ctx, t_iter, thr, plan, cuts=None, cuts_stride: int = 0, stream=None) -> None:
+    """arena_estimate with the library's tables in its static device scratch
+    (no device allocation); arguments as arena_estimate."""
+    sp = 0 if stream is None else int(stream)
+    _check(ctx, load().arena_estimate_noalloc(ctx, _ptr(t_iter), _ptr(thr), _ptr(plan), _ptr(cuts),
+                                              int(cuts_stride), sp))
+
+
 def arena_set_workspace_limit(ctx, nbytes: int) -> None:
     _check(ctx, load().arena_set_workspace_limit(ctx, int(nbytes)))
 
@@ -380,10 +392,14 @@ class Estimator:
         else:
             arena_set_comm_tables(self.ctx, *tables)
 
-    def estimate(self, stream=None) -> None:
+    def estimate(self, stream=None, noalloc: bool = False) -> None:
+        """Estimate every cell into the estimator's outputs; noalloc=True takes
+        the entry point that allocates nothing (its tables in the library's
+        static device scratch)."""
         s = self.torch.cuda.current_stream(self.dev) if stream is None else stream
-        arena_estimate(self.ctx, self.t_iter, self.thr, self.plan, self.cuts,
-                       CUTS_STRIDE if self.cuts is not None else 0, s.cuda_stream)
+        fn = arena_estimate_noalloc if noalloc else arena_estimate
+        fn(self.ctx, self.t_iter, self.thr, self.plan, self.cuts,
+           CUTS_STRIDE if self.cuts is not None else 0, s.cuda_stream)
 
     def set_workspace_limit(self, nbytes: int) -> None:
         arena_set_workspace_limit(self.ctx, nbytes)

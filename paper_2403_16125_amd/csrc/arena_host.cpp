@@ -19,6 +19,8 @@
 
 using arena::TypeDev;
 
+static_assert(ARENA_NOALLOC_SCRATCH_BYTES == arena::kNoallocScratchBytes, "scratch size of the header and the kernels");
+
 struct arena_ctx {
     int device = 0;
     std::string err;
@@ -361,7 +363,8 @@ arena_status upload_orders(arena_ctx* c, hipStream_t stream)
 }
 
 // Library-owned device memory of one estimate, section by section, each
-// section starting at a 256-byte boundary.
+// section starting at a 256-byte boundary (the layout of the no-allocation
+// entry point's scratch; the allocating path holds the same buffers).
 struct Workspace {
     size_t counters, queue, off, batch, types, counts, kappa, items, corder, tab, total;
 };
@@ -799,6 +802,81 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     c->last_counters = c->d_counters;
+    return ARENA_OK;
+}
+
+arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts,
+                                    int32_t cuts_stride, void* stream_ptr)
+{
+    if (!c) return ARENA_ERR_INVALID_ARG;
+    c->err.clear();
+    arena_status st = check_estimate(c, t_iter, thr, plan, cuts, cuts_stride);
+    if (st != ARENA_OK) return st;
+    const Workspace ws = workspace_layout(c);
+    if (ws.total > arena::kNoallocScratchBytes)
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY,
+                    "estimate_noalloc: the bound workload needs %zu bytes of scratch (max %zu): "
+                    "use arena_estimate", ws.total, (size_t)arena::kNoallocScratchBytes);
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    DeviceGuard guard(c->device);
+    if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    hipError_t e;
+    char* base = nullptr;
+    if ((e = arena::scratch_address(c->device, (void**)&base))) return hip_fail(c, e, "scratch address");
+    if (c->n_cus == 0 &&
+        (e = hipDeviceGetAttribute(&c->n_cus, hipDeviceAttributeMultiprocessorCount, c->device)))
+        return hip_fail(c, e, "hipDeviceGetAttribute");
+    auto* d_counters = (unsigned long long*)(base + ws.counters);
+    auto* d_queue = (unsigned long long*)(base + ws.queue);
+    auto* d_off = (int32_t*)(base + ws.off);
+    auto* d_batch = (int32_t*)(base + ws.batch);
+    auto* d_types = (TypeDev*)(base + ws.types);
+    auto* d_counts = (int32_t*)(base + ws.counts);
+    auto* d_kappa = (float*)(base + ws.kappa);
+    auto* d_items = (int32_t*)(base + ws.items);
+    auto* d_corder = (int32_t*)(base + ws.corder);
+    auto* d_tab = (double*)(base + ws.tab);
+    compute_orders(c);
+    const size_t J = (size_t)c->n_jobs, T = (size_t)c->n_types, NC = (size_t)c->n_counts;
+    // the scratch is shared by every call on this device: every table is
+    // copied again (pageable host sources: each copy has read its source
+    // when it returns)
+    if ((e = hipMemcpyAsync(d_off, c->off.data(), sizeof(int32_t) * (J + 1), hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(d_batch, c->batch.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, stream)))
+        return hip_fail(c, e, "job table copy");
+    if (!c->jobs_checked) {
+        arena::ValidateArgs v;
+        v.layer_offset = d_off;
+        v.n_jobs = c->n_jobs;
+        v.arrays[0] = c->t; v.arrays[1] = c->p; v.arrays[2] = c->a; v.arrays[3] = c->x; v.arrays[4] = c->q;
+        v.bad = d_counters;
+        unsigned long long bad = 0;
+        if ((e = arena::launch_zero_counters(d_counters, 1, stream)) || (e = arena::launch_validate(v, stream)) ||
+            (e = hipMemcpyAsync(&bad, d_counters, sizeof(bad), hipMemcpyDeviceToHost, stream)) ||
+            (e = hipStreamSynchronize(stream)))
+            return hip_fail(c, e, "job value check");
+        if (bad != 0)
+            return fail(c, ARENA_ERR_INVALID_ARG, "jobs: %llu per-layer values are negative or not finite", bad);
+        c->jobs_checked = true;
+    }
+    if ((e = hipMemcpyAsync(d_types, c->types.data(), sizeof(TypeDev) * T, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(d_counts, c->counts.data(), sizeof(int32_t) * NC, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(d_kappa, c->kappa.data(), sizeof(float) * T * NC, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(d_items, c->h_iorder.data(), sizeof(int32_t) * J * T, hipMemcpyHostToDevice,
+                            stream)) ||
+        (e = hipMemcpyAsync(d_corder, c->h_corder.data(), sizeof(int32_t) * NC, hipMemcpyHostToDevice, stream)))
+        return hip_fail(c, e, "table copy");
+    if (c->tab_k > 0 &&
+        (e = hipMemcpyAsync(d_tab, c->tab.data(), sizeof(double) * c->tab.size(), hipMemcpyHostToDevice, stream)))
+        return hip_fail(c, e, "comm table copy");
+    const arena::EstimateArgs A = estimate_args(c, d_off, d_batch, d_types, d_counts, d_kappa, d_items, d_corder,
+                                                d_queue, d_tab, d_counters, t_iter, thr, plan, cuts, cuts_stride);
+    // zeroed by a kernel, not a memset node
+    if ((e = arena::launch_zero_counters(d_counters, arena::kNumCounters, stream)) ||
+        (e = arena::launch_zero_counters(d_queue, 1, stream)))
+        return hip_fail(c, e, "counter reset");
+    if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
+    c->last_counters = d_counters;
     return ARENA_OK;
 }
 

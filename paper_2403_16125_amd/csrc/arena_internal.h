@@ -131,6 +131,12 @@ struct SchedArgs {
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);
 
+// Scratch of the no-allocation estimate: a statically sized device array,
+// one copy per device.  scratch_address returns its device address on
+// `device`, which must be the current device (looked up once per device).
+constexpr size_t kNoallocScratchBytes = size_t(4) << 20;
+constexpr int kMaxScratchDevices = 64;
+hipError_t scratch_address(int device, void** out);
 hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream);
 hipError_t launch_zero_counters(unsigned long long* counters, int n, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& args, hipStream_t stream);

@@ -22,6 +22,8 @@
 // tree order.
 #include <math.h>
 
+#include <mutex>
+
 #include "arena_internal.h"
 
 namespace arena {
@@ -1868,6 +1870,28 @@ __global__ __launch_bounds__(64) void validate_kernel(ValidateArgs V)
 }
 
 }  // namespace
+
+// The no-allocation estimate's scratch: library-owned tables, work order and
+// counters of one call, on every device the library runs on, held until the
+// process ends.  Host code never passes this name to a kernel (on the host it
+// only stands for the symbol); it uses the address scratch_address returns.
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+hipError_t scratch_address(int device, void** out)
+{
+    static std::mutex mu;
+    static void* addr[kMaxScratchDevices] = {};
+    if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[device] = p;
+    }
+    *out = addr[device];
+    return hipSuccess;
+}
 
 hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
 {

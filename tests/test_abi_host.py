@@ -390,3 +390,14 @@ def test_workspace_limit_out_of_memory(ctx):
     approx = 4 * (J + 1) + 4 * J + 40 * T + 8 * NC + 4 * T * NC + 4 * J * T
     assert approx <= need <= approx + 2560
 
+
+def test_noalloc_rejects_a_workload_beyond_its_scratch(ctx):
+    """The no-allocation entry point takes the same host checks as
+    arena_estimate and rejects a workload whose tables exceed its static
+    scratch with OUT_OF_MEMORY (here 200,000 jobs x 8 types), before any
+    device call."""
+    _expect(4, arena.arena_estimate_noalloc, ctx, FAKE, FAKE, FAKE, match="bind")
+    _bind_host_only(ctx, 200_000)
+    _expect(1, arena.arena_estimate_noalloc, ctx, FAKE, 0, FAKE, match="output")
+    _expect(2, arena.arena_estimate_noalloc, ctx, FAKE, FAKE, FAKE, match="scratch")
+    assert arena.NOALLOC_SCRATCH_BYTES == 4 << 20

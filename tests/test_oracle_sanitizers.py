@@ -169,6 +169,7 @@ int main()
     float* F = (float*)0x1000;        // never dereferenced on the host
     uint32_t* P = (uint32_t*)0x1000;
     EXPECT(arena_estimate(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_NOT_READY);
+    EXPECT(arena_estimate_noalloc(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_NOT_READY);
     EXPECT(arena_bind_jobs(ctx, nullptr), ARENA_ERR_INVALID_ARG);
     const int J = 50000;
     std::vector<int32_t> off(J + 1), bat(J, 64);
@@ -233,6 +234,14 @@ int main()
     EXPECT(arena_set_workspace_limit(ctx, -5), ARENA_ERR_INVALID_ARG);
     EXPECT(arena_set_workspace_limit(ctx, 1 << 20), ARENA_OK);
     EXPECT(arena_estimate(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_OUT_OF_MEMORY);
+    // 50,000 jobs x 8 types: 1.6 MB of work order fit the scratch; 200,000 do not
+    const int J2 = 200000;
+    std::vector<int32_t> off2(J2 + 1), bat2(J2, 64);
+    for (int j = 0; j <= J2; ++j) off2[j] = 4 * j;
+    arena_jobs_desc jd2{J2, 4 * J2, off2.data(), bat2.data(), F, F, F, F, F};
+    EXPECT(arena_bind_jobs(ctx, &jd2), ARENA_OK);
+    EXPECT(arena_estimate_noalloc(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_OUT_OF_MEMORY);
+    EXPECT(arena_estimate(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_OUT_OF_MEMORY);
     arena_counters cn;
     EXPECT(arena_get_counters(ctx, &cn), ARENA_ERR_NOT_READY);
     EXPECT(arena_get_counters(ctx, nullptr), ARENA_ERR_INVALID_ARG);
@@ -259,6 +268,7 @@ hipError_t launch_schedule(const SchedArgs&, hipStream_t) { return hipErrorNoDev
 hipError_t launch_proxy(const ProxyArgs&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_zero_counters(unsigned long long*, int, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_validate(const ValidateArgs&, hipStream_t) { return hipErrorNoDevice; }
+hipError_t scratch_address(int, void**) { return hipErrorNoDevice; }
 }
 """
 
