@@ -34,6 +34,7 @@ constexpr int kSlotsShared = 10;   // 1 pure problem + up to 9 tensor-degree pro
 constexpr int kPad = 8;            // prefix arrays hold +inf past the last layer
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
+constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
 
 struct WaveLds {
     // the wave's current problem, pairs (U_j, D_j): U the cost prefix (+inf
@@ -45,6 +46,8 @@ struct WaveLds {
     int32_t mq[kMaxM];            // those microbatch counts
     double lbnd[kLmax];           // lower bound of the iteration time, by pipeline degree - 1
     uint8_t tq[64];               // a problem's requested degrees, compacted
+    double cand_lb[kMaxCand];     // the cell's tensor-degree problems: least lower bound of their plans
+    uint8_t cand_tp[kMaxCand];    //   and their tensor degree
     uint8_t cutrow[kLmax];        // with cuts on: the cut row of the plan holding the best time
     double cut_T;                 //   that time (+inf: none yet)
     int32_t cut_tp, cut_pp;       //   and its degrees
@@ -56,8 +59,6 @@ struct WaveLds {
         double R[kLmax + 1];                 // memory rule: its recursion row (never live with J)
     };
 };
-
-constexpr int kStageCells = 136;   // counts whose outputs a block stages in LDS
 
 template <int SLOTS>
 struct BlockLds {
@@ -80,11 +81,6 @@ struct BlockLds {
     int32_t next_cell;
     int32_t uniform;              // one kappa for every count of this type
     int32_t moe;
-    // the block's output row (its cells are contiguous in every output
-    // array), written out once all counts are done when it fits
-    float st_t[kStageCells];
-    float st_thr[kStageCells];
-    uint32_t st_plan[kStageCells];
     WaveLds w[kWavesPerBlock];
 };
 
@@ -931,34 +927,50 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     return best_t;
 }
 
+// 1/x to within a few ulps: the hardware estimate refined by one Newton step
+// (only lower bounds use it; their margin of 1e-9 covers it many times over).
+__device__ __forceinline__ double rcp_approx(double x)
+{
+    const double r = __builtin_amdgcn_rcp(x);
+    return fma(fma(-x, r, 1.0), r, r);
+}
+
+// What the lower bounds of one problem's plans share: its tensor degree, n /
+// tp, a lower bound of its summed per-sample layer costs, and the gradient
+// all-reduce seconds per parameter byte over the intra- and inter-node links
+// without the ring factor (kappa 2 / (tp B)).
+struct BoundCtx {
+    int tp, qn;
+    double rtp;
+    double UL;
+    double ar_intra, ar_inter;
+};
+
 // Lower bound of the iteration time of every plan of degree pp (any listed m)
-// of a problem whose per-sample layer costs sum to UL, or +inf when no split
-// of the layers into pp stages fits memory.  Bounded below without the cuts:
+// of problem bc, or +inf when no split of the layers into pp stages fits
+// memory.  Bounded below without the cuts:
 //   W*(pp) >= UL / pp (the stages tile the layers) and >= Wpure(pp) / tp (the
 //   problem's layer costs are at least the pure-compute ones over tp);
 //   the p2p bytes over the pp-1 stage boundaries >= (pp-1) min_l x_l;
 //   the largest stage's parameters >= max(P / pp, max_l p_l).
 // For fixed dp, T = Bg/dp W + Bg/(dp m) (fill - W) + AR falls as m grows
-// (fill >= W), so the largest admissible m gives the bound.  A relative
-// margin of 1e-9 covers rounding.
+// (fill >= W), so the largest admissible m gives the bound.  Reciprocals are
+// estimates; a relative margin of 1e-9 covers them and the rounding.
 template <int SLOTS>
 __device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const TypeDev& ty, const Cell& cell,
-                               unsigned gpn_divs, int tp, int pp, double UL)
+                               unsigned gpn_divs, const BoundCtx& bc, int pp)
 {
-    const int qn = cell.n / tp;
-    const int dp = (int)rintf((float)qn * __builtin_amdgcn_rcpf((float)pp));   // exact: pp divides qn
+    const double rpp = rcp_approx((double)pp);
+    const int dp = (int)rint((double)bc.qn * rpp);                     // exact: pp divides qn
     const int m = B.mmax[dp - 1];
-    const double P = B.Pp[jb.L];
-    const double plb = fmax(P / (double)pp, B.p_layer_max);
-    if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
-    const double b = (double)jb.Bg / (double)(dp * m);
-    const double Wlb = fmax(UL / (double)pp, B.Wtab[0][pp] / (double)tp);
-    const double fill = UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
-    const int grp = dp * tp;
-    const double B_dp = link_bw(grp < 32 && ((gpn_divs >> grp) & 1u), ty);
-    const double ar = dp > 1
-        ? plb * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
-        : 0.0;
+    const double plb = fmax(B.Pp[jb.L] * rpp, B.p_layer_max);
+    if (4.0 * plb > ty.mem * (double)bc.tp * (1.0 + 1e-9)) return kInf;
+    const double b = rint((double)jb.Bg * rcp_approx((double)(dp * m)));   // exact: dp m divides Bg
+    const double Wlb = fmax(bc.UL * rpp, B.Wtab[0][pp] * bc.rtp);
+    const double fill = bc.UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
+    const int grp = dp * bc.tp;
+    const double c_ar = (grp < 32 && ((gpn_divs >> grp) & 1u)) ? bc.ar_intra : bc.ar_inter;
+    const double ar = dp > 1 ? plb * (c_ar * ((double)(dp - 1) * rcp_approx((double)dp))) : 0.0;
     return (b * fill + (double)(m - 1) * (b * Wlb) + ar) * (1.0 - 1e-9);
 }
 
@@ -976,11 +988,12 @@ __device__ __forceinline__ unsigned long long dropped_plans(const BlockLds<SLOTS
 }
 
 // Lower bounds of the degrees in `tm` into Wv.lbnd[pp - 1], one lane per
-// degree (a problem requests at most 32 degrees: the divisors of n / tp).
+// degree (a problem requests at most 32 degrees: the divisors of n / tp);
+// returns the least of them (+inf: no degree fits memory).
 template <int SLOTS>
-__device__ __forceinline__ void degree_bounds(const BlockLds<SLOTS>& B, WaveLds& Wv, const Mask& tm, int lane,
-                                              const JobCtx& jb, const TypeDev& ty, const Cell& cell,
-                                              unsigned gpn_divs, int tp, double UL)
+__device__ __forceinline__ double degree_bounds(const BlockLds<SLOTS>& B, WaveLds& Wv, const Mask& tm, int lane,
+                                                const JobCtx& jb, const TypeDev& ty, const Cell& cell,
+                                                unsigned gpn_divs, const BoundCtx& bc)
 {
     const bool b0 = (tm.lo >> lane) & 1ull, b1 = (tm.hi >> lane) & 1ull;
     const unsigned r0 = __builtin_amdgcn_mbcnt_hi((unsigned)(tm.lo >> 32),
@@ -991,11 +1004,29 @@ __device__ __forceinline__ void degree_bounds(const BlockLds<SLOTS>& B, WaveLds&
     if (b0 && r0 < 64u) Wv.tq[r0] = (uint8_t)(1 + lane);
     if (b1 && r1 < 64u) Wv.tq[r1] = (uint8_t)(65 + lane);
     wave_sync();
+    double lb = kInf;
     if (lane < tm.count()) {
         const int pp = Wv.tq[lane];
-        Wv.lbnd[pp - 1] = target_bound(B, jb, ty, cell, gpn_divs, tp, pp, UL);
+        lb = target_bound(B, jb, ty, cell, gpn_divs, bc, pp);
+        Wv.lbnd[pp - 1] = lb;
     }
     wave_sync();
+    return wave_reduce1<OpMin>(lb);
+}
+
+// The bound context of the cell's problem of tensor degree tp; the pure-
+// compute problem (tp = 1 without all-to-all) takes its exact cost sum.
+__device__ __forceinline__ BoundCtx bound_ctx(const Cell& cell, int tp, double UL, double ar_intra1,
+                                              double ar_inter1)
+{
+    BoundCtx bc;
+    bc.tp = tp;
+    bc.qn = cell.n / tp;
+    bc.rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
+    bc.UL = UL;
+    bc.ar_intra = ar_intra1 * bc.rtp;
+    bc.ar_inter = ar_inter1 * bc.rtp;
+    return bc;
 }
 
 // Slot of the shared problem (tp, variant), -1 if the cell solves its own.
@@ -1023,7 +1054,6 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
     WaveLds& Wv = B.w[wid];
     double* const R = MEM ? Wv.R : nullptr;
 
-    const bool stage = A.n_counts <= kStageCells;
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
     const int off = A.layer_offset[j];
@@ -1165,6 +1195,12 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         int np = 0;
         double best = kInf;          // time of a fitting plan priced so far: bounds the cell's best
         if (lane == 0) Wv.cut_T = kInf;
+        // per-cell pieces of the bounds: all-reduce seconds per byte (tp = 1),
+        // and the tensor-parallel and all-to-all parts of a problem's cost sum
+        const double ar_intra1 = cell.kappa * 2.0 / ty.bw_intra;
+        const double ar_inter1 = cell.kappa * 2.0 / ty.bw_inter;
+        const double ul_tp = cell.kappa * 8.0 * B.x_sum / ty.bw_intra;
+        const double ul_a2a = jb.moe ? cell.kappa * B.q_sum / ty.bw_inter : 0.0;
 
         // plans of the pure-compute problem first: their bottlenecks are shared
         {
@@ -1174,7 +1210,8 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
             if (tm.any()) {
                 // bounds with the exact bottleneck; a degree is priced unless its
                 // bound is past the tie window of the best plan so far
-                degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, 1, B.Upure[jb.L]);
+                degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
+                              bound_ctx(cell, 1, B.Upure[jb.L], ar_intra1, ar_inter1));
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
                     if (A.prune && !(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
@@ -1187,23 +1224,54 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                 }
             }
         }
-        // the other problems, largest tensor degree first; a degree whose
-        // lower bound exceeds the tie window of `best` cannot hold the cell's
-        // plan and is skipped, and the recursion stops after the last degree
-        // still wanted
+        // the other problems, best first: every tensor degree's problem gets the
+        // least lower bound of its plans, then the problem of least bound is
+        // solved while that bound lies within the tie window of `best` (so the
+        // first problem solved is the most promising one and its plans tighten
+        // the window for the rest).  Within a problem a degree whose bound
+        // exceeds the window cannot hold the cell's plan and is skipped, and the
+        // recursion stops after the last degree still wanted.
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
+        int ncand = 0;
         for (int tp = tpmax; tp >= 1; --tp) {
             if (cell.n % tp != 0 || ((gpn_divs >> tp) & 1u) == 0) continue;
             if (tp == 1 && !jb.moe) continue;          // the pure-compute problem
-            Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
-                                  target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
+            const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
+                                        target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
             if (!tm.any()) continue;
             // the layer costs sum to at least this (the job's sums of x and of the
             // all-to-all bytes in the cost formula; margin for the rounding)
-            double ULb = B.Upure[jb.L] / (double)tp +
-                         cell.kappa * 8.0 * (double)(tp - 1) / (double)tp * B.x_sum / ty.bw_intra;
-            if (jb.moe) ULb += cell.kappa * B.q_sum / ty.bw_inter;
-            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, tp, ULb * (1.0 - 1e-12));
+            const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
+            const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
+            const double lb = degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
+                                            bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1));
+            if (lane == 0) {
+                Wv.cand_tp[ncand] = (uint8_t)tp;
+                Wv.cand_lb[ncand] = lb;
+            }
+            ++ncand;
+        }
+        wave_sync();
+        unsigned solved = 0;           // bit c: candidate c has been taken
+        for (;;) {
+            int csel = -1;
+            double lsel = kInf;
+            for (int c = 0; c < ncand; ++c) {
+                const double v = Wv.cand_lb[c];
+                if (!((solved >> c) & 1u) && (csel < 0 || v < lsel)) {
+                    csel = c;
+                    lsel = v;
+                }
+            }
+            if (csel < 0) break;
+            if (A.prune && !(lsel < kInf && lsel <= best * (1.0 + A.tie_eps))) break;
+            solved |= 1u << csel;
+            const int tp = Wv.cand_tp[csel];
+            Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
+                                  target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
+            const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
+            const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
+            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1));
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
             {
                 const double lb0 = Wv.lbnd[lane], lb1 = Wv.lbnd[lane + 64];
@@ -1248,6 +1316,14 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                 tally(Wv, lane, kProblems, 1);
             }
         }
+        // problems never taken: none of their plans can hold the cell's best
+        for (int c = 0; c < ncand; ++c) {
+            if ((solved >> c) & 1u) continue;
+            const int tp = Wv.cand_tp[c];
+            const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
+                                        target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
+            tally(Wv, lane, kSkipped, dropped_plans(B, tm, Mask{0ull, 0ull}, lane, cell.n / tp));
+        }
         wave_sync();
 
         // best plan of the cell: smallest key among plans within the tie window
@@ -1259,15 +1335,9 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         if (!(tmin < kInf)) {
             tally(Wv, lane, kInfeasible, 1);
             if (lane == 0) {
-                if (stage) {
-                    B.st_t[ci] = __builtin_huge_valf();
-                    B.st_thr[ci] = 0.0f;
-                    B.st_plan[ci] = 0u;
-                } else {
-                    A.t_iter[cidx] = __builtin_huge_valf();
-                    A.thr[cidx] = 0.0f;
-                    A.plan[cidx] = 0u;
-                }
+                A.t_iter[cidx] = __builtin_huge_valf();
+                A.thr[cidx] = 0.0f;
+                A.plan[cidx] = 0u;
             }
             if (A.cuts) {
                 uint8_t* row = A.cuts + cidx * A.cuts_stride;
@@ -1295,15 +1365,9 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
             const float tt = (float)Tb, th = (float)((double)jb.Bg / Tb);
             const uint32_t pw = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) |
                                 ((unsigned)m << 24) | (1u << 31);
-            if (stage) {
-                B.st_t[ci] = tt;
-                B.st_thr[ci] = th;
-                B.st_plan[ci] = pw;
-            } else {
-                A.t_iter[cidx] = tt;
-                A.thr[cidx] = th;
-                A.plan[cidx] = pw;
-            }
+            A.t_iter[cidx] = tt;
+            A.thr[cidx] = th;
+            A.plan[cidx] = pw;
         }
         const bool kept = Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf &&
                           (!MEM || (Wv.cut_m == 0 ? m >= Wv.cut_mfit : Wv.cut_m == m));
@@ -1362,15 +1426,6 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         wave_sync();
     }
 
-    if (stage) {
-        __syncthreads();
-        const long long base = ((long long)j * A.n_types + g) * A.n_counts;
-        for (int e = tid; e < A.n_counts; e += 256) {
-            A.t_iter[base + e] = B.st_t[e];
-            A.thr[base + e] = B.st_thr[e];
-            A.plan[base + e] = B.st_plan[e];
-        }
-    }
     if (lane == 0) {
         if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
         const unsigned long long* t = Wv.tally;
