@@ -15,7 +15,9 @@ the same 16384 x 8 x 131 shape, and prints that line.  With
 trace-like workload and scores its plans against the exhaustive estimate.
 With --partition memory the estimate prices each plan with the balanced
 partition among the stage splits that fit memory instead of the balanced
-partition followed by the memory check.  With --comm-tables communication
+partition followed by the memory check; with --partition exact-t on the split
+of least iteration time among those that fit (trace-like workload: jobs of
+at most 96 layers).  With --comm-tables communication
 latency is interpolated in synthetic profiled (volume, latency) tables per
 link instead of volume / bandwidth.
 """
@@ -94,7 +96,7 @@ def _oracle_threads(fn, ids, threads: int) -> float:
     return time.perf_counter() - t0
 
 
-def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None) -> dict:
+def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None, cell_every: int = 1) -> dict:
     """The oracle (C, fp64, one cell at a time) on a bounded sample of the
     same workload: jobs j = 0, every, 2*every, ... times every grid of one
     round, under partition rule `rule` or with communication latency from
@@ -106,7 +108,7 @@ def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None
     info = host_info()
     per = w.n_types * w.n_counts
     jobs = list(range(0, w.n_jobs, every))
-    ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)
+    ids = np.concatenate([np.arange(j * per, (j + 1) * per) for j in jobs]).astype(np.int64)[::cell_every]
 
     def run(sub):
         if tables is None:
@@ -117,8 +119,10 @@ def cpu_baseline(w, every: int, kappa_round: int = 0, rule: int = 0, tables=None
     dt_all = _oracle_threads(run, ids, info["threads"])
     dt_one = _oracle_threads(run, ids, 1)
     return {"value": len(ids) / dt_all, "unit": "cells/s", "cores": info["threads"], "kind": "oracle",
-            "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids, contention round {kappa_round}: "
-                      f"{len(ids)} cells, {dt_all:.1f} s on {info['threads']} threads, {dt_one:.1f} s on one",
+            "sample": f"{len(jobs)} jobs (every {every}th) x {per} grids"
+                      + (f", every {cell_every}th of those cells" if cell_every > 1 else "")
+                      + f", contention round {kappa_round}: {len(ids)} cells, {dt_all:.1f} s on {info['threads']} "
+                        f"threads, {dt_one:.1f} s on one",
             "single_core": {"value": len(ids) / dt_one, "unit": "cells/s", "cores": 1},
             "host": info}
 
@@ -346,8 +350,9 @@ def main() -> int:
     ap.add_argument("--cpu-every", type=int, default=None,
                     help="oracle sample: every k-th job (default 256; 2048 with --partition memory, "
                          "1024 with --comm-tables)")
-    ap.add_argument("--partition", default="balanced", choices=["balanced", "memory"],
-                    help="stage partition rule of the estimate")
+    ap.add_argument("--partition", default="balanced", choices=["balanced", "memory", "exact-t"],
+                    help="stage partition rule of the estimate (exact-t: the trace-like workload unless "
+                         "--workload names another of at most 96 layers per job)")
     ap.add_argument("--comm-tables", action="store_true",
                     help="communication latency from synthetic profiled tables (interpolated by volume)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -391,6 +396,8 @@ def main() -> int:
         print(json.dumps({"copy_calibration_bytes": COPY_BYTES}), flush=True)
         return 0
 
+    if args.partition == "exact-t" and args.workload == "full":
+        args.workload = "trace"             # the exact-T rule takes jobs of at most 96 layers
     log(f"generating workload {args.workload}")
     w = workloads.make(args.workload)
     log(f"{w.n_jobs} jobs, {w.n_types} types, {w.n_counts} counts, {w.n_cells} cells, "
@@ -401,7 +408,8 @@ def main() -> int:
         f"{work['ops_truncated']:.4g} ops")
 
     dev = torch.device("cuda", 0)
-    rule = arena.PARTITION_MEMORY if args.partition == "memory" else arena.PARTITION_BALANCED
+    rule = {"balanced": arena.PARTITION_BALANCED, "memory": arena.PARTITION_MEMORY,
+            "exact-t": arena.PARTITION_EXACT_T}[args.partition]
     tables = workloads.comm_tables(w) if args.comm_tables else None
     if tables is not None and rule != arena.PARTITION_BALANCED:
         print("--comm-tables works with the balanced partition only", file=sys.stderr, flush=True)
@@ -507,8 +515,9 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
-        every = args.cpu_every or (256 if plain else (1024 if tables is not None else 2048))
-        line["cpu_baseline"] = cpu_baseline(w, every, rule=rule, tables=tables)
+        exact = rule == arena.PARTITION_EXACT_T
+        every = args.cpu_every or (256 if plain else (1024 if tables is not None or exact else 2048))
+        line["cpu_baseline"] = cpu_baseline(w, every, rule=rule, tables=tables, cell_every=10 if exact else 1)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -186,6 +186,8 @@ arena_status arena_set_bound_pruning(arena_ctx* ctx, int32_t enabled);
 /* Partition rules (arena_set_partition_rule). */
 #define ARENA_PARTITION_BALANCED 0
 #define ARENA_PARTITION_MEMORY 1
+#define ARENA_PARTITION_EXACT_T 2
+#define ARENA_EXACT_T_MAX_LAYERS 96   /* layers per job under ARENA_PARTITION_EXACT_T */
 
 /* Which stage partition prices a plan (default ARENA_PARTITION_BALANCED).
  *   BALANCED  the canonical balanced partition (Sec. 3.2: a pipeline runs at
@@ -199,6 +201,23 @@ arena_status arena_set_bound_pruning(arena_ctx* ctx, int32_t enabled);
  *             largest stage cost.  A plan is infeasible only when no split
  *             fits.  Plans whose balanced split fits are priced as under
  *             BALANCED, so no cell gets slower; cut rows follow the rule.
+ *   EXACT_T   the split of least iteration time: the whole 1F1B time of Sec.
+ *             3.4 (with Eq. 4's all-reduce) among the splits whose every
+ *             stage fits memory (the MEMORY rule's test, a stage's bytes as
+ *             differences of running totals).  The stage costs summed over
+ *             the stages do not depend on the split, so it minimises
+ *             Phi = ((m-1) b Smax + cX X) + cP Pmax, evaluated in that order:
+ *             Smax the slowest stage per sample, X = x_{c_1-1} + (x_{c_2-1} +
+ *             ...) the boundary bytes added from the back, Pmax the largest
+ *             stage's parameter bytes, cX = kappa 2 b / B_pp, cP = kappa 2
+ *             (dp-1)/dp / (tp B_dp) (0 when dp = 1).  Ties: the least (Phi,
+ *             Smax, Pmax, X), then the lexicographically smallest cuts.  No
+ *             cell is slower than under MEMORY, and the cell's best time
+ *             never grows with a link bandwidth.  t_iter = b U_L + Phi.
+ *             Jobs of at most ARENA_EXACT_T_MAX_LAYERS layers (the exact
+ *             method visits pairs of thresholds, each a recursion over
+ *             stages); arena_estimate returns UNSUPPORTED beyond, and with
+ *             comm tables.
  * Takes effect at the next arena_estimate; INVALID_ARG for other values. */
 arena_status arena_set_partition_rule(arena_ctx* ctx, int32_t rule);
 

@@ -412,30 +412,380 @@ static int build_views(int j, int g, const int32_t* off, const float* t, const f
     return (jb->L >= 1 && jb->L <= ORACLE_MAX_L) ? 0 : -1;
 }
 
+/* ------------------------------------------------------------------ */
+/* Exact-T stage partition                                             */
+/* ------------------------------------------------------------------ */
+
+/* The stages that minimise the plan's whole iteration time (Sec. 3.4: first
+ * microbatch through every stage, B-1 more on the slowest, point-to-point
+ * overlapped in the steady state; Eq. 4's once-per-iteration all-reduce).
+ * The stage times summed over the stages are the same for every cut vector
+ * (the stages tile the layers), so the cut-dependent part of T is
+ *   Phi = (cS Smax + cX X) + cP Pmax, evaluated in that order, where
+ *   Smax = max_k (U_{c_{k+1}} - U_{c_k})       slowest stage, per sample
+ *   X    = x_{c_1 - 1} + (x_{c_2 - 1} + (... + x_{c_{pp-1} - 1}))   boundary bytes
+ *   Pmax = max_k P_k                           largest stage's parameter bytes
+ *   cS   = (m-1) b,   cX = kappa 2 b / B_pp,   cP = kappa 2 (dp-1) / dp / (tp B_dp)
+ *          (cP = 0 when dp = 1), the coefficients of the steady state, the
+ *          point-to-point fill and the all-reduce in the pricing.
+ * Only cut vectors whose every stage fits memory count (the memory rule's
+ * test, with a stage's parameter and activation bytes taken as differences of
+ * the running totals over the layers).
+ * Ties: the least (Phi, Smax, Pmax, X), then the lexicographically smallest
+ * cut vector. */
+typedef struct {
+    const double* U;
+    const omem* M;
+    const double* x;        /* boundary activation bytes of each layer */
+    int L, pp;
+    double cS, cX, cP;
+    double segP[ORACLE_MAX_L + 1][ORACLE_MAX_L + 1];   /* [lo][hi]: parameter bytes of [lo, hi) */
+    double segA[ORACLE_MAX_L + 1][ORACLE_MAX_L + 1];   /* [lo][hi]: activation bytes per sample */
+} oext;
+
+typedef struct { double phi, s, p, x; } okey;
+
+static int okey_less(const okey* a, const okey* b)
+{
+    if (a->phi != b->phi) return a->phi < b->phi;
+    if (a->s != b->s) return a->s < b->s;
+    if (a->p != b->p) return a->p < b->p;
+    return a->x < b->x;
+}
+
+static double ext_phi(const oext* E, double sm, double x, double pm)
+{
+    return (E->cS * sm + E->cX * x) + E->cP * pm;
+}
+
+/* A stage's parameter and activation bytes under this rule: differences of
+ * the running totals over the layers (summed left to right), like its cost. */
+static void ext_tables(oext* E)
+{
+    double Pp[ORACLE_MAX_L + 1], Ap[ORACLE_MAX_L + 1];
+    Pp[0] = 0.0;
+    Ap[0] = 0.0;
+    for (int l = 0; l < E->L; ++l) {
+        Pp[l + 1] = Pp[l] + E->M->p[l];
+        Ap[l + 1] = Ap[l] + E->M->a[l];
+    }
+    for (int lo = 0; lo <= E->L; ++lo)
+        for (int hi = lo; hi <= E->L; ++hi) {
+            E->segP[lo][hi] = Pp[hi] - Pp[lo];
+            E->segA[lo][hi] = Ap[hi] - Ap[lo];
+        }
+}
+
+/* Stage [lo, hi) as stage k (0-based) of pp fits memory (the memory rule's test). */
+static int ext_fits(const oext* E, int lo, int hi, int k)
+{
+    return fits_sums(E->M, E->segP[lo][hi], E->segA[lo][hi], k, E->pp);
+}
+
+/* Brute force, the definition written out: every cut vector in lexicographic
+ * order, the first with the least key among those whose stages all fit.
+ * Returns Phi (+inf if none fits); cuts, key filled. */
+typedef struct {
+    const oext* E;
+    int cur[ORACLE_MAX_L + 1];
+    int best[ORACLE_MAX_L + 1];
+    okey bkey;
+    int found;
+} oext_bf;
+
+static void ext_bf_rec(oext_bf* b, int k)
+{
+    const oext* E = b->E;
+    if (k == E->pp) {
+        b->cur[k] = E->L;
+        for (int q = 0; q < E->pp; ++q)
+            if (!ext_fits(E, b->cur[q], b->cur[q + 1], q)) return;
+        double sm = -INFINITY, pm = -INFINITY, x = 0.0;
+        for (int q = 0; q < E->pp; ++q) {
+            double sv = seg(E->U, b->cur[q], b->cur[q + 1]);
+            double pv = E->segP[b->cur[q]][b->cur[q + 1]];
+            if (sv > sm) sm = sv;
+            if (pv > pm) pm = pv;
+        }
+        for (int q = E->pp - 1; q >= 1; --q) x = E->x[b->cur[q] - 1] + x;
+        okey key = {ext_phi(E, sm, x, pm), sm, pm, x};
+        if (!b->found || okey_less(&key, &b->bkey)) {
+            b->bkey = key;
+            b->found = 1;
+            memcpy(b->best, b->cur, sizeof(int) * (size_t)(E->pp + 1));
+        }
+        return;
+    }
+    for (int c = b->cur[k - 1] + 1; c <= E->L - (E->pp - k); ++c) {
+        b->cur[k] = c;
+        ext_bf_rec(b, k + 1);
+    }
+}
+
+static double exact_t_bruteforce(const oext* E, int* cuts, okey* key)
+{
+    oext_bf* b = (oext_bf*)xrealloc(NULL, sizeof(oext_bf));
+    b->E = E;
+    b->found = 0;
+    b->cur[0] = 0;
+    ext_bf_rec(b, 1);
+    double phi = INFINITY;
+    if (b->found) {
+        phi = b->bkey.phi;
+        if (key) *key = b->bkey;
+        for (int k = 1; k < E->pp; ++k) cuts[k - 1] = b->best[k];
+    }
+    free(b);
+    return phi;
+}
+
+/* Stage [i, e) allowed as stage k under the thresholds: its per-sample cost
+ * at most tS, its parameter bytes at most tP, and it fits memory. */
+static int ext_allowed(const oext* E, int i, int e, int k, double tS, double tP)
+{
+    return seg(E->U, i, e) <= tS && E->segP[i][e] <= tP && ext_fits(E, i, e, k);
+}
+
+/* Least X over the splits whose stages are all allowed, by a recursion over
+ * suffixes: H[t][i] = least X of layers [i, L) as the last t stages (stage
+ * pp - t first), with H[1][i] = 0 when [i, L) is allowed as the last stage and
+ *   H[t][i] = min over e of x_{e-1} + H[t-1][e],  [i, e) allowed as stage pp-t.
+ * (The sum is accumulated from the back, as X is defined.)  +inf if none. */
+static double ext_xmin(const oext* E, double tS, double tP, double* H)
+{
+    int L = E->L, L1 = L + 1, pp = E->pp;
+    for (int t = 0; t <= pp; ++t)
+        for (int i = 0; i <= L; ++i) H[t * L1 + i] = INFINITY;
+    for (int i = 0; i < L; ++i)
+        if (ext_allowed(E, i, L, pp - 1, tS, tP)) H[1 * L1 + i] = 0.0;
+    for (int t = 2; t <= pp; ++t)
+        for (int i = 0; i <= L - t; ++i) {
+            double best = INFINITY;
+            for (int e = i + 1; e <= L - t + 1; ++e) {
+                double h = H[(t - 1) * L1 + e];
+                if (h == INFINITY || !ext_allowed(E, i, e, pp - t, tS, tP)) continue;
+                double v = E->x[e - 1] + h;
+                if (v < best) best = v;
+            }
+            H[t * L1 + i] = best;
+        }
+    return H[pp * L1 + 0];
+}
+
+/* Least largest stage value over the splits whose stages are allowed under
+ * (tS, tP): F[t][i] = min over e of max(V(i, e), F[t-1][e]), F[1][i] = V(i, L),
+ * as ext_xmin; V the stage's parameter bytes (which = 1) or its per-sample
+ * cost (which = 0). */
+static double ext_minmax(const oext* E, int which, double tS, double tP, double* F)
+{
+    int L = E->L, L1 = L + 1, pp = E->pp;
+    for (int t = 0; t <= pp; ++t)
+        for (int i = 0; i <= L; ++i) F[t * L1 + i] = INFINITY;
+    for (int i = 0; i < L; ++i)
+        if (ext_allowed(E, i, L, pp - 1, tS, tP)) F[1 * L1 + i] = which ? E->segP[i][L] : seg(E->U, i, L);
+    for (int t = 2; t <= pp; ++t)
+        for (int i = 0; i <= L - t; ++i) {
+            double best = INFINITY;
+            for (int e = i + 1; e <= L - t + 1; ++e) {
+                double f = F[(t - 1) * L1 + e];
+                if (f == INFINITY || !ext_allowed(E, i, e, pp - t, tS, tP)) continue;
+                double vs = which ? E->segP[i][e] : seg(E->U, i, e);
+                double v = vs > f ? vs : f;
+                if (v < best) best = v;
+            }
+            F[t * L1 + i] = best;
+        }
+    return F[pp * L1 + 0];
+}
+
+static int cmp_double(const void* a, const void* b)
+{
+    double x = *(const double*)a, y = *(const double*)b;
+    return (x > y) - (x < y);
+}
+
+/* Sorted distinct values of v[lo][hi] (0 <= lo < hi <= L) or of the U segments. */
+static int ext_candidates(const oext* E, int which, double* out)
+{
+    int n = 0;
+    for (int lo = 0; lo < E->L; ++lo)
+        for (int hi = lo + 1; hi <= E->L; ++hi)
+            out[n++] = which == 0 ? seg(E->U, lo, hi) : E->segP[lo][hi];
+    qsort(out, (size_t)n, sizeof(double), cmp_double);
+    int u = 0;
+    for (int i = 0; i < n; ++i)
+        if (u == 0 || out[i] != out[u - 1]) out[u++] = out[i];
+    return u;
+}
+
+/* Exact-T by thresholds: for every pair (tS, tP) of a segment cost and a
+ * segment parameter sum, the least X of the splits within them gives the key
+ * ((cS tS + cX X) + cP tP, tS, tP, X); the least key over the pairs is the
+ * least key over the splits (a split is counted at the pair of its own
+ * maxima, and a pair's best split is no worse than the pair's key).  Pairs
+ * are visited by tS, then tP, ascending; a pair after the best key found so
+ * far in that order wins only with a smaller Phi, so the visit stops where a
+ * lower bound of Phi reaches the best:
+ *   tS runs from the least Smax of any split that fits; each tS stops the
+ *   visit once (cS tS + cX Xlo) + cP Plo reaches the best (Xlo, Plo the least
+ *   X and Pmax of any split that fits), or, when cS = 0, once the best equals
+ *   the least Phi of any split;
+ *   tP runs from the least Pmax of the splits within tS and stops once
+ *   (cS tS + cX Xs) + cP tP reaches the best (Xs the least X within tS) or
+ *   once its X is Xs.
+ * The cuts are the lexicographically smallest split of least X within the
+ * best pair, chosen left to right on the suffix table. */
+static double exact_t(const oext* E, int* cuts, okey* key)
+{
+    int L = E->L, L1 = L + 1, pp = E->pp;
+    size_t nc = (size_t)L * (size_t)(L + 1) / 2;
+    double* cs = (double*)xrealloc(NULL, sizeof(double) * nc);
+    double* cp = (double*)xrealloc(NULL, sizeof(double) * nc);
+    double* H = (double*)xrealloc(NULL, sizeof(double) * (size_t)(pp + 1) * (size_t)L1);
+    int ns = ext_candidates(E, 0, cs), np = ext_candidates(E, 1, cp);
+    okey best = {INFINITY, INFINITY, INFINITY, INFINITY};
+    int found = 0;
+    double bs = 0.0, bp = 0.0;
+    double p_lo = ext_minmax(E, 1, INFINITY, INFINITY, H);
+    if (p_lo < INFINITY) {
+        double s_lo = ext_minmax(E, 0, INFINITY, INFINITY, H);
+        double x_lo = ext_xmin(E, INFINITY, INFINITY, H);
+        /* cS = 0: the least Phi of any split, (cX X) + cP tP over tP */
+        double phi_all = INFINITY;
+        if (E->cS == 0.0) {
+            for (int q = 0; q < np; ++q) {
+                double tP = cp[q];
+                if (tP < p_lo) continue;
+                double X = ext_xmin(E, INFINITY, tP, H);
+                if (X == INFINITY) continue;
+                double v = (0.0 + E->cX * X) + E->cP * tP;
+                if (v < phi_all) phi_all = v;
+                if (X == x_lo) break;
+            }
+        }
+        for (int a = 0; a < ns; ++a) {
+            double tS = cs[a];
+            if (tS < s_lo) continue;
+            if (found && (E->cS == 0.0 ? best.phi <= phi_all : ext_phi(E, tS, x_lo, p_lo) >= best.phi)) break;
+            double pmin = ext_minmax(E, 1, tS, INFINITY, H);
+            if (pmin == INFINITY) continue;
+            double xs = ext_xmin(E, tS, INFINITY, H);
+            for (int q = 0; q < np; ++q) {
+                double tP = cp[q];
+                if (tP < pmin) continue;
+                if (found && ext_phi(E, tS, xs, tP) >= best.phi) break;
+                double X = ext_xmin(E, tS, tP, H);
+                if (X == INFINITY) continue;
+                okey k = {ext_phi(E, tS, X, tP), tS, tP, X};
+                if (!found || okey_less(&k, &best)) {
+                    best = k;
+                    bs = tS;
+                    bp = tP;
+                    found = 1;
+                }
+                if (X == xs) break;
+            }
+        }
+    }
+    double phi = INFINITY;
+    if (found) {
+        phi = best.phi;
+        if (key) *key = best;
+        ext_xmin(E, bs, bp, H);
+        int i = 0;
+        for (int k = 1; k < pp; ++k) {
+            int t = pp - k + 1, c = -1;
+            for (int e = i + 1; e <= L - t + 1; ++e) {
+                double h = H[(t - 1) * L1 + e];
+                if (h == INFINITY || !ext_allowed(E, i, e, k - 1, bs, bp)) continue;
+                if (E->x[e - 1] + h == H[t * L1 + i]) { c = e; break; }
+            }
+            if (c < 0) {
+                fprintf(stderr, "arena oracle: exact-T cut reconstruction failed\n");
+                abort();
+            }
+            cuts[k - 1] = c;
+            i = c;
+        }
+    }
+    free(cs);
+    free(cp);
+    free(H);
+    return phi;
+}
+
+/* The coefficients of Phi for plan (dp, tp, pp, m) of a cell of n GPUs. */
+static void ext_coefs(const ojob* jb, const otype* ty, int n, double kappa, int dp, int tp, int m, double* cS,
+                      double* cX, double* cP)
+{
+    double b = (double)jb->Bg / (double)(dp * m);
+    double B_pp = (n <= ty->gpn) ? ty->bw_intra : ty->bw_inter;
+    int grp = dp * tp;
+    double B_dp = (grp <= ty->gpn && ty->gpn % grp == 0) ? ty->bw_intra : ty->bw_inter;
+    *cS = (double)(m - 1) * b;
+    *cX = kappa * 2.0 * b / B_pp;
+    *cP = dp > 1 ? kappa * 2.0 * (double)(dp - 1) / (double)dp / ((double)tp * B_dp) : 0.0;
+}
+
+/* Exposed for tests: the exact-T partition of one problem.  U: the per-sample
+ * cost prefix; p, a, x: per-layer bytes; memory of the plan (m, b, tp, mem);
+ * coefficients cS, cX, cP.  brute: enumerate every cut vector.  Returns Phi
+ * (+inf if no split fits); cuts receives pp - 1 cuts and out[0..3] the key
+ * (Phi, Smax, Pmax, X). */
+double oracle_exact_t(const double* U, const double* p, const double* a, const double* x, int L, int pp,
+                      int m, double b, int tp, double mem, double cS, double cX, double cP, int brute,
+                      int* cuts, double* out)
+{
+    if (L < 1 || pp < 1 || pp > L || L > ORACLE_MAX_L || m < 1 || tp < 1) return NAN;
+    omem M;
+    M.p = p; M.a = a; M.L = L; M.m = m; M.tp = tp; M.b = b; M.mem = mem;
+    oext* E = (oext*)xrealloc(NULL, sizeof(oext));
+    E->U = U; E->M = &M; E->x = x; E->L = L; E->pp = pp; E->cS = cS; E->cX = cX; E->cP = cP;
+    ext_tables(E);
+    okey key = {INFINITY, INFINITY, INFINITY, INFINITY};
+    double phi = brute ? exact_t_bruteforce(E, cuts, &key) : exact_t(E, cuts, &key);
+    if (out) { out[0] = key.phi; out[1] = key.s; out[2] = key.p; out[3] = key.x; }
+    free(E);
+    return phi;
+}
+
 /* Price one plan of one cell.  If cuts_in is NULL the partition is the
  * canonical optimal one; otherwise cuts_in (pp-1 first-layer indices of
  * stages 1..pp-1) is priced as given.  out[0..3] = T, mem_max, s_max,
  * feasible; cuts_out (nullable) receives the cuts used.  Returns 0 on
  * success. */
-/* The stage cuts of plan (dp, tp, pp, m) under partition rule `rule`:
+/* The stage cuts of plan (dp, tp, pp, m) of a cell of n GPUs under partition
+ * rule `rule`:
  * 0 = the canonical balanced partition (memory checked after pricing),
- * 1 = the canonical balanced partition among those whose every stage fits.
- * Returns 0, or -1 when rule 1 finds no split that fits. */
-static int plan_cuts(const ojob* jb, const otype* ty, int rule, int dp, int tp, int pp, int m,
-                     const double* U, int* cuts)
+ * 1 = the canonical balanced partition among those whose every stage fits,
+ * 2 = the exact-T partition (least iteration time among those that fit).
+ * Returns 0, or -1 when rule 1 or 2 finds no split that fits. */
+static int plan_cuts(const ojob* jb, const otype* ty, int rule, int n, double kappa, int dp, int tp, int pp,
+                     int m, const double* U, int* cuts)
 {
     if (rule == 0) {
         double W = oracle_bottleneck_dp(U, jb->L, pp);
         oracle_canonical_cuts(U, jb->L, pp, W, cuts);
         return 0;
     }
-    double pd[ORACLE_MAX_L], ad[ORACLE_MAX_L];
-    for (int l = 0; l < jb->L; ++l) { pd[l] = (double)jb->p[l]; ad[l] = (double)jb->a[l]; }
-    omem M;
-    M.p = pd; M.a = ad; M.L = jb->L; M.m = m; M.tp = tp;
-    M.b = (double)jb->Bg / (double)(dp * m);
-    M.mem = ty->mem;
-    return bottleneck_mem(U, &M, pp, cuts) < INFINITY ? 0 : -1;
+    double pd[ORACLE_MAX_L], ad[ORACLE_MAX_L], xd[ORACLE_MAX_L];
+    for (int l = 0; l < jb->L; ++l) {
+        pd[l] = (double)jb->p[l];
+        ad[l] = (double)jb->a[l];
+        xd[l] = (double)jb->x[l];
+    }
+    double b = (double)jb->Bg / (double)(dp * m);
+    if (rule == 1) {
+        omem M;
+        M.p = pd; M.a = ad; M.L = jb->L; M.m = m; M.tp = tp;
+        M.b = b;
+        M.mem = ty->mem;
+        return bottleneck_mem(U, &M, pp, cuts) < INFINITY ? 0 : -1;
+    }
+    double cS, cX, cP;
+    ext_coefs(jb, ty, n, kappa, dp, tp, m, &cS, &cX, &cP);
+    double phi = oracle_exact_t(U, pd, ad, xd, jb->L, pp, m, b, tp, ty->mem, cS, cX, cP, 0, cuts, NULL);
+    return phi < INFINITY ? 0 : -1;
 }
 
 int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, int m,
@@ -448,7 +798,7 @@ int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, 
     ojob jb; otype ty;
     if (build_views(j, g, off, t, p, a, x, a2a, batch, speed, mem, bwi, bwe, gpn, &jb, &ty)) return -1;
     if (dp < 1 || tp < 1 || pp < 1 || m < 1 || dp * tp * pp != n || pp > jb.L) return -1;
-    if (rule != 0 && rule != 1) return -1;
+    if (rule < 0 || rule > 2) return -1;
     double u[ORACLE_MAX_L], U[ORACLE_MAX_L + 1];
     int cuts[ORACLE_MAX_L];
     layer_costs(&jb, &ty, kappa, dp, tp, u);
@@ -459,8 +809,8 @@ int oracle_eval_plan(int j, int g, int n, double kappa, int dp, int tp, int pp, 
             int prevc = k == 0 ? 0 : cuts[k - 1];
             if (cuts[k] <= prevc || cuts[k] >= jb.L) return -1;
         }
-    } else if (plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) != 0) {
-        /* rule 1 and no split fits memory */
+    } else if (plan_cuts(&jb, &ty, rule, n, kappa, dp, tp, pp, m, U, cuts) != 0) {
+        /* rule 1 or 2 and no split fits memory */
         out[0] = INFINITY; out[1] = INFINITY; out[2] = INFINITY; out[3] = 0.0;
         return 0;
     }
@@ -529,13 +879,13 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
             layer_costs(&jb, &ty, kappa, dp, tp, u);
             oracle_prefix(u, L, U);
             /* the balanced partition does not depend on m: solved once per degree */
-            if (rule == 0) plan_cuts(&jb, &ty, 0, dp, tp, pp, 1, U, cuts);
+            if (rule == 0) plan_cuts(&jb, &ty, 0, n, kappa, dp, tp, pp, 1, U, cuts);
             for (int mi = 0; mi < n_m; ++mi) {
                 int m = m_values[mi];
                 if (jb.Bg % (dp * m) != 0) continue;
                 if (nc == cap) { cap *= 2; cand = (ocand*)xrealloc(cand, sizeof(ocand) * (size_t)cap); }
                 cand[nc].dp = dp; cand[nc].tp = tp; cand[nc].pp = pp; cand[nc].m = m;
-                if (rule == 0 || plan_cuts(&jb, &ty, rule, dp, tp, pp, m, U, cuts) == 0) {
+                if (rule == 0 || plan_cuts(&jb, &ty, rule, n, kappa, dp, tp, pp, m, U, cuts) == 0) {
                     oplan r = price_plan(&jb, &ty, n, kappa, dp, tp, pp, m, U, cuts);
                     cand[nc].T = r.T;
                     cand[nc].feasible = r.feasible;
@@ -570,7 +920,7 @@ int oracle_cell(int j, int g, int ci, const int32_t* off, const float* t, const 
         if (cuts_out) {
             layer_costs(&jb, &ty, kappa, w->dp, w->tp, u);
             oracle_prefix(u, L, U);
-            plan_cuts(&jb, &ty, rule, w->dp, w->tp, w->pp, w->m, U, cuts);
+            plan_cuts(&jb, &ty, rule, n, kappa, w->dp, w->tp, w->pp, w->m, U, cuts);
             for (int k = 0; k < w->pp - 1; ++k) cuts_out[k] = cuts[k];
         }
     }
@@ -590,7 +940,7 @@ int oracle_cells(int n_sel, const int64_t* cells, int n_types, int n_counts,
                  double* res, int32_t* plan, int32_t* cuts, int cuts_stride, int32_t* nplans,
                  int rule)
 {
-    if (rule != 0 && rule != 1) return -1;
+    if (rule < 0 || rule > 2) return -1;
     for (int s = 0; s < n_sel; ++s) {
         int64_t c = cells[s];
         int ci = (int)(c % n_counts);

@@ -63,6 +63,9 @@ def load():
     lib.oracle_bottleneck_mem.argtypes = [_f64p, _f64p, _f64p, c_int, c_int, c_int, c_double, c_int,
                                           c_double, c_int, _i32p]
     lib.oracle_bottleneck_mem.restype = c_double
+    lib.oracle_exact_t.argtypes = [_f64p, _f64p, _f64p, _f64p, c_int, c_int, c_int, c_double, c_int, c_double,
+                                   c_double, c_double, c_double, c_int, _i32p, _f64p]
+    lib.oracle_exact_t.restype = c_double
     lib.oracle_eval_plan.argtypes = [c_int, c_int, c_int, c_double, c_int, c_int, c_int, c_int] + tables + [
         ctypes.c_void_p, ctypes.c_void_p, _f64p, c_int]
     lib.oracle_eval_plan.restype = c_int
@@ -127,6 +130,26 @@ def bottleneck_mem(U, p, a, pp: int, m: int, b: float, tp: int, mem: float, brut
     return w, [int(c) for c in cuts[:pp - 1]]
 
 
+def exact_t(U, p, a, x, pp: int, m: int, b: float, tp: int, mem: float, cS: float, cX: float, cP: float,
+            brute: bool = False):
+    """The exact-T partition of one problem: among the cut vectors whose every
+    stage fits memory, the least Phi = (cS Smax + cX X) + cP Pmax (ties: least
+    Smax, Pmax, X, then the lexicographically smallest cuts).  Returns
+    (Phi, cuts, (Phi, Smax, Pmax, X)); Phi = inf and cuts None when no split
+    fits.  brute=True enumerates every cut vector."""
+    U = np.ascontiguousarray(U, np.float64)
+    p = np.ascontiguousarray(p, np.float64)
+    a = np.ascontiguousarray(a, np.float64)
+    x = np.ascontiguousarray(x, np.float64)
+    cuts = np.zeros(max(pp - 1, 1), np.int32)
+    out = np.zeros(4, np.float64)
+    phi = load().oracle_exact_t(U, p, a, x, len(U) - 1, int(pp), int(m), float(b), int(tp), float(mem),
+                                float(cS), float(cX), float(cP), int(bool(brute)), cuts, out)
+    if not np.isfinite(phi):
+        return phi, None, None
+    return phi, [int(c) for c in cuts[:pp - 1]], tuple(float(v) for v in out)
+
+
 # ------------------------------------------------------------ workload access
 
 def _tables(w):
@@ -146,9 +169,10 @@ def layer_costs(w, j, g, kappa, dp, tp) -> np.ndarray:
 
 
 def eval_plan(w, j, g, n, kappa, dp, tp, pp, m, cuts=None, rule: int = 0):
-    """Price one plan.  cuts=None uses the canonical balanced partition of the
-    partition rule (0: balanced, memory checked after; 1: balanced among the
-    splits that fit memory).  Returns dict(T, mem_max, s_max, feasible, cuts)."""
+    """Price one plan.  cuts=None uses the partition of the partition rule (0:
+    balanced, memory checked after; 1: balanced among the splits that fit
+    memory; 2: exact-T, the least iteration time among the splits that fit).
+    Returns dict(T, mem_max, s_max, feasible, cuts)."""
     out = np.zeros(4, np.float64)
     cuts_out = np.zeros(max(pp - 1, 1), np.int32)
     cin = None

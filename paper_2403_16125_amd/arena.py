@@ -38,6 +38,8 @@ NOALLOC_SCRATCH_BYTES = 4 << 20
 
 PARTITION_BALANCED = 0
 PARTITION_MEMORY = 1
+PARTITION_EXACT_T = 2
+EXACT_T_MAX_LAYERS = 96
 SCHED_THROUGHPUT = 0
 SCHED_FAIRNESS = 1
 _OBJECTIVES = {"throughput": SCHED_THROUGHPUT, "fairness": SCHED_FAIRNESS}

@@ -20,6 +20,7 @@
 using arena::TypeDev;
 
 static_assert(ARENA_NOALLOC_SCRATCH_BYTES == arena::kNoallocScratchBytes, "scratch size of the header and the kernels");
+static_assert(ARENA_EXACT_T_MAX_LAYERS == arena::kExactTMaxLayers, "exact-T layer limit of the header and the kernels");
 
 struct arena_ctx {
     int device = 0;
@@ -621,8 +622,9 @@ arena_status arena_set_partition_rule(arena_ctx* c, int32_t rule)
 {
     if (!c) return ARENA_ERR_INVALID_ARG;
     c->err.clear();
-    if (rule != ARENA_PARTITION_BALANCED && rule != ARENA_PARTITION_MEMORY)
-        return fail(c, ARENA_ERR_INVALID_ARG, "partition rule: %d is neither BALANCED (0) nor MEMORY (1)", rule);
+    if (rule != ARENA_PARTITION_BALANCED && rule != ARENA_PARTITION_MEMORY && rule != ARENA_PARTITION_EXACT_T)
+        return fail(c, ARENA_ERR_INVALID_ARG, "partition rule: %d is not BALANCED (0), MEMORY (1) or EXACT_T (2)",
+                    rule);
     c->partition_rule = rule;
     return ARENA_OK;
 }
@@ -706,7 +708,10 @@ arena_status check_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
         return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: a cell admits %d plans (max %d)",
                     c->size.max_plans_per_cell, arena::kMaxPlans);
     if (c->tab_k > 0 && c->partition_rule != ARENA_PARTITION_BALANCED)
-        return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: comm tables with the memory partition rule");
+        return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: comm tables with the memory or exact-T partition rule");
+    if (c->partition_rule == ARENA_PARTITION_EXACT_T && c->max_layers > arena::kExactTMaxLayers)
+        return fail(c, ARENA_ERR_UNSUPPORTED, "estimate: the exact-T rule takes jobs of at most %d layers (a job has %d)",
+                    arena::kExactTMaxLayers, c->max_layers);
     if (c->tab_k > 0 && c->tab_types != c->n_types)
         return fail(c, ARENA_ERR_NOT_READY, "estimate: comm tables were set for %d types, %d are bound",
                     c->tab_types, c->n_types);
@@ -747,6 +752,7 @@ arena::EstimateArgs estimate_args(const arena_ctx* c, const int32_t* d_off, cons
     A.tie_eps = c->tie_eps;
     A.prune = c->prune ? 1 : 0;
     A.mem_rule = c->partition_rule == ARENA_PARTITION_MEMORY ? 1 : 0;
+    A.exact_t = c->partition_rule == ARENA_PARTITION_EXACT_T ? 1 : 0;
     if (c->tab_k > 0) {
         A.tab_k = c->tab_k;
         A.tab_vol = d_tab;

@@ -14,6 +14,7 @@ constexpr int kMaxM = 16;           // microbatch choices
 constexpr int kWavesPerBlock = 4;   // waves of one (job, type) block, each on its own cells
 constexpr int kMaxDp = 1024;        // largest data-parallel degree (counts are <= 1024)
 constexpr int kMaxTabPoints = 16;   // samples per communication latency table
+constexpr int kExactTMaxLayers = 96; // layers per job under the exact-T rule
 
 // GPU type as the kernels read it (doubles converted from the f32 inputs).
 struct TypeDev {
@@ -49,6 +50,7 @@ struct EstimateArgs {
     double tie_eps;
     int32_t prune;                // bound pruning on
     int32_t mem_rule;             // partition rule 1: balanced among the splits that fit memory
+    int32_t exact_t;              // partition rule 2: the split of least iteration time that fits memory
     // interpolated communication latency: tab_k points per (type, link),
     // volumes then latencies, each [T][2][tab_k]; tab_k = 0: volume / bandwidth
     const double* tab_vol;

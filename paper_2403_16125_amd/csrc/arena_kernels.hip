@@ -795,6 +795,308 @@ __device__ __noinline__ double mem_counts(const Lds<double>* Ul, const Lds<doubl
     return best_t;
 }
 
+// ------------------------------------------------------------ exact-T partition
+
+// The exact-T rule: the split minimising the plan's whole iteration time
+// among the splits whose every stage fits memory.  The stage costs summed over
+// the stages do not depend on the split (the stages tile the layers), so the
+// split minimises Phi = (cS Smax + cX X) + cP Pmax: Smax the slowest stage
+// per sample, X the boundary bytes x_{c_1-1} + (x_{c_2-1} + ...) added from
+// the back, Pmax the largest stage's parameter bytes, with the coefficients
+// of the steady state, the fill's point-to-point and the all-reduce (Sec. 3.4,
+// Eq. 4).  Ties: the least (Phi, Smax, Pmax, X), then the lexicographically
+// smallest cuts.  A stage's parameter and activation bytes are differences of
+// the running totals Pp, Ap; memory as the pricing: 4 P / tp + min(m, pp-k)
+// b A / tp <= mem for stage k.
+struct ExtCtx {
+    int L, pp, m;
+    double b, tpd, mem;
+    double cS, cX, cP;
+};
+
+struct ExtKey {
+    double phi, s, p, x;
+};
+
+__device__ __forceinline__ bool ext_less(const ExtKey& a, const ExtKey& b)
+{
+    if (a.phi != b.phi) return a.phi < b.phi;
+    if (a.s != b.s) return a.s < b.s;
+    if (a.p != b.p) return a.p < b.p;
+    return a.x < b.x;
+}
+
+__device__ __forceinline__ double ext_phi(const ExtCtx& E, double sm, double x, double pm)
+{
+    return (E.cS * sm + E.cX * x) + E.cP * pm;
+}
+
+// Stage [i, e) as stage k within the thresholds: cost at most tS, parameter
+// bytes at most tP, and it fits memory (each holds on a prefix of the ends e).
+template <int S>
+__device__ __forceinline__ bool ext_ok(const ExtCtx& E, const double* U, const double* Pp, const double* Ap, int i,
+                                       int e, int k, double tS, double tP)
+{
+    const double P = Pp[e] - Pp[i];
+    const double Am = Ap[e] - Ap[i];
+    const int r = E.pp - k;
+    const int infl = E.m < r ? E.m : r;
+    const double mem = 4.0 * P / E.tpd + (double)infl * E.b * Am / E.tpd;
+    return U[e * S] - U[i * S] <= tS && P <= tP && mem <= E.mem;
+}
+
+// Suffix recursion over the splits within the thresholds, rows t = 1..tmax
+// into H (L + 1 doubles, in place: row t at i reads row t-1 only right of i):
+//   KIND 0: H_t(i) = least X of layers [i, L) as the last t stages,
+//           H_1(i) = 0, H_t(i) = min_e x_{e-1} + H_{t-1}(e);
+//   KIND 1: H_t(i) = least largest stage parameter bytes of that suffix,
+//           H_1(i) = P(i, L), H_t(i) = min_e max(P(i, e), H_{t-1}(e));
+//   KIND 2: the same with the stages' per-sample costs;
+// over the ends e whose stage [i, e) is allowed as stage pp - t (+inf: none).
+// Returns H_tmax(0).  Lanes own i = lane and lane + 64 and scan their ends in
+// step, stopping at the first stage not allowed.
+template <int S, int KIND>
+__device__ double ext_rows(const ExtCtx& E, const double* U, const double* Pp, const double* Ap, const float* x,
+                           double* H, int lane, double tS, double tP, int tmax)
+{
+    const int L = E.L, pp = E.pp;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int i = lane + 64 * h;
+        if (i <= L) {
+            double v = kInf;
+            if (i < L && ext_ok<S>(E, U, Pp, Ap, i, L, pp - 1, tS, tP))
+                v = KIND == 0 ? 0.0 : (KIND == 1 ? Pp[L] - Pp[i] : U[L * S] - U[i * S]);
+            H[i] = v;
+        }
+    }
+    wave_sync();
+    for (int t = 2; t <= tmax; ++t) {
+        const int k = pp - t, last = L - t + 1;
+        const int i0 = lane, i1 = lane + 64;
+        double b0 = kInf, b1 = kInf;
+        bool g0 = i0 <= L - t, g1 = i1 <= L - t;
+        int e0 = i0 + 1, e1 = i1 + 1;
+        while (g0 || g1) {
+            if (g0) {
+                if (e0 > last || !ext_ok<S>(E, U, Pp, Ap, i0, e0, k, tS, tP)) {
+                    g0 = false;
+                } else {
+                    const double h = H[e0];
+                    if (h < kInf)
+                        b0 = fmin(b0, KIND == 0 ? (double)x[e0 - 1] + h
+                                                : fmax(KIND == 1 ? Pp[e0] - Pp[i0] : U[e0 * S] - U[i0 * S], h));
+                    ++e0;
+                }
+            }
+            if (g1) {
+                if (e1 > last || !ext_ok<S>(E, U, Pp, Ap, i1, e1, k, tS, tP)) {
+                    g1 = false;
+                } else {
+                    const double h = H[e1];
+                    if (h < kInf)
+                        b1 = fmin(b1, KIND == 0 ? (double)x[e1 - 1] + h
+                                                : fmax(KIND == 1 ? Pp[e1] - Pp[i1] : U[e1 * S] - U[i1 * S], h));
+                    ++e1;
+                }
+            }
+        }
+        // every lane has read row t-1 before any lane overwrites it
+        __asm__ volatile("" ::: "memory");
+        if (i0 <= L) H[i0] = i0 <= L - t ? b0 : kInf;
+        if (i1 <= L) H[i1] = i1 <= L - t ? b1 : kInf;
+        wave_sync();
+    }
+    const double r = H[0];
+    wave_sync();
+    return r;
+}
+
+// The least value V(s, e) = V[e] - V[s] (element e at V[e * VS]) of any
+// segment above th (+inf if none): each lane bisects the ends of its starts.
+template <int VS>
+__device__ double ext_next(const double* V, int lane, int L, double th)
+{
+    double best = kInf;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int s = lane + 64 * h;
+        if (s < L) {
+            const double Vs = V[s * VS];
+            int lo = s + 1, hi = L + 1;          // first e in [s+1, L] with V(s, e) > th, L + 1: none
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (V[mid * VS] - Vs > th) hi = mid; else lo = mid + 1;
+            }
+            if (lo <= L) best = fmin(best, V[lo * VS] - Vs);
+        }
+    }
+    return wave_reduce1<OpMin>(best);
+}
+
+// Exact-T key of one plan (false: no split fits).  Thresholds are visited by
+// tS then tP ascending; each pair's least X gives the key ((cS tS + cX X) +
+// cP tP, tS, tP, X), and the least key over the pairs is the least key over
+// the splits.  A pair after the best key found so far wins only with a
+// smaller Phi, so the visit stops where a lower bound of Phi reaches the best:
+//   tS runs from the least Smax of any split that fits and stops once (cS tS
+//   + cX Xlo) + cP Plo reaches the best (Xlo, Plo the least X and Pmax of any
+//   split that fits), or, when cS = 0, once the best is the least Phi of any
+//   split;
+//   tP runs from the least Pmax within tS and stops once (cS tS + cX Xs) +
+//   cP tP reaches the best (Xs the least X within tS) or its X is Xs.
+template <int S>
+__device__ bool ext_solve(const ExtCtx& E, const double* U, const double* Pp, const double* Ap, const float* x,
+                          double* H, int lane, ExtKey& best)
+{
+    const double p_lo = ext_rows<S, 1>(E, U, Pp, Ap, x, H, lane, kInf, kInf, E.pp);
+    if (!(p_lo < kInf)) return false;
+    const double s_lo = ext_rows<S, 2>(E, U, Pp, Ap, x, H, lane, kInf, kInf, E.pp);
+    const double x_lo = ext_rows<S, 0>(E, U, Pp, Ap, x, H, lane, kInf, kInf, E.pp);
+    double phi_all = kInf;
+    if (E.cS == 0.0) {
+        for (double tP = p_lo; tP < kInf; tP = ext_next<1>(Pp, lane, E.L, tP)) {
+            const double X = ext_rows<S, 0>(E, U, Pp, Ap, x, H, lane, kInf, tP, E.pp);
+            if (X < kInf) phi_all = fmin(phi_all, (0.0 + E.cX * X) + E.cP * tP);
+            if (X == x_lo) break;
+        }
+    }
+    bool found = false;
+    for (double tS = s_lo; tS < kInf; tS = ext_next<S>(U, lane, E.L, tS)) {
+        if (found && (E.cS == 0.0 ? best.phi <= phi_all : ext_phi(E, tS, x_lo, p_lo) >= best.phi)) break;
+        const double pmin = ext_rows<S, 1>(E, U, Pp, Ap, x, H, lane, tS, kInf, E.pp);
+        if (!(pmin < kInf)) continue;
+        const double xs = ext_rows<S, 0>(E, U, Pp, Ap, x, H, lane, tS, kInf, E.pp);
+        for (double tP = pmin; tP < kInf; tP = ext_next<1>(Pp, lane, E.L, tP)) {
+            if (found && ext_phi(E, tS, xs, tP) >= best.phi) break;
+            const double X = ext_rows<S, 0>(E, U, Pp, Ap, x, H, lane, tS, tP, E.pp);
+            if (X < kInf) {
+                const ExtKey k = {ext_phi(E, tS, X, tP), tS, tP, X};
+                if (!found || ext_less(k, best)) {
+                    best = k;
+                    found = true;
+                }
+            }
+            if (X == xs) break;
+        }
+    }
+    return found;
+}
+
+// The lexicographically smallest split of least X within the key's
+// thresholds, cut by cut from the left: c_k is the first end e of an allowed
+// stage k-1 from c_{k-1} with x_{e-1} + H_{pp-k}(e) equal to the X left.
+// The suffix rows are recomputed for each cut.  Returns the stage bounds.
+template <int S>
+__device__ Stages ext_cuts(const ExtCtx& E, const double* U, const double* Pp, const double* Ap, const float* x,
+                           double* H, int lane, const ExtKey& key)
+{
+    int cA = 0, cB = 0;
+    int i = 0;
+    double rest = key.x;
+    for (int k = 1; k < E.pp; ++k) {
+        const int t = E.pp - k + 1;
+        ext_rows<S, 0>(E, U, Pp, Ap, x, H, lane, key.s, key.p, t - 1);
+        int c = -1;
+        for (int base = i + 1; base <= E.L - t + 1 && c < 0; base += 64) {
+            const int e = base + lane;
+            bool ok = false;
+            if (e <= E.L - t + 1 && ext_ok<S>(E, U, Pp, Ap, i, e, k - 1, key.s, key.p)) {
+                const double h = H[e];
+                ok = h < kInf && (double)x[e - 1] + h == rest;
+            }
+            const unsigned long long bm = __ballot(ok);
+            if (bm) c = base + __ffsll((long long)bm) - 1;
+        }
+        // a split of the key exists, so some end passes; keep the cuts ordered regardless
+        c = c < 0 ? i + 1 : c;
+        rest = H[c];
+        wave_sync();
+        cA = lane == k ? c : cA;
+        cB = lane + 64 == k ? c : cB;
+        i = c;
+    }
+    return stages_from_cuts(cA, cB, lane, E.L, E.pp);
+}
+
+// The exact-T plans of degree pp (dp, tp fixed): every admissible microbatch
+// count, largest first, gets its own split; a count whose lower bound (as in
+// mem_counts, with the least slowest stage W of any split) lies past the tie
+// window of the best time so far is not solved.  Plan slots, tallies and the
+// returned least time as price_target.  The cut row of the cell's winner is
+// rebuilt at the end of the cell.
+template <int SLOTS, int S>
+__device__ double price_exact(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
+                              const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp, double W,
+                              int& np, double best, double tie_eps, bool prune)
+{
+    const int dp = cell.n / (tp * pp);
+    const int grp = dp * tp;
+    const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
+    bool adm = false;
+    double b = 0.0;
+    if (mv > 0) {
+        const double dm = (double)(dp * mv);
+        const double q = rint((double)jb.Bg / dm);
+        adm = q * dm == (double)jb.Bg;
+        b = q;
+    }
+    const unsigned long long amask = __ballot(adm);
+    const int nadm = __popcll(amask);
+    tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull));
+    if (nadm == 0) return kInf;
+    const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
+    if (adm) {
+        Wv.bq[rank] = b;
+        Wv.mq[rank] = mv;
+    }
+    wave_sync();
+    const int base = np;
+    np += nadm;
+    if (np > kMaxPlans) {
+        tally(Wv, lane, kOverflow, 1);
+        np = kMaxPlans;
+    }
+    const double UL = U[jb.L * S];
+    const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
+    const double cP = dp > 1 ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp / ((double)tp * B_dp) : 0.0;
+    double lim = prune ? best * (1.0 + tie_eps) : kInf;
+    double best_t = kInf;
+    for (int rk = nadm - 1; rk >= 0; --rk) {
+        const double bm = Wv.bq[rk];
+        const int m = Wv.mq[rk];
+        double T = kInf;
+        const double lbT = (bm * (UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min)) + (double)(m - 1) * (bm * W) +
+                            plb * cP) * (1.0 - 1e-9);
+        if (!(lim < kInf) || lbT <= lim) {
+            ExtCtx E;
+            E.L = jb.L;
+            E.pp = pp;
+            E.m = m;
+            E.b = bm;
+            E.tpd = (double)tp;
+            E.mem = ty.mem;
+            E.cS = (double)(m - 1) * bm;
+            E.cX = cell.kappa * 2.0 * bm / cell.B_pp;
+            E.cP = cP;
+            ExtKey key;
+            if (ext_solve<S>(E, U, B.Pp, B.Ap, B.x, Wv.R, lane, key)) {
+                // the stage costs sum to U_L; the cut-dependent rest is the key's Phi
+                T = bm * UL + key.phi;
+                best_t = fmin(best_t, T);
+                if (prune) lim = fmin(lim, T * (1.0 + tie_eps));
+            }
+            tally(Wv, lane, kMemParts, 1);
+        }
+        if (lane == 0 && base + rk < kMaxPlans) {
+            Wv.planT[base + rk] = T;
+            Wv.planKey[base + rk] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
+        }
+        wave_sync();
+    }
+    return best_t;
+}
+
 // Price every admissible microbatch count of plan (dp, tp, pp) with the
 // canonical stages of bottleneck W; appends to the wave's plan buffer.  Lane
 // mi < n_m holds m_values[mi] (ascending) in `mv`: the lanes price one count
@@ -808,12 +1110,14 @@ __device__ __noinline__ double mem_counts(const Lds<double>* Ul, const Lds<doubl
 // tie window (tie_eps) of `best` or of a count priced here.  Returns the
 // least time of the plans priced that fit (+inf if none): a plan of the
 // cell, so an upper bound of the cell's best time.
-template <int SLOTS, int S, bool MEM>
+template <int SLOTS, int S, bool MEM, bool EXT = false>
 __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
                                double W, int& np, bool keep_cuts, double* R, double best, double tie_eps,
                                bool prune)
 {
+    if constexpr (EXT) return price_exact<SLOTS, S>(B, Wv, U, lane, mv, jb, ty, cell, tp, pp, W, np, best, tie_eps,
+                                                     prune);
     const Stages sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
@@ -1043,8 +1347,9 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
 // ------------------------------------------------------------ the kernel
 
 // MEM: the memory-constrained partition rule (each wave has one more LDS
-// row for its recursion).
-template <int SLOTS, bool MEM>
+// row for its recursion); EXT: the exact-T rule (that row holds its
+// suffix recursion).
+template <int SLOTS, bool MEM, bool EXT = false>
 __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 {
     __shared__ BlockLds<SLOTS> B;
@@ -1218,7 +1523,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / pp - 1]);
                         continue;
                     }
-                    best = fmin(best, price_target<SLOTS, 1, MEM>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
+                    best = fmin(best, price_target<SLOTS, 1, MEM, EXT>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
                                                                   B.Wtab[0][pp], np, A.cuts != nullptr, R, best,
                                                                   A.tie_eps, A.prune != 0));
                 }
@@ -1295,13 +1600,13 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                         tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
                         continue;
                     }
-                    best = fmin(best, price_target<SLOTS, 2, MEM>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp,
+                    best = fmin(best, price_target<SLOTS, 2, MEM, EXT>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp,
                                                                   B.Wtab[slot][pp], np, A.cuts != nullptr, R, best,
                                                                   A.tie_eps, A.prune != 0));
                 }
             } else {
                 solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
-                    best = fmin(best, price_target<SLOTS, 2, MEM>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W,
+                    best = fmin(best, price_target<SLOTS, 2, MEM, EXT>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W,
                                                                   np, A.cuts != nullptr, R, best, A.tie_eps,
                                                                   A.prune != 0));
                     const double lim = best * (1.0 + A.tie_eps);
@@ -1369,7 +1674,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
             A.thr[cidx] = th;
             A.plan[cidx] = pw;
         }
-        const bool kept = Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf &&
+        const bool kept = !EXT && Wv.cut_tp == tp && Wv.cut_pp == pp && Wv.cut_T < kInf &&
                           (!MEM || (Wv.cut_m == 0 ? m >= Wv.cut_mfit : Wv.cut_m == m));
         if (A.cuts && kept) {
             // the winner is the plan kept while pricing (balanced cuts depend on
@@ -1402,7 +1707,28 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                 });
                 if (lane == 0) Wv.tally[kDpEntries] = e0;
             }
-            Stages sg = canonical_stages<2>(U, Wv.J, lane, jb.L, pp, W);
+            Stages sg;
+            if constexpr (EXT) {
+                // the winner's exact-T split, solved again for its count
+                const double bw = rint((double)jb.Bg / (double)(dp * m));
+                const int grp = dp * tp;
+                const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
+                ExtCtx E;
+                E.L = jb.L;
+                E.pp = pp;
+                E.m = m;
+                E.b = bw;
+                E.tpd = (double)tp;
+                E.mem = ty.mem;
+                E.cS = (double)(m - 1) * bw;
+                E.cX = cell.kappa * 2.0 * bw / cell.B_pp;
+                E.cP = dp > 1 ? cell.kappa * 2.0 * (double)(dp - 1) / (double)dp / ((double)tp * B_dp) : 0.0;
+                ExtKey key;
+                ext_solve<2>(E, U, B.Pp, B.Ap, B.x, Wv.R, lane, key);
+                sg = ext_cuts<2>(E, U, B.Pp, B.Ap, B.x, Wv.R, lane, key);
+            } else {
+                sg = canonical_stages<2>(U, Wv.J, lane, jb.L, pp, W);
+            }
             if constexpr (MEM) {
                 // the balanced split if it fits with the winner's m, else the rule's
                 const double dm = (double)(dp * m);
@@ -1462,6 +1788,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     __shared__ int slot;
     for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
         estimate_body<SLOTS, false>(A, item);
+        __syncthreads();
+    }
+}
+
+// The exact-T rule: each plan's split minimises its iteration time.
+template <int SLOTS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_ext_kernel(EstimateArgs A)
+{
+    __shared__ int slot;
+    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
+        estimate_body<SLOTS, false, true>(A, item);
         __syncthreads();
     }
 }
@@ -1954,6 +2291,11 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream)
     const dim3 grid((unsigned)args.n_blocks), block(256);
     if (args.tab_k > 0) {
         hipLaunchKernelGGL(estimate_tab_kernel, grid, block, 0, stream, args);
+    } else if (args.exact_t) {
+        if (args.share_tp)
+            hipLaunchKernelGGL((estimate_ext_kernel<kSlotsShared>), grid, block, 0, stream, args);
+        else
+            hipLaunchKernelGGL((estimate_ext_kernel<1>), grid, block, 0, stream, args);
     } else if (args.mem_rule) {
         if (args.share_tp)
             hipLaunchKernelGGL((estimate_mem_kernel<kSlotsShared>), grid, block, 0, stream, args);

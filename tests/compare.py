@@ -115,6 +115,19 @@ def compare(w, gpu, ids, oracle, kappa_round=0, ref=None, rule=0, tables=None):
     return rep
 
 
+def oracle_cells_parallel(oracle, w, ids, threads=None, **kw):
+    """oracle.cells over `ids` split across host threads (the oracle's C
+    calls keep no global state and release the interpreter lock)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    ids = np.asarray(ids, np.int64)
+    threads = threads or max(1, min(16, os.cpu_count() or 1))
+    chunks = [c for c in np.array_split(ids, threads) if len(c)]
+    with ThreadPoolExecutor(max_workers=len(chunks)) as ex:
+        parts = list(ex.map(lambda c: oracle.cells(w, c, **kw), chunks))
+    return {k: np.concatenate([part[k] for part in parts]) for k in parts[0]}
+
+
 def select(res, ids):
     """Rows `ids` of a full-matrix result dict (numpy)."""
     out = {}

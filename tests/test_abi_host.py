@@ -182,13 +182,31 @@ def test_bound_pruning_switch(ctx):
 def test_partition_rule_switch(ctx):
     lib = arena.load()
     assert lib.arena_set_partition_rule(None, 0) == arena.ARENA_ERR_INVALID_ARG
-    for bad in (-1, 2, 7):
+    for bad in (-1, 3, 7):
         _expect(arena.ARENA_ERR_INVALID_ARG, arena.arena_set_partition_rule, ctx, bad, match="partition rule")
     arena.arena_set_partition_rule(ctx, arena.PARTITION_MEMORY)
+    arena.arena_set_partition_rule(ctx, arena.PARTITION_EXACT_T)
     arena.arena_set_partition_rule(ctx, arena.PARTITION_BALANCED)
     src = open(HEADER).read()
     assert re.search(r"#define ARENA_PARTITION_BALANCED 0\b", src)
     assert re.search(r"#define ARENA_PARTITION_MEMORY 1\b", src)
+    assert re.search(r"#define ARENA_PARTITION_EXACT_T 2\b", src)
+    assert re.search(rf"#define ARENA_EXACT_T_MAX_LAYERS {arena.EXACT_T_MAX_LAYERS}\b", src)
+
+
+def test_exact_t_refuses_long_jobs_and_comm_tables(ctx):
+    # host-side: both refusals come before any device call
+    w = wl.tiny()
+    arena.arena_bind_grids(ctx, w.speed, w.mem, w.bw_intra, w.bw_inter, w.gpus_per_node, w.counts)
+    arena.arena_set_plan_space(ctx, w.m_values, 1e-6)
+    arena.arena_set_partition_rule(ctx, arena.PARTITION_EXACT_T)
+    L = arena.EXACT_T_MAX_LAYERS + 1
+    arena.arena_bind_jobs(ctx, np.array([0, 3, 3 + L], np.int32), np.array([8, 8], np.int32),
+                          FAKE, FAKE, FAKE, FAKE, FAKE)
+    _expect(arena.ARENA_ERR_UNSUPPORTED, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="exact-T")
+    arena.arena_bind_jobs(ctx, w.layer_offset, w.batch, FAKE, FAKE, FAKE, FAKE, FAKE)
+    arena.arena_set_comm_tables(ctx, *wl.comm_tables(w))
+    _expect(arena.ARENA_ERR_UNSUPPORTED, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="comm tables")
 
 
 def test_comm_tables_validation(ctx):

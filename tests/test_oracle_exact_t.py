@@ -1,14 +1,21 @@
-"""How far the balanced partition is from the partition that minimises the
-whole iteration time (the exact-T partition), by brute force on the tiny
-workload (L = 12: every cut vector of every plan priced by the oracle).
+"""Pins of the oracle's exact-T partition (CPU only).
 
-The balanced rule (reading R11) picks the split with the least slowest stage
-and prices the plan on it; the full iteration time (Sec. 3.4, 1F1B) also has
-the p2p sum and the largest DP all-reduce, so another split can be faster.
-Pins: for every plan the brute-force optimum is never above the balanced or
-the memory-constrained price, equals them at pp = 1, and a plan is feasible
-under the memory-constrained rule exactly when some split fits memory.  The
-gaps are printed (CPU only)."""
+The exact-T rule (partition rule 2) prices each plan on the split that
+minimises its whole 1F1B iteration time (Sec. 3.4; the all-reduce of Eq. 4)
+among the splits whose every stage fits memory.  The stage times summed over
+the stages do not depend on the split, so the oracle minimises
+Phi = (cS Smax + cX X) + cP Pmax (ties: least Smax, Pmax, X, then the
+lexicographically smallest cuts) by enumerating thresholds of the two maxima.
+Pinned here by:
+* brute force over every cut vector (the definition written out) on random
+  problems with exact ties, zero and constant terms, binding memory, m = 1 and
+  dp = 1 (cS = 0, cP = 0): the same key and the same cuts;
+* a hand-derived plan where the all-reduce makes an unbalanced split faster;
+* every plan of the tiny workload against the price of every cut vector;
+* theorems: never slower than the balanced or memory-constrained price, as
+  feasible as the memory rule, and the cell's best time non-increasing in
+  every link bandwidth (not a theorem under the balanced rule).
+"""
 import dataclasses
 import itertools
 
@@ -17,13 +24,112 @@ import pytest
 
 from paper_2403_16125_amd import workloads as wl
 
+RULE_EXACT_T = 2
+
+
+def _random_problem(rng):
+    L = int(rng.integers(1, 13))
+    pp = int(rng.integers(1, L + 1))
+    kind = rng.integers(0, 4)
+    if kind == 0:
+        u = rng.integers(0, 4, L).astype(float)            # integers: many exact ties
+    elif kind == 1:
+        u = rng.lognormal(0.0, 0.6, L)
+    elif kind == 2:
+        u = np.full(L, 0.75)
+    else:
+        u = rng.uniform(0.0, 1.0, L)
+        u[rng.integers(0, L)] = 0.0
+    U = np.concatenate([[0.0], np.cumsum(u)])
+    U = np.zeros(L + 1)
+    for i in range(L):
+        U[i + 1] = U[i] + u[i]                              # left to right, as the oracle's prefix
+    p = rng.integers(0, 5, L).astype(float) * (1.0 if rng.random() < 0.7 else 2.5)
+    a = rng.integers(0, 4, L).astype(float)
+    x = np.full(L, 0.5) if rng.random() < 0.4 else rng.integers(0, 4, L).astype(float)
+    m = int(rng.integers(1, 9))
+    b = float(rng.choice([1.0, 2.0, 0.5]))
+    tp = int(rng.choice([1, 2]))
+    # memory: unlimited, loose, or binding (around the largest balanced stage)
+    tot = 4.0 * p.sum() + m * b * a.sum()
+    mem = float(rng.choice([1e30, tot / tp, tot / (tp * max(1, pp) * rng.uniform(0.5, 1.2))]))
+    cS = float(rng.choice([0.0, (m - 1) * b, rng.uniform(0, 3)]))
+    cX = float(rng.choice([0.0, rng.uniform(0, 1)]))
+    cP = float(rng.choice([0.0, rng.uniform(0, 0.5)]))
+    return U, p, a, x, pp, m, b, tp, mem, cS, cX, cP
+
+
+def test_threshold_method_equals_brute_force(oracle):
+    rng = np.random.default_rng(2403)
+    n_fit = n_tie = 0
+    for case in range(700):
+        args = _random_problem(rng)
+        got = oracle.exact_t(*args)
+        want = oracle.exact_t(*args, brute=True)
+        assert np.isfinite(got[0]) == np.isfinite(want[0]), (case, got, want)
+        if not np.isfinite(want[0]):
+            continue
+        n_fit += 1
+        assert got[2] == want[2], (case, got, want)          # (Phi, Smax, Pmax, X) bit for bit
+        assert got[1] == want[1], (case, got, want)          # the same cuts
+        pp = args[4]
+        n_tie += pp > 2
+    assert n_fit > 300 and n_tie > 100
+
+
+def _key_of(U, p, x, cuts, cS, cX, cP):
+    """Phi, Smax, Pmax, X of an explicit cut vector (written independently)."""
+    bnd = [0] + list(cuts) + [len(U) - 1]
+    sm = max(U[bnd[k + 1]] - U[bnd[k]] for k in range(len(bnd) - 1))
+    pm = max(sum(p[bnd[k]:bnd[k + 1]]) for k in range(len(bnd) - 1))
+    X = 0.0
+    for c in reversed(cuts):
+        X = x[c - 1] + X
+    return (cS * sm + cX * X) + cP * pm, sm, pm, X
+
+
+def test_exact_t_key_is_the_key_of_its_cuts(oracle):
+    """The reported key is the key of the reported cut vector, and no cut
+    vector that fits has a smaller Phi (checked without the oracle's code)."""
+    rng = np.random.default_rng(7)
+    for case in range(200):
+        U, p, a, x, pp, m, b, tp, mem, cS, cX, cP = _random_problem(rng)
+        phi, cuts, key = oracle.exact_t(U, p, a, x, pp, m, b, tp, mem, cS, cX, cP)
+        if not np.isfinite(phi):
+            continue
+        L = len(U) - 1
+        assert _key_of(U, p, x, cuts, cS, cX, cP) == key
+        for cv in itertools.combinations(range(1, L), pp - 1):
+            bnd = [0] + list(cv) + [L]
+            fits = all(4.0 * sum(p[bnd[k]:bnd[k + 1]]) / tp + min(m, pp - k) * b * sum(a[bnd[k]:bnd[k + 1]]) / tp
+                       <= mem * (1 + 1e-12) for k in range(pp))
+            if fits:
+                assert _key_of(U, p, x, cv, cS, cX, cP)[0] >= phi * (1 - 1e-12) - 1e-300
+
+
+def _hand_workload():
+    # four layers of equal cost (u = 1 per sample), the parameters in the last
+    # two; dp = 2, tp = 1, pp = 2, m = 2, b = 1 on a node of 4 GPUs with links
+    # of 4 B/s: cS = (m-1) b = 1, cX = 2 b / 4 = 0.5 (x = 0), cP = 2 (1/2) / 4 = 0.25.
+    # Split after layer 2: Smax 2, Pmax 16, Phi = 2 + 4 = 6, T = 4 + 6 = 10 (balanced)
+    # Split after layer 3: Smax 3, Pmax 8,  Phi = 3 + 2 = 5, T = 4 + 5 = 9  (exact-T)
+    job = dict(t=[4.0] * 4, p=[0.0, 0.0, 8.0, 8.0], a=[0.0] * 4, x=[0.0] * 4, a2a=[0.0] * 4, batch=4)
+    ty = dict(speed=1.0, mem=1e12, bw_intra=4.0, bw_inter=4.0, gpus_per_node=4)
+    return wl.from_lists([job], [ty], [4], [2], kappa=1.0)
+
+
+def test_hand_plan_all_reduce_moves_the_cut(oracle):
+    w = _hand_workload()
+    bal = oracle.eval_plan(w, 0, 0, 4, 1.0, 2, 1, 2, 2)
+    mem = oracle.eval_plan(w, 0, 0, 4, 1.0, 2, 1, 2, 2, rule=1)
+    ext = oracle.eval_plan(w, 0, 0, 4, 1.0, 2, 1, 2, 2, rule=RULE_EXACT_T)
+    assert bal["cuts"] == [2] and bal["T"] == 10.0
+    assert mem["cuts"] == [2] and mem["T"] == 10.0
+    assert ext["cuts"] == [3] and ext["T"] == 9.0 and ext["feasible"]
+
 
 def _plans(w, j, g, n):
-    """(dp, tp, pp, m) of cell (j, g, n): dp tp pp = n, tp divides n and the
-    node size, pp <= L, dp m divides the global batch (Eq. 1)."""
-    L = w.layers(j)
-    Bg = int(w.batch[j])
-    gpn = int(w.gpus_per_node[g])
+    L, Bg, gpn = w.layers(j), int(w.batch[j]), int(w.gpus_per_node[g])
     out = []
     for tp in range(1, n + 1):
         if n % tp or gpn % tp:
@@ -39,52 +145,97 @@ def _plans(w, j, g, n):
 
 
 @pytest.mark.parametrize("mem_scale", [1.0, 0.05])
-def test_exact_t_by_brute_force_on_tiny(oracle, mem_scale):
-    # mem_scale 0.05: GPU memory cut to 2 / 4 GB, so that the limit binds for most plans
+def test_exact_t_plans_of_tiny_against_every_cut_vector(oracle, mem_scale):
+    """Every plan of the tiny workload (L = 12; memory as configured, and cut
+    to 5 % so that the limit binds): the exact-T price equals the least price
+    over every cut vector that fits (up to the rounding of the stage sum), is
+    never above the balanced or memory-rule price, and exists exactly when
+    the memory rule finds a split.  The gap of the other rules' best plan per
+    cell is bounded."""
     w = wl.make("tiny")
     w = dataclasses.replace(w, mem=(w.mem * mem_scale).astype(np.float32))
-    n_fit = 0
-    gaps, cell_gaps, cell_gaps_mem = [], [], []
-    n_plans = n_opt = 0
+    n_plans = n_diff = 0
+    cell_gap_bal, cell_gap_mem = [], []
     for j in range(w.n_jobs):
         L = w.layers(j)
         for g in range(w.n_types):
             for ci, n in enumerate(int(c) for c in w.counts):
                 kap = float(w.kappa[0][g * w.n_counts + ci])
-                best_bal = best_mem = best_exact = np.inf
+                best = {0: np.inf, 1: np.inf, 2: np.inf}
                 for dp, tp, pp, m in _plans(w, j, g, n):
-                    bal = oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m)
-                    mem = oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m, rule=1)
-                    exact = np.inf
+                    res = {r: oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m, rule=r) for r in (0, 1, 2)}
+                    brute = np.inf
                     for cuts in itertools.combinations(range(1, L), pp - 1):
                         e = oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m, cuts=list(cuts))
                         if e["feasible"]:
-                            exact = min(exact, e["T"])
+                            brute = min(brute, e["T"])
+                    ext = res[2]
+                    assert ext["feasible"] == np.isfinite(brute) == res[1]["feasible"]
                     n_plans += 1
-                    n_fit += bool(np.isfinite(exact))
-                    assert mem["feasible"] == np.isfinite(exact)       # rule 1 finds a fitting split iff one exists
-                    for r in (bal, mem):
-                        if r["feasible"]:
-                            assert exact <= r["T"] * (1 + 1e-12)
-                            if pp == 1:
-                                assert exact == r["T"]
-                    if bal["feasible"]:
-                        gaps.append(bal["T"] / exact - 1.0)
-                        n_opt += bal["T"] <= exact * (1 + 1e-12)
-                        best_bal = min(best_bal, bal["T"])
-                    if mem["feasible"]:
-                        best_mem = min(best_mem, mem["T"])
-                    best_exact = min(best_exact, exact)
-                if np.isfinite(best_bal):
-                    cell_gaps.append(best_bal / best_exact - 1.0)
-                if np.isfinite(best_mem):
-                    cell_gaps_mem.append(best_mem / best_exact - 1.0)
-    gaps, cell_gaps, cell_gaps_mem = np.asarray(gaps), np.asarray(cell_gaps), np.asarray(cell_gaps_mem)
-    print(f"[exact-T] tiny, memory x{mem_scale}: {n_plans} plans, {n_fit} with a split that fits, "
-          f"{len(gaps)} feasible under the balanced rule; balanced split "
-          f"optimal for {n_opt} ({100 * n_opt / len(gaps):.1f} %); plan gap mean {100 * gaps.mean():.3f} % "
-          f"max {100 * gaps.max():.3f} %; best-plan gap per cell mean {100 * cell_gaps.mean():.3f} % "
-          f"max {100 * cell_gaps.max():.3f} % over {len(cell_gaps)} cells; memory rule's best plan: mean "
-          f"{100 * cell_gaps_mem.mean():.3f} % max {100 * cell_gaps_mem.max():.3f} % over {len(cell_gaps_mem)} cells")
-    assert (gaps >= -1e-12).all() and (cell_gaps >= -1e-12).all() and (cell_gaps_mem >= -1e-12).all()
-    assert n_plans > 100 and len(cell_gaps) > 5
+                    if ext["feasible"]:
+                        assert abs(ext["T"] - brute) <= 1e-12 * brute
+                        for r in (0, 1):
+                            if res[r]["feasible"]:
+                                assert ext["T"] <= res[r]["T"] * (1 + 1e-12)
+                        n_diff += ext["cuts"] != res[1]["cuts"]
+                    for r in (0, 1, 2):
+                        if res[r]["feasible"]:
+                            best[r] = min(best[r], res[r]["T"])
+                if np.isfinite(best[2]):
+                    if np.isfinite(best[0]):
+                        cell_gap_bal.append(best[0] / best[2] - 1.0)
+                    cell_gap_mem.append(best[1] / best[2] - 1.0)
+    cell_gap_bal, cell_gap_mem = np.asarray(cell_gap_bal), np.asarray(cell_gap_mem)
+    print(f"[exact-T] tiny, memory x{mem_scale}: {n_plans} plans, {n_diff} with other cuts than the memory "
+          f"rule; best plan per cell, balanced rule: mean gap {100 * cell_gap_bal.mean():.3f} % max "
+          f"{100 * cell_gap_bal.max():.3f} %; memory rule: mean {100 * cell_gap_mem.mean():.3f} % max "
+          f"{100 * cell_gap_mem.max():.3f} %")
+    assert n_plans > 100 and n_diff > 0
+    assert (cell_gap_bal >= -1e-12).all() and (cell_gap_mem >= -1e-12).all()
+    # measured on this workload: the memory rule's best plan is within 2 % of
+    # the exact-T best per cell, within 0.2 % on average
+    assert cell_gap_mem.max() < 0.02 and cell_gap_mem.mean() < 0.002
+
+
+def test_cells_rule_exact_t_equals_the_least_plan(oracle):
+    """The cell choice under rule 2: the best plan of every tiny cell is the
+    least exact-T price over the cell's plans (ties by (pp, tp, m))."""
+    w = wl.make("tiny")
+    res = oracle.cells(w, np.arange(w.n_cells), rule=RULE_EXACT_T)
+    for c in range(w.n_cells):
+        j, g, ci = c // (w.n_types * w.n_counts), (c // w.n_counts) % w.n_types, c % w.n_counts
+        n = int(w.counts[ci])
+        kap = float(w.kappa[0][g * w.n_counts + ci])
+        cands = []
+        for dp, tp, pp, m in _plans(w, j, g, n):
+            e = oracle.eval_plan(w, j, g, n, kap, dp, tp, pp, m, rule=RULE_EXACT_T)
+            if e["feasible"]:
+                cands.append((e["T"], (pp, tp, m), dp, e["cuts"]))
+        if not cands:
+            assert not np.isfinite(res["T"][c])
+            continue
+        tmin = min(t for t, *_ in cands)
+        win = min((k, dp, cuts, t) for t, k, dp, cuts in cands if t <= tmin * (1 + w.tie_eps))
+        (pp, tp, m), dp, cuts, t = win
+        assert (res["dp"][c], res["tp"][c], res["pp"][c], res["m"][c]) == (dp, tp, pp, m)
+        assert res["T"][c] == t
+        assert list(res["cuts"][c][:pp - 1]) == cuts
+
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_bandwidth_monotonicity_is_a_theorem_under_exact_t(oracle, name):
+    """Faster links never slow a cell down under exact-T: each plan's time is
+    the least over splits of times that do not grow with bandwidth, on the same
+    memory-feasible splits (under the balanced rule a cut shift can make a cell
+    slower, so there it is only reported)."""
+    w = wl.make(name)
+    ids = np.arange(w.n_cells) if name == "tiny" else np.arange(0, w.n_cells, 7)
+    base = oracle.cells(w, ids, rule=RULE_EXACT_T)
+    for scale in ("intra", "inter", "both"):
+        bi = w.bw_intra * (1.5 if scale in ("intra", "both") else 1.0)
+        be = w.bw_inter * (1.5 if scale in ("inter", "both") else 1.0)
+        w2 = dataclasses.replace(w, bw_intra=bi.astype(np.float32), bw_inter=be.astype(np.float32))
+        fast = oracle.cells(w2, ids, rule=RULE_EXACT_T)
+        fin = np.isfinite(base["T"])
+        assert (np.isfinite(fast["T"]) == fin).all()
+        assert (fast["T"][fin] <= base["T"][fin] * (1 + 1e-12)).all(), scale

@@ -301,3 +301,43 @@ def test_unmodified_copy_passes_the_table_pins(tmp_path):
 def test_planted_table_mistake_is_caught(tmp_path, name):
     rc, out = _run_tab_pins(_build(tmp_path, "tab_" + name, TAB_MUTANTS[name]))
     assert rc != 0, f"mistake {name} survived every pin: {out}"
+
+
+# Mistakes in the exact-T partition (the key, its suffix recursions, the
+# threshold search and the cut reconstruction), against test_oracle_exact_t.py.
+EXACT_T_MUTANTS = {
+    "phi_without_allreduce": ("return (E->cS * sm + E->cX * x) + E->cP * pm;", "return E->cS * sm + E->cX * x;"),
+    "suffix_stage_index_off_by_one": ("if (h == INFINITY || !ext_allowed(E, i, e, pp - t, tS, tP)) continue;",
+                                      "if (h == INFINITY || !ext_allowed(E, i, e, pp - t + 1, tS, tP)) continue;"),
+    "inner_search_stops_at_first_pair": ("                if (X == xs) break;", "                break;"),
+    "last_matching_cut_not_first": ("if (E->x[e - 1] + h == H[t * L1 + i]) { c = e; break; }",
+                                    "if (E->x[e - 1] + h == H[t * L1 + i]) { c = e; }"),
+    "every_stage_holds_the_first_stage_memory": (
+        "return fits_sums(E->M, E->segP[lo][hi], E->segA[lo][hi], k, E->pp);",
+        "return fits_sums(E->M, E->segP[lo][hi], E->segA[lo][hi], 0, E->pp);"),
+    "p2p_coefficient_without_b": ("*cX = kappa * 2.0 * b / B_pp;", "*cX = kappa * 2.0 / B_pp;"),
+    "steady_state_m_not_m_minus_1": ("*cS = (double)(m - 1) * b;", "*cS = (double)m * b;"),
+}
+
+
+def _run_exact_t_pins(lib):
+    env = dict(os.environ, ARENA_ORACLE_LIB=lib)
+    files = [os.path.join(ROOT, "tests", "test_oracle_exact_t.py")]
+    try:
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                            "-p", "no:xdist"] + files, capture_output=True, text=True, timeout=300, env=env,
+                           cwd=ROOT)
+    except subprocess.TimeoutExpired:
+        return None, "timed out"
+    return r.returncode, (r.stdout + r.stderr)[-2000:]
+
+
+def test_unmodified_copy_passes_the_exact_t_pins(tmp_path):
+    rc, out = _run_exact_t_pins(_build(tmp_path, "control_exact_t", None))
+    assert rc == 0, out
+
+
+@pytest.mark.parametrize("name", sorted(EXACT_T_MUTANTS))
+def test_planted_exact_t_mistake_is_caught(tmp_path, name):
+    rc, out = _run_exact_t_pins(_build(tmp_path, name, EXACT_T_MUTANTS[name]))
+    assert rc != 0, f"mistake {name} survived every pin: {out}"

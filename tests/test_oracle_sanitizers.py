@@ -5,8 +5,8 @@
   against those copies in a child process.
 * AddressSanitizer + UBSan: a driver executable links the oracle sources and
   evaluates whole workloads (tiny, small, the edge shapes, sampled trace-like
-  and MoE cells; balanced and memory rules, communication tables, the proxy
-  planner) from input arrays allocated to their exact sizes; its outputs must
+  and MoE cells; balanced, memory and exact-T rules, communication tables,
+  the proxy planner) from input arrays allocated to their exact sizes; its outputs must
   equal, bit for bit, those of the regular build loaded in this process.
 * AddressSanitizer + UBSan on the host side of the library: arena_host.cpp
   built with g++ (no device code: the kernel launchers are stubs that report
@@ -106,6 +106,8 @@ def test_oracles_under_asan_match_the_regular_build(tmp_path):
         runs.append((f"{name} balanced", 0, 0, w, ids, None))
     runs.append(("small memory rule", 0, 1, cases[1][1], cases[1][2][::3], None))
     runs.append(("edge memory rule", 0, 1, e, cases[2][2], None))
+    runs.append(("small exact-T", 0, 2, cases[1][1], cases[1][2][::97], None))
+    runs.append(("trace exact-T", 0, 2, cases[3][1], cases[3][2][:6], None))
     runs.append(("small tables", 1, 0, cases[1][1], cases[1][2][::5], wl.comm_tables(cases[1][1])))
     runs.append(("edge tables", 1, 0, e, cases[2][2], wl.comm_tables(e)))
     runs.append(("small proxy", 2, 0, cases[1][1], cases[1][2][::4], None))
