@@ -75,6 +75,7 @@ struct arena_ctx {
     bool order_dirty = true;
     bool horder_valid = false;                  // host copies of the work order below are current
     std::vector<int32_t> h_iorder, h_corder;
+    int32_t h_qoff[arena::kQueues + 1] = {};    // queue q's items: h_iorder[h_qoff[q] .. h_qoff[q+1])
     int64_t ws_limit = 0;                       // cap on library-owned device bytes, 0: none
     unsigned long long* d_counters = nullptr;
     const unsigned long long* last_counters = nullptr;   // tallies of the last estimate
@@ -225,7 +226,7 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
             return e == hipErrorOutOfMemory ? fail(c, ARENA_ERR_OUT_OF_MEMORY, "counters") : hip_fail(c, e, "hipMalloc");
         if ((e = hipHostMalloc((void**)&c->h_counters, sizeof(unsigned long long) * arena::kNumCounters, 0)))
             return hip_fail(c, e, "hipHostMalloc");
-        if ((e = hipMalloc((void**)&c->d_queue, sizeof(unsigned long long))))
+        if ((e = hipMalloc((void**)&c->d_queue, sizeof(unsigned long long) * arena::kQueues)))
             return e == hipErrorOutOfMemory ? fail(c, ARENA_ERR_OUT_OF_MEMORY, "queue") : hip_fail(c, e, "hipMalloc");
         if ((e = hipDeviceGetAttribute(&c->n_cus, hipDeviceAttributeMultiprocessorCount, c->device)))
             return hip_fail(c, e, "hipDeviceGetAttribute");
@@ -307,10 +308,12 @@ arena_status ensure_device(arena_ctx* c, hipStream_t stream)
     return ARENA_OK;
 }
 
-// Work order: (job, type) blocks with the most estimated work first (so the
-// longest blocks do not form the tail), and within a block the largest GPU
-// counts first.  The estimate is plans x layers per cell.  Host copies,
-// rebuilt when the bindings change.
+// Work order: jobs are dealt to the kernels' kQueues item queues (one per
+// XCD) heaviest first, each to the queue with the least work so far; a queue
+// lists its jobs heaviest first (so the longest items do not form the tail)
+// with the (job, type) items of one job adjacent, heaviest type first, and
+// within an item the largest GPU counts come first.  The estimate of work is
+// plans x layers per cell.  Host copies, rebuilt when the bindings change.
 void compute_orders(arena_ctx* c)
 {
     if (c->horder_valid) return;
@@ -336,12 +339,37 @@ void compute_orders(arena_ctx* c)
         }
         for (int g = 0; g < c->n_types; ++g) icost[(size_t)j * c->n_types + g] = it->second[g];
     }
-    // the kernels' resident blocks take items from a queue in this order:
-    // heaviest first, so the last items to start are the light ones
+    const int T = c->n_types;
+    std::vector<double> jcost((size_t)c->n_jobs, 0.0);
+    for (int j = 0; j < c->n_jobs; ++j)
+        for (int g = 0; g < T; ++g) jcost[j] += icost[(size_t)j * T + g];
+    std::vector<int32_t> jorder((size_t)c->n_jobs);
+    std::iota(jorder.begin(), jorder.end(), 0);
+    std::stable_sort(jorder.begin(), jorder.end(), [&](int a, int b) { return jcost[a] > jcost[b]; });
+    std::vector<std::vector<int32_t>> qjobs(arena::kQueues);
+    double qload[arena::kQueues] = {};
+    for (int j : jorder) {
+        int best = 0;
+        for (int q = 1; q < arena::kQueues; ++q)
+            if (qload[q] < qload[best]) best = q;
+        qjobs[best].push_back(j);
+        qload[best] += jcost[j];
+    }
     std::vector<int32_t>& iorder = c->h_iorder;
-    iorder.resize(items);
-    std::iota(iorder.begin(), iorder.end(), 0);
-    std::stable_sort(iorder.begin(), iorder.end(), [&](int a, int b) { return icost[a] > icost[b]; });
+    iorder.clear();
+    iorder.reserve(items);
+    std::vector<int32_t> types((size_t)T);
+    for (int q = 0; q < arena::kQueues; ++q) {
+        c->h_qoff[q] = (int32_t)iorder.size();
+        for (int j : qjobs[q]) {
+            std::iota(types.begin(), types.end(), 0);
+            std::stable_sort(types.begin(), types.end(), [&](int a, int b) {
+                return icost[(size_t)j * T + a] > icost[(size_t)j * T + b];
+            });
+            for (int g : types) iorder.push_back(j * T + g);
+        }
+    }
+    c->h_qoff[arena::kQueues] = (int32_t)iorder.size();
     c->horder_valid = true;
 }
 
@@ -377,7 +405,7 @@ Workspace workspace_layout(const arena_ctx* c)
     Workspace w;
     size_t o = 0;
     w.counters = o; o = up(o + sizeof(unsigned long long) * arena::kNumCounters);
-    w.queue = o;    o = up(o + sizeof(unsigned long long));
+    w.queue = o;    o = up(o + sizeof(unsigned long long) * arena::kQueues);
     w.off = o;      o = up(o + sizeof(int32_t) * (J + 1));
     w.batch = o;    o = up(o + sizeof(int32_t) * J);
     w.types = o;    o = up(o + sizeof(TypeDev) * T);
@@ -740,6 +768,7 @@ arena::EstimateArgs estimate_args(const arena_ctx* c, const int32_t* d_off, cons
     A.item_order = d_items;
     A.count_order = d_corder;
     A.queue = d_queue;
+    for (int q = 0; q <= arena::kQueues; ++q) A.queue_off[q] = c->h_qoff[q];
     A.n_items = c->n_jobs * c->n_types;
     // one block per resident slot (four per CU); each takes items from the queue
     A.n_blocks = std::min(A.n_items, 4 * std::max(c->n_cus, 1));
@@ -804,7 +833,7 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
         estimate_args(c, c->d_off, c->d_batch, c->d_types, c->d_counts, c->d_kappa, c->d_item_order,
                       c->d_count_order, c->d_queue, c->d_tab, c->d_counters, t_iter, thr, plan, cuts, cuts_stride);
     if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)) ||
-        (e = arena::launch_zero_counters(c->d_queue, 1, stream)))
+        (e = arena::launch_zero_counters(c->d_queue, arena::kQueues, stream)))
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     c->last_counters = c->d_counters;
@@ -879,7 +908,7 @@ arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uin
                                                 d_queue, d_tab, d_counters, t_iter, thr, plan, cuts, cuts_stride);
     // zeroed by a kernel, not a memset node
     if ((e = arena::launch_zero_counters(d_counters, arena::kNumCounters, stream)) ||
-        (e = arena::launch_zero_counters(d_queue, 1, stream)))
+        (e = arena::launch_zero_counters(d_queue, arena::kQueues, stream)))
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     c->last_counters = d_counters;

@@ -15,6 +15,7 @@ constexpr int kWavesPerBlock = 4;   // waves of one (job, type) block, each on i
 constexpr int kMaxDp = 1024;        // largest data-parallel degree (counts are <= 1024)
 constexpr int kMaxTabPoints = 16;   // samples per communication latency table
 constexpr int kExactTMaxLayers = 96; // layers per job under the exact-T rule
+constexpr int kQueues = 8;          // item queues, one per XCD (each XCD has its own L2)
 
 // GPU type as the kernels read it (doubles converted from the f32 inputs).
 struct TypeDev {
@@ -38,8 +39,9 @@ struct EstimateArgs {
     const TypeDev* types;         // [T]
     const int32_t* counts;        // [NC]
     const float* kappa;           // [T*NC]
-    const int32_t* item_order;    // [J*T] (job, type) items, most work first
-    unsigned long long* queue;    // [1] next item to take (zeroed before each launch)
+    const int32_t* item_order;    // [J*T] (job, type) items: queue q holds [queue_off[q], queue_off[q+1])
+    unsigned long long* queue;    // [kQueues] next item of each queue (zeroed before each launch)
+    int32_t queue_off[kQueues + 1];
     int32_t n_items;              // J * T
     int32_t n_blocks;             // resident blocks launched; each takes items until none is left
     const int32_t* count_order;   // [NC] count indices, largest count first

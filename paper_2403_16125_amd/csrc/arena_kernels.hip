@@ -1262,7 +1262,7 @@ struct BoundCtx {
 // estimates; a relative margin of 1e-9 covers them and the rounding.
 template <int SLOTS>
 __device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const TypeDev& ty, const Cell& cell,
-                               unsigned gpn_divs, const BoundCtx& bc, int pp)
+                               unsigned gpn_divs, BoundCtx bc, int pp)
 {
     const double rpp = rcp_approx((double)pp);
     const int dp = (int)rint((double)bc.qn * rpp);                     // exact: pp divides qn
@@ -1346,6 +1346,28 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
 
 // ------------------------------------------------------------ the kernel
 
+// A block's work tallies live in its waves' LDS for the whole launch: zeroed
+// before its first item and added to the device counters once, after its
+// last (a device-wide atomic per item and counter would cost HBM writes).
+constexpr int kZeroTallies = -2;
+constexpr int kFlushTallies = -1;
+
+__device__ __forceinline__ void block_tallies(const EstimateArgs& A, WaveLds& Wv, int lane, int op)
+{
+    if (op == kZeroTallies) {
+        if (lane < kNumCounters) Wv.tally[lane] = 0ull;
+        wave_sync();
+        return;
+    }
+    if (lane == 0) {
+        const unsigned long long* t = Wv.tally;
+        for (int c = 0; c < kNumCounters; ++c) {
+            const unsigned long long v = c == kAlgOps ? t[kAlgOps] + 8ull * t[kDpEntries] : t[c];
+            if (v) atomicAdd(&A.counters[c], v);
+        }
+    }
+}
+
 // MEM: the memory-constrained partition rule (each wave has one more LDS
 // row for its recursion); EXT: the exact-T rule (that row holds its
 // suffix recursion).
@@ -1353,11 +1375,19 @@ template <int SLOTS, bool MEM, bool EXT = false>
 __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 {
     __shared__ BlockLds<SLOTS> B;
-    const int tid = threadIdx.x;
+    // the thread index passes through an empty asm statement once per item, so
+    // nothing derived from it is hoisted out of the item loop and held in
+    // registers across every item (it would be spilled)
+    int tid;
+    __asm__ volatile("" : "=v"(tid) : "0"((int)threadIdx.x));
     const int lane = tid & 63;
-    const int wid = tid >> 6;
+    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
     WaveLds& Wv = B.w[wid];
     double* const R = MEM ? Wv.R : nullptr;
+    if (item < 0) {
+        block_tallies(A, Wv, lane, item);
+        return;
+    }
 
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
@@ -1448,9 +1478,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
     }
     __syncthreads();
     const int n_slots = B.n_slots;
-
-    if (lane < kNumCounters) Wv.tally[lane] = 0ull;
-    wave_sync();
+    if (wid == 0) tally(Wv, lane, kCells, (unsigned long long)A.n_counts);
 
     for (int s = wid; s < n_slots; s += kWavesPerBlock) {
         const int tp = B.slot_tp[s], var = B.slot_var[s];
@@ -1487,6 +1515,10 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 
     // ---- cells: take counts, largest first, from the block's work counter
     for (;;) {
+        // the lane index is re-derived per cell, for the same reason as the
+        // thread index per item
+        int lane;
+        __asm__ volatile("" : "=v"(lane) : "0"(tid & 63));
         int cix = 0;
         if (lane == 0) cix = atomicAdd(&B.next_cell, 1);
         cix = __builtin_amdgcn_readfirstlane(cix);
@@ -1751,30 +1783,29 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         }
         wave_sync();
     }
-
-    if (lane == 0) {
-        if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
-        const unsigned long long* t = Wv.tally;
-        atomicAdd(&A.counters[kPlans], t[kPlans]);
-        atomicAdd(&A.counters[kProblems], t[kProblems]);
-        atomicAdd(&A.counters[kDpEntries], t[kDpEntries]);
-        atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
-        if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
-        atomicAdd(&A.counters[kSkipped], t[kSkipped]);
-        atomicAdd(&A.counters[kMemParts], t[kMemParts]);
-        atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
-    }
 }
 
-// The (job, type) item a block works on next: the queue hands items out in
-// the host's order (heaviest first) to whichever resident block is free, so
-// the work balances over the CUs whatever the items really cost.  Returns
-// the item, or -1 once the queue is empty (every block then leaves).
+// The (job, type) item a block works on next.  The host deals whole jobs to
+// kQueues queues of about equal work, heaviest first, with the items of one
+// job adjacent; a block takes the next item of the queue of its XCD
+// (workgroups are handed to the XCDs round robin, so block b runs on XCD
+// b mod 8), so the types of one job run on one XCD and its layer tables are
+// fetched into that XCD's L2 once.  A block whose queue is empty takes from
+// the next queues in turn, so the work still balances over every CU whatever
+// the items really cost.  Returns the item, or -1 once every queue is empty
+// (every block then leaves).
 __device__ __forceinline__ int take_item(const EstimateArgs& A, int* slot)
 {
     if (threadIdx.x == 0) {
-        const unsigned long long q = atomicAdd(A.queue, 1ull);
-        *slot = q < (unsigned long long)A.n_items ? A.item_order[q] : -1;
+        int item = -1;
+        for (int r = 0; r < kQueues && item < 0; ++r) {
+            const int qi = (int)((blockIdx.x + r) % kQueues);
+            const unsigned long long len = (unsigned long long)(A.queue_off[qi + 1] - A.queue_off[qi]);
+            if (len == 0ull) continue;
+            const unsigned long long q = atomicAdd(&A.queue[qi], 1ull);
+            if (q < len) item = A.item_order[A.queue_off[qi] + (int)q];
+        }
+        *slot = item;
     }
     __syncthreads();
     const int item = *slot;
@@ -1786,10 +1817,12 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
 {
     __shared__ int slot;
+    estimate_body<SLOTS, false>(A, kZeroTallies);
     for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
         estimate_body<SLOTS, false>(A, item);
         __syncthreads();
     }
+    estimate_body<SLOTS, false>(A, kFlushTallies);
 }
 
 // The exact-T rule: each plan's split minimises its iteration time.
@@ -1797,10 +1830,12 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_ext_kernel(EstimateArgs A)
 {
     __shared__ int slot;
+    estimate_body<SLOTS, false, true>(A, kZeroTallies);
     for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
         estimate_body<SLOTS, false, true>(A, item);
         __syncthreads();
     }
+    estimate_body<SLOTS, false, true>(A, kFlushTallies);
 }
 
 // The memory rule's out-of-line solve raises register use; its kernel still
@@ -1811,10 +1846,12 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_mem_kernel(EstimateArgs A)
 {
     __shared__ int slot;
+    estimate_body<SLOTS, true>(A, kZeroTallies);
     for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
         estimate_body<SLOTS, true>(A, item);
         __syncthreads();
     }
+    estimate_body<SLOTS, true>(A, kFlushTallies);
 }
 
 // ------------------------------------------------------------ interpolated communication latency
@@ -1985,6 +2022,10 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
     const int lane = tid & 63;
     const int wid = tid >> 6;
     WaveLds& Wv = B.w[wid];
+    if (item < 0) {
+        block_tallies(A, Wv, lane, item);
+        return;
+    }
 
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
@@ -2023,7 +2064,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         if (lane == 0) B.x_layer_min = xm;
     }
     if (tid == 0) B.next_cell = 0;
-    if (lane < kNumCounters) Wv.tally[lane] = 0ull;
+    if (wid == 0) tally(Wv, lane, kCells, (unsigned long long)A.n_counts);
     __syncthreads();
 
     for (;;) {
@@ -2216,26 +2257,17 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         wave_sync();
     }
 
-    if (lane == 0) {
-        if (wid == 0) atomicAdd(&A.counters[kCells], (unsigned long long)A.n_counts);
-        const unsigned long long* t = Wv.tally;
-        atomicAdd(&A.counters[kPlans], t[kPlans]);
-        atomicAdd(&A.counters[kProblems], t[kProblems]);
-        atomicAdd(&A.counters[kDpEntries], t[kDpEntries]);
-        atomicAdd(&A.counters[kInfeasible], t[kInfeasible]);
-        if (t[kOverflow]) atomicAdd(&A.counters[kOverflow], 1ull);
-        atomicAdd(&A.counters[kSkipped], t[kSkipped]);
-        atomicAdd(&A.counters[kAlgOps], t[kAlgOps] + 8ull * t[kDpEntries]);
-    }
 }
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
 {
     __shared__ int slot;
+    estimate_tab_body(A, kZeroTallies);
     for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
         estimate_tab_body(A, item);
         __syncthreads();
     }
+    estimate_tab_body(A, kFlushTallies);
 }
 
 __global__ void zero_kernel(unsigned long long* p, int n)
