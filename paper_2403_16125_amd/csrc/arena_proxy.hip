@@ -75,19 +75,61 @@ struct Cell {
     double speed, mem, bwi, bwe, kap;
 };
 
+// (key, idx) of another lane picked by one DPP control; lanes of the rows
+// the row mask leaves out read the identity (+inf, INT_MAX).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void dpp_pair(double k, int i, double& ok, int& oi)
+{
+    const unsigned long long b = (unsigned long long)__double_as_longlong(k);
+    const unsigned long long e = (unsigned long long)__double_as_longlong(kInfP);
+    const int lo = __builtin_amdgcn_update_dpp((int)(unsigned)e, (int)(unsigned)b, CTRL, ROWS, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(unsigned)(e >> 32), (int)(unsigned)(b >> 32), CTRL, ROWS,
+                                               0xf, false);
+    ok = __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) |
+                                          (unsigned long long)(unsigned)lo));
+    oi = __builtin_amdgcn_update_dpp(0x7fffffff, i, CTRL, ROWS, 0xf, false);
+}
+
+__device__ __forceinline__ void take_less(double& k, int& i, double ok, int oi)
+{
+    const bool t = (ok < k) | ((ok == k) & (oi < i));
+    k = t ? ok : k;
+    i = t ? oi : i;
+}
+
+// Least (key, idx) of the wave (smaller key, then smaller idx), in every
+// lane: quad swaps and row rotations give each row its least pair, row
+// broadcasts carry it to the last row, lane 63 hands the result out.  DPP
+// moves need no lane addresses (a shuffle's would be held in registers).
+__device__ __forceinline__ void wave_argmin(double& k, int& i)
+{
+    double ok;
+    int oi;
+    dpp_pair<0xB1, 0xf>(k, i, ok, oi);    // quad_perm [1,0,3,2]
+    take_less(k, i, ok, oi);
+    dpp_pair<0x4E, 0xf>(k, i, ok, oi);    // quad_perm [2,3,0,1]
+    take_less(k, i, ok, oi);
+    dpp_pair<0x124, 0xf>(k, i, ok, oi);   // row_ror:4
+    take_less(k, i, ok, oi);
+    dpp_pair<0x128, 0xf>(k, i, ok, oi);   // row_ror:8
+    take_less(k, i, ok, oi);
+    dpp_pair<0x142, 0xa>(k, i, ok, oi);   // row_bcast:15 into rows 1 and 3
+    take_less(k, i, ok, oi);
+    dpp_pair<0x143, 0xc>(k, i, ok, oi);   // row_bcast:31 into rows 2 and 3
+    take_less(k, i, ok, oi);
+    const unsigned long long b = (unsigned long long)__double_as_longlong(k);
+    const int lo = __builtin_amdgcn_readlane((int)(unsigned)b, 63);
+    const int hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), 63);
+    k = __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) |
+                                         (unsigned long long)(unsigned)lo));
+    i = __builtin_amdgcn_readlane(i, 63);
+}
+
 // Block-wide arg-min of (key, idx) (smaller key, then smaller idx).
 __device__ __forceinline__ void block_argmin(double& key, int& idx, ProxyLds& S)
 {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const double ok = __shfl_xor(key, off);
-        const int oi = __shfl_xor(idx, off);
-        if (ok < key || (ok == key && oi < idx)) {
-            key = ok;
-            idx = oi;
-        }
-    }
+    wave_argmin(key, idx);
     if (lane == 0) {
         S.rkey[w] = key;
         S.ridx[w] = idx;
@@ -407,7 +449,11 @@ __device__ __forceinline__ double price(const Cell c, const ProxyLds& S, unsigne
 
 __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int cell)
 {
-    const int tid = threadIdx.x;
+    // the thread index passes through an empty asm statement once per cell, so
+    // nothing derived from it is hoisted out of the cell loop and held in
+    // registers across every cell (it would be spilled)
+    int tid;
+    __asm__ volatile("" : "=v"(tid) : "0"((int)threadIdx.x));
     const int ci = cell % A.n_counts;
     const int g = (cell / A.n_counts) % A.n_types;
     const int jb = cell / (A.n_counts * A.n_types);
@@ -577,20 +623,13 @@ __device__ __forceinline__ void proxy_cell(const ProxyArgs& A, ProxyLds& S, int 
                     idx[k] = r;
                 }
         }
-        const int lane = tid & 63, wv = tid >> 6;
+        const int lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
         for (int k = 0; k < kMaxM; ++k) {
             if (k < A.n_m) {
                 double kk = key[k];
                 int ii = idx[k];
-                for (int off = 32; off >= 1; off >>= 1) {
-                    const double ok = __shfl_xor(kk, off);
-                    const int oi = __shfl_xor(ii, off);
-                    if (ok < kk || (ok == kk && oi < ii)) {
-                        kk = ok;
-                        ii = oi;
-                    }
-                }
+                wave_argmin(kk, ii);
                 if (lane == 0) {
                     S.wkey[wv][k] = kk;
                     S.widx[wv][k] = ii;
