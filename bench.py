@@ -340,6 +340,42 @@ def bench_schedule(args) -> int:
     return 0
 
 
+VALU_OPS = (("fma", 1), ("add", 1), ("minmax", 2), ("select", 3))   # (class, operations per step)
+
+
+def bench_valu_rate() -> int:
+    """Issue rate of the estimate kernels' operation classes in fp64 and fp32
+    (csrc/valu_rate.hip): 2048 blocks of 256 threads (eight waves per SIMD),
+    eight independent chains per thread.  Prints one JSON line: per class and
+    type, chain steps per second and their fp64 / fp32 ratio."""
+    import ctypes
+    from paper_2403_16125_amd import build
+    lib = ctypes.CDLL(build.VALU_RATE_OUT)
+    lib.valu_rate_run.restype = ctypes.c_int
+    lib.valu_rate_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                  ctypes.POINTER(ctypes.c_double)]
+    blocks, iters, reps = 2048, 32768, 5
+    steps = blocks * 256 * 8 * iters                   # chain steps per launch
+    out = {"what": "VALU issue rate: chain steps per second by operation class and type "
+                   "(2048 x 256 threads, 8 independent chains each, no packed fp32)",
+           "blocks": blocks, "iters": iters, "steps_per_launch": steps, "classes": {}}
+    for op, (name, n_ops) in enumerate(VALU_OPS):
+        row = {"ops_per_step": n_ops}
+        for is_double, tname in ((1, "f64"), (0, "f32")):
+            ms = (ctypes.c_double * reps)()
+            rc = lib.valu_rate_run(op, is_double, blocks, iters, reps, ms)
+            if rc != 0:
+                print(f"valu_rate_run({name}, {tname}) failed: HIP error {rc}", file=sys.stderr, flush=True)
+                return 1
+            best = min(ms[i] for i in range(reps))
+            row[tname] = {"ms": best, "steps_per_s": steps / (best * 1e-3)}
+            log(f"{name} {tname}: {best:.3f} ms, {steps / (best * 1e-3):.4g} steps/s")
+        row["f64_over_f32"] = row["f64"]["steps_per_s"] / row["f32"]["steps_per_s"]
+        out["classes"][name] = row
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -349,7 +385,7 @@ def main() -> int:
     ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
     ap.add_argument("--cpu-every", type=int, default=None,
                     help="oracle sample: every k-th job (default 256; 2048 with --partition memory, "
-                         "1024 with --comm-tables)")
+                         "1024 with --comm-tables, 8 with --partition exact-t)")
     ap.add_argument("--partition", default="balanced", choices=["balanced", "memory", "exact-t"],
                     help="stage partition rule of the estimate (exact-t: the trace-like workload unless "
                          "--workload names another of at most 96 layers per job)")
@@ -367,6 +403,8 @@ def main() -> int:
     ap.add_argument("--proxy-cpu-every", type=int, default=199, help="proxy oracle sample: every k-th cell")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain elementwise copy of known size (HBM counter calibration)")
+    ap.add_argument("--valu-rate", action="store_true",
+                    help="run only the fp64-vs-fp32 VALU issue-rate microbenchmark")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -376,6 +414,8 @@ def main() -> int:
               file=sys.stderr, flush=True)
         return 2
 
+    if args.valu_rate:
+        return bench_valu_rate()
     if args.schedule:
         return bench_schedule(args)
     if args.proxy:
@@ -516,7 +556,7 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
         exact = rule == arena.PARTITION_EXACT_T
-        every = args.cpu_every or (256 if plain else (1024 if tables is not None or exact else 2048))
+        every = args.cpu_every or (256 if plain else (8 if exact else (1024 if tables is not None else 2048)))
         line["cpu_baseline"] = cpu_baseline(w, every, rule=rule, tables=tables, cell_every=10 if exact else 1)
     print(json.dumps(line), flush=True)
     return 0

@@ -12,6 +12,9 @@ OUT = os.path.join(PKG, "_build", "libarena.so")
 SOURCES = [os.path.join(CSRC, "arena_host.cpp"), os.path.join(CSRC, "arena_kernels.hip"),
            os.path.join(CSRC, "arena_sched.hip"), os.path.join(CSRC, "arena_proxy.hip")]
 
+VALU_RATE_SRC = os.path.join(CSRC, "valu_rate.hip")
+VALU_RATE_OUT = os.path.join(PKG, "_build", "libvalu_rate.so")   # fp64-vs-fp32 issue-rate microbenchmark
+
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -30,6 +33,12 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, OUT)
+    tmp = VALU_RATE_OUT + ".tmp"
+    cmd = [HIPCC] + FLAGS + ["-o", tmp, VALU_RATE_SRC]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, VALU_RATE_OUT)
     return OUT
 
 

@@ -1867,6 +1867,9 @@ __device__ __forceinline__ double tab_lat(const double* vol, const double* lat, 
     return lat[k - 1] + (v - vol[k - 1]) * (lat[k] - lat[k - 1]) / (vol[k] - vol[k - 1]);
 }
 
+constexpr int kTabCacheBits = 8;
+constexpr unsigned kTabCache = 1u << kTabCacheBits;   // bottleneck cache entries per block
+
 struct TabBlockLds {
     float t[kLmax];
     float x[kLmax];
@@ -1878,8 +1881,65 @@ struct TabBlockLds {
     double p_layer_max;               // largest parameter bytes of one layer
     double x_layer_min;               // smallest boundary activation bytes of one layer
     int32_t next_cell;
+    int32_t share;                    // one kappa for all counts of the type: bottlenecks are shared
     WaveLds w[kWavesPerBlock];
+    double cW[kTabCache];             // bottleneck cache of the (job, type): bottlenecks
+    uint32_t ckey[kTabCache];         //   and their keys (0 empty)
 };
+
+// Bottleneck cache.  With one kappa for all counts of a type, a plan's
+// per-microbatch layer costs depend on the cell only through (tp, b, whether
+// dp tp > 1), so the bottleneck of pp stages over them is the same in every
+// cell of the (job, type) that has a plan with that key: the first cell to
+// solve it stores it, later cells price the degree without the recursion.
+// Keys pack pp (8 bits), tp (5), the flag (1) and b (17 bits; larger batches
+// do not share); bit 31 marks an entry whose value is still being written.
+// Open addressing with linear probing; a full cache only stops sharing.
+constexpr unsigned kTabBusy = 1u << 31;
+constexpr int kTabProbe = 8;
+
+__device__ __forceinline__ unsigned tab_key(int tp, bool flag, double b, int pp)
+{
+    return ((unsigned)b << 14) | ((flag ? 1u : 0u) << 13) | ((unsigned)tp << 8) | (unsigned)pp;
+}
+
+__device__ __forceinline__ unsigned tab_slot(unsigned key)
+{
+    return (key * 2654435761u) >> (32 - kTabCacheBits);
+}
+
+// Lane-parallel lookup: true and W when the bottleneck of `key` is cached.
+__device__ __forceinline__ bool tab_cache_find(const TabBlockLds& B, unsigned key, double& W)
+{
+    unsigned h = tab_slot(key);
+    for (int p = 0; p < kTabProbe; ++p) {
+        const unsigned k = __hip_atomic_load(&B.ckey[h], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (k == key) {
+            W = B.cW[h];
+            return true;
+        }
+        if (k == 0u) return false;
+        h = (h + 1u) & (kTabCache - 1u);
+    }
+    return false;
+}
+
+// One lane stores the bottleneck of `key` (nothing if the key is present or
+// its probe window is full).
+__device__ __forceinline__ void tab_cache_put(TabBlockLds& B, unsigned key, double W)
+{
+    unsigned h = tab_slot(key);
+    for (int p = 0; p < kTabProbe; ++p) {
+        const unsigned old = atomicCAS(&B.ckey[h], 0u, key | kTabBusy);
+        if (old == 0u) {
+            B.cW[h] = W;
+            __hip_atomic_store(&B.ckey[h], key, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            return;
+        }
+        if ((old & ~kTabBusy) == key) return;
+        h = (h + 1u) & (kTabCache - 1u);
+    }
+}
 
 // Per-microbatch cost of layers lane and lane+64 of plan (dp, tp) with b
 // samples per microbatch (0 past L): compute, four tensor-parallel ring
@@ -2062,10 +2122,17 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         const double x1 = lane + 64 < jb.L ? (double)A.x[off + lane + 64] : kInf;
         const double xm = wave_reduce1<OpMin>(fmin(x0, x1));
         if (lane == 0) B.x_layer_min = xm;
+    } else {
+        bool same = true;
+        for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
+        const bool uni = __ballot(!same) == 0ull;
+        for (int h = lane; h < (int)kTabCache; h += 64) B.ckey[h] = 0u;
+        if (lane == 0) B.share = (uni && A.n_counts > 1 && jb.Bg < (1 << 17)) ? 1 : 0;
     }
     if (tid == 0) B.next_cell = 0;
     if (wid == 0) tally(Wv, lane, kCells, (unsigned long long)A.n_counts);
     __syncthreads();
+    const bool share = B.share != 0;
 
     for (;;) {
         int cix = 0;
@@ -2137,10 +2204,10 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
             double c[2];
             tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp0, tp0, bq0, c);
             seq_prefix<2, 2>(c[0], c[1], jb.L, lane, Wv.UD, Wv.UD + 1, true);
-            tally(Wv, lane, kProblems, 1);
             tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
             double bst = best_in;
-            solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask mk) {
+            // prices degree pp of the group at bottleneck W; returns the degrees still wanted
+            auto price_deg = [&](int pp, double W, Mask mk) -> Mask {
                 const int e = (int)Wv.lbnd[pp - 1];
                 const int dp = cell.n / (tp0 * pp);
                 const int m = (int)(Wv.planKey[e] & 0x7Fu);
@@ -2164,7 +2231,26 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
                 const bool ka = ea >= 0 && Wv.planT[ea] <= lim;
                 const bool kb = eb >= 0 && Wv.planT[eb] <= lim;
                 return rest & ballot_mask(ka, kb);
-            });
+            };
+            // degrees another cell of this (job, type) has solved are priced
+            // first, from the cache; the recursion runs for the others only
+            Mask want = tm, hit{0ull, 0ull};
+            if (share) {
+                double w0 = 0.0, w1 = 0.0;
+                const bool h0 = ((tm.lo >> lane) & 1ull) && tab_cache_find(B, tab_key(tp0, fl0, bq0, 1 + lane), w0);
+                const bool h1 = ((tm.hi >> lane) & 1ull) && tab_cache_find(B, tab_key(tp0, fl0, bq0, 65 + lane), w1);
+                hit = ballot_mask(h0, h1);
+                for (int pp = hit.next(1); pp; pp = hit.next(pp + 1))
+                    if (want.test(pp)) want = price_deg(pp, pp <= 64 ? bcast(w0, pp - 1) : bcast(w1, pp - 65), want);
+            }
+            const Mask todo{want.lo & ~hit.lo, want.hi & ~hit.hi};
+            if (todo.any()) {
+                tally(Wv, lane, kProblems, 1);
+                solve_dp(Wv, jb.L, todo, lane, [&](int pp, double W, Mask mk) {
+                    if (share && lane == 0) tab_cache_put(B, tab_key(tp0, fl0, bq0, pp), W);
+                    return price_deg(pp, W, mk);
+                });
+            }
             return bst;
         };
         if (A.prune) {

@@ -5,6 +5,7 @@ Every plan gets the balanced partition of its own per-microbatch costs, with
 each communication term's latency interpolated in its link's table.  Small
 workloads are compared cell by cell, the large ones run in full on the GPU
 and are compared on sampled cells.  Each case prints its name first."""
+import dataclasses
 import sys
 
 import numpy as np
@@ -158,3 +159,25 @@ def test_bound_pruning_is_exact(name):
     assert c0["plans_skipped"] == 0 and c0["plans"] == size["plans"]
     assert c1["plans"] + c1["plans_skipped"] == size["plans"] and c1["plans_skipped"] > 0
     _say(f"{name}: {c1['plans_skipped']} of {size['plans']} plans skipped")
+
+
+def test_shared_bottlenecks_are_exact():
+    """With one kappa for all counts of a type, cells of a (job, type) share the
+    bottlenecks of their (tp, microbatch size) groups.  Raising the kappa of one
+    count by one ulp turns the sharing off for that type: every other cell must
+    come out bitwise the same, with fewer recursions when shared."""
+    w = wl.moe(n_jobs=256)
+    tabs = wl.comm_tables(w)
+    k2 = w.kappa.copy()
+    last = np.arange(w.n_types) * w.n_counts + (w.n_counts - 1)
+    k2[:, last] = np.nextafter(k2[:, last], np.float32(2.0))
+    w2 = dataclasses.replace(w, kappa=k2)
+    _say(f"moe[256 jobs]: {w.n_cells} cells, kappa uniform vs one count off by an ulp")
+    r1, c1, _ = _run(w, tabs)
+    r2, c2, _ = _run(w2, tabs)
+    keep = np.ones(w.n_cells, bool)
+    keep[(np.arange(w.n_cells) % w.n_counts) == w.n_counts - 1] = False
+    for k in ("t_iter", "thr", "plan", "cuts"):
+        assert np.array_equal(r1[k][keep], r2[k][keep]), k
+    _say(f"  recursions {c1['problems']} shared, {c2['problems']} unshared")
+    assert c1["problems"] < c2["problems"]
