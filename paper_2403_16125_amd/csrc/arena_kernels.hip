@@ -75,6 +75,8 @@ struct BlockLds {
     double p_layer_max;           // largest parameter bytes of one layer
     double x_layer_min;           // smallest boundary activation bytes of one layer
     double x_sum, q_sum;          // sums over the layers of x and of the all-to-all bytes
+    float xwin[kLmax + 1];        // [pp]: least x bytes of a window of layers whose pure-compute cost
+    float qwin[kLmax + 1];        //   reaches Wtab[0][pp], and least all-to-all bytes (rounded down)
     int32_t slot_tp[SLOTS];
     int32_t slot_var[SLOTS];
     int32_t n_slots;
@@ -1248,13 +1250,16 @@ struct BoundCtx {
     double rtp;
     double UL;
     double ar_intra, ar_inter;
+    double cx, cq;                // seconds per sample per x byte and per all-to-all byte of a layer
 };
 
 // Lower bound of the iteration time of every plan of degree pp (any listed m)
 // of problem bc, or +inf when no split of the layers into pp stages fits
 // memory.  Bounded below without the cuts:
-//   W*(pp) >= UL / pp (the stages tile the layers) and >= Wpure(pp) / tp (the
-//   problem's layer costs are at least the pure-compute ones over tp);
+//   W*(pp) >= UL / pp (the stages tile the layers), and the stage of the
+//   optimal split whose pure-compute cost is largest reaches Wpure(pp) (no
+//   split of pp stages does better), so it is a window of layers reaching
+//   Wpure(pp): W*(pp) >= Wpure(pp) / tp + cx xwin(pp) + cq qwin(pp);
 //   the p2p bytes over the pp-1 stage boundaries >= (pp-1) min_l x_l;
 //   the largest stage's parameters >= max(P / pp, max_l p_l).
 // For fixed dp, T = Bg/dp W + Bg/(dp m) (fill - W) + AR falls as m grows
@@ -1270,7 +1275,8 @@ __device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const
     const double plb = fmax(B.Pp[jb.L] * rpp, B.p_layer_max);
     if (4.0 * plb > ty.mem * (double)bc.tp * (1.0 + 1e-9)) return kInf;
     const double b = rint((double)jb.Bg * rcp_approx((double)(dp * m)));   // exact: dp m divides Bg
-    const double Wlb = fmax(bc.UL * rpp, B.Wtab[0][pp] * bc.rtp);
+    const double Wlb = fmax(bc.UL * rpp, B.Wtab[0][pp] * bc.rtp + (bc.cx * (double)B.xwin[pp] +
+                                                                    bc.cq * (double)B.qwin[pp]));
     const double fill = bc.UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
     const int grp = dp * bc.tp;
     const double c_ar = (grp < 32 && ((gpn_divs >> grp) & 1u)) ? bc.ar_intra : bc.ar_inter;
@@ -1321,7 +1327,7 @@ __device__ __forceinline__ double degree_bounds(const BlockLds<SLOTS>& B, WaveLd
 // The bound context of the cell's problem of tensor degree tp; the pure-
 // compute problem (tp = 1 without all-to-all) takes its exact cost sum.
 __device__ __forceinline__ BoundCtx bound_ctx(const Cell& cell, int tp, double UL, double ar_intra1,
-                                              double ar_inter1)
+                                              double ar_inter1, double cx1 = 0.0, double cq = 0.0)
 {
     BoundCtx bc;
     bc.tp = tp;
@@ -1330,6 +1336,8 @@ __device__ __forceinline__ BoundCtx bound_ctx(const Cell& cell, int tp, double U
     bc.UL = UL;
     bc.ar_intra = ar_intra1 * bc.rtp;
     bc.ar_inter = ar_inter1 * bc.rtp;
+    bc.cx = cx1 * ((double)(tp - 1) * bc.rtp);
+    bc.cq = cq;
     return bc;
 }
 
@@ -1342,6 +1350,76 @@ __device__ __forceinline__ int find_slot(const BlockLds<SLOTS>& B, int n_slots, 
     for (int s = 1; s < n_slots; ++s)
         if (B.slot_tp[s] == tp && B.slot_var[s] == var) slot = s;
     return slot;
+}
+
+// Inclusive prefix sum over the wave (row shifts, then row broadcasts): the
+// order of the additions is a tree's, which is all a bound needs.
+__device__ __forceinline__ double wave_incl_sum(double v)
+{
+    v += dpp<0x111, 0xf>(v, 0.0);   // row_shr:1
+    v += dpp<0x112, 0xf>(v, 0.0);   // row_shr:2
+    v += dpp<0x114, 0xf>(v, 0.0);   // row_shr:4
+    v += dpp<0x118, 0xf>(v, 0.0);   // row_shr:8
+    v += dpp<0x142, 0xa>(v, 0.0);   // row_bcast:15 into rows 1 and 3
+    v += dpp<0x143, 0xc>(v, 0.0);   // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
+// For every degree pp <= L: the least x bytes and the least all-to-all bytes
+// of a window of consecutive layers whose pure-compute cost (a difference of
+// Upure, as the recursion forms it) reaches Wtab[0][pp], rounded down with a
+// relative margin for the sums' rounding.  The waves share the degrees; the
+// x and all-to-all prefixes sit in each wave's UD (x even, all-to-all odd).
+template <int SLOTS>
+__device__ void window_minima(BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int wid, int L, const float* xg,
+                              const float* qg)
+{
+    double* P = Wv.UD;
+    const double x0 = lane < L ? (double)xg[lane] : 0.0, x1 = lane + 64 < L ? (double)xg[lane + 64] : 0.0;
+    const double q0 = lane < L ? (double)qg[lane] : 0.0, q1 = lane + 64 < L ? (double)qg[lane + 64] : 0.0;
+    const double sx0 = wave_incl_sum(x0), sq0 = wave_incl_sum(q0);
+    const double tx = bcast(sx0, 63), tq = bcast(sq0, 63);
+    const double sx1 = wave_incl_sum(x1) + tx, sq1 = wave_incl_sum(q1) + tq;
+    if (lane == 0) {            // zero (lane 0's sum is its own value), kept out of a constant register
+        P[0] = sx0 - x0;
+        P[1] = sq0 - q0;
+    }
+    if (lane < L) {
+        P[2 * (lane + 1)] = sx0;
+        P[2 * (lane + 1) + 1] = sq0;
+    }
+    if (lane + 64 < L) {
+        P[2 * (lane + 65)] = sx1;
+        P[2 * (lane + 65) + 1] = sq1;
+    }
+    wave_sync();
+    const double* U = B.Upure;
+    for (int pp = wid + 1; pp <= L; pp += kWavesPerBlock) {
+        const double th = B.Wtab[0][pp];
+        double bx = kInf, bq = kInf;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i = lane + 64 * h;
+            if (i < L) {
+                const double Ui = U[i];
+                if (U[L] - Ui >= th) {
+                    int lo = i + 1, hi = L;         // the first end whose window reaches th
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (U[mid] - Ui >= th) hi = mid; else lo = mid + 1;
+                    }
+                    bx = fmin(bx, P[2 * lo] - P[2 * i]);
+                    bq = fmin(bq, P[2 * lo + 1] - P[2 * i + 1]);
+                }
+            }
+        }
+        bx = wave_reduce1<OpMin>(bx);
+        bq = wave_reduce1<OpMin>(bq);
+        if (lane == 0) {
+            B.xwin[pp] = __double2float_rd(fmax(bx, 0.0) * (1.0 - 1e-9));
+            B.qwin[pp] = __double2float_rd(fmax(bq, 0.0) * (1.0 - 1e-9));
+        }
+    }
 }
 
 // ------------------------------------------------------------ the kernel
@@ -1375,13 +1453,15 @@ template <int SLOTS, bool MEM, bool EXT = false>
 __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 {
     __shared__ BlockLds<SLOTS> B;
-    // the thread index passes through an empty asm statement once per item, so
-    // nothing derived from it is hoisted out of the item loop and held in
-    // registers across every item (it would be spilled)
-    int tid;
-    __asm__ volatile("" : "=v"(tid) : "0"((int)threadIdx.x));
-    const int lane = tid & 63;
-    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // the lane index (counted by mbcnt, not kept from the launch) passes
+    // through an empty asm statement once per item, so nothing derived from
+    // it is hoisted out of the item loop and held in registers across every
+    // item (it would be spilled)
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    int lane0;
+    __asm__ volatile("" : "=v"(lane0) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
+    const int lane = lane0;
+    const int tid = wid * 64 + lane;
     WaveLds& Wv = B.w[wid];
     double* const R = MEM ? Wv.R : nullptr;
     if (item < 0) {
@@ -1512,13 +1592,15 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
     }
     __syncthreads();
+    window_minima(B, Wv, lane, wid, jb.L, A.x + off, A.q + off);
+    __syncthreads();
 
     // ---- cells: take counts, largest first, from the block's work counter
     for (;;) {
         // the lane index is re-derived per cell, for the same reason as the
         // thread index per item
         int lane;
-        __asm__ volatile("" : "=v"(lane) : "0"(tid & 63));
+        __asm__ volatile("" : "=v"(lane) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
         int cix = 0;
         if (lane == 0) cix = atomicAdd(&B.next_cell, 1);
         cix = __builtin_amdgcn_readfirstlane(cix);
@@ -1538,6 +1620,9 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         const double ar_inter1 = cell.kappa * 2.0 / ty.bw_inter;
         const double ul_tp = cell.kappa * 8.0 * B.x_sum / ty.bw_intra;
         const double ul_a2a = jb.moe ? cell.kappa * B.q_sum / ty.bw_inter : 0.0;
+        // per byte of a layer: tensor-parallel seconds (times (tp-1)/tp) and all-to-all seconds
+        const double cx1 = cell.kappa * 8.0 / ty.bw_intra;
+        const double cq1 = jb.moe ? cell.kappa / ty.bw_inter : 0.0;
 
         // plans of the pure-compute problem first: their bottlenecks are shared
         {
@@ -1581,7 +1666,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
             const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
             const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
             const double lb = degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
-                                            bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1));
+                                            bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1, cx1, cq1));
             if (lane == 0) {
                 Wv.cand_tp[ncand] = (uint8_t)tp;
                 Wv.cand_lb[ncand] = lb;
@@ -1608,7 +1693,8 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                                   target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
             const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
             const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
-            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs, bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1));
+            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
+                          bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1, cx1, cq1));
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
             {
                 const double lb0 = Wv.lbnd[lane], lb1 = Wv.lbnd[lane + 64];
