@@ -180,8 +180,20 @@ __device__ __forceinline__ void seq_prefix(double v0, double v1, int L, int lane
     if (lane == 0) {
         double acc = 0.0;
         out[0] = 0.0;
-#pragma unroll 8
-        for (int i = 0; i < L; ++i) {
+        // eight loads issued before their adds and stores (a store may alias a
+        // later load, so the compiler would otherwise wait on each load in turn)
+        int i = 0;
+        for (; i + 8 <= L; i += 8) {
+            double v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = tmp[(i + k) * TS];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                acc = acc + v[k];
+                out[(i + k + 1) * OS] = acc;
+            }
+        }
+        for (; i < L; ++i) {
             acc = acc + tmp[i * TS];
             out[(i + 1) * OS] = acc;
         }
