@@ -385,7 +385,7 @@ def main() -> int:
     ap.add_argument("--cuts", action="store_true", help="also write the stage cuts of every cell")
     ap.add_argument("--cpu-every", type=int, default=None,
                     help="oracle sample: every k-th job (default 256; 2048 with --partition memory, "
-                         "1024 with --comm-tables, 8 with --partition exact-t)")
+                         "1024 with --comm-tables, 12 with --partition exact-t)")
     ap.add_argument("--partition", default="balanced", choices=["balanced", "memory", "exact-t"],
                     help="stage partition rule of the estimate (exact-t: the trace-like workload unless "
                          "--workload names another of at most 96 layers per job)")
@@ -556,7 +556,7 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
         exact = rule == arena.PARTITION_EXACT_T
-        every = args.cpu_every or (256 if plain else (8 if exact else (1024 if tables is not None else 2048)))
+        every = args.cpu_every or (256 if plain else (12 if exact else (1024 if tables is not None else 2048)))
         line["cpu_baseline"] = cpu_baseline(w, every, rule=rule, tables=tables, cell_every=10 if exact else 1)
     print(json.dumps(line), flush=True)
     return 0
