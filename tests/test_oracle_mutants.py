@@ -30,8 +30,8 @@ MUTANTS = {
     "strict_memory_limit": ("return Mem <= M->mem;", "return Mem < M->mem;"),
     "stages_counted_from_the_front": ("if (!fits_sums(M, P, A, pp - t, pp)) continue;",
                                       "if (!fits_sums(M, P, A, t - 1, pp)) continue;"),
-    "microbatch_size_without_m": ("M.b = (double)jb->Bg / (double)(dp * m);",
-                                  "M.b = (double)jb->Bg / (double)dp;"),
+    "microbatch_size_without_m": ("M.b = b;\n        M.mem = ty->mem;",
+                                  "M.b = (double)jb->Bg / (double)dp;\n        M.mem = ty->mem;"),
     # (checking the stage being closed as the next one is no mistake: the
     # smallest cut that leaves a splittable rest always gives a stage that
     # fits, so that check never binds; the completion test is what matters)
