@@ -39,3 +39,22 @@ def test_settle_and_planted_differences(oracle):
     assert sorted(rest.tolist()) == sorted([a, b, c])
     rep = compare(w, select(gpu, rest), rest, oracle, ref={k: v[rest] for k, v in ref.items()})
     assert len(rep["mismatch"]) == 3 and rep["exact"] == 0
+
+
+def test_settle_without_cut_rows(oracle):
+    """The timed launch writes no cut rows: plans, times and throughputs are
+    still settled, and a planted difference in the plan or the time is left
+    to the per-cell comparison."""
+    w = wl.make("small")
+    ids = np.arange(w.n_cells)
+    ref = oracle.cells(w, ids)
+    gpu = _as_gpu(ref)
+    del gpu["cuts"]
+    ok, _ = wp.settle(gpu, ref, 0, w.n_cells)
+    assert ok.all()
+    feas = np.nonzero(np.isfinite(ref["T"]) & (ref["pp"] > 1))[0]
+    a, c = int(feas[0]), int(feas[1])
+    gpu["pp"][a] = 1 if gpu["pp"][a] != 1 else 2            # another plan
+    gpu["t_iter"][c] *= np.float32(1.001)                   # another time
+    ok, _ = wp.settle(gpu, ref, 0, w.n_cells)
+    assert sorted(np.nonzero(~ok)[0].tolist()) == sorted([a, c])

@@ -54,13 +54,17 @@ def settle(gpu, ref, lo, hi):
     o_feas = np.isfinite(ref["T"])
     t = gpu["t_iter"][lo:hi].astype(np.float64)
     thr = gpu["thr"][lo:hi].astype(np.float64)
-    gc = gpu["cuts"][lo:hi].astype(np.int32)
-    oc = ref["cuts"]
-    both_inf = ~g_feas & ~o_feas & np.isinf(t) & (thr == 0) & (gpu["dp"][lo:hi] == 0) & (gc == 0xFF).all(axis=1)
-    pp = gpu["pp"][lo:hi].astype(np.int32)
-    col = np.arange(gc.shape[1], dtype=np.int32)[None, :]
-    inside = col < (pp - 1)[:, None]
-    cuts_ok = np.where(inside, gc == oc[:, :gc.shape[1]], gc == 0xFF).all(axis=1)
+    both_inf = ~g_feas & ~o_feas & np.isinf(t) & (thr == 0) & (gpu["dp"][lo:hi] == 0)
+    if gpu.get("cuts") is not None:
+        gc = gpu["cuts"][lo:hi].astype(np.int32)
+        oc = ref["cuts"]
+        both_inf &= (gc == 0xFF).all(axis=1)
+        pp = gpu["pp"][lo:hi].astype(np.int32)
+        col = np.arange(gc.shape[1], dtype=np.int32)[None, :]
+        inside = col < (pp - 1)[:, None]
+        cuts_ok = np.where(inside, gc == oc[:, :gc.shape[1]], gc == 0xFF).all(axis=1)
+    else:                                # the timed launch writes no cut rows
+        cuts_ok = np.ones(hi - lo, bool)
     with np.errstate(invalid="ignore", divide="ignore"):
         relT = np.abs(t - ref["T"]) / ref["T"]
         relthr = np.abs(thr - ref["thr"]) / ref["thr"]
@@ -104,6 +108,8 @@ def main() -> int:
     ap.add_argument("--partition", default="balanced", choices=["balanced", "memory"])
     ap.add_argument("--comm-tables", action="store_true")
     ap.add_argument("--proxy", action="store_true")
+    ap.add_argument("--no-cuts", action="store_true",
+                    help="estimate without cut rows, as bench.py times it (plans, T, throughput compared)")
     ap.add_argument("--job-every", type=int, default=1,
                     help="compare the cells of every k-th job only (all grids of each); the GPU still "
                          "estimates the whole workload")
@@ -128,7 +134,7 @@ def main() -> int:
     mode = ("proxy planner" if args.proxy else "memory rule" if rule else
             "comm tables" if tables is not None else "balanced")
     say(f"{args.workload} round {args.round} ({mode}): {w.n_cells} cells; estimating on the GPU")
-    est = arena.Estimator(w, with_cuts=not args.proxy,
+    est = arena.Estimator(w, with_cuts=not (args.proxy or args.no_cuts),
                           rule=arena.PARTITION_MEMORY if rule else arena.PARTITION_BALANCED,
                           comm_tables=tables)
     try:
@@ -158,7 +164,7 @@ def main() -> int:
     def work(ch):
         ids = (ch[:, None] * per_job + np.arange(per_job, dtype=np.int64)[None, :]).ravel()
         lo, hi = 0, len(ids)
-        sub_gpu = {k: v[ids] for k, v in gpu.items()}
+        sub_gpu = {k: (v[ids] if v is not None else None) for k, v in gpu.items()}
         if args.proxy:
             want = px.cells(w, ids, kappa_round=args.round, f_ref=wl.F_REF, n_ops=16)
             bad = proxy_mismatches(sub_gpu, want, lo, hi)
