@@ -207,6 +207,15 @@ __device__ __forceinline__ void tally(WaveLds& Wv, int lane, int which, unsigned
     if (lane == 0) Wv.tally[which] += v;
 }
 
+// 1/x to within a few ulps: the hardware estimate refined by one Newton step
+// (lower bounds use it under a margin of 1e-9; integer quotients rounded from
+// it are exact when the division is).
+__device__ __forceinline__ double rcp_approx(double x)
+{
+    const double r = __builtin_amdgcn_rcp(x);
+    return fma(fma(-x, r, 1.0), r, r);
+}
+
 // ------------------------------------------------------------ model pieces
 
 // Link bandwidth by value (a conditional over two fields of one struct would
@@ -348,7 +357,7 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
 {
     // U_j = UD[2j], D_j = UD[2j+1]
     const bool act = i <= hi;
-    double v = 0.0;
+    double v;                                // set and stored only where act
     if (act) {
         const double Ui = UD[2 * i];
         const int a = lb > k - 1 ? lb : k - 1;   // every j < a fails
@@ -387,7 +396,8 @@ __device__ __forceinline__ void dp_entry(double* UD, int k, int hi, int i, int l
         const double t = Ui - UD[2 * c - 2];
         v = (c >= k && t < dc) ? t : dc;
     }
-    // every lane has read row k-1 before any lane overwrites it
+    // every lane has read row k-1 (gallop included) before any lane
+    // overwrites it: the store stays after the branch
     __asm__ volatile("" ::: "memory");
     if (act) UD[2 * i + 1] = v;
 }
@@ -429,10 +439,11 @@ __device__ void solve_dp(WaveLds& Wv, int L, Mask tm, int lane, OnTarget&& on_ta
         // lower bounds: own crossing (i-1, row k-1) and the next lane's (i, row k-1)
         const int top1 = __builtin_amdgcn_readlane(jp1, 0);
         const int nb0 = from_next_lane(jp0, top1);
-        const int nb1 = from_next_lane(jp1, jp1);
         const int lb0 = jp0 > nb0 ? jp0 : nb0;
-        const int lb1 = jp1 > nb1 ? jp1 : nb1;
-        if (hi - k >= 64) dp_entry(UD, k, hi, k + 64 + lane, lb1, jp1);   // high part first: in place
+        if (hi - k >= 64) {                    // high part first: in place
+            const int nb1 = from_next_lane(jp1, jp1);
+            dp_entry(UD, k, hi, k + 64 + lane, jp1 > nb1 ? jp1 : nb1, jp1);
+        }
         dp_entry(UD, k, hi, k + lane, lb0, jp0);
         if (lane == 0) UD[2 * hi + 3] = kInf;
         n_ent += (unsigned)(hi - k + 1);
@@ -1050,8 +1061,10 @@ __device__ double price_exact(const BlockLds<SLOTS>& B, WaveLds& Wv, const doubl
     bool adm = false;
     double b = 0.0;
     if (mv > 0) {
+        // the nearest integer to Bg / (dp m) from a reciprocal estimate: exact
+        // when dp m divides Bg, and the product test decides divisibility
         const double dm = (double)(dp * mv);
-        const double q = rint((double)jb.Bg / dm);
+        const double q = rint((double)jb.Bg * rcp_approx(dm));
         adm = q * dm == (double)jb.Bg;
         b = q;
     }
@@ -1166,8 +1179,10 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     bool adm = false;
     double b = 0.0;
     if (mv > 0) {
+        // the nearest integer to Bg / (dp m) from a reciprocal estimate: exact
+        // when dp m divides Bg, and the product test decides divisibility
         const double dm = (double)(dp * mv);
-        const double q = rint((double)jb.Bg / dm);
+        const double q = rint((double)jb.Bg * rcp_approx(dm));
         adm = q * dm == (double)jb.Bg;
         b = q;
     }
@@ -1188,6 +1203,15 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     const double fP0 = 4.0 * P0, fP1 = 4.0 * P1;
     const int r0 = pp - lane, r1 = pp - lane - 64;         // stages from the lane's to the last
     int lo = 0, hi = nadm;                                  // first fitting rank in [lo, hi]
+    {
+        // every count fits when the smallest does (the common case): one test
+        const double bm = Wv.bq[0];
+        const int m = Wv.mq[0];
+        const double i0 = (double)(m < r0 ? m : r0) * bm;
+        const double i1 = (double)(m < r1 ? m : r1) * bm;
+        const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
+        if (__ballot(over) == 0ull) hi = 0; else lo = 1;
+    }
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
         const double bm = Wv.bq[mid];
@@ -1245,13 +1269,6 @@ __device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const doub
     return best_t;
 }
 
-// 1/x to within a few ulps: the hardware estimate refined by one Newton step
-// (only lower bounds use it; their margin of 1e-9 covers it many times over).
-__device__ __forceinline__ double rcp_approx(double x)
-{
-    const double r = __builtin_amdgcn_rcp(x);
-    return fma(fma(-x, r, 1.0), r, r);
-}
 
 // What the lower bounds of one problem's plans share: its tensor degree, n /
 // tp, a lower bound of its summed per-sample layer costs, and the gradient
