@@ -35,6 +35,7 @@ constexpr int kPad = 8;            // prefix arrays hold +inf past the last laye
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
+constexpr int kCertMinDegree = 16; // a bottleneck certificate is tried for degrees from here up
 
 struct WaveLds {
     // the wave's current problem, pairs (U_j, D_j): U the cost prefix (+inf
@@ -550,6 +551,86 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     r.lo1 = cB;
     r.hi1 = from_next_lane(cB, pp == 128 ? L : 0);
     return r;
+}
+
+// Does every split of the L layers into pp stages have a stage costing more
+// than th (a stage's cost a difference of U, stride S, as the recursion forms
+// it)?  Right to left, prev(e) is the smallest c with U_e - U_c <= th (e
+// itself when layer e-1 alone exceeds th): the fewest stages with costs <= th
+// take prev steps from L to 0, and a split into fewer stages refines into pp
+// (costs only fall), so the answer is no exactly when prev^(pp-1)(L) reaches
+// a node n with prev(n) = 0.  prev^(2^s) tables by binary lifting as in
+// canonical_stages, one walk.  Uniform result.
+template <int S>
+__device__ bool bottleneck_exceeds(const double* U, uint8_t* J, int lane, int L, int pp, double th)
+{
+    if (th < 0.0) return true;         // every stage costs at least 0
+    if (!(th >= 0.0)) return false;
+    // from here c = e passes for every e, so prev(e) <= e <= L: every node
+    // and table entry stays in [0, L]
+    const bool two = L > 64;
+    const int e0 = 1 + lane, e1 = 65 + lane;
+    int cur0 = 0, cur1 = 0;
+    {
+        // the failing c (U_e - U_c > th) form a prefix of [0, e]
+        const double Ue0 = U[e0 * S];
+        if (two) {
+            const double Ue1 = U[e1 * S];
+            cur1 = Ue1 - U[63 * S] > th ? 64 : 0;
+#pragma unroll
+            for (int step = 32; step >= 1; step >>= 1) {
+                const bool g0 = Ue0 - U[(cur0 + step - 1) * S] > th;
+                const bool g1 = Ue1 - U[(cur1 + step - 1) * S] > th;
+                cur0 += g0 ? step : 0;
+                cur1 += g1 ? step : 0;
+            }
+        } else {
+#pragma unroll
+            for (int step = 32; step >= 1; step >>= 1)
+                cur0 += Ue0 - U[(cur0 + step - 1) * S] > th ? step : 0;
+        }
+    }
+    cur0 = e0 <= L ? cur0 : 0;
+    cur1 = (two && e1 <= L) ? cur1 : 0;
+    if (e0 <= L) J[e0] = (uint8_t)cur0;
+    if (two && e1 <= L) J[e1] = (uint8_t)cur1;
+    const int levels = pp > 1 ? 32 - __clz(pp - 1) : 1;   // 2^levels > pp - 1
+    if (lane < levels) J[lane * kLevelStride] = 0;
+    wave_sync();
+    for (int s = 1; s < levels; ++s) {
+        const uint8_t* prev = J + (s - 1) * kLevelStride;
+        uint8_t* lev = J + s * kLevelStride;
+        cur0 = prev[cur0];
+        if (two) cur1 = prev[cur1];
+        if (e0 <= L) lev[e0] = (uint8_t)cur0;
+        if (two && e1 <= L) lev[e1] = (uint8_t)cur1;
+        wave_sync();
+    }
+    int n = L;
+    for (int s = 0; s < levels; ++s)
+        if (((pp - 1) >> s) & 1) n = J[s * kLevelStride + n];
+    const bool ok = n == 0 || J[n] == 0;
+    wave_sync();
+    return !ok;
+}
+
+// The bottleneck of pp stages over the problem's prefix U (stride 2) when the
+// pure-compute problem's canonical split certifies it, else -1.  That split
+// (cuts of Upure at Wpure(pp)) costs UB = its largest stage on U, so the
+// bottleneck is at most UB; if no split keeps every stage below UB (the test
+// above at the largest double below UB) it is UB exactly.
+template <int SLOTS>
+__device__ double certified_bottleneck(const BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int L, int pp)
+{
+    const Stages sg = canonical_stages<1>(B.Upure, Wv.J, lane, L, pp, B.Wtab[0][pp]);
+    double c = 0.0;
+    if (lane < pp) c = Wv.UD[2 * sg.hi0] - Wv.UD[2 * sg.lo0];
+    if (lane + 64 < pp) c = fmax(c, Wv.UD[2 * sg.hi1] - Wv.UD[2 * sg.lo1]);
+    const double ub = wave_reduce1<OpMax>(c);
+    wave_sync();
+    if (!(ub > 0.0 && ub < kInf)) return -1.0;
+    const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
+    return bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below) ? ub : -1.0;
 }
 
 // ------------------------------------------------------------ memory-constrained partition
@@ -1752,7 +1833,8 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                                                                   A.tie_eps, A.prune != 0));
                 }
             } else {
-                solve_dp(Wv, jb.L, tm, lane, [&](int pp, double W, Mask m) {
+                // prices degree pp at bottleneck W; returns the degrees still wanted
+                auto price_deg = [&](int pp, double W, Mask m) -> Mask {
                     best = fmin(best, price_target<SLOTS, 2, MEM, EXT>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp, W,
                                                                   np, A.cuts != nullptr, R, best, A.tie_eps,
                                                                   A.prune != 0));
@@ -1764,8 +1846,18 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                     if (keep.lo != rest.lo || keep.hi != rest.hi)
                         tally(Wv, lane, kSkipped, dropped_plans(B, rest, keep, lane, cell.n / tp));
                     return keep;
-                });
-                tally(Wv, lane, kProblems, 1);
+                };
+                // the largest requested degrees first: where the pure-compute split
+                // certifies the bottleneck, the recursion is spared their rows
+                for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
+                    const double wc = certified_bottleneck(B, Wv, lane, jb.L, pc);
+                    if (!(wc >= 0.0)) break;
+                    tm = price_deg(pc, wc, tm);
+                }
+                if (tm.any()) {
+                    solve_dp(Wv, jb.L, tm, lane, price_deg);
+                    tally(Wv, lane, kProblems, 1);
+                }
             }
         }
         // problems never taken: none of their plans can hold the cell's best
