@@ -35,7 +35,8 @@ constexpr int kPad = 8;            // prefix arrays hold +inf past the last laye
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
-constexpr int kCertMinDegree = 16; // a bottleneck certificate is tried for degrees from here up
+constexpr int kCertMinDegree = 2;  // a bottleneck certificate is tried for degrees from here up
+constexpr int kCertRounds = 2;     // splits tried per certificate
 
 struct WaveLds {
     // the wave's current problem, pairs (U_j, D_j): U the cost prefix (+inf
@@ -614,23 +615,37 @@ __device__ bool bottleneck_exceeds(const double* U, uint8_t* J, int lane, int L,
     return !ok;
 }
 
-// The bottleneck of pp stages over the problem's prefix U (stride 2) when the
-// pure-compute problem's canonical split certifies it, else -1.  That split
-// (cuts of Upure at Wpure(pp)) costs UB = its largest stage on U, so the
+// The largest stage cost, on the problem's prefix U (stride 2), of split sg.
+__device__ __forceinline__ double split_cost(const double* UD, const Stages& sg, int lane, int pp)
+{
+    double c = 0.0;
+    if (lane < pp) c = UD[2 * sg.hi0] - UD[2 * sg.lo0];
+    if (lane + 64 < pp) c = fmax(c, UD[2 * sg.hi1] - UD[2 * sg.lo1]);
+    const double ub = wave_reduce1<OpMax>(c);
+    wave_sync();
+    return ub;
+}
+
+// The bottleneck of pp stages over the problem's prefix U (stride 2) when a
+// few splits certify it, else -1.  The first is the pure-compute problem's
+// canonical split (cuts of Upure at Wpure(pp)): it costs UB on U, so the
 // bottleneck is at most UB; if no split keeps every stage below UB (the test
-// above at the largest double below UB) it is UB exactly.
+// above at the largest double under UB) the bottleneck is UB exactly.
+// Otherwise some split does, and the canonical split of U under that double
+// costs less than UB: it is the next one tried.
 template <int SLOTS>
 __device__ double certified_bottleneck(const BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int L, int pp)
 {
-    const Stages sg = canonical_stages<1>(B.Upure, Wv.J, lane, L, pp, B.Wtab[0][pp]);
-    double c = 0.0;
-    if (lane < pp) c = Wv.UD[2 * sg.hi0] - Wv.UD[2 * sg.lo0];
-    if (lane + 64 < pp) c = fmax(c, Wv.UD[2 * sg.hi1] - Wv.UD[2 * sg.lo1]);
-    const double ub = wave_reduce1<OpMax>(c);
-    wave_sync();
-    if (!(ub > 0.0 && ub < kInf)) return -1.0;
-    const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
-    return bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below) ? ub : -1.0;
+    double ub = split_cost(Wv.UD, canonical_stages<1>(B.Upure, Wv.J, lane, L, pp, B.Wtab[0][pp]), lane, pp);
+    for (int r = 0;; ++r) {
+        if (!(ub > 0.0 && ub < kInf)) return -1.0;
+        const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
+        if (bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below)) return ub;
+        if (r + 1 == kCertRounds) return -1.0;
+        // a split with every stage at most `below` exists, and every single
+        // layer costs at most that (else the test would have passed)
+        ub = split_cost(Wv.UD, canonical_stages<2>(Wv.UD, Wv.J, lane, L, pp, below), lane, pp);
+    }
 }
 
 // ------------------------------------------------------------ memory-constrained partition
@@ -1847,8 +1862,8 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                         tally(Wv, lane, kSkipped, dropped_plans(B, rest, keep, lane, cell.n / tp));
                     return keep;
                 };
-                // the largest requested degrees first: where the pure-compute split
-                // certifies the bottleneck, the recursion is spared their rows
+                // the largest requested degrees first: where a certificate gives the
+                // bottleneck, the recursion is spared their rows
                 for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
                     const double wc = certified_bottleneck(B, Wv, lane, jb.L, pc);
                     if (!(wc >= 0.0)) break;
