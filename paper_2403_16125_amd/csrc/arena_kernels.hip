@@ -628,15 +628,15 @@ __device__ __forceinline__ double split_cost(const double* UD, const Stages& sg,
 
 // The bottleneck of pp stages over the problem's prefix U (stride 2) when a
 // few splits certify it, else -1.  The first is the pure-compute problem's
-// canonical split (cuts of Upure at Wpure(pp)): it costs UB on U, so the
+// canonical split (cuts of its prefix Upure at its bottleneck wpure = Wpure(pp)):
+// it costs UB on U, so the
 // bottleneck is at most UB; if no split keeps every stage below UB (the test
 // above at the largest double under UB) the bottleneck is UB exactly.
 // Otherwise some split does, and the canonical split of U under that double
 // costs less than UB: it is the next one tried.
-template <int SLOTS>
-__device__ double certified_bottleneck(const BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int L, int pp)
+__device__ double certified_bottleneck(const double* Upure, double wpure, WaveLds& Wv, int lane, int L, int pp)
 {
-    double ub = split_cost(Wv.UD, canonical_stages<1>(B.Upure, Wv.J, lane, L, pp, B.Wtab[0][pp]), lane, pp);
+    double ub = split_cost(Wv.UD, canonical_stages<1>(Upure, Wv.J, lane, L, pp, wpure), lane, pp);
     for (int r = 0;; ++r) {
         if (!(ub > 0.0 && ub < kInf)) return -1.0;
         const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
@@ -1865,7 +1865,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                 // the largest requested degrees first: where a certificate gives the
                 // bottleneck, the recursion is spared their rows
                 for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
-                    const double wc = certified_bottleneck(B, Wv, lane, jb.L, pc);
+                    const double wc = certified_bottleneck(B.Upure, B.Wtab[0][pc], Wv, lane, jb.L, pc);
                     if (!(wc >= 0.0)) break;
                     tm = price_deg(pc, wc, tm);
                 }
@@ -2104,6 +2104,8 @@ struct TabBlockLds {
     double x_layer_min;               // smallest boundary activation bytes of one layer
     int32_t next_cell;
     int32_t share;                    // one kappa for all counts of the type: bottlenecks are shared
+    double Upure[kLmax + kPad];       // prefix of the pure-compute per-sample cost (+inf padded)
+    double Wpure[kLmax + 1];          // its bottleneck by degree (every degree up to the layer count)
     WaveLds w[kWavesPerBlock];
     double cW[kTabCache];             // bottleneck cache of the (job, type): bottlenecks
     uint32_t ckey[kTabCache];         //   and their keys (0 empty)
@@ -2300,9 +2302,12 @@ constexpr unsigned kTabKeyMask = kTabPriced - 1u;
 __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int item)
 {
     __shared__ TabBlockLds B;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wid = tid >> 6;
+    // lane index counted per item and per cell (as in estimate_body)
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    int lane0;
+    __asm__ volatile("" : "=v"(lane0) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
+    const int lane = lane0;
+    const int tid = wid * 64 + lane;
     WaveLds& Wv = B.w[wid];
     if (item < 0) {
         block_tallies(A, Wv, lane, item);
@@ -2344,6 +2349,17 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         const double x1 = lane + 64 < jb.L ? (double)A.x[off + lane + 64] : kInf;
         const double xm = wave_reduce1<OpMin>(fmin(x0, x1));
         if (lane == 0) B.x_layer_min = xm;
+        // the pure-compute problem for every degree: its canonical splits are
+        // the first candidates of the groups' bottleneck certificates
+        build_prefix_u<1>(A.t + off, A.x + off, A.q + off, B.Upure, Wv.UD + 1, lane, jb, ty, 1.0, 1, false);
+        for (int e = lane; e < kLmax + kPad; e += 64) Wv.UD[2 * e] = B.Upure[e];
+        wave_sync();
+        solve_dp(Wv, jb.L, ballot_mask(1 + lane <= jb.L, 65 + lane <= jb.L), lane, [&](int pp, double W, Mask m) {
+            if (lane == 0) B.Wpure[pp] = W;
+            return m;
+        });
+        tally(Wv, lane, kProblems, 1);
+        tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
     } else {
         bool same = true;
         for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
@@ -2357,6 +2373,8 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
     const bool share = B.share != 0;
 
     for (;;) {
+        int lane;
+        __asm__ volatile("" : "=v"(lane) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
         int cix = 0;
         if (lane == 0) cix = atomicAdd(&B.next_cell, 1);
         cix = __builtin_amdgcn_readfirstlane(cix);
@@ -2465,7 +2483,15 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
                 for (int pp = hit.next(1); pp; pp = hit.next(pp + 1))
                     if (want.test(pp)) want = price_deg(pp, pp <= 64 ? bcast(w0, pp - 1) : bcast(w1, pp - 65), want);
             }
-            const Mask todo{want.lo & ~hit.lo, want.hi & ~hit.hi};
+            Mask todo{want.lo & ~hit.lo, want.hi & ~hit.hi};
+            // the largest degrees left first: a certified bottleneck spares the
+            // recursion their rows
+            for (int pc = todo.last(); pc >= kCertMinDegree; pc = todo.last()) {
+                const double wc = certified_bottleneck(B.Upure, B.Wpure[pc], Wv, lane, jb.L, pc);
+                if (!(wc >= 0.0)) break;
+                if (share && lane == 0) tab_cache_put(B, tab_key(tp0, fl0, bq0, pc), wc);
+                todo = price_deg(pc, wc, todo);
+            }
             if (todo.any()) {
                 tally(Wv, lane, kProblems, 1);
                 solve_dp(Wv, jb.L, todo, lane, [&](int pp, double W, Mask mk) {
