@@ -1863,11 +1863,15 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                     return keep;
                 };
                 // the largest requested degrees first: where a certificate gives the
-                // bottleneck, the recursion is spared their rows
-                for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
-                    const double wc = certified_bottleneck(B.Upure, B.Wtab[0][pc], Wv, lane, jb.L, pc);
-                    if (!(wc >= 0.0)) break;
-                    tm = price_deg(pc, wc, tm);
+                // bottleneck, the recursion is spared their rows (not under the
+                // exact-T rule, whose pricing outweighs its few recursions: taken
+                // largest first it prices more plans than it saves rows)
+                if constexpr (!EXT) {
+                    for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
+                        const double wc = certified_bottleneck(B.Upure, B.Wtab[0][pc], Wv, lane, jb.L, pc);
+                        if (!(wc >= 0.0)) break;
+                        tm = price_deg(pc, wc, tm);
+                    }
                 }
                 if (tm.any()) {
                     solve_dp(Wv, jb.L, tm, lane, price_deg);
