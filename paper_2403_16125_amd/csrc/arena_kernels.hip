@@ -472,18 +472,15 @@ struct Stages {
     int lo0, lo1, hi0, hi1;
 };
 
+// The successor tables of threshold W: level s of J holds next^(2^s), next(e)
+// the smallest c with U_e - U_c <= W (node 0 maps to itself), for levels
+// 0 .. levels-1.
 template <int S>
-__device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L, int pp, double W)
+__device__ void successor_tables(const double* U, uint8_t* J, int lane, int L, int levels, double W)
 {
-    Stages r;
-    if (pp == 1) {
-        r.lo0 = 0; r.hi0 = L; r.lo1 = 0; r.hi1 = 0;
-        return r;
-    }
-    const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
     // next(e): the failing c (U_e - U_c > W) form a prefix of [0, e); c = e-1
-    // passes (W is at least every single-layer cost) and so does every c > e-1
-    // (U is non-decreasing and +inf past L)
+    // passes when W is at least every single-layer cost, and so does every
+    // c > e-1 (U is non-decreasing and +inf past L)
     // binary lifting of both halves in step (lanes past L read the +inf
     // padding and store nothing)
     const bool two = L > 64;
@@ -523,8 +520,15 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
         if (two && e1 <= L) lev[e1] = (uint8_t)cur1;
         wave_sync();
     }
-    // c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0, c_pp = L.  Every
-    // lane walks (nodes stay in [0, L]); only lanes 1 <= k < pp keep the result.
+}
+
+// The canonical stages of pp >= 2 from successor tables of levels
+// 32 - clz(pp - 1): c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0,
+// c_pp = L.  Every lane walks (nodes stay in [0, L]); only lanes
+// 1 <= k < pp keep the result.
+__device__ Stages stages_from_tables(const uint8_t* J, int lane, int L, int pp, int levels)
+{
+    Stages r;
     const bool hi_half = pp >= 64;
     const int k0 = lane, k1 = lane + 64;
     const int d0 = pp - k0, d1 = pp - k1;
@@ -554,6 +558,19 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     return r;
 }
 
+template <int S>
+__device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L, int pp, double W)
+{
+    if (pp == 1) {
+        Stages r;
+        r.lo0 = 0; r.hi0 = L; r.lo1 = 0; r.hi1 = 0;
+        return r;
+    }
+    const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
+    successor_tables<S>(U, J, lane, L, levels, W);
+    return stages_from_tables(J, lane, L, pp, levels);
+}
+
 // Does every split of the L layers into pp stages have a stage costing more
 // than th (a stage's cost a difference of U, stride S, as the recursion forms
 // it)?  Right to left, prev(e) is the smallest c with U_e - U_c <= th (e
@@ -569,44 +586,8 @@ __device__ bool bottleneck_exceeds(const double* U, uint8_t* J, int lane, int L,
     if (!(th >= 0.0)) return false;
     // from here c = e passes for every e, so prev(e) <= e <= L: every node
     // and table entry stays in [0, L]
-    const bool two = L > 64;
-    const int e0 = 1 + lane, e1 = 65 + lane;
-    int cur0 = 0, cur1 = 0;
-    {
-        // the failing c (U_e - U_c > th) form a prefix of [0, e]
-        const double Ue0 = U[e0 * S];
-        if (two) {
-            const double Ue1 = U[e1 * S];
-            cur1 = Ue1 - U[63 * S] > th ? 64 : 0;
-#pragma unroll
-            for (int step = 32; step >= 1; step >>= 1) {
-                const bool g0 = Ue0 - U[(cur0 + step - 1) * S] > th;
-                const bool g1 = Ue1 - U[(cur1 + step - 1) * S] > th;
-                cur0 += g0 ? step : 0;
-                cur1 += g1 ? step : 0;
-            }
-        } else {
-#pragma unroll
-            for (int step = 32; step >= 1; step >>= 1)
-                cur0 += Ue0 - U[(cur0 + step - 1) * S] > th ? step : 0;
-        }
-    }
-    cur0 = e0 <= L ? cur0 : 0;
-    cur1 = (two && e1 <= L) ? cur1 : 0;
-    if (e0 <= L) J[e0] = (uint8_t)cur0;
-    if (two && e1 <= L) J[e1] = (uint8_t)cur1;
     const int levels = pp > 1 ? 32 - __clz(pp - 1) : 1;   // 2^levels > pp - 1
-    if (lane < levels) J[lane * kLevelStride] = 0;
-    wave_sync();
-    for (int s = 1; s < levels; ++s) {
-        const uint8_t* prev = J + (s - 1) * kLevelStride;
-        uint8_t* lev = J + s * kLevelStride;
-        cur0 = prev[cur0];
-        if (two) cur1 = prev[cur1];
-        if (e0 <= L) lev[e0] = (uint8_t)cur0;
-        if (two && e1 <= L) lev[e1] = (uint8_t)cur1;
-        wave_sync();
-    }
+    successor_tables<S>(U, J, lane, L, levels, th);
     int n = L;
     for (int s = 0; s < levels; ++s)
         if (((pp - 1) >> s) & 1) n = J[s * kLevelStride + n];
@@ -643,8 +624,9 @@ __device__ double certified_bottleneck(const double* Upure, double wpure, WaveLd
         if (bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below)) return ub;
         if (r + 1 == kCertRounds) return -1.0;
         // a split with every stage at most `below` exists, and every single
-        // layer costs at most that (else the test would have passed)
-        ub = split_cost(Wv.UD, canonical_stages<2>(Wv.UD, Wv.J, lane, L, pp, below), lane, pp);
+        // layer costs at most that (else the test would have passed): the
+        // test's tables are those of its canonical split
+        ub = split_cost(Wv.UD, stages_from_tables(Wv.J, lane, L, pp, 32 - __clz(pp - 1)), lane, pp);
     }
 }
 
