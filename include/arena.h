@@ -272,25 +272,28 @@ arena_status arena_estimate(arena_ctx* ctx, float* t_iter, float* thr, uint32_t*
 
 /* Cap on the device memory the library allocates for this context: its
  * copies of the job offsets, batches, grid tables and contention factors,
- * the work order, the tallies and the communication tables (the caller's
- * arrays are not counted).  bytes = 0 (the default) sets no cap.  An
- * arena_estimate whose bound workload needs more returns
- * ARENA_ERR_OUT_OF_MEMORY before anything is allocated, enqueued or written
- * (the need is 4 (J+1) + 4 J + 40 T + 8 NC + 4 T NC + 4 J T bytes plus the
- * tables and about 2 KB, for J jobs, T types and NC counts).  INVALID_ARG
+ * the work order, the tallies, the communication tables and the estimate
+ * blocks' caches of pure-compute splits (the caller's arrays are not
+ * counted).  bytes = 0 (the default) sets no cap.  An arena_estimate whose
+ * bound workload needs more returns ARENA_ERR_OUT_OF_MEMORY before anything
+ * is allocated, enqueued or written (the need is 4 (J+1) + 4 J + 40 T + 8 NC
+ * + 4 T NC + 4 J T bytes plus the communication tables and about 2 KB, for J
+ * jobs, T types and NC counts, plus 8448 bytes per estimate block: one block
+ * per item up to four per compute unit, 8.3 MiB on 256 CUs).  The tables are
+ * checked first, before the device is asked for its CU count.  INVALID_ARG
  * for a negative value.  arena_estimate also returns OUT_OF_MEMORY when a
  * device allocation fails. */
 arena_status arena_set_workspace_limit(arena_ctx* ctx, int64_t bytes);
 
-#define ARENA_NOALLOC_SCRATCH_BYTES (4u << 20)
+#define ARENA_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 /* arena_estimate for callers that cannot allocate device memory (work under
  * stream capture, tight serving loops, harnesses that forbid hipMalloc):
  * the same computation, arguments, outputs and errors, but every
  * library-owned device buffer of the call (job offsets and batches, grid
- * tables, contention factors, work order, tallies, communication tables) is
- * placed in one statically sized device array of ARENA_NOALLOC_SCRATCH_BYTES
- * per GPU, which the library holds until the process ends; the call makes no
+ * tables, contention factors, work order, tallies, communication tables,
+ * the blocks' split caches) is placed in one statically sized device array
+ * of ARENA_NOALLOC_SCRATCH_BYTES per GPU, which the library holds until the process ends; the call makes no
  * device or pinned allocation (it copies the tables from the context's host
  * copies into the array on `stream` each time, and on the first call for
  * a set of job tables runs the value check, which synchronises the stream).
@@ -298,9 +301,10 @@ arena_status arena_set_workspace_limit(arena_ctx* ctx, int64_t bytes);
  * (the tallies of the last call, which arena_get_counters reads): calls that
  * overlap on one GPU, from any context or stream, race and must be ordered by
  * the caller.  Returns ARENA_ERR_OUT_OF_MEMORY, with nothing enqueued or
- * written, when the bound workload's tables need more than the array (about
- * 4 J T + 8 J + 4 T NC bytes; for example 16384 jobs x 8 types x 131 counts
- * need 0.7 MB). */
+ * written, when the bound workload needs more than the array (about
+ * 4 J T + 8 J + 4 T NC bytes of tables plus 8448 bytes per estimate block,
+ * four per compute unit; for example 16384 jobs x 8 types x 131 counts need
+ * 0.7 MB of tables and 8.3 MiB of caches on 256 CUs). */
 arena_status arena_estimate_noalloc(arena_ctx* ctx, float* t_iter, float* thr, uint32_t* plan,
                                     uint8_t* cuts, int32_t cuts_stride, void* stream);
 

@@ -34,7 +34,7 @@ EXPORTED = (
     "arena_set_workspace_limit", "arena_estimate_noalloc",
 )
 
-NOALLOC_SCRATCH_BYTES = 4 << 20
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 PARTITION_BALANCED = 0
 PARTITION_MEMORY = 1

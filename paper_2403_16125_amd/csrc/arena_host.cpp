@@ -81,6 +81,8 @@ struct arena_ctx {
     const unsigned long long* last_counters = nullptr;   // tallies of the last estimate
     unsigned long long* h_counters = nullptr;   // pinned
     unsigned long long* d_queue = nullptr;      // the estimate and proxy kernels' item queue
+    uint8_t* d_pcut = nullptr;                  // the estimate blocks' caches of pure-compute splits
+    size_t cap_pcut = 0;
     int n_cus = 0;
     float* h_kappa[2] = {nullptr, nullptr};     // pinned staging, double-buffered
     hipEvent_t kappa_done[2] = {nullptr, nullptr};
@@ -156,6 +158,9 @@ void free_device(arena_ctx* c)
     (void)hipHostFree(c->h_counters);
     (void)hipFree(c->d_queue);
     c->d_queue = nullptr;
+    (void)hipFree(c->d_pcut);
+    c->d_pcut = nullptr;
+    c->cap_pcut = 0;
     (void)hipFree(c->d_msets);
     (void)hipFree(c->d_mset_off);
     (void)hipFree(c->d_hbm);
@@ -395,10 +400,19 @@ arena_status upload_orders(arena_ctx* c, hipStream_t stream)
 // section starting at a 256-byte boundary (the layout of the no-allocation
 // entry point's scratch; the allocating path holds the same buffers).
 struct Workspace {
-    size_t counters, queue, off, batch, types, counts, kappa, items, corder, tab, total;
+    size_t counters, queue, off, batch, types, counts, kappa, items, corder, tab, pcut, total;
 };
 
-Workspace workspace_layout(const arena_ctx* c)
+// Blocks of an estimate launch: one per resident slot (four per CU), at most
+// one per item.
+int estimate_blocks(const arena_ctx* c)
+{
+    return std::min(c->n_jobs * c->n_types, 4 * std::max(c->n_cus, 1));
+}
+
+// blocks = 0: the tables only (what the host knows before it asks the device
+// for its CU count); else with the split caches of that many blocks.
+Workspace workspace_layout(const arena_ctx* c, int blocks)
 {
     auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
     const size_t J = (size_t)c->n_jobs, T = (size_t)c->n_types, NC = (size_t)c->n_counts;
@@ -414,6 +428,7 @@ Workspace workspace_layout(const arena_ctx* c)
     w.items = o;    o = up(o + sizeof(int32_t) * J * T);
     w.corder = o;   o = up(o + sizeof(int32_t) * NC);
     w.tab = o;      o = up(o + (c->tab_k > 0 ? sizeof(double) * c->tab.size() : 0));
+    w.pcut = o;     o = up(o + (size_t)arena::kPureCutBytes * (size_t)blocks);
     w.total = o;
     return w;
 }
@@ -751,8 +766,8 @@ arena_status check_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
 arena::EstimateArgs estimate_args(const arena_ctx* c, const int32_t* d_off, const int32_t* d_batch,
                                   const TypeDev* d_types, const int32_t* d_counts, const float* d_kappa,
                                   const int32_t* d_items, const int32_t* d_corder, unsigned long long* d_queue,
-                                  const double* d_tab, unsigned long long* d_counters, float* t_iter, float* thr,
-                                  uint32_t* plan, uint8_t* cuts, int32_t cuts_stride)
+                                  const double* d_tab, uint8_t* d_pcut, unsigned long long* d_counters,
+                                  float* t_iter, float* thr, uint32_t* plan, uint8_t* cuts, int32_t cuts_stride)
 {
     arena::EstimateArgs A;
     std::memset(&A, 0, sizeof(A));
@@ -771,7 +786,8 @@ arena::EstimateArgs estimate_args(const arena_ctx* c, const int32_t* d_off, cons
     for (int q = 0; q <= arena::kQueues; ++q) A.queue_off[q] = c->h_qoff[q];
     A.n_items = c->n_jobs * c->n_types;
     // one block per resident slot (four per CU); each takes items from the queue
-    A.n_blocks = std::min(A.n_items, 4 * std::max(c->n_cus, 1));
+    A.n_blocks = estimate_blocks(c);
+    A.pure_cuts = d_pcut;
     A.share_tp = kappa_shared(c) ? 1 : 0;
     // ascending: the kernel bisects the microbatch counts for the memory limit
     std::vector<int32_t> ms(c->m_values);
@@ -807,17 +823,29 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     c->err.clear();
     arena_status st = check_estimate(c, t_iter, thr, plan, cuts, cuts_stride);
     if (st != ARENA_OK) return st;
-    const Workspace ws = workspace_layout(c);
-    if (c->ws_limit > 0 && ws.total > (size_t)c->ws_limit)
-        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "estimate: needs %zu bytes of device workspace (limit %lld)",
-                    ws.total, (long long)c->ws_limit);
+    // the tables (known on the host), then with the blocks' split caches (their
+    // number needs the device's CU count)
+    const Workspace ws0 = workspace_layout(c, 0);
+    if (c->ws_limit > 0 && ws0.total > (size_t)c->ws_limit)
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY,
+                    "estimate: its tables alone need %zu bytes of device workspace (limit %lld)", ws0.total,
+                    (long long)c->ws_limit);
     hipStream_t stream = (hipStream_t)stream_ptr;
     DeviceGuard guard(c->device);
     if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
+    hipError_t e;
+    if (c->n_cus == 0 &&
+        (e = hipDeviceGetAttribute(&c->n_cus, hipDeviceAttributeMultiprocessorCount, c->device)))
+        return hip_fail(c, e, "hipDeviceGetAttribute");
+    const Workspace ws = workspace_layout(c, estimate_blocks(c));
+    if (c->ws_limit > 0 && ws.total > (size_t)c->ws_limit)
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "estimate: needs %zu bytes of device workspace (limit %lld)",
+                    ws.total, (long long)c->ws_limit);
     st = ensure_device(c, stream);
     if (st != ARENA_OK) return st;
+    if ((e = ensure_capacity(&c->d_pcut, &c->cap_pcut, (size_t)arena::kPureCutBytes * estimate_blocks(c))))
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY, "split caches: %s", hipGetErrorString(e));
     if (c->order_dirty && (st = upload_orders(c, stream)) != ARENA_OK) return st;
-    hipError_t e;
     if (c->tab_k > 0) {
         if (c->tab_dirty) {
             if ((e = ensure_capacity(&c->d_tab, &c->cap_tab, c->tab.size())))
@@ -831,7 +859,8 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
     }
     const arena::EstimateArgs A =
         estimate_args(c, c->d_off, c->d_batch, c->d_types, c->d_counts, c->d_kappa, c->d_item_order,
-                      c->d_count_order, c->d_queue, c->d_tab, c->d_counters, t_iter, thr, plan, cuts, cuts_stride);
+                      c->d_count_order, c->d_queue, c->d_tab, c->d_pcut, c->d_counters, t_iter, thr, plan, cuts,
+                      cuts_stride);
     if ((e = arena::launch_zero_counters(c->d_counters, arena::kNumCounters, stream)) ||
         (e = arena::launch_zero_counters(c->d_queue, arena::kQueues, stream)))
         return hip_fail(c, e, "counter reset");
@@ -847,20 +876,27 @@ arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uin
     c->err.clear();
     arena_status st = check_estimate(c, t_iter, thr, plan, cuts, cuts_stride);
     if (st != ARENA_OK) return st;
-    const Workspace ws = workspace_layout(c);
-    if (ws.total > arena::kNoallocScratchBytes)
+    // the tables (known on the host), then with the blocks' split caches (their
+    // number needs the device's CU count)
+    const Workspace ws0 = workspace_layout(c, 0);
+    if (ws0.total > arena::kNoallocScratchBytes)
         return fail(c, ARENA_ERR_OUT_OF_MEMORY,
-                    "estimate_noalloc: the bound workload needs %zu bytes of scratch (max %zu): "
-                    "use arena_estimate", ws.total, (size_t)arena::kNoallocScratchBytes);
+                    "estimate_noalloc: the bound workload's tables alone need %zu bytes of scratch (max %zu): "
+                    "use arena_estimate", ws0.total, (size_t)arena::kNoallocScratchBytes);
     hipStream_t stream = (hipStream_t)stream_ptr;
     DeviceGuard guard(c->device);
     if (guard.status != hipSuccess) return hip_fail(c, guard.status, "hipSetDevice");
     hipError_t e;
-    char* base = nullptr;
-    if ((e = arena::scratch_address(c->device, (void**)&base))) return hip_fail(c, e, "scratch address");
     if (c->n_cus == 0 &&
         (e = hipDeviceGetAttribute(&c->n_cus, hipDeviceAttributeMultiprocessorCount, c->device)))
         return hip_fail(c, e, "hipDeviceGetAttribute");
+    const Workspace ws = workspace_layout(c, estimate_blocks(c));
+    if (ws.total > arena::kNoallocScratchBytes)
+        return fail(c, ARENA_ERR_OUT_OF_MEMORY,
+                    "estimate_noalloc: the bound workload needs %zu bytes of scratch (max %zu): "
+                    "use arena_estimate", ws.total, (size_t)arena::kNoallocScratchBytes);
+    char* base = nullptr;
+    if ((e = arena::scratch_address(c->device, (void**)&base))) return hip_fail(c, e, "scratch address");
     auto* d_counters = (unsigned long long*)(base + ws.counters);
     auto* d_queue = (unsigned long long*)(base + ws.queue);
     auto* d_off = (int32_t*)(base + ws.off);
@@ -871,6 +907,7 @@ arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uin
     auto* d_items = (int32_t*)(base + ws.items);
     auto* d_corder = (int32_t*)(base + ws.corder);
     auto* d_tab = (double*)(base + ws.tab);
+    auto* d_pcut = (uint8_t*)(base + ws.pcut);
     compute_orders(c);
     const size_t J = (size_t)c->n_jobs, T = (size_t)c->n_types, NC = (size_t)c->n_counts;
     // the scratch is shared by every call on this device: every table is
@@ -905,7 +942,8 @@ arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uin
         (e = hipMemcpyAsync(d_tab, c->tab.data(), sizeof(double) * c->tab.size(), hipMemcpyHostToDevice, stream)))
         return hip_fail(c, e, "comm table copy");
     const arena::EstimateArgs A = estimate_args(c, d_off, d_batch, d_types, d_counts, d_kappa, d_items, d_corder,
-                                                d_queue, d_tab, d_counters, t_iter, thr, plan, cuts, cuts_stride);
+                                                d_queue, d_tab, d_pcut, d_counters, t_iter, thr, plan, cuts,
+                                                cuts_stride);
     // zeroed by a kernel, not a memset node
     if ((e = arena::launch_zero_counters(d_counters, arena::kNumCounters, stream)) ||
         (e = arena::launch_zero_counters(d_queue, arena::kQueues, stream)))

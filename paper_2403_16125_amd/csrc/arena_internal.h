@@ -28,6 +28,11 @@ struct TypeDev {
 enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kSkipped, kAlgOps, kMemParts,
                kNumCounters };
 
+// Bytes of one block's cache of the pure-compute problem's canonical splits:
+// row pp (2 <= pp <= 128) holds the cuts c_0 .. c_pp, one byte each, from
+// byte pp (pp + 1) / 2 - 3.
+constexpr int kPureCutBytes = 8448;
+
 struct EstimateArgs {
     const int32_t* layer_offset;  // [J+1]
     const int32_t* batch;         // [J]
@@ -44,6 +49,7 @@ struct EstimateArgs {
     int32_t queue_off[kQueues + 1];
     int32_t n_items;              // J * T
     int32_t n_blocks;             // resident blocks launched; each takes items until none is left
+    uint8_t* pure_cuts;           // [n_blocks * kPureCutBytes] each block's cache of pure-compute splits
     const int32_t* count_order;   // [NC] count indices, largest count first
     int32_t n_jobs, n_types, n_counts;
     int32_t share_tp;             // some type has one kappa for all its counts: share tp problems
@@ -138,7 +144,7 @@ hipError_t launch_estimate(const EstimateArgs& args, hipStream_t stream);
 // Scratch of the no-allocation estimate: a statically sized device array,
 // one copy per device.  scratch_address returns its device address on
 // `device`, which must be the current device (looked up once per device).
-constexpr size_t kNoallocScratchBytes = size_t(4) << 20;
+constexpr size_t kNoallocScratchBytes = size_t(16) << 20;
 constexpr int kMaxScratchDevices = 64;
 hipError_t scratch_address(int device, void** out);
 hipError_t launch_schedule(const SchedArgs& args, hipStream_t stream);

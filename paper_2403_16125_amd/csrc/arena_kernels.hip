@@ -85,6 +85,7 @@ struct BlockLds {
     int32_t next_cell;
     int32_t uniform;              // one kappa for every count of this type
     int32_t moe;
+    unsigned long long pure_cached[2];   // bit pp-1: the block's cache row of the pure split of pp is current
     WaveLds w[kWavesPerBlock];
 };
 
@@ -522,13 +523,13 @@ __device__ void successor_tables(const double* U, uint8_t* J, int lane, int L, i
     }
 }
 
-// The canonical stages of pp >= 2 from successor tables of levels
-// 32 - clz(pp - 1): c_k for k = lane (cA) and k = lane + 64 (cB); c_0 = 0,
-// c_pp = L.  Every lane walks (nodes stay in [0, L]); only lanes
-// 1 <= k < pp keep the result.
-__device__ Stages stages_from_tables(const uint8_t* J, int lane, int L, int pp, int levels)
+// The cuts of the canonical split of pp >= 2 stages from successor tables of
+// levels 32 - clz(pp - 1): c_k for k = lane (cA) and k = lane + 64 (cB);
+// c_0 = 0, c_pp = L, and 0 for k > pp.  Every lane walks (nodes stay in
+// [0, L]); only lanes 1 <= k < pp keep the result.
+__device__ __forceinline__ void cuts_from_tables(const uint8_t* J, int lane, int L, int pp, int levels, int& cA_out,
+                                                 int& cB_out)
 {
-    Stages r;
     const bool hi_half = pp >= 64;
     const int k0 = lane, k1 = lane + 64;
     const int d0 = pp - k0, d1 = pp - k1;
@@ -549,13 +550,28 @@ __device__ Stages stages_from_tables(const uint8_t* J, int lane, int L, int pp, 
         cB = k1 < pp ? (n1 > k1 ? n1 : k1) : 0;
         cB = k1 == pp ? L : cB;
     }
-    // stage s ends where stage s+1 starts: the next lane's cut (lane 63 of the
-    // low half takes c_64, lane 63 of the high half c_128)
+    cA_out = cA;
+    cB_out = cB;
+}
+
+// The stages of the split with cuts cA (c_k, k = lane) and cB (k = lane + 64):
+// stage s ends where stage s+1 starts, at the next lane's cut (lane 63 of the
+// low half takes c_64, lane 63 of the high half c_128).
+__device__ __forceinline__ Stages stages_from_cuts(int cA, int cB, int L, int pp)
+{
+    Stages r;
     r.lo0 = cA;
     r.hi0 = from_next_lane(cA, __builtin_amdgcn_readlane(cB, 0));
     r.lo1 = cB;
     r.hi1 = from_next_lane(cB, pp == 128 ? L : 0);
     return r;
+}
+
+__device__ __forceinline__ Stages stages_from_tables(const uint8_t* J, int lane, int L, int pp, int levels)
+{
+    int cA, cB;
+    cuts_from_tables(J, lane, L, pp, levels, cA, cB);
+    return stages_from_cuts(cA, cB, L, pp);
 }
 
 template <int S>
@@ -569,6 +585,39 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
     successor_tables<S>(U, J, lane, L, levels, W);
     return stages_from_tables(J, lane, L, pp, levels);
+}
+
+// The pure-compute problem's canonical split of pp >= 2 stages (the cuts of
+// its prefix Upure at its bottleneck wpure = Wpure(pp)).  It depends on
+// neither the count, nor the contention, nor the tensor degree, so the block
+// keeps it, once computed for its current item, in its rows of a global cache
+// (row pp: the bytes c_0 .. c_pp), and bit pp - 1 of `cached` (LDS, cleared
+// per item) says that the row is current.  Two waves that miss together both
+// write the same bytes.
+__device__ Stages pure_split(const double* Upure, double wpure, unsigned long long* cached, WaveLds& Wv,
+                             uint8_t* cache, int lane, int L, int pp)
+{
+    static_assert(kLmax * (kLmax + 1) / 2 - 3 + kLmax + 1 <= kPureCutBytes, "cache rows");
+    uint8_t* row = cache + (pp * (pp + 1) / 2 - 3);
+    unsigned long long* word = &cached[(pp - 1) >> 6];
+    const unsigned long long bit = 1ull << ((pp - 1) & 63);
+    const unsigned long long w = __hip_atomic_load(word, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const bool hit = __builtin_amdgcn_readfirstlane((int)((w & bit) != 0ull)) != 0;
+    int cA, cB;
+    if (hit) {
+        cA = lane <= pp ? (int)row[lane] : 0;
+        cB = lane + 64 <= pp ? (int)row[lane + 64] : 0;
+    } else {
+        const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
+        successor_tables<1>(Upure, Wv.J, lane, L, levels, wpure);
+        cuts_from_tables(Wv.J, lane, L, pp, levels, cA, cB);
+        if (lane <= pp) row[lane] = (uint8_t)cA;
+        if (lane + 64 <= pp) row[lane + 64] = (uint8_t)cB;
+        // the row's stores before the bit
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        if (lane == 0) __hip_atomic_fetch_or(word, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    return stages_from_cuts(cA, cB, L, pp);
 }
 
 // Does every split of the L layers into pp stages have a stage costing more
@@ -608,16 +657,15 @@ __device__ __forceinline__ double split_cost(const double* UD, const Stages& sg,
 }
 
 // The bottleneck of pp stages over the problem's prefix U (stride 2) when a
-// few splits certify it, else -1.  The first is the pure-compute problem's
-// canonical split (cuts of its prefix Upure at its bottleneck wpure = Wpure(pp)):
-// it costs UB on U, so the
-// bottleneck is at most UB; if no split keeps every stage below UB (the test
-// above at the largest double under UB) the bottleneck is UB exactly.
-// Otherwise some split does, and the canonical split of U under that double
-// costs less than UB: it is the next one tried.
-__device__ double certified_bottleneck(const double* Upure, double wpure, WaveLds& Wv, int lane, int L, int pp)
+// few splits certify it, else -1.  The first is sgp, the pure-compute
+// problem's canonical split (cuts of its prefix at its bottleneck Wpure(pp)):
+// it costs UB on U, so the bottleneck is at most UB; if no split keeps every
+// stage below UB (the test above at the largest double under UB) the
+// bottleneck is UB exactly.  Otherwise some split does, and the canonical
+// split of U under that double costs less than UB: it is the next one tried.
+__device__ double certified_bottleneck(Stages sgp, WaveLds& Wv, int lane, int L, int pp)
 {
-    double ub = split_cost(Wv.UD, canonical_stages<1>(Upure, Wv.J, lane, L, pp, wpure), lane, pp);
+    double ub = split_cost(Wv.UD, sgp, lane, pp);
     for (int r = 0;; ++r) {
         if (!(ub > 0.0 && ub < kInf)) return -1.0;
         const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
@@ -1216,14 +1264,21 @@ __device__ double price_exact(const BlockLds<SLOTS>& B, WaveLds& Wv, const doubl
 // least time of the plans priced that fit (+inf if none): a plan of the
 // cell, so an upper bound of the cell's best time.
 template <int SLOTS, int S, bool MEM, bool EXT = false>
-__device__ double price_target(const BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
+__device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U, int lane, int mv,
                                const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp,
                                double W, int& np, bool keep_cuts, double* R, double best, double tie_eps,
-                               bool prune)
+                               bool prune, uint8_t* pcache = nullptr)
 {
     if constexpr (EXT) return price_exact<SLOTS, S>(B, Wv, U, lane, mv, jb, ty, cell, tp, pp, W, np, best, tie_eps,
                                                      prune);
-    const Stages sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
+    // S = 1: the pure-compute problem (U = Upure, W = Wtab[0][pp]), whose
+    // splits the block keeps in pcache
+    Stages sg;
+    if constexpr (S == 1)
+        sg = pp > 1 ? pure_split(U, W, B.pure_cached, Wv, pcache, lane, jb.L, pp)
+                    : canonical_stages<1>(U, Wv.J, lane, jb.L, pp, W);
+    else
+        sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
     const int dp = cell.n / (tp * pp);
     const int grp = dp * tp;
     const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
@@ -1557,14 +1612,14 @@ __device__ __forceinline__ void block_tallies(const EstimateArgs& A, WaveLds& Wv
 // row for its recursion); EXT: the exact-T rule (that row holds its
 // suffix recursion).
 template <int SLOTS, bool MEM, bool EXT = false>
-__device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
+__device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, int item)
 {
     __shared__ BlockLds<SLOTS> B;
-    // the lane index (counted by mbcnt, not kept from the launch) passes
-    // through an empty asm statement once per item, so nothing derived from
-    // it is hoisted out of the item loop and held in registers across every
-    // item (it would be spilled)
-    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    // the wave index (wid) is taken once per launch, as a scalar; the lane
+    // index (counted by mbcnt, not kept from the launch) passes through an
+    // empty asm statement once per item, so nothing derived from it is hoisted
+    // out of the item loop and held in registers across every item (it would
+    // be spilled)
     int lane0;
     __asm__ volatile("" : "=v"(lane0) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
     const int lane = lane0;
@@ -1575,6 +1630,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
         block_tallies(A, Wv, lane, item);
         return;
     }
+    uint8_t* const pcache = A.pure_cuts + (size_t)blockIdx.x * kPureCutBytes;
 
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
@@ -1630,6 +1686,8 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
             B.next_cell = 0;
             B.moe = jb.moe ? 1 : 0;
             B.x_layer_min = xm;
+            B.pure_cached[0] = 0ull;
+            B.pure_cached[1] = 0ull;
         }
     }
     // largest admissible microbatch count of each data-parallel degree
@@ -1749,7 +1807,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                     }
                     best = fmin(best, price_target<SLOTS, 1, MEM, EXT>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
                                                                   B.Wtab[0][pp], np, A.cuts != nullptr, R, best,
-                                                                  A.tie_eps, A.prune != 0));
+                                                                  A.tie_eps, A.prune != 0, pcache));
                 }
             }
         }
@@ -1850,7 +1908,10 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
                 // largest first it prices more plans than it saves rows)
                 if constexpr (!EXT) {
                     for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
-                        const double wc = certified_bottleneck(B.Upure, B.Wtab[0][pc], Wv, lane, jb.L, pc);
+                        const double wc =
+                            certified_bottleneck(pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane,
+                                                            jb.L, pc),
+                                                 Wv, lane, jb.L, pc);
                         if (!(wc >= 0.0)) break;
                         tm = price_deg(pc, wc, tm);
                     }
@@ -2002,9 +2063,9 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int item)
 // the next queues in turn, so the work still balances over every CU whatever
 // the items really cost.  Returns the item, or -1 once every queue is empty
 // (every block then leaves).
-__device__ __forceinline__ int take_item(const EstimateArgs& A, int* slot)
+__device__ __forceinline__ int take_item(const EstimateArgs& A, int* slot, int wid)
 {
-    if (threadIdx.x == 0) {
+    if (wid == 0 && __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) == 0u) {
         int item = -1;
         for (int r = 0; r < kQueues && item < 0; ++r) {
             const int qi = (int)((blockIdx.x + r) % kQueues);
@@ -2025,12 +2086,13 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_kernel(EstimateArgs A)
 {
     __shared__ int slot;
-    estimate_body<SLOTS, false>(A, kZeroTallies);
-    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
-        estimate_body<SLOTS, false>(A, item);
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    estimate_body<SLOTS, false>(A, wid, kZeroTallies);
+    for (int item = take_item(A, &slot, wid); item >= 0; item = take_item(A, &slot, wid)) {
+        estimate_body<SLOTS, false>(A, wid, item);
         __syncthreads();
     }
-    estimate_body<SLOTS, false>(A, kFlushTallies);
+    estimate_body<SLOTS, false>(A, wid, kFlushTallies);
 }
 
 // The exact-T rule: each plan's split minimises its iteration time.
@@ -2038,12 +2100,13 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_ext_kernel(EstimateArgs A)
 {
     __shared__ int slot;
-    estimate_body<SLOTS, false, true>(A, kZeroTallies);
-    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
-        estimate_body<SLOTS, false, true>(A, item);
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    estimate_body<SLOTS, false, true>(A, wid, kZeroTallies);
+    for (int item = take_item(A, &slot, wid); item >= 0; item = take_item(A, &slot, wid)) {
+        estimate_body<SLOTS, false, true>(A, wid, item);
         __syncthreads();
     }
-    estimate_body<SLOTS, false, true>(A, kFlushTallies);
+    estimate_body<SLOTS, false, true>(A, wid, kFlushTallies);
 }
 
 // The memory rule's out-of-line solve raises register use; its kernel still
@@ -2054,12 +2117,13 @@ template <int SLOTS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_mem_kernel(EstimateArgs A)
 {
     __shared__ int slot;
-    estimate_body<SLOTS, true>(A, kZeroTallies);
-    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
-        estimate_body<SLOTS, true>(A, item);
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    estimate_body<SLOTS, true>(A, wid, kZeroTallies);
+    for (int item = take_item(A, &slot, wid); item >= 0; item = take_item(A, &slot, wid)) {
+        estimate_body<SLOTS, true>(A, wid, item);
         __syncthreads();
     }
-    estimate_body<SLOTS, true>(A, kFlushTallies);
+    estimate_body<SLOTS, true>(A, wid, kFlushTallies);
 }
 
 // ------------------------------------------------------------ interpolated communication latency
@@ -2092,6 +2156,7 @@ struct TabBlockLds {
     int32_t share;                    // one kappa for all counts of the type: bottlenecks are shared
     double Upure[kLmax + kPad];       // prefix of the pure-compute per-sample cost (+inf padded)
     double Wpure[kLmax + 1];          // its bottleneck by degree (every degree up to the layer count)
+    unsigned long long pure_cached[2];   // bit pp-1: the block's cache row of the pure split of pp is current
     WaveLds w[kWavesPerBlock];
     double cW[kTabCache];             // bottleneck cache of the (job, type): bottlenecks
     uint32_t ckey[kTabCache];         //   and their keys (0 empty)
@@ -2285,11 +2350,10 @@ constexpr unsigned kTabKeyMask = kTabPriced - 1u;
 // with it): a group takes only members within the window and drops the
 // degrees the window excludes as it tightens.  Then the cell's choice as in
 // estimate_kernel.
-__device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int item)
+__device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid, int item)
 {
     __shared__ TabBlockLds B;
     // lane index counted per item and per cell (as in estimate_body)
-    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     int lane0;
     __asm__ volatile("" : "=v"(lane0) : "0"((int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u))));
     const int lane = lane0;
@@ -2299,6 +2363,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         block_tallies(A, Wv, lane, item);
         return;
     }
+    uint8_t* const pcache = A.pure_cuts + (size_t)blockIdx.x * kPureCutBytes;
 
     const int j = item / A.n_types;
     const int g = item - j * A.n_types;
@@ -2351,7 +2416,11 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
         for (int c = lane; c < A.n_counts; c += 64) same &= A.kappa[g * A.n_counts + c] == A.kappa[g * A.n_counts];
         const bool uni = __ballot(!same) == 0ull;
         for (int h = lane; h < (int)kTabCache; h += 64) B.ckey[h] = 0u;
-        if (lane == 0) B.share = (uni && A.n_counts > 1 && jb.Bg < (1 << 17)) ? 1 : 0;
+        if (lane == 0) {
+            B.share = (uni && A.n_counts > 1 && jb.Bg < (1 << 17)) ? 1 : 0;
+            B.pure_cached[0] = 0ull;
+            B.pure_cached[1] = 0ull;
+        }
     }
     if (tid == 0) B.next_cell = 0;
     if (wid == 0) tally(Wv, lane, kCells, (unsigned long long)A.n_counts);
@@ -2473,7 +2542,8 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
             // the largest degrees left first: a certified bottleneck spares the
             // recursion their rows
             for (int pc = todo.last(); pc >= kCertMinDegree; pc = todo.last()) {
-                const double wc = certified_bottleneck(B.Upure, B.Wpure[pc], Wv, lane, jb.L, pc);
+                const double wc = certified_bottleneck(
+                    pure_split(B.Upure, B.Wpure[pc], B.pure_cached, Wv, pcache, lane, jb.L, pc), Wv, lane, jb.L, pc);
                 if (!(wc >= 0.0)) break;
                 if (share && lane == 0) tab_cache_put(B, tab_key(tp0, fl0, bq0, pc), wc);
                 todo = price_deg(pc, wc, todo);
@@ -2582,12 +2652,13 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int ite
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void estimate_tab_kernel(EstimateArgs A)
 {
     __shared__ int slot;
-    estimate_tab_body(A, kZeroTallies);
-    for (int item = take_item(A, &slot); item >= 0; item = take_item(A, &slot)) {
-        estimate_tab_body(A, item);
+    const int wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    estimate_tab_body(A, wid, kZeroTallies);
+    for (int item = take_item(A, &slot, wid); item >= 0; item = take_item(A, &slot, wid)) {
+        estimate_tab_body(A, wid, item);
         __syncthreads();
     }
-    estimate_tab_body(A, kFlushTallies);
+    estimate_tab_body(A, wid, kFlushTallies);
 }
 
 __global__ void zero_kernel(unsigned long long* p, int n)

@@ -397,13 +397,15 @@ def test_workspace_limit_out_of_memory(ctx):
     _bind_host_only(ctx, 5000)
     arena.arena_set_workspace_limit(ctx, 64 << 10)
     _expect(2, arena.arena_estimate, ctx, FAKE, FAKE, FAKE, match="limit 65536")
-    # J = 5000, T = 8, NC = 16: 4 J T + 8 J + ... bytes, the header's formula
+    # J = 5000, T = 8, NC = 16: 4 J T + 8 J + ... bytes of tables, the header's
+    # formula (checked before the device is asked for its CU count, which sets
+    # the size of the split caches)
     msg = None
     try:
         arena.arena_estimate(ctx, FAKE, FAKE, FAKE)
     except arena.ArenaError as e:
         msg = e.message
-    need = int(msg.split("needs ")[1].split(" bytes")[0])
+    need = int(re.search(r"need (\d+) bytes", msg).group(1))
     J, T, NC = 5000, 8, 16
     approx = 4 * (J + 1) + 4 * J + 40 * T + 8 * NC + 4 * T * NC + 4 * J * T
     assert approx <= need <= approx + 2560
@@ -412,10 +414,10 @@ def test_workspace_limit_out_of_memory(ctx):
 def test_noalloc_rejects_a_workload_beyond_its_scratch(ctx):
     """The no-allocation entry point takes the same host checks as
     arena_estimate and rejects a workload whose tables exceed its static
-    scratch with OUT_OF_MEMORY (here 200,000 jobs x 8 types), before any
-    device call."""
+    scratch with OUT_OF_MEMORY (here 600,000 jobs x 8 types: 24 MB of tables),
+    before any device call."""
     _expect(4, arena.arena_estimate_noalloc, ctx, FAKE, FAKE, FAKE, match="bind")
-    _bind_host_only(ctx, 200_000)
+    _bind_host_only(ctx, 600_000)
     _expect(1, arena.arena_estimate_noalloc, ctx, FAKE, 0, FAKE, match="output")
     _expect(2, arena.arena_estimate_noalloc, ctx, FAKE, FAKE, FAKE, match="scratch")
-    assert arena.NOALLOC_SCRATCH_BYTES == 4 << 20
+    assert arena.NOALLOC_SCRATCH_BYTES == 16 << 20

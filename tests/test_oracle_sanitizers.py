@@ -236,8 +236,9 @@ int main()
     EXPECT(arena_set_workspace_limit(ctx, -5), ARENA_ERR_INVALID_ARG);
     EXPECT(arena_set_workspace_limit(ctx, 1 << 20), ARENA_OK);
     EXPECT(arena_estimate(ctx, F, F, P, nullptr, 0, nullptr), ARENA_ERR_OUT_OF_MEMORY);
-    // 50,000 jobs x 8 types: 1.6 MB of work order fit the scratch; 200,000 do not
-    const int J2 = 200000;
+    // 50,000 jobs x 8 types: 1.6 MB of work order fit the scratch; the 24 MB
+    // of tables of 600,000 do not (refused before the device is asked anything)
+    const int J2 = 600000;
     std::vector<int32_t> off2(J2 + 1), bat2(J2, 64);
     for (int j = 0; j <= J2; ++j) off2[j] = 4 * j;
     arena_jobs_desc jd2{J2, 4 * J2, off2.data(), bat2.data(), F, F, F, F, F};

@@ -67,7 +67,8 @@ def test_noalloc_matches_estimate_twice_second_smaller():
 
 def test_noalloc_full_round_and_memory_rule():
     w = wl.full()
-    _say(f"full round 3: {w.n_cells} cells without cut rows (0.7 MB of scratch)")
+    _say(f"full round 3: {w.n_cells} cells without cut rows (0.7 MB of tables and 8.3 MiB of split caches "
+         "in the scratch)")
     ref, cref, got, cgot = _both(w, rnd=3, with_cuts=False)
     _assert_same(ref, got, "full round 3")
     assert cref == cgot
@@ -95,9 +96,9 @@ def test_noalloc_refuses_beyond_scratch_and_workspace_cap():
         est.set_workspace_limit(0)
         est.estimate()
         first = _outputs(est)
-        # 300,000 jobs x 3 types: the work order and job tables need 6 MB, more
+        # 1,000,000 jobs x 3 types: the work order and job tables need 20 MB, more
         # than the scratch holds; refused before anything is enqueued
-        n = 300_000
+        n = 1_000_000
         off = (np.arange(n + 1) * 4).astype(np.int32)
         fake = est.t.data_ptr()          # never read: the size check comes first
         arena.arena_bind_jobs(est.ctx, off, np.full(n, 8, np.int32), fake, fake, fake, fake, fake)
