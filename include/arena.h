@@ -115,7 +115,8 @@ typedef struct arena_grids_desc {
     const int32_t* counts;        /* 1..ARENA_MAX_GPU_COUNT, distinct */
 } arena_grids_desc;
 
-/* Work of the last arena_estimate (device-side tallies). */
+/* Work of the last arena_estimate (device-side tallies; plans_skipped is the
+ * plan space less the plans priced). */
 typedef struct arena_counters {
     int64_t cells;            /* cells written */
     int64_t plans;            /* plans priced */

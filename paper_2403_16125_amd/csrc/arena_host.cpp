@@ -79,6 +79,7 @@ struct arena_ctx {
     int64_t ws_limit = 0;                       // cap on library-owned device bytes, 0: none
     unsigned long long* d_counters = nullptr;
     const unsigned long long* last_counters = nullptr;   // tallies of the last estimate
+    int64_t last_space_plans = 0;               // the plan space of the last estimate
     unsigned long long* h_counters = nullptr;   // pinned
     unsigned long long* d_queue = nullptr;      // the estimate and proxy kernels' item queue
     uint8_t* d_pcut = nullptr;                  // the estimate blocks' caches of pure-compute splits
@@ -866,6 +867,7 @@ arena_status arena_estimate(arena_ctx* c, float* t_iter, float* thr, uint32_t* p
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     c->last_counters = c->d_counters;
+    c->last_space_plans = c->size.plans;
     return ARENA_OK;
 }
 
@@ -950,6 +952,7 @@ arena_status arena_estimate_noalloc(arena_ctx* c, float* t_iter, float* thr, uin
         return hip_fail(c, e, "counter reset");
     if ((e = arena::launch_estimate(A, stream))) return hip_fail(c, e, "estimate launch");
     c->last_counters = d_counters;
+    c->last_space_plans = c->size.plans;
     return ARENA_OK;
 }
 
@@ -971,7 +974,8 @@ arena_status arena_get_counters(arena_ctx* c, arena_counters* out)
     out->problems = (int64_t)h[arena::kProblems];
     out->dp_entries = (int64_t)h[arena::kDpEntries];
     out->infeasible_cells = (int64_t)h[arena::kInfeasible];
-    out->plans_skipped = (int64_t)h[arena::kSkipped];
+    // every plan of the space is priced or skipped (the kernels count the priced)
+    out->plans_skipped = c->last_space_plans - out->plans;
     out->alg_ops = (int64_t)h[arena::kAlgOps];
     out->mem_partitions = (int64_t)h[arena::kMemParts];
     if (h[arena::kOverflow]) return fail(c, ARENA_ERR_UNSUPPORTED, "counters: plan buffer overflow");

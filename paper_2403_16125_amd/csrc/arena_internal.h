@@ -25,7 +25,7 @@ struct TypeDev {
 };
 
 // Device tallies, zeroed before each estimate.
-enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kSkipped, kAlgOps, kMemParts,
+enum Counter { kCells = 0, kPlans, kProblems, kDpEntries, kInfeasible, kOverflow, kAlgOps, kMemParts,
                kNumCounters };
 
 // Bytes of one block's cache of the pure-compute problem's canonical splits:

@@ -1446,19 +1446,6 @@ __device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const
     return (b * fill + (double)(m - 1) * (b * Wlb) + ar) * (1.0 - 1e-9);
 }
 
-// Plans of the degrees in `before` but not in `after` (qn = n / tp).
-template <int SLOTS>
-__device__ __forceinline__ unsigned long long dropped_plans(const BlockLds<SLOTS>& B, const Mask& before,
-                                                            const Mask& after, int lane, int qn)
-{
-    const bool d0 = ((before.lo & ~after.lo) >> lane) & 1ull;
-    const bool d1 = ((before.hi & ~after.hi) >> lane) & 1ull;
-    double c = 0.0;
-    if (d0) c += (double)B.mcnt[(int)rintf((float)qn * __builtin_amdgcn_rcpf((float)(1 + lane))) - 1];
-    if (d1) c += (double)B.mcnt[(int)rintf((float)qn * __builtin_amdgcn_rcpf((float)(65 + lane))) - 1];
-    return (unsigned long long)wave_reduce1<OpSum>(c);
-}
-
 // Lower bounds of the degrees in `tm` into Wv.lbnd[pp - 1], one lane per
 // degree (a problem requests at most 32 degrees: the divisors of n / tp);
 // returns the least of them (+inf: no degree fits memory).
@@ -1801,10 +1788,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                               bound_ctx(cell, 1, B.Upure[jb.L], ar_intra1, ar_inter1));
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
-                    if (A.prune && !(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) {
-                        tally(Wv, lane, kSkipped, B.mcnt[cell.n / pp - 1]);
-                        continue;
-                    }
+                    if (A.prune && !(lbp < kInf && lbp <= best * (1.0 + A.tie_eps))) continue;
                     best = fmin(best, price_target<SLOTS, 1, MEM, EXT>(B, Wv, B.Upure, lane, mv, jb, ty, cell, 1, pp,
                                                                   B.Wtab[0][pp], np, A.cuts != nullptr, R, best,
                                                                   A.tie_eps, A.prune != 0, pcache));
@@ -1864,11 +1848,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
             {
                 const double lb0 = Wv.lbnd[lane], lb1 = Wv.lbnd[lane + 64];
                 const double lim = best * (1.0 + A.tie_eps);
-                const Mask keep = A.prune ? tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim)
-                                          : tm;
-                if (keep.lo != tm.lo || keep.hi != tm.hi)
-                    tally(Wv, lane, kSkipped, dropped_plans(B, tm, keep, lane, cell.n / tp));
-                tm = keep;
+                if (A.prune) tm = tm & ballot_mask(lb0 < kInf && lb0 <= lim, lb1 < kInf && lb1 <= lim);
             }
             if (!tm.any()) continue;
             double u[2];
@@ -1879,10 +1859,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
             if (slot > 0) {
                 for (int pp = tm.next(1); pp; pp = tm.next(pp + 1)) {
                     const double lbp = Wv.lbnd[pp - 1];
-                    if (A.prune && !(lbp <= best * (1.0 + A.tie_eps))) {
-                        tally(Wv, lane, kSkipped, B.mcnt[cell.n / (tp * pp) - 1]);
-                        continue;
-                    }
+                    if (A.prune && !(lbp <= best * (1.0 + A.tie_eps))) continue;
                     best = fmin(best, price_target<SLOTS, 2, MEM, EXT>(B, Wv, Wv.UD, lane, mv, jb, ty, cell, tp, pp,
                                                                   B.Wtab[slot][pp], np, A.cuts != nullptr, R, best,
                                                                   A.tie_eps, A.prune != 0));
@@ -1896,11 +1873,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                     const double lim = best * (1.0 + A.tie_eps);
                     Mask rest = m;                       // degrees still to come
                     if (pp <= 64) rest.lo &= ~(1ull << (pp - 1)); else rest.hi &= ~(1ull << (pp - 65));
-                    const Mask keep = A.prune ? rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim)
-                                              : rest;
-                    if (keep.lo != rest.lo || keep.hi != rest.hi)
-                        tally(Wv, lane, kSkipped, dropped_plans(B, rest, keep, lane, cell.n / tp));
-                    return keep;
+                    return A.prune ? rest & ballot_mask(Wv.lbnd[lane] <= lim, Wv.lbnd[lane + 64] <= lim) : rest;
                 };
                 // the largest requested degrees first: where a certificate gives the
                 // bottleneck, the recursion is spared their rows (not under the
@@ -1921,14 +1894,6 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                     tally(Wv, lane, kProblems, 1);
                 }
             }
-        }
-        // problems never taken: none of their plans can hold the cell's best
-        for (int c = 0; c < ncand; ++c) {
-            if ((solved >> c) & 1u) continue;
-            const int tp = Wv.cand_tp[c];
-            const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
-                                        target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
-            tally(Wv, lane, kSkipped, dropped_plans(B, tm, Mask{0ull, 0ull}, lane, cell.n / tp));
         }
         wave_sync();
 
@@ -2585,7 +2550,6 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
             for (int e = 0; e < np; ++e)
                 if (!(Wv.planKey[e] & kTabPriced)) price_group(e, kInf);
         }
-        tally(Wv, lane, kSkipped, (unsigned long long)nskip);
         wave_sync();
 
         double tl = kInf;

@@ -57,7 +57,8 @@ def test_every_cell(oracle, name):
     rep = compare(w, res, ids, oracle)
     _check(rep, name)
     assert cnt["cells"] == w.n_cells
-    # every plan of the space is either priced or skipped by its bound
+    # no plan is priced twice (the skipped count is the rest of the space)
+    assert 0 < cnt["plans"] <= size["plans"]
     assert cnt["plans"] + cnt["plans_skipped"] == size["plans"]
     assert cnt["infeasible_cells"] == rep["infeasible"]
 
