@@ -36,7 +36,8 @@ constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage coun
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
 constexpr int kCertMinDegree = 2;  // a bottleneck certificate is tried for degrees from here up
-constexpr int kCertRounds = 2;     // splits tried per certificate
+constexpr int kCertRounds = 3;     // splits tried per certificate (2 under the memory rule, whose
+                                   // pricing order they change to its cost)
 
 struct WaveLds {
     // the wave's current problem, pairs (U_j, D_j): U the cost prefix (+inf
@@ -663,6 +664,7 @@ __device__ __forceinline__ double split_cost(const double* UD, const Stages& sg,
 // stage below UB (the test above at the largest double under UB) the
 // bottleneck is UB exactly.  Otherwise some split does, and the canonical
 // split of U under that double costs less than UB: it is the next one tried.
+template <int ROUNDS = kCertRounds>
 __device__ double certified_bottleneck(Stages sgp, WaveLds& Wv, int lane, int L, int pp)
 {
     double ub = split_cost(Wv.UD, sgp, lane, pp);
@@ -670,7 +672,7 @@ __device__ double certified_bottleneck(Stages sgp, WaveLds& Wv, int lane, int L,
         if (!(ub > 0.0 && ub < kInf)) return -1.0;
         const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
         if (bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below)) return ub;
-        if (r + 1 == kCertRounds) return -1.0;
+        if (r + 1 == ROUNDS) return -1.0;
         // a split with every stage at most `below` exists, and every single
         // layer costs at most that (else the test would have passed): the
         // test's tables are those of its canonical split
@@ -1881,10 +1883,9 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                 // largest first it prices more plans than it saves rows)
                 if constexpr (!EXT) {
                     for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
-                        const double wc =
-                            certified_bottleneck(pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane,
-                                                            jb.L, pc),
-                                                 Wv, lane, jb.L, pc);
+                        const double wc = certified_bottleneck<MEM ? 2 : kCertRounds>(
+                            pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane, jb.L, pc), Wv, lane,
+                            jb.L, pc);
                         if (!(wc >= 0.0)) break;
                         tm = price_deg(pc, wc, tm);
                     }
