@@ -35,6 +35,7 @@ constexpr int kPad = 8;            // prefix arrays hold +inf past the last laye
 constexpr int kLevels = 7;         // successor tables: 2^7 > largest stage count - 1
 constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
+static_assert(kMaxPlans <= 256, "plan entries are packed below the key in 8 bits");
 constexpr int kCertMinDegree = 2;  // a bottleneck certificate is tried for degrees from here up
 constexpr int kCertRounds = 3;     // splits tried per certificate (2 under the memory rule, whose
                                    // pricing order they change to its cost)
@@ -1769,14 +1770,21 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
         double best = kInf;          // time of a fitting plan priced so far: bounds the cell's best
         if (lane == 0) Wv.cut_T = kInf;
         // per-cell pieces of the bounds: all-reduce seconds per byte (tp = 1),
-        // and the tensor-parallel and all-to-all parts of a problem's cost sum
-        const double ar_intra1 = cell.kappa * 2.0 / ty.bw_intra;
-        const double ar_inter1 = cell.kappa * 2.0 / ty.bw_inter;
-        const double ul_tp = cell.kappa * 8.0 * B.x_sum / ty.bw_intra;
-        const double ul_a2a = jb.moe ? cell.kappa * B.q_sum / ty.bw_inter : 0.0;
+        // and the tensor-parallel and all-to-all parts of a problem's cost sum.
+        // Bounds only: their relative margins cover reciprocal estimates (the
+        // memory rule's kernel keeps the divisions, which measured faster there);
+        // a bandwidth of +inf (no such link) gives 0, as the division does
+        auto bdiv = [](double x, double y) {
+            if constexpr (MEM) return x / y;
+            else return y < kInf ? x * rcp_approx(y) : 0.0;
+        };
+        const double ar_intra1 = bdiv(cell.kappa * 2.0, ty.bw_intra);
+        const double ar_inter1 = bdiv(cell.kappa * 2.0, ty.bw_inter);
+        const double ul_tp = bdiv(cell.kappa * 8.0 * B.x_sum, ty.bw_intra);
+        const double ul_a2a = jb.moe ? bdiv(cell.kappa * B.q_sum, ty.bw_inter) : 0.0;
         // per byte of a layer: tensor-parallel seconds (times (tp-1)/tp) and all-to-all seconds
-        const double cx1 = cell.kappa * 8.0 / ty.bw_intra;
-        const double cq1 = jb.moe ? cell.kappa / ty.bw_inter : 0.0;
+        const double cx1 = bdiv(cell.kappa * 8.0, ty.bw_intra);
+        const double cq1 = jb.moe ? bdiv(cell.kappa, ty.bw_inter) : 0.0;
 
         // plans of the pure-compute problem first: their bottlenecks are shared
         {
@@ -1806,7 +1814,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
         // recursion stops after the last degree still wanted.
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
         int ncand = 0;
-        for (int tp = tpmax; tp >= 1; --tp) {
+        for (int tp = 1; tp <= tpmax; ++tp) {
             if (cell.n % tp != 0 || ((gpn_divs >> tp) & 1u) == 0) continue;
             if (tp == 1 && !jb.moe) continue;          // the pure-compute problem
             const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
@@ -1838,14 +1846,20 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
             }
             if (csel < 0) break;
             if (A.prune && !(lsel < kInf && lsel <= best * (1.0 + A.tie_eps))) break;
+            // the first problem taken, if it is the last one bounded above, still has
+            // its degrees' bounds in lbnd (tp ascending: the largest tp, whose
+            // problem is most often taken first on the full round, is bounded last)
+            const bool fresh = solved == 0u && csel == ncand - 1;
             solved |= 1u << csel;
             const int tp = Wv.cand_tp[csel];
             Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
                                   target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
-            const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
-            const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
-            degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
-                          bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1, cx1, cq1));
+            if (!fresh) {
+                const double rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
+                const double ULb = ((B.Upure[jb.L] + (double)(tp - 1) * ul_tp) * rtp + ul_a2a) * (1.0 - 1e-12);
+                degree_bounds(B, Wv, tm, lane, jb, ty, cell, gpn_divs,
+                              bound_ctx(cell, tp, ULb, ar_intra1, ar_inter1, cx1, cq1));
+            }
             // kept: no bound yet (+inf: memory rules the degree out), or within the window
             {
                 const double lb0 = Wv.lbnd[lane], lb1 = Wv.lbnd[lane + 64];
@@ -1919,14 +1933,14 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
             continue;
         }
         const double tlim = tmin * (1.0 + A.tie_eps);
+        // the smallest key within the window and its entry in one reduction
+        // (keys are unique in a cell; key 256 + entry < 2^28 is exact)
         double kl = kInf;
         for (int e = lane; e < np; e += 64)
-            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)Wv.planKey[e]);
-        const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
-        double il = -1.0;
-        for (int e = lane; e < np; e += 64)
-            if (Wv.planKey[e] == kbest) il = (double)e;
-        int ib = (int)wave_reduce1<OpMax>(il);
+            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)Wv.planKey[e] * 256.0 + (double)e);
+        const double kv = wave_reduce1<OpMin>(kl);
+        const unsigned kbest = (unsigned)(kv * (1.0 / 256.0));
+        int ib = (int)(kv - (double)kbest * 256.0);
         ib = ib < 0 ? 0 : (ib >= np ? np - 1 : ib);
         const double Tb = Wv.planT[ib];
         const int pp = (int)(kbest >> 12);
@@ -2573,14 +2587,13 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
             continue;
         }
         const double tlim = tmin * (1.0 + A.tie_eps);
+        // the smallest key within the window and its entry in one reduction
         double kl = kInf;
         for (int e = lane; e < np; e += 64)
-            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)(Wv.planKey[e] & kTabKeyMask));
-        const unsigned kbest = (unsigned)wave_reduce1<OpMin>(kl);
-        double il = -1.0;
-        for (int e = lane; e < np; e += 64)
-            if ((Wv.planKey[e] & kTabKeyMask) == kbest) il = (double)e;
-        int ib = (int)wave_reduce1<OpMax>(il);
+            if (Wv.planT[e] <= tlim) kl = fmin(kl, (double)(Wv.planKey[e] & kTabKeyMask) * 256.0 + (double)e);
+        const double kv = wave_reduce1<OpMin>(kl);
+        const unsigned kbest = (unsigned)(kv * (1.0 / 256.0));
+        int ib = (int)(kv - (double)kbest * 256.0);
         ib = ib < 0 ? 0 : (ib >= np ? np - 1 : ib);
         const double Tb = Wv.planT[ib];
         const int pp = (int)(kbest >> 12);
