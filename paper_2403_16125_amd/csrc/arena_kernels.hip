@@ -1299,16 +1299,6 @@ __device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U,
         A1 = B.Ap[sg.hi1] - B.Ap[sg.lo1];
         if (lane + 64 < pp - 1) sx += (double)B.x[sg.hi1 - 1];
     }
-    double rs[1] = {sx}, rm[1] = {fmax(P0, P1)};
-    wave_reduce<OpSum, 1>(rs);
-    wave_reduce<OpMax, 1>(rm);
-    const double sumX = rs[0];
-    const double pmax = rm[0];
-    const double sumS = U[jb.L * S];   // the stages tile the layers: sum of stage costs
-    const double ar = (dp > 1)
-        ? pmax * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
-        : 0.0;
-    const double per_sample = sumS + cell.c_p2p * sumX;   // fill time per sample
 
     // lanes over the microbatch counts: admissible when dp m divides the batch
     // (the quotient of a correctly rounded division is exact then)
@@ -1338,25 +1328,44 @@ __device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U,
     const double cap = ty.mem * (double)tp;
     const double fP0 = 4.0 * P0, fP1 = 4.0 * P1;
     const int r0 = pp - lane, r1 = pp - lane - 64;         // stages from the lane's to the last
-    int lo = 0, hi = nadm;                                  // first fitting rank in [lo, hi]
-    {
-        // every count fits when the smallest does (the common case): one test
-        const double bm = Wv.bq[0];
-        const int m = Wv.mq[0];
+    auto over_at = [&](int rk) {                            // does some stage overflow at rank rk?
+        const double bm = Wv.bq[rk];
+        const int m = Wv.mq[rk];
         const double i0 = (double)(m < r0 ? m : r0) * bm;
         const double i1 = (double)(m < r1 ? m : r1) * bm;
         const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
-        if (__ballot(over) == 0ull) hi = 0; else lo = 1;
+        return __ballot(over) != 0ull;
+    };
+    int lo = 0, hi = nadm;                                  // first fitting rank in [lo, hi]
+    if constexpr (!MEM) {
+        // a stage's memory falls as m grows: when the largest admissible count
+        // does not fit, none does, and the degree's plans are priced infeasible
+        // here (nothing of them enters the plan buffer)
+        if (over_at(nadm - 1)) {
+            tally(Wv, lane, kPlans, (unsigned long long)nadm);
+            return kInf;
+        }
+        hi = nadm - 1;
+    }
+    // every count fits when the smallest does (the common case): one test
+    if (lo < hi) {
+        if (!over_at(0)) hi = 0; else lo = 1;
     }
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        const double bm = Wv.bq[mid];
-        const int m = Wv.mq[mid];
-        const double i0 = (double)(m < r0 ? m : r0) * bm;
-        const double i1 = (double)(m < r1 ? m : r1) * bm;
-        const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
-        if (__ballot(over) == 0ull) hi = mid; else lo = mid + 1;
+        if (!over_at(mid)) hi = mid; else lo = mid + 1;
     }
+
+    double rs[1] = {sx}, rm[1] = {fmax(P0, P1)};
+    wave_reduce<OpSum, 1>(rs);
+    wave_reduce<OpMax, 1>(rm);
+    const double sumX = rs[0];
+    const double pmax = rm[0];
+    const double sumS = U[jb.L * S];   // the stages tile the layers: sum of stage costs
+    const double ar = (dp > 1)
+        ? pmax * (cell.kappa * 2.0 * (double)(dp - 1) / ((double)dp * (double)tp * B_dp))
+        : 0.0;
+    const double per_sample = sumS + cell.c_p2p * sumX;   // fill time per sample
 
     double T = kInf;
     if (adm) {
