@@ -665,19 +665,34 @@ __device__ __forceinline__ double split_cost(const double* UD, const Stages& sg,
 // stage below UB (the test above at the largest double under UB) the
 // bottleneck is UB exactly.  Otherwise some split does, and the canonical
 // split of U under that double costs less than UB: it is the next one tried.
-template <int ROUNDS = kCertRounds>
-__device__ double certified_bottleneck(Stages sgp, WaveLds& Wv, int lane, int L, int pp)
+// Returns -2 when no microbatch count can fit the degree's plans: a canonical
+// split at a threshold of at least the bottleneck has its cuts at or left of
+// the bottleneck's, so its first stage is contained in the priced split's first
+// stage; if that smaller stage already overflows memory with the largest
+// admissible count (minf = min(m, pp) microbatches in flight, bm samples each,
+// cap = mem tp, the pricing's test term by term), so does the priced one, and
+// with every smaller count too (MEMTEST: the test is made).
+template <int ROUNDS = kCertRounds, bool MEMTEST = false>
+__device__ double certified_bottleneck(Stages sgp, WaveLds& Wv, int lane, int L, int pp, const double* Pp = nullptr,
+                                       const double* Ap = nullptr, double cap = kInf, double bm = 0.0, int minf = 0)
 {
     double ub = split_cost(Wv.UD, sgp, lane, pp);
     for (int r = 0;; ++r) {
         if (!(ub > 0.0 && ub < kInf)) return -1.0;
         const double below = __longlong_as_double(__double_as_longlong(ub) - 1);
         if (bottleneck_exceeds<2>(Wv.UD, Wv.J, lane, L, pp, below)) return ub;
-        if (r + 1 == ROUNDS) return -1.0;
         // a split with every stage at most `below` exists, and every single
         // layer costs at most that (else the test would have passed): the
         // test's tables are those of its canonical split
-        ub = split_cost(Wv.UD, stages_from_tables(Wv.J, lane, L, pp, 32 - __clz(pp - 1)), lane, pp);
+        if (!MEMTEST && r + 1 == ROUNDS) return -1.0;
+        const Stages sg = stages_from_tables(Wv.J, lane, L, pp, 32 - __clz(pp - 1));
+        if constexpr (MEMTEST) {
+            const int c1 = __builtin_amdgcn_readfirstlane(sg.hi0);   // lane 0: stage 0 = [0, c_1)
+            const double i0 = (double)minf * bm;
+            if (4.0 * Pp[c1] + i0 * Ap[c1] > cap) return -2.0;
+            if (r + 1 == ROUNDS) return -1.0;
+        }
+        ub = split_cost(Wv.UD, sg, lane, pp);
     }
 }
 
@@ -1906,9 +1921,27 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                 // largest first it prices more plans than it saves rows)
                 if constexpr (!EXT) {
                     for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
-                        const double wc = certified_bottleneck<MEM ? 2 : kCertRounds>(
-                            pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane, jb.L, pc), Wv, lane,
-                            jb.L, pc);
+                        // the memory test of the degree's largest admissible count
+                        // (not under the memory rule, whose splits differ)
+                        const int dpc = cell.n / (tp * pc);
+                        double wc;
+                        if constexpr (MEM) {
+                            wc = certified_bottleneck<2>(
+                                pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane, jb.L, pc), Wv,
+                                lane, jb.L, pc);
+                        } else {
+                            const int mx = B.mmax[dpc - 1];
+                            const double bmx = rint((double)jb.Bg * rcp_approx((double)(dpc * mx)));   // exact
+                            wc = certified_bottleneck<kCertRounds, true>(
+                                pure_split(B.Upure, B.Wtab[0][pc], B.pure_cached, Wv, pcache, lane, jb.L, pc), Wv,
+                                lane, jb.L, pc, B.Pp, B.Ap, ty.mem * (double)tp, bmx, mx < pc ? mx : pc);
+                        }
+                        if (wc == -2.0) {
+                            // no count fits: its plans are priced infeasible without the bottleneck
+                            tally(Wv, lane, kPlans, (unsigned long long)B.mcnt[dpc - 1]);
+                            if (pc <= 64) tm.lo &= ~(1ull << (pc - 1)); else tm.hi &= ~(1ull << (pc - 65));
+                            continue;
+                        }
                         if (!(wc >= 0.0)) break;
                         tm = price_deg(pc, wc, tm);
                     }
