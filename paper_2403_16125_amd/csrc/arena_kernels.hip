@@ -37,6 +37,7 @@ constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
 static_assert(kMaxPlans <= 256, "plan entries are packed below the key in 8 bits");
 constexpr int kCertMinDegree = 2;  // a bottleneck certificate is tried for degrees from here up
+constexpr int kHeadLayers = 4;     // leading layers whose own memory bounds every plan (lower bounds)
 constexpr int kCertRounds = 3;     // splits tried per certificate (2 under the memory rule, whose
                                    // pricing order they change to its cost)
 
@@ -79,6 +80,8 @@ struct BlockLds {
     double p_layer_max;           // largest parameter bytes of one layer
     double x_layer_min;           // smallest boundary activation bytes of one layer
     double x_sum, q_sum;          // sums over the layers of x and of the all-to-all bytes
+    double head_p[kHeadLayers];   // parameter and activation bytes of the leading layers, as prefix
+    double head_a[kHeadLayers];   //   differences (0 past the layer count)
     float xwin[kLmax + 1];        // [pp]: least x bytes of a window of layers whose pure-compute cost
     float qwin[kLmax + 1];        //   reaches Wtab[0][pp], and least all-to-all bytes (rounded down)
     int32_t slot_tp[SLOTS];
@@ -1451,6 +1454,12 @@ struct BoundCtx {
 //   Wpure(pp): W*(pp) >= Wpure(pp) / tp + cx xwin(pp) + cq qwin(pp);
 //   the p2p bytes over the pp-1 stage boundaries >= (pp-1) min_l x_l;
 //   the largest stage's parameters >= max(P / pp, max_l p_l).
+// Memory: besides the parameter bound, the stage holding layer l has at most
+// l - 1 stages before it, so at least min(m, pp - l + 1) microbatches in
+// flight; for l = 1..4, that layer's own bytes with that many microbatches at
+// the largest admissible m lower-bound the pricing's test of that stage term
+// by term (prefix differences, exact integer counts), so when they overflow,
+// no split fits with any m (memory falls as m grows).
 // For fixed dp, T = Bg/dp W + Bg/(dp m) (fill - W) + AR falls as m grows
 // (fill >= W), so the largest admissible m gives the bound.  Reciprocals are
 // estimates; a relative margin of 1e-9 covers them and the rounding.
@@ -1464,6 +1473,17 @@ __device__ double target_bound(const BlockLds<SLOTS>& B, const JobCtx& jb, const
     const double plb = fmax(B.Pp[jb.L] * rpp, B.p_layer_max);
     if (4.0 * plb > ty.mem * (double)bc.tp * (1.0 + 1e-9)) return kInf;
     const double b = rint((double)jb.Bg * rcp_approx((double)(dp * m)));   // exact: dp m divides Bg
+    {
+        const double cap = ty.mem * (double)bc.tp;
+        bool over = false;
+#pragma unroll
+        for (int l = 1; l <= kHeadLayers; ++l) {
+            const int r = pp - l + 1;
+            const int f = m < r ? m : (r > 1 ? r : 1);
+            over |= 4.0 * B.head_p[l - 1] + (double)f * b * B.head_a[l - 1] > cap;
+        }
+        if (over) return kInf;
+    }
     const double Wlb = fmax(bc.UL * rpp, B.Wtab[0][pp] * bc.rtp + (bc.cx * (double)B.xwin[pp] +
                                                                     bc.cq * (double)B.qwin[pp]));
     const double fill = bc.UL + cell.c_p2p * ((double)(pp - 1) * B.x_layer_min);
@@ -1737,6 +1757,10 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
     }
     __syncthreads();
     const int n_slots = B.n_slots;
+    if (tid < kHeadLayers) {
+        B.head_p[tid] = tid < jb.L ? B.Pp[tid + 1] - B.Pp[tid] : 0.0;
+        B.head_a[tid] = tid < jb.L ? B.Ap[tid + 1] - B.Ap[tid] : 0.0;
+    }
     if (wid == 0) tally(Wv, lane, kCells, (unsigned long long)A.n_counts);
 
     for (int s = wid; s < n_slots; s += kWavesPerBlock) {
