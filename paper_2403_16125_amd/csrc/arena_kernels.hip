@@ -37,7 +37,7 @@ constexpr int kLevelStride = 132;  // bytes per successor table (>= kLmax + 1)
 constexpr int kMaxCand = 8;        // tensor degrees of one cell (divisors of a node size <= 31)
 static_assert(kMaxPlans <= 256, "plan entries are packed below the key in 8 bits");
 constexpr int kCertMinDegree = 2;  // a bottleneck certificate is tried for degrees from here up
-constexpr int kHeadLayers = 4;     // leading layers whose own memory bounds every plan (lower bounds)
+constexpr int kHeadLayers = 2;     // leading layers whose own memory bounds every plan (lower bounds)
 constexpr int kCertRounds = 3;     // splits tried per certificate (2 under the memory rule, whose
                                    // pricing order they change to its cost)
 
@@ -1456,7 +1456,7 @@ struct BoundCtx {
 //   the largest stage's parameters >= max(P / pp, max_l p_l).
 // Memory: besides the parameter bound, the stage holding layer l has at most
 // l - 1 stages before it, so at least min(m, pp - l + 1) microbatches in
-// flight; for l = 1..4, that layer's own bytes with that many microbatches at
+// flight; for l = 1, 2, that layer's own bytes with that many microbatches at
 // the largest admissible m lower-bound the pricing's test of that stage term
 // by term (prefix differences, exact integer counts), so when they overflow,
 // no split fits with any m (memory falls as m grows).
