@@ -1590,6 +1590,9 @@ __device__ void window_minima(BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int wid
     }
     wave_sync();
     const double* U = B.Upure;
+    // the bottlenecks fall as pp grows (a split refines into one more stage), so
+    // a start's first reaching end does too: each search ends at the last one
+    int end[2] = {L, L};
     for (int pp = wid + 1; pp <= L; pp += kWavesPerBlock) {
         const double th = B.Wtab[0][pp];
         double bx = kInf, bq = kInf;
@@ -1599,11 +1602,12 @@ __device__ void window_minima(BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int wid
             if (i < L) {
                 const double Ui = U[i];
                 if (U[L] - Ui >= th) {
-                    int lo = i + 1, hi = L;         // the first end whose window reaches th
+                    int lo = i + 1, hi = end[h];    // the first end whose window reaches th
                     while (lo < hi) {
                         const int mid = (lo + hi) >> 1;
                         if (U[mid] - Ui >= th) hi = mid; else lo = mid + 1;
                     }
+                    end[h] = lo;
                     bx = fmin(bx, P[2 * lo] - P[2 * i]);
                     bq = fmin(bq, P[2 * lo + 1] - P[2 * i + 1]);
                 }
