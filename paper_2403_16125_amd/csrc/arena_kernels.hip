@@ -1568,11 +1568,12 @@ __device__ __forceinline__ double wave_incl_sum(double v)
 // x and all-to-all prefixes sit in each wave's UD (x even, all-to-all odd).
 template <int SLOTS>
 __device__ void window_minima(BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int wid, int L, const float* xg,
-                              const float* qg)
+                              const float* qg, bool moe)
 {
     double* P = Wv.UD;
     const double x0 = lane < L ? (double)xg[lane] : 0.0, x1 = lane + 64 < L ? (double)xg[lane + 64] : 0.0;
-    const double q0 = lane < L ? (double)qg[lane] : 0.0, q1 = lane + 64 < L ? (double)qg[lane + 64] : 0.0;
+    // without all-to-all layers every q is 0 and so is every window's
+    const double q0 = moe && lane < L ? (double)qg[lane] : 0.0, q1 = moe && lane + 64 < L ? (double)qg[lane + 64] : 0.0;
     const double sx0 = wave_incl_sum(x0), sq0 = wave_incl_sum(q0);
     const double tx = bcast(sx0, 63), tq = bcast(sq0, 63);
     const double sx1 = wave_incl_sum(x1) + tx, sq1 = wave_incl_sum(q1) + tq;
@@ -1609,15 +1610,15 @@ __device__ void window_minima(BlockLds<SLOTS>& B, WaveLds& Wv, int lane, int wid
                     }
                     end[h] = lo;
                     bx = fmin(bx, P[2 * lo] - P[2 * i]);
-                    bq = fmin(bq, P[2 * lo + 1] - P[2 * i + 1]);
+                    if (moe) bq = fmin(bq, P[2 * lo + 1] - P[2 * i + 1]);
                 }
             }
         }
         bx = wave_reduce1<OpMin>(bx);
-        bq = wave_reduce1<OpMin>(bq);
+        if (moe) bq = wave_reduce1<OpMin>(bq);
         if (lane == 0) {
             B.xwin[pp] = __double2float_rd(fmax(bx, 0.0) * (1.0 - 1e-9));
-            B.qwin[pp] = __double2float_rd(fmax(bq, 0.0) * (1.0 - 1e-9));
+            B.qwin[pp] = moe ? __double2float_rd(fmax(bq, 0.0) * (1.0 - 1e-9)) : 0.0f;
         }
     }
 }
@@ -1799,7 +1800,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
         tally(Wv, lane, kAlgOps, 8ull * (unsigned)jb.L);
     }
     __syncthreads();
-    window_minima(B, Wv, lane, wid, jb.L, A.x + off, A.q + off);
+    window_minima(B, Wv, lane, wid, jb.L, A.x + off, A.q + off, jb.moe);
     __syncthreads();
 
     // ---- cells: take counts, largest first, from the block's work counter
