@@ -1729,14 +1729,32 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
             B.pure_cached[1] = 0ull;
         }
     }
-    // largest admissible microbatch count of each data-parallel degree
+    // largest admissible microbatch count of each data-parallel degree.  Below
+    // 2^20 samples the quotients come from float reciprocals (relative error
+    // about 2^-23, so rounding gives the exact quotient of a divisor) and a
+    // product check decides divisibility; larger batches take integer remainders.
+    const bool small_batch = jb.Bg < (1 << 20);
     for (int dp = tid + 1; dp <= kMaxDp; dp += 256) {
         int mm = 0, mc = 0;
-        for (int i = 0; i < A.n_m; ++i)
-            if (jb.Bg % (dp * A.m_values[i]) == 0) {
-                mm = A.m_values[i] > mm ? A.m_values[i] : mm;
-                ++mc;
+        if (small_batch) {
+            const int q = (int)rintf((float)jb.Bg * __builtin_amdgcn_rcpf((float)dp));
+            if (q * dp == jb.Bg) {
+                for (int i = 0; i < A.n_m; ++i) {
+                    const int m = A.m_values[i];
+                    const int r = (int)rintf((float)q * __builtin_amdgcn_rcpf((float)m));
+                    if (r * m == q) {
+                        mm = m > mm ? m : mm;
+                        ++mc;
+                    }
+                }
             }
+        } else {
+            for (int i = 0; i < A.n_m; ++i)
+                if (jb.Bg % (dp * A.m_values[i]) == 0) {
+                    mm = A.m_values[i] > mm ? A.m_values[i] : mm;
+                    ++mc;
+                }
+        }
         B.mmax[dp - 1] = (uint8_t)mm;
         B.mcnt[dp - 1] = (uint8_t)mc;
     }
