@@ -2225,6 +2225,8 @@ struct TabBlockLds {
     int32_t share;                    // one kappa for all counts of the type: bottlenecks are shared
     double Upure[kLmax + kPad];       // prefix of the pure-compute per-sample cost (+inf padded)
     double Wpure[kLmax + 1];          // its bottleneck by degree (every degree up to the layer count)
+    double head_p[kHeadLayers];       // parameter and activation bytes of the leading layers, as prefix
+    double head_a[kHeadLayers];       //   differences (0 past the layer count)
     unsigned long long pure_cached[2];   // bit pp-1: the block's cache row of the pure split of pp is current
     WaveLds w[kWavesPerBlock];
     double cW[kTabCache];             // bottleneck cache of the (job, type): bottlenecks
@@ -2380,14 +2382,24 @@ __device__ __forceinline__ double tab_price(const TabBlockLds& B, WaveLds& Wv, i
 __device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, const JobCtx& jb, const TypeDev& ty,
                                             int K, const Cell& cell, int dp, int tp, int pp, int m, double b)
 {
+    const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
+    if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
+    // the stage holding layer l (l <= kHeadLayers) has at most l - 1 stages
+    // before it: at least min(m, pp - l + 1) microbatches in flight, and that
+    // layer's own bytes lower-bound its memory term by term
+#pragma unroll
+    for (int l = 1; l <= kHeadLayers; ++l) {
+        const int r = pp - l + 1;
+        const int f = m < r ? m : (r > 1 ? r : 1);
+        const double memb = 4.0 * B.head_p[l - 1] / (double)tp + (double)f * b * B.head_a[l - 1] / (double)tp;
+        if (!(memb <= ty.mem)) return kInf;
+    }
     double c[2];
     tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp, tp, b, c);
     double rs[1] = {c[0] + c[1]};
     double rm[1] = {fmax(c[0], c[1])};
     wave_reduce<OpSum, 1>(rs);
     wave_reduce<OpMax, 1>(rm);
-    const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
-    if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
     const double UL = rs[0];
     const double Wlb = fmax(UL / (double)pp, rm[0]);
     const int lpp = cell.n <= ty.gpn ? 0 : 1;
@@ -2460,6 +2472,10 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
         const double v0 = lane < jb.L ? (double)src[lane] : 0.0;
         const double v1 = lane + 64 < jb.L ? (double)src[lane + 64] : 0.0;
         seq_prefix<1, 2>(v0, v1, jb.L, lane, wid == 0 ? B.Pp : B.Ap, Wv.UD + 1, false);
+        if (lane < kHeadLayers) {
+            const double* pre = wid == 0 ? B.Pp : B.Ap;
+            (wid == 0 ? B.head_p : B.head_a)[lane] = lane < jb.L ? pre[lane + 1] - pre[lane] : 0.0;
+        }
         if (wid == 0) {
             const double pm = wave_reduce1<OpMax>(fmax(v0, v1));
             if (lane == 0) B.p_layer_max = pm;
