@@ -586,7 +586,9 @@ arena_status arena_bind_grids(arena_ctx* c, const arena_grids_desc* d)
         ty[g].bw_intra = d->bw_intra[g];
         ty[g].bw_inter = d->bw_inter[g];
         ty[g].gpn = gpn;
-        ty[g].pad = 0;
+        ty[g].divs = 0u;
+        for (int dd = 1; dd <= gpn; ++dd)
+            if (gpn % dd == 0) ty[g].divs |= 1u << dd;
     }
     for (int i = 0; i < d->n_counts; ++i) {
         const int n = d->counts[i];

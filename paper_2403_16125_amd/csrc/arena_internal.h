@@ -21,7 +21,7 @@ constexpr int kQueues = 8;          // item queues, one per XCD (each XCD has it
 struct TypeDev {
     double speed, mem, bw_intra, bw_inter;
     int32_t gpn;
-    int32_t pad;
+    uint32_t divs;    // bit d: d divides gpn (gpn <= 31)
 };
 
 // Device tallies, zeroed before each estimate.

@@ -228,6 +228,19 @@ __device__ __forceinline__ double rcp_approx(double x)
 
 // Link bandwidth by value (a conditional over two fields of one struct would
 // select an address and keep the struct in private memory).
+// Does a group of grp GPUs (>= 1) tile a node (grp divides the node size)?
+__device__ __forceinline__ bool tiles_node(const TypeDev& ty, int grp)
+{
+    return grp < 32 && ((ty.divs >> grp) & 1u);
+}
+
+// n / d for d dividing n <= ARENA_MAX_GPU_COUNT: the float quotient is
+// within 1e-6 relative of the integer, which rounding recovers.
+__device__ __forceinline__ int exact_quot(int n, int d)
+{
+    return (int)rintf((float)n * __builtin_amdgcn_rcpf((float)d));
+}
+
 __device__ __forceinline__ double link_bw(bool intra, const TypeDev& ty)
 {
     const double a = ty.bw_intra;
@@ -284,14 +297,14 @@ __device__ __forceinline__ bool adm_ok(const uint8_t* mmax, int dp)
     return mmax[dp - 1] != 0;
 }
 
-// Is pp a requested degree of problem (n, tp, variant)?  pp divides n/tp, is
+// Is pp a requested degree of problem (n, tp, variant), tp dividing n?  pp divides n/tp, is
 // at most the layer count, leaves an admissible data-parallel degree, and
 // meets the all-to-all condition of the variant (variant 1: the MoE job's
 // single-GPU-per-stage plan dp = tp = 1, which has no all-to-all).
 __device__ __forceinline__ bool target_ok(const uint8_t* adm, const JobCtx& jb, int n, int tp,
                                           int variant, int pp)
 {
-    const int qn = n / tp;
+    const int qn = exact_quot(n, tp);
     if (pp > jb.L || pp > qn) return false;
     // qn / pp when pp divides qn (qn <= 1024: the float quotient is within 1e-3)
     const int d = (int)rintf((float)qn * __builtin_amdgcn_rcpf((float)pp));
@@ -1202,9 +1215,9 @@ __device__ double price_exact(const BlockLds<SLOTS>& B, WaveLds& Wv, const doubl
                               const JobCtx& jb, const TypeDev& ty, const Cell& cell, int tp, int pp, double W,
                               int& np, double best, double tie_eps, bool prune)
 {
-    const int dp = cell.n / (tp * pp);
+    const int dp = exact_quot(cell.n, tp * pp);
     const int grp = dp * tp;
-    const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
+    const double B_dp = link_bw(tiles_node(ty, grp), ty);
     bool adm = false;
     double b = 0.0;
     if (mv > 0) {
@@ -1300,9 +1313,9 @@ __device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U,
                     : canonical_stages<1>(U, Wv.J, lane, jb.L, pp, W);
     else
         sg = canonical_stages<S>(U, Wv.J, lane, jb.L, pp, W);
-    const int dp = cell.n / (tp * pp);
+    const int dp = exact_quot(cell.n, tp * pp);
     const int grp = dp * tp;
-    const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
+    const double B_dp = link_bw(tiles_node(ty, grp), ty);
 
     // per-stage parameter and activation bytes of the lane's stages
     const bool act0 = lane < pp, act1 = lane + 64 < pp;
@@ -1527,7 +1540,7 @@ __device__ __forceinline__ BoundCtx bound_ctx(const Cell& cell, int tp, double U
 {
     BoundCtx bc;
     bc.tp = tp;
-    bc.qn = cell.n / tp;
+    bc.qn = exact_quot(cell.n, tp);
     bc.rtp = tp == 1 ? 1.0 : rcp_approx((double)tp);
     bc.UL = UL;
     bc.ar_intra = ar_intra1 * bc.rtp;
@@ -1682,9 +1695,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
 #pragma unroll
     for (int i = 0; i < kMaxM; ++i)
         if (lane == i && i < A.n_m) mv = A.m_values[i];
-    unsigned gpn_divs = 0;           // bit d: d divides the node size
-    for (int d = 1; d <= ty.gpn; ++d)
-        if (ty.gpn % d == 0) gpn_divs |= 1u << d;
+    const unsigned gpn_divs = ty.divs;   // bit d: d divides the node size
 
     // ---- stage the job
     bool has_q = false;
@@ -1886,7 +1897,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
         const int tpmax = cell.n < ty.gpn ? cell.n : ty.gpn;
         int ncand = 0;
         for (int tp = 1; tp <= tpmax; ++tp) {
-            if (cell.n % tp != 0 || ((gpn_divs >> tp) & 1u) == 0) continue;
+            if (((gpn_divs >> tp) & 1u) == 0 || exact_quot(cell.n, tp) * tp != cell.n) continue;
             if (tp == 1 && !jb.moe) continue;          // the pure-compute problem
             const Mask tm = ballot_mask(target_ok(B.mmax, jb, cell.n, tp, 0, 1 + lane),
                                         target_ok(B.mmax, jb, cell.n, tp, 0, 65 + lane));
@@ -1970,7 +1981,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                     for (int pc = tm.last(); pc >= kCertMinDegree; pc = tm.last()) {
                         // the memory test of the degree's largest admissible count
                         // (not under the memory rule, whose splits differ)
-                        const int dpc = cell.n / (tp * pc);
+                        const int dpc = exact_quot(cell.n, tp * pc);
                         double wc;
                         if constexpr (MEM) {
                             wc = certified_bottleneck<2>(
@@ -2035,7 +2046,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
         const int pp = (int)(kbest >> 12);
         const int tp = (int)((kbest >> 7) & 0x1Fu);
         const int m = (int)(kbest & 0x7Fu);
-        const int dp = cell.n / (tp * pp);
+        const int dp = exact_quot(cell.n, tp * pp);
         if (lane == 0) {
             const float tt = (float)Tb, th = (float)((double)jb.Bg / Tb);
             const uint32_t pw = (unsigned)dp | ((unsigned)tp << 11) | ((unsigned)pp << 16) |
@@ -2082,7 +2093,7 @@ __device__ __forceinline__ void estimate_body(const EstimateArgs& A, int wid, in
                 // the winner's exact-T split, solved again for its count
                 const double bw = rint((double)jb.Bg / (double)(dp * m));
                 const int grp = dp * tp;
-                const double B_dp = link_bw(grp <= ty.gpn && ty.gpn % grp == 0, ty);
+                const double B_dp = link_bw(tiles_node(ty, grp), ty);
                 ExtCtx E;
                 E.L = jb.L;
                 E.pp = pp;
@@ -2341,7 +2352,7 @@ __device__ __forceinline__ double tab_price(const TabBlockLds& B, WaveLds& Wv, i
 {
     const int lpp = cell.n <= ty.gpn ? 0 : 1;
     const int grp = dp * tp;
-    const int ldp = (grp <= ty.gpn && ty.gpn % grp == 0) ? 0 : 1;
+    const int ldp = tiles_node(ty, grp) ? 0 : 1;
     const double fdp = 2.0 * (double)(dp - 1) / (double)dp;
     double fill = 0.0, wmax = 0.0, armax = 0.0, memmax = 0.0;
 #pragma unroll
@@ -2404,7 +2415,7 @@ __device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, cons
     const double Wlb = fmax(UL / (double)pp, rm[0]);
     const int lpp = cell.n <= ty.gpn ? 0 : 1;
     const int grp = dp * tp;
-    const int ldp = (grp <= ty.gpn && ty.gpn % grp == 0) ? 0 : 1;
+    const int ldp = tiles_node(ty, grp) ? 0 : 1;
     const double p2p = pp > 1 ? cell.kappa * (2.0 * tab_lat(B.vol[lpp], B.lat[lpp], K, b * B.x_layer_min)) : 0.0;
     const double ar = dp > 1
         ? cell.kappa * tab_lat(B.vol[ldp], B.lat[ldp], K, 2.0 * (double)(dp - 1) / (double)dp * (plb / (double)tp))
@@ -2528,15 +2539,15 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
         // the plans: keys and lower bounds
         int np = 0, nskip = 0;
         for (int tp = 1; tp <= cell.n && tp <= ty.gpn; ++tp) {
-            if (cell.n % tp != 0 || ty.gpn % tp != 0) continue;
-            const int qn = cell.n / tp;
+            if (!tiles_node(ty, tp) || exact_quot(cell.n, tp) * tp != cell.n) continue;
+            const int qn = exact_quot(cell.n, tp);
             for (int pp = 1; pp <= qn && pp <= jb.L; ++pp) {
-                if (qn % pp != 0) continue;
-                const int dp = qn / pp;
+                const int dp = exact_quot(qn, pp);
+                if (dp * pp != qn) continue;
                 for (int mi = 0; mi < A.n_m; ++mi) {
                     const int m = A.m_values[mi];
                     const double dm = (double)(dp * m);
-                    const double bq = rint((double)jb.Bg / dm);
+                    const double bq = rint((double)jb.Bg * rcp_approx(dm));   // exact when dm divides Bg
                     if (!(bq * dm == (double)jb.Bg)) continue;
                     const double lb = A.prune ? tab_bound(B, lane, jb, ty, K, cell, dp, tp, pp, m, bq) : 0.0;
                     if (lane == 0 && np < kMaxPlans) {
@@ -2560,7 +2571,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
             const unsigned key0 = Wv.planKey[e0] & kTabKeyMask;
             const int pp0 = (int)(key0 >> 12);
             const int tp0 = (int)((key0 >> 7) & 0x1Fu);
-            const int dp0 = cell.n / (tp0 * pp0);
+            const int dp0 = exact_quot(cell.n, tp0 * pp0);
             const double bq0 = rint((double)jb.Bg / (double)(dp0 * (int)(key0 & 0x7Fu)));
             const bool fl0 = dp0 * tp0 > 1;
             const double lim0 = best_in * (1.0 + A.tie_eps);
@@ -2573,7 +2584,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
                 const int pp = (int)(k >> 12);
                 const int tp = (int)((k >> 7) & 0x1Fu);
                 if (tp != tp0) continue;
-                const int dp = cell.n / (tp * pp);
+                const int dp = exact_quot(cell.n, tp * pp);
                 if ((dp * tp > 1) != fl0 || rint((double)jb.Bg / (double)(dp * (int)(k & 0x7Fu))) != bq0) continue;
                 const double lbe = Wv.planT[e];
                 if (e != e0 && A.prune && !(lbe < kInf && lbe <= lim0)) continue;
@@ -2589,7 +2600,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
             // prices degree pp of the group at bottleneck W; returns the degrees still wanted
             auto price_deg = [&](int pp, double W, Mask mk) -> Mask {
                 const int e = (int)Wv.lbnd[pp - 1];
-                const int dp = cell.n / (tp0 * pp);
+                const int dp = exact_quot(cell.n, tp0 * pp);
                 const int m = (int)(Wv.planKey[e] & 0x7Fu);
                 const Stages sg = canonical_stages<2>(Wv.UD, Wv.J, lane, jb.L, pp, W);
                 const double T = tab_price(B, Wv, lane, jb, ty, K, cell, dp, tp0, pp, m, bq0, sg);
@@ -2704,7 +2715,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
         const int pp = (int)(kbest >> 12);
         const int tp = (int)((kbest >> 7) & 0x1Fu);
         const int m = (int)(kbest & 0x7Fu);
-        const int dp = cell.n / (tp * pp);
+        const int dp = exact_quot(cell.n, tp * pp);
         if (lane == 0) {
             A.t_iter[cidx] = (float)Tb;
             A.thr[cidx] = (float)((double)jb.Bg / Tb);
