@@ -226,8 +226,6 @@ __device__ __forceinline__ double rcp_approx(double x)
 
 // ------------------------------------------------------------ model pieces
 
-// Link bandwidth by value (a conditional over two fields of one struct would
-// select an address and keep the struct in private memory).
 // Does a group of grp GPUs (>= 1) tile a node (grp divides the node size)?
 __device__ __forceinline__ bool tiles_node(const TypeDev& ty, int grp)
 {
@@ -241,6 +239,8 @@ __device__ __forceinline__ int exact_quot(int n, int d)
     return (int)rintf((float)n * __builtin_amdgcn_rcpf((float)d));
 }
 
+// Link bandwidth by value (a conditional over two fields of one struct would
+// select an address and keep the struct in private memory).
 __device__ __forceinline__ double link_bw(bool intra, const TypeDev& ty)
 {
     const double a = ty.bw_intra;
