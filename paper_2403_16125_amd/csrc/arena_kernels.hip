@@ -2390,8 +2390,14 @@ __device__ __forceinline__ double tab_price(const TabBlockLds& B, WaveLds& Wv, i
 // boundaries moves at least the smallest boundary activation, the largest
 // stage holds at least max(P / pp, max p_l) of parameters, and f is
 // non-decreasing.  A relative margin of 1e-9 covers the sums' rounding.
-__device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, const JobCtx& jb, const TypeDev& ty,
-                                            int K, const Cell& cell, int dp, int tp, int pp, int m, double b)
+// The sum and the largest of the per-microbatch costs depend on the plan only
+// through (tp, b, dp tp > 1): the wave keeps those of the cell's current tp in
+// a small table in its UD row (unused until the plans are priced): keys at
+// [0, 64) (b, negated when dp tp = 1), sums at [64, 128), largest at [128, 192);
+// `nc` entries (uniform).
+__device__ __forceinline__ double tab_bound(const TabBlockLds& B, WaveLds& Wv, int lane, const JobCtx& jb,
+                                            const TypeDev& ty, int K, const Cell& cell, int dp, int tp, int pp,
+                                            int m, double b, int& nc)
 {
     const double plb = fmax(B.Pp[jb.L] / (double)pp, B.p_layer_max);
     if (4.0 * plb > ty.mem * (double)tp * (1.0 + 1e-9)) return kInf;
@@ -2405,14 +2411,34 @@ __device__ __forceinline__ double tab_bound(const TabBlockLds& B, int lane, cons
         const double memb = 4.0 * B.head_p[l - 1] / (double)tp + (double)f * b * B.head_a[l - 1] / (double)tp;
         if (!(memb <= ty.mem)) return kInf;
     }
-    double c[2];
-    tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp, tp, b, c);
-    double rs[1] = {c[0] + c[1]};
-    double rm[1] = {fmax(c[0], c[1])};
-    wave_reduce<OpSum, 1>(rs);
-    wave_reduce<OpMax, 1>(rm);
-    const double UL = rs[0];
-    const double Wlb = fmax(UL / (double)pp, rm[0]);
+    const double key = dp * tp > 1 ? b : -b;
+    const unsigned long long hit = __ballot(lane < nc && Wv.UD[lane] == key);
+    double UL, cmax;
+    if (hit) {
+        const int e = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(hit));
+        UL = Wv.UD[64 + e];
+        cmax = Wv.UD[128 + e];
+    } else {
+        double c[2];
+        tab_layer_costs(B, lane, jb, ty, K, cell.kappa, dp, tp, b, c);
+        double rs[1] = {c[0] + c[1]};
+        double rm[1] = {fmax(c[0], c[1])};
+        wave_reduce<OpSum, 1>(rs);
+        wave_reduce<OpMax, 1>(rm);
+        UL = rs[0];
+        cmax = rm[0];
+        tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
+        if (nc < 64) {
+            if (lane == 0) {
+                Wv.UD[nc] = key;
+                Wv.UD[64 + nc] = UL;
+                Wv.UD[128 + nc] = cmax;
+            }
+            wave_sync();
+            ++nc;
+        }
+    }
+    const double Wlb = fmax(UL / (double)pp, cmax);
     const int lpp = cell.n <= ty.gpn ? 0 : 1;
     const int grp = dp * tp;
     const int ldp = tiles_node(ty, grp) ? 0 : 1;
@@ -2541,6 +2567,7 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
         for (int tp = 1; tp <= cell.n && tp <= ty.gpn; ++tp) {
             if (!tiles_node(ty, tp) || exact_quot(cell.n, tp) * tp != cell.n) continue;
             const int qn = exact_quot(cell.n, tp);
+            int nc = 0;                     // the bounds' cost sums of this tp
             for (int pp = 1; pp <= qn && pp <= jb.L; ++pp) {
                 const int dp = exact_quot(qn, pp);
                 if (dp * pp != qn) continue;
@@ -2549,13 +2576,12 @@ __device__ __forceinline__ void estimate_tab_body(const EstimateArgs& A, int wid
                     const double dm = (double)(dp * m);
                     const double bq = rint((double)jb.Bg * rcp_approx(dm));   // exact when dm divides Bg
                     if (!(bq * dm == (double)jb.Bg)) continue;
-                    const double lb = A.prune ? tab_bound(B, lane, jb, ty, K, cell, dp, tp, pp, m, bq) : 0.0;
+                    const double lb = A.prune ? tab_bound(B, Wv, lane, jb, ty, K, cell, dp, tp, pp, m, bq, nc) : 0.0;
                     if (lane == 0 && np < kMaxPlans) {
                         Wv.planT[np] = lb;
                         Wv.planKey[np] = ((unsigned)pp << 12) | ((unsigned)tp << 7) | (unsigned)m;
                     }
                     ++np;
-                    if (A.prune) tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L);
                 }
             }
         }
