@@ -305,12 +305,16 @@ __device__ __forceinline__ bool target_ok(const uint8_t* adm, const JobCtx& jb, 
                                           int variant, int pp)
 {
     const int qn = exact_quot(n, tp);
-    // qn / pp when pp divides qn (qn <= 1024: the float quotient is within 1e-3);
-    // the tests combine without branches (lanes differ in pp)
+    if (pp > jb.L || pp > qn) return false;
+    // qn / pp when pp divides qn (qn <= 1024: the float quotient is within 1e-3)
     const int d = (int)rintf((float)qn * __builtin_amdgcn_rcpf((float)pp));
-    bool ok = (pp <= jb.L) & (pp <= qn) & (__umul24(d, pp) == (unsigned)qn);
-    ok &= variant == 0 ? !(jb.moe & (pp >= n)) : pp == n;
-    return ok & adm_ok(adm, ok ? d : 1);     // d >= 1 where ok
+    if (__umul24(d, pp) != qn) return false;
+    if (variant == 0) {
+        if (jb.moe && pp >= n) return false;
+    } else if (pp != n) {
+        return false;
+    }
+    return adm_ok(adm, d);
 }
 
 // Degrees as a 128-bit mask (bit pp-1), uniform across the wave.
@@ -1226,7 +1230,7 @@ __device__ double price_exact(const BlockLds<SLOTS>& B, WaveLds& Wv, const doubl
     }
     const unsigned long long amask = __ballot(adm);
     const int nadm = __popcll(amask);
-    tally(Wv, lane, kAlgOps, (unsigned long long)(4u * (unsigned)jb.L + (unsigned)nadm * (12u * (unsigned)pp + 40u)));
+    tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull));
     if (nadm == 0) return kInf;
     const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
     if (adm) {
@@ -1341,7 +1345,7 @@ __device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U,
     }
     const unsigned long long amask = __ballot(adm);
     const int nadm = __popcll(amask);
-    tally(Wv, lane, kAlgOps, (unsigned long long)(4u * (unsigned)jb.L + (unsigned)nadm * (12u * (unsigned)pp + 40u)));
+    tally(Wv, lane, kAlgOps, 4ull * (unsigned)jb.L + (unsigned long long)nadm * (12ull * (unsigned)pp + 40ull));
     if (nadm == 0) return kInf;
     const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(amask >> 32),
                                                __builtin_amdgcn_mbcnt_lo((unsigned)amask, 0u));
@@ -1360,7 +1364,7 @@ __device__ double price_target(BlockLds<SLOTS>& B, WaveLds& Wv, const double* U,
         const int m = Wv.mq[rk];
         const double i0 = (double)(m < r0 ? m : r0) * bm;
         const double i1 = (double)(m < r1 ? m : r1) * bm;
-        const bool over = act0 ? ((fP0 + i0 * A0 > cap) | (act1 & (fP1 + i1 * A1 > cap))) : false;
+        const bool over = (act0 && fP0 + i0 * A0 > cap) || (act1 && fP1 + i1 * A1 > cap);
         return __ballot(over) != 0ull;
     };
     int lo = 0, hi = nadm;                                  // first fitting rank in [lo, hi]
