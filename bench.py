@@ -443,7 +443,7 @@ def main() -> int:
     log(f"{w.n_jobs} jobs, {w.n_types} types, {w.n_counts} counts, {w.n_cells} cells, "
         f"{w.n_rounds} rounds of contention factors")
     work = workcount.count(w, kappa_round=0)
-    log(f"work per round (survey convention): {work['ops']:.4g} ops ({work['dp_entries_full']:.4g} recursion "
+    log(f"work per round (exhaustive plan space): {work['ops']:.4g} ops ({work['dp_entries_full']:.4g} recursion "
         f"entries), {work['plans']} plans, {work['problems']} partition problems; truncated rows "
         f"{work['ops_truncated']:.4g} ops")
 
@@ -496,7 +496,7 @@ def main() -> int:
     traffic = stored_traffic(args.workload) if plain else None
     cells_per_s = w.n_cells * args.steps / wall
     launch_s = float(np.sum(launch_ms)) / 1e3
-    # numerator: the survey's count of the method's work per round (8 L + 8 L P
+    # numerator: the method's work per round over the exhaustive plan space (8 L + 8 L P
     # + 4 L |S| per distinct partition problem, 12 pp + 40 per plan); it does not
     # depend on the contention round.  Beside it: the same units with
     # truncated recursion rows, and the device's tally of the work it did.
@@ -538,7 +538,7 @@ def main() -> int:
             "frac": achieved / PEAK_LANE_OPS,
             "traffic": traffic,
             "ops_per_launch": ops_round if plain else float(np.mean(ops_done)),
-            "ops_convention": ("survey: 8 L + 8 L P + 4 L |S| per distinct partition problem + 12 pp + 40 per plan"
+            "ops_convention": ("exhaustive: 8 L + 8 L P + 4 L |S| per distinct partition problem + 12 pp + 40 per plan"
                                if plain else "device tally of the work done"),
             "launch_ms": launch_s / args.steps * 1e3,
             "frac_truncated_rows": (float(work["ops_truncated"]) * args.steps / launch_s / PEAK_LANE_OPS
