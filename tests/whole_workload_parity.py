@@ -8,9 +8,10 @@ calls release the interpreter lock and keep no global state) and takes
 minutes.
 
     python tests/whole_workload_parity.py [--workload full|trace|moe] [--round R]
-        [--partition balanced|memory | --comm-tables | --proxy] [--threads N]
+        [--partition balanced|memory|exact-t | --comm-tables | --proxy] [--threads N]
 
---partition memory and --comm-tables compare the estimator's variants with
+--partition memory, --partition exact-t (jobs of at most 96 layers: the
+trace-like workload) and --comm-tables compare the estimator's variants with
 the oracle's; --proxy compares the proxy-plan planner with its oracle (plan
 identical -- stage count, microbatches, stage bounds, GPUs and tensor degree
 per stage -- and T within 1e-6 relative).
@@ -105,7 +106,7 @@ def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="full", choices=["full", "trace", "moe"])
     ap.add_argument("--round", type=int, default=0, help="contention round (0..9)")
-    ap.add_argument("--partition", default="balanced", choices=["balanced", "memory"])
+    ap.add_argument("--partition", default="balanced", choices=["balanced", "memory", "exact-t"])
     ap.add_argument("--comm-tables", action="store_true")
     ap.add_argument("--proxy", action="store_true")
     ap.add_argument("--no-cuts", action="store_true",
@@ -115,11 +116,11 @@ def main() -> int:
                          "estimates the whole workload")
     ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--chunk-jobs", type=int, default=None,
-                    help="jobs per oracle call (default 32; 4 with --partition memory and 2 with --proxy, "
-                         "whose oracles are slower)")
+                    help="jobs per oracle call (default 32; 4 with --partition memory, 2 with --partition "
+                         "exact-t and --proxy, whose oracles are slower)")
     args = ap.parse_args()
-    if sum([args.partition == "memory", args.comm_tables, args.proxy]) > 1:
-        ap.error("choose one of --partition memory, --comm-tables, --proxy")
+    if sum([args.partition != "balanced", args.comm_tables, args.proxy]) > 1:
+        ap.error("choose one of --partition memory|exact-t, --comm-tables, --proxy")
 
     from oracle import oracle
     from oracle import proxy as px
@@ -129,13 +130,13 @@ def main() -> int:
 
     oracle.load()
     w = wl.make(args.workload)
-    rule = 1 if args.partition == "memory" else 0
+    rule = {"balanced": 0, "memory": 1, "exact-t": 2}[args.partition]
     tables = wl.comm_tables(w) if args.comm_tables else None
-    mode = ("proxy planner" if args.proxy else "memory rule" if rule else
+    mode = ("proxy planner" if args.proxy else "memory rule" if rule == 1 else "exact-T rule" if rule == 2 else
             "comm tables" if tables is not None else "balanced")
     say(f"{args.workload} round {args.round} ({mode}): {w.n_cells} cells; estimating on the GPU")
     est = arena.Estimator(w, with_cuts=not (args.proxy or args.no_cuts),
-                          rule=arena.PARTITION_MEMORY if rule else arena.PARTITION_BALANCED,
+                          rule=(arena.PARTITION_BALANCED, arena.PARTITION_MEMORY, arena.PARTITION_EXACT_T)[rule],
                           comm_tables=tables)
     try:
         if args.round:
@@ -150,7 +151,7 @@ def main() -> int:
         est.close()
     per_job = w.n_types * w.n_counts
     if args.chunk_jobs is None:          # about 10-30 s of oracle work per chunk
-        args.chunk_jobs = 2 if args.proxy else 4 if rule else 32
+        args.chunk_jobs = 2 if args.proxy or rule == 2 else 4 if rule else 32
     jobs = np.arange(0, w.n_jobs, args.job_every, dtype=np.int64)
     chunks = [jobs[i:i + args.chunk_jobs] for i in range(0, len(jobs), args.chunk_jobs)]
     n_want = len(jobs) * per_job
