@@ -605,13 +605,18 @@ __device__ Stages canonical_stages(const double* U, uint8_t* J, int lane, int L,
     return stages_from_tables(J, lane, L, pp, levels);
 }
 
+constexpr int kPureCachedDegrees = 96;
+
 // The pure-compute problem's canonical split of pp >= 2 stages (the cuts of
 // its prefix Upure at its bottleneck wpure = Wpure(pp)).  It depends on
 // neither the count, nor the contention, nor the tensor degree, so the block
 // keeps it, once computed for its current item, in its rows of a global cache
 // (row pp: the bytes c_0 .. c_pp), and bit pp - 1 of `cached` (LDS, cleared
 // per item) says that the row is current.  Two waves that miss together both
-// write the same bytes.
+// write the same bytes.  Degrees above kPureCachedDegrees are recomputed: few
+// items use them, so their rows leave L2 between uses and each write of one
+// came back as HBM write-back (a fifth of the kernel's traffic) while saving
+// little time.
 __device__ Stages pure_split(const double* Upure, double wpure, unsigned long long* cached, WaveLds& Wv,
                              uint8_t* cache, int lane, int L, int pp)
 {
@@ -620,7 +625,7 @@ __device__ Stages pure_split(const double* Upure, double wpure, unsigned long lo
     unsigned long long* word = &cached[(pp - 1) >> 6];
     const unsigned long long bit = 1ull << ((pp - 1) & 63);
     const unsigned long long w = __hip_atomic_load(word, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    const bool hit = __builtin_amdgcn_readfirstlane((int)((w & bit) != 0ull)) != 0;
+    const bool hit = pp <= kPureCachedDegrees && __builtin_amdgcn_readfirstlane((int)((w & bit) != 0ull)) != 0;
     int cA, cB;
     if (hit) {
         cA = lane <= pp ? (int)row[lane] : 0;
@@ -629,11 +634,13 @@ __device__ Stages pure_split(const double* Upure, double wpure, unsigned long lo
         const int levels = 32 - __clz(pp - 1);   // 2^levels > pp - 1
         successor_tables<1>(Upure, Wv.J, lane, L, levels, wpure);
         cuts_from_tables(Wv.J, lane, L, pp, levels, cA, cB);
-        if (lane <= pp) row[lane] = (uint8_t)cA;
-        if (lane + 64 <= pp) row[lane + 64] = (uint8_t)cB;
-        // the row's stores before the bit
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        if (lane == 0) __hip_atomic_fetch_or(word, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (pp <= kPureCachedDegrees) {
+            if (lane <= pp) row[lane] = (uint8_t)cA;
+            if (lane + 64 <= pp) row[lane + 64] = (uint8_t)cB;
+            // the row's stores before the bit
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            if (lane == 0) __hip_atomic_fetch_or(word, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
     }
     return stages_from_cuts(cA, cB, L, pp);
 }
